@@ -1,0 +1,176 @@
+"""CPU oracle of the GLIDE hybrid-attention layer -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product library never calls it,
+and it shares no code with the GPU path: the arithmetic lives in
+``glide_oracle.c`` (plain C, float64, scalar loops); this module only
+marshals numpy arrays into it.
+
+Definition implemented (GLIDE, Sec. III-B first three displayed equations
+with the window split read as W = w - delta; Sec. II-B recurrence; Sec. II-C
+window; shared-denominator merge of Sec. II-A / III-B): see the header of
+``glide_oracle.c``.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_c_double_p = ctypes.POINTER(ctypes.c_double)
+_c_int64_p = ctypes.POINTER(ctypes.c_int64)
+
+
+class OracleLayer(ctypes.Structure):
+    _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("feat_dim", ctypes.c_int32),
+                ("window", ctypes.c_int32), ("linear", ctypes.c_int32),
+                ("tau", ctypes.c_double)]
+
+
+_LIBS = {}
+
+
+def load(path=None):
+    """Load (building first if absent) the oracle library at ``path``."""
+    path = path or _build.LIB
+    if path in _LIBS:
+        return _LIBS[path]
+    if not os.path.exists(path):
+        if path != _build.LIB:
+            raise FileNotFoundError(path)
+        _build.build(path)
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER(OracleLayer)
+    lib.oracle_phi.argtypes = [P, _c_double_p, ctypes.c_int64, _c_double_p, _c_double_p]
+    lib.oracle_phi.restype = None
+    lib.oracle_attend.argtypes = [P, _c_double_p, ctypes.c_int64, _c_double_p, _c_double_p,
+                                  _c_double_p, ctypes.c_int64, _c_int64_p, _c_double_p]
+    lib.oracle_attend.restype = ctypes.c_int
+    lib.oracle_state.argtypes = [P, _c_double_p, ctypes.c_int64, _c_double_p, _c_double_p,
+                                 _c_double_p, _c_double_p]
+    lib.oracle_state.restype = ctypes.c_int
+    lib.oracle_decode_batch.argtypes = [P, _c_double_p, ctypes.c_int32, _c_double_p, _c_double_p,
+                                        _c_double_p, _c_double_p, _c_int64_p, _c_double_p,
+                                        _c_double_p, _c_double_p, _c_double_p]
+    lib.oracle_decode_batch.restype = ctypes.c_int
+    _LIBS[path] = lib
+    return lib
+
+
+def _d(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+    return a, a.ctypes.data_as(_c_double_p)
+
+
+class Oracle:
+    """One layer's oracle: Hq, Hkv, d, Df, window W, linear on/off, tau."""
+
+    def __init__(self, n_q_heads, n_kv_heads, head_dim, feat_dim, window, linear=True,
+                 tau=None, lib=None):
+        if tau is None:
+            tau = 1.0 / np.sqrt(head_dim)
+        self.L = OracleLayer(n_q_heads, n_kv_heads, head_dim, feat_dim, window,
+                             1 if linear else 0, float(tau))
+        self.lib = lib if lib is not None else load()
+
+    # -- feature map -------------------------------------------------------
+    def phi(self, Wf, x):
+        """phi(x) = max(0, x @ Wf) over the last axis; x [..., d] -> [..., Df]."""
+        L = self.L
+        x, xp = _d(x)
+        Wf, wp = _d(Wf)
+        rows = x.size // L.head_dim
+        out = np.empty(x.shape[:-1] + (L.feat_dim,), np.float64)
+        self.lib.oracle_phi(ctypes.byref(L), wp, rows, xp, out.ctypes.data_as(_c_double_p))
+        return out
+
+    # -- definition (quadratic) form ----------------------------------------
+    def attend(self, Wf, q, k, v, positions=None):
+        """O_t for one sequence.  q [n][Hq][d], k/v [n][Hkv][d].
+
+        ``positions``: the t to evaluate (default: all).  Returns [len][Hq][d].
+        """
+        L = self.L
+        q, qp = _d(q)
+        k, kp = _d(k)
+        v, vp = _d(v)
+        Wf, wp = _d(Wf)
+        n = q.shape[0]
+        if positions is None:
+            positions = np.arange(n, dtype=np.int64)
+        pos = np.ascontiguousarray(np.asarray(positions, dtype=np.int64))
+        out = np.empty((pos.size, L.n_q_heads, L.head_dim), np.float64)
+        rc = self.lib.oracle_attend(ctypes.byref(L), wp, n, qp, kp, vp, pos.size,
+                                    pos.ctypes.data_as(_c_int64_p),
+                                    out.ctypes.data_as(_c_double_p))
+        if rc != 0:
+            raise ValueError("oracle_attend rejected its arguments")
+        return out
+
+    def state(self, Wf, k, v, p=None):
+        """(S [Hkv][Df][d], z [Hkv][Df]) after the first p tokens (default all)."""
+        L = self.L
+        k, kp = _d(k)
+        v, vp = _d(v)
+        Wf, wp = _d(Wf)
+        if p is None:
+            p = k.shape[0]
+        S = np.empty((L.n_kv_heads, L.feat_dim, L.head_dim), np.float64)
+        z = np.empty((L.n_kv_heads, L.feat_dim), np.float64)
+        rc = self.lib.oracle_state(ctypes.byref(L), wp, int(p), kp, vp,
+                                   S.ctypes.data_as(_c_double_p), z.ctypes.data_as(_c_double_p))
+        if rc != 0:
+            raise ValueError("oracle_state rejected its arguments")
+        return S, z
+
+    # -- recurrent form ------------------------------------------------------
+    def empty_state(self, batch):
+        L = self.L
+        W = L.window
+        return {
+            "S": np.zeros((batch, L.n_kv_heads, L.feat_dim, L.head_dim)),
+            "z": np.zeros((batch, L.n_kv_heads, L.feat_dim)),
+            "wk": np.zeros((batch, L.n_kv_heads, W, L.head_dim)),
+            "wv": np.zeros((batch, L.n_kv_heads, W, L.head_dim)),
+            "pos": np.zeros((batch,), np.int64),
+        }
+
+    def decode(self, Wf, st, q, k, v):
+        """One decode step for a batch.  q [B][Hq][d], k/v [B][Hkv][d].
+
+        ``st`` (from empty_state, or built by the caller) is updated in place.
+        Returns out [B][Hq][d].
+        """
+        L = self.L
+        B = st["pos"].shape[0]
+        for key in ("S", "z", "wk", "wv"):
+            st[key] = np.ascontiguousarray(st[key], dtype=np.float64)
+        st["pos"] = np.ascontiguousarray(st["pos"], dtype=np.int64)
+        q, qp = _d(q)
+        k, kp = _d(k)
+        v, vp = _d(v)
+        Wf, wp = _d(Wf)
+        out = np.empty((B, L.n_q_heads, L.head_dim), np.float64)
+        P = lambda a: a.ctypes.data_as(_c_double_p)
+        rc = self.lib.oracle_decode_batch(ctypes.byref(L), wp, B, P(st["S"]), P(st["z"]),
+                                          P(st["wk"]), P(st["wv"]),
+                                          st["pos"].ctypes.data_as(_c_int64_p), qp, kp, vp, P(out))
+        if rc != 0:
+            raise ValueError("oracle_decode_batch rejected its arguments")
+        return out
+
+    def state_from_history(self, Wf, k, v, p):
+        """Recurrent-form state of one sequence after p tokens, built by direct
+        sums plus the literal window (the last min(W, p) tokens)."""
+        L = self.L
+        S, z = self.state(Wf, k, v, p)
+        W = L.window
+        nwin = min(W, p)
+        wk = np.zeros((L.n_kv_heads, W, L.head_dim))
+        wv = np.zeros((L.n_kv_heads, W, L.head_dim))
+        if nwin:
+            wk[:, :nwin] = np.transpose(np.asarray(k, np.float64)[p - nwin:p], (1, 0, 2))
+            wv[:, :nwin] = np.transpose(np.asarray(v, np.float64)[p - nwin:p], (1, 0, 2))
+        return S, z, wk, wv

@@ -1,0 +1,359 @@
+/*
+ * GLIDE hybrid-attention layer: plain CPU oracle (test infrastructure only).
+ *
+ * This file is the reference the GPU kernels are judged against.  It is
+ * deliberately slow and literal: scalar loops, double precision, no BLAS,
+ * no blocking.  Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg may load it; the product library never does, and the two
+ * share no source, header or helper.
+ *
+ * What is computed (GLIDE paper, Sec. III-B, the first displayed equation of
+ * the section and the two that expand it; Sec. II-B for linear attention;
+ * Sec. II-C for the sliding window):
+ *
+ *   For layer window W >= 0, query position t (0-indexed) and query head h
+ *   that reads KV head g = h / G (G = Hq / Hkv, contiguous groups):
+ *
+ *     beta(t)   = max(0, t + 1 - W)
+ *     linear set   L = [0, beta)        (empty when the linear part is off)
+ *     softmax set  X = [beta, t]        (min(W, t+1) tokens, current included)
+ *     phi(x)_f  = max(0, sum_c x_c Wf[c][f])        (ReLU feature map)
+ *     a_j       = phi(q_t) . phi(k_j)               for j in L
+ *     A = sum_{j in L} a_j v_j ,  a = sum_{j in L} a_j
+ *     s_j = tau * q_t . k_j                          for j in X
+ *     O_t = (sum_{j in X} e^{s_j} v_j + A) / (sum_{j in X} e^{s_j} + a)
+ *
+ *   i.e. the softmax window and the linear state share one denominator (the
+ *   "merge weighted by the normalising denominators" of Sec. II-A / III-B).
+ *   The expression is evaluated with a stabiliser c = max(m, ln a)
+ *   (m = max_j s_j; c = m when a == 0); any c gives the same exact value.
+ *   With W = 0 the softmax set is empty and O_t = A / a; 0/0 is defined as 0.
+ *
+ *   Recurrent state after p tokens (Sec. II-B recurrence, applied to the
+ *   tokens that have left the window, Appendix hybrid form 1):
+ *     S = sum_{j < p - W} phi(k_j)^T v_j   (Df x d),  z = sum_{j < p - W} phi(k_j)
+ *
+ *   A decode step at position p first folds the token leaving the window
+ *   (token p - W when p >= W; the current token when W = 0), then appends the
+ *   new token to the window, then reads out with the updated S and z.
+ *
+ * Two independent evaluations are provided: oracle_attend() evaluates the
+ * definition directly (the quadratic form, Appendix eq. for O^Linear before
+ * the rearrangement), oracle_decode_batch() runs the recurrence.  The tests
+ * check that the two agree.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef struct {
+  int32_t n_q_heads;   /* Hq */
+  int32_t n_kv_heads;  /* Hkv, Hq % Hkv == 0 */
+  int32_t head_dim;    /* d */
+  int32_t feat_dim;    /* Df */
+  int32_t window;      /* W >= 0 */
+  int32_t linear;      /* 1: linear part on (GLIDE), 0: pure sliding window */
+  double  tau;         /* softmax scale */
+} oracle_layer;
+
+/* Planted-mistake switch, used only by the mutation tests that prove the
+ * pins catch plausible errors.  0 = the correct oracle. */
+#ifndef ORACLE_MUTANT
+#define ORACLE_MUTANT 0
+#endif
+
+static int valid(const oracle_layer* L) {
+  if (!L) return 0;
+  if (L->n_q_heads <= 0 || L->n_kv_heads <= 0 || L->n_q_heads % L->n_kv_heads) return 0;
+  if (L->head_dim <= 0 || L->feat_dim <= 0 || L->window < 0) return 0;
+  if (L->window == 0 && !L->linear) return 0;   /* empty attention set */
+  return 1;
+}
+
+/* phi(x)_f = max(0, sum_c x_c Wf[c][f]);  Wf is d x Df, row-major. */
+static void phi_row(int d, int Df, const double* Wf, const double* x, double* out) {
+  for (int f = 0; f < Df; ++f) {
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) {
+#if ORACLE_MUTANT == 4
+      acc += x[c] * Wf[(size_t)f * d + c];        /* mutant: Wf transposed */
+#else
+      acc += x[c] * Wf[(size_t)c * Df + f];
+#endif
+    }
+    out[f] = acc > 0.0 ? acc : 0.0;
+  }
+}
+
+void oracle_phi(const oracle_layer* L, const double* Wf, int64_t rows, const double* x, double* out) {
+  const int d = L->head_dim, Df = L->feat_dim;
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) phi_row(d, Df, Wf, x + r * d, out + r * Df);
+}
+
+static double dot(int n, const double* a, const double* b) {
+  double s = 0.0;
+  for (int i = 0; i < n; ++i) s += a[i] * b[i];
+  return s;
+}
+
+/*
+ * Shared-denominator merge of the two parts for one query head.
+ *   sm_num[d], sm_den, m : softmax part as sum e^{s_j - m} v_j, sum e^{s_j - m}
+ *                          (has_sm == 0 when the softmax set is empty)
+ *   A[d], a              : linear part, unscaled
+ */
+static void merge(int d, int has_sm, const double* sm_num, double sm_den, double m,
+                  const double* A, double a, double* out) {
+  if (!has_sm) {
+    for (int c = 0; c < d; ++c) out[c] = a > 0.0 ? A[c] / a : 0.0;
+    return;
+  }
+#if ORACLE_MUTANT == 3
+  /* mutant: two separately normalised outputs added ("+" form) */
+  for (int c = 0; c < d; ++c) out[c] = sm_num[c] / sm_den + (a > 0.0 ? A[c] / a : 0.0);
+  return;
+#elif ORACLE_MUTANT == 6
+  /* mutant: stabiliser applied to the softmax terms only */
+  for (int c = 0; c < d; ++c) out[c] = (sm_num[c] + A[c]) / (sm_den + a);
+  (void)m;
+  return;
+#else
+  double cst = m;
+  if (a > 0.0 && log(a) > cst) cst = log(a);
+  const double ws = exp(m - cst), wl = exp(-cst);
+  const double den = sm_den * ws + a * wl;
+  for (int c = 0; c < d; ++c) out[c] = (sm_num[c] * ws + A[c] * wl) / den;
+#endif
+}
+
+/*
+ * Definition form for ONE sequence of n tokens (q [n][Hq][d], k,v [n][Hkv][d]).
+ * Computes O_t for every position listed in pos[n_out], all Hq heads:
+ * out [n_out][Hq][d].  phi(k_j) is evaluated once per key and reused.
+ * Returns 0, or -1 on invalid arguments.
+ */
+int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
+                  const double* q, const double* k, const double* v,
+                  int64_t n_out, const int64_t* pos, double* out) {
+  if (!valid(L) || n < 0 || n_out < 0) return -1;
+  for (int64_t i = 0; i < n_out; ++i)
+    if (pos[i] < 0 || pos[i] >= n) return -1;
+  const int Hq = L->n_q_heads, Hkv = L->n_kv_heads, d = L->head_dim, Df = L->feat_dim;
+  const int G = Hq / Hkv, W = L->window;
+  int64_t tmax = -1;
+  for (int64_t i = 0; i < n_out; ++i) if (pos[i] > tmax) tmax = pos[i];
+  /* phi of every key that can be in a linear set */
+  double* phik = NULL;
+  if (L->linear && tmax >= 0) {
+    phik = (double*)malloc(sizeof(double) * (size_t)(tmax + 1) * Hkv * Df);
+    if (!phik) return -1;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < (tmax + 1) * Hkv; ++r) phi_row(d, Df, Wf, k + r * d, phik + r * Df);
+  }
+  int err = 0;
+#pragma omp parallel
+  {
+    double* phq = (double*)malloc(sizeof(double) * Df);
+    double* A = (double*)malloc(sizeof(double) * d);
+    double* num = (double*)malloc(sizeof(double) * d);
+    if (!phq || !A || !num) {
+#pragma omp atomic write
+      err = 1;
+    } else {
+#pragma omp for collapse(2) schedule(dynamic, 4)
+      for (int64_t i = 0; i < n_out; ++i) {
+        for (int h = 0; h < Hq; ++h) {
+          const int64_t t = pos[i];
+          const int g = h / G;
+          const double* qt = q + ((size_t)t * Hq + h) * d;
+#if ORACLE_MUTANT == 1
+          int64_t beta = t - W;                    /* mutant: window one token too long */
+#else
+          int64_t beta = t + 1 - W;
+#endif
+          if (beta < 0) beta = 0;
+          /* linear part over [0, beta) */
+          double a = 0.0;
+          for (int c = 0; c < d; ++c) A[c] = 0.0;
+#if ORACLE_MUTANT != 2
+          if (L->linear && beta > 0) {
+            phi_row(d, Df, Wf, qt, phq);
+            for (int64_t j = 0; j < beta; ++j) {
+              const double aj = dot(Df, phq, phik + ((size_t)j * Hkv + g) * Df);
+              const double* vj = v + ((size_t)j * Hkv + g) * d;
+              for (int c = 0; c < d; ++c) A[c] += aj * vj[c];
+              a += aj;
+            }
+          }
+#endif
+          /* softmax part over [beta, t] */
+          const int has_sm = (t >= beta);
+          double m = -INFINITY, den = 0.0;
+          for (int c = 0; c < d; ++c) num[c] = 0.0;
+          if (has_sm) {
+            for (int64_t j = beta; j <= t; ++j) {
+#if ORACLE_MUTANT == 7
+              const double s = dot(d, qt, k + ((size_t)j * Hkv + g) * d);   /* mutant: no tau */
+#else
+              const double s = L->tau * dot(d, qt, k + ((size_t)j * Hkv + g) * d);
+#endif
+              if (s > m) m = s;
+            }
+            for (int64_t j = beta; j <= t; ++j) {
+              const double s = L->tau * dot(d, qt, k + ((size_t)j * Hkv + g) * d);
+#if ORACLE_MUTANT == 7
+              const double e = exp(dot(d, qt, k + ((size_t)j * Hkv + g) * d) - m);
+#else
+              const double e = exp(s - m);
+#endif
+              (void)s;
+              const double* vj = v + ((size_t)j * Hkv + g) * d;
+              for (int c = 0; c < d; ++c) num[c] += e * vj[c];
+              den += e;
+            }
+          }
+          merge(d, has_sm, num, den, m, A, a, out + ((size_t)i * Hq + h) * d);
+        }
+      }
+    }
+    free(phq); free(A); free(num);
+  }
+  free(phik);
+  return err ? -1 : 0;
+}
+
+/*
+ * Recurrent state after consuming p tokens of one sequence, by direct sums:
+ * S [Hkv][Df][d] = sum_{j < p-W} phi(k_j)^T v_j,  z [Hkv][Df] = sum phi(k_j).
+ * Both zero when p <= W or when the linear part is off.
+ */
+int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
+                 const double* k, const double* v, double* S, double* z) {
+  if (!valid(L) || p < 0) return -1;
+  const int Hkv = L->n_kv_heads, d = L->head_dim, Df = L->feat_dim, W = L->window;
+  memset(S, 0, sizeof(double) * (size_t)Hkv * Df * d);
+  memset(z, 0, sizeof(double) * (size_t)Hkv * Df);
+  const int64_t nfold = L->linear ? (p - W > 0 ? p - W : 0) : 0;
+  int err = 0;
+#pragma omp parallel for schedule(static)
+  for (int g = 0; g < Hkv; ++g) {
+    double* pk = (double*)malloc(sizeof(double) * Df);
+    if (!pk) { err = 1; continue; }
+    for (int64_t j = 0; j < nfold; ++j) {
+      phi_row(d, Df, Wf, k + ((size_t)j * Hkv + g) * d, pk);
+      const double* vj = v + ((size_t)j * Hkv + g) * d;
+      for (int f = 0; f < Df; ++f) {
+        double* Sr = S + ((size_t)g * Df + f) * d;
+        for (int c = 0; c < d; ++c) Sr[c] += pk[f] * vj[c];
+        z[(size_t)g * Df + f] += pk[f];
+      }
+    }
+    free(pk);
+  }
+  return err ? -1 : 0;
+}
+
+/*
+ * Recurrent form: one decode step for a batch of B sequences of one layer.
+ *   S   [B][Hkv][Df][d], z [B][Hkv][Df]            (in/out)
+ *   wk, wv [B][Hkv][W][d]: the window, oldest token first; sequence b holds
+ *       min(W, pos[b]) tokens                       (in/out)
+ *   pos [B]: tokens consumed so far                 (in/out, += 1)
+ *   q [B][Hq][d], k, v [B][Hkv][d]: the new token;  out [B][Hq][d]
+ * Order per (sequence, KV head): fold the token leaving the window into S, z
+ * (the oldest window token when the window is full; the new token itself
+ * when W = 0), append the new token, then read out every query head of the
+ * group from the updated state and window.
+ */
+int oracle_decode_batch(const oracle_layer* L, const double* Wf, int32_t B,
+                        double* S, double* z, double* wk, double* wv, int64_t* pos,
+                        const double* q, const double* k, const double* v, double* out) {
+  if (!valid(L) || B < 0) return -1;
+  const int Hq = L->n_q_heads, Hkv = L->n_kv_heads, d = L->head_dim, Df = L->feat_dim;
+  const int G = Hq / Hkv, W = L->window;
+  for (int b = 0; b < B; ++b) if (pos[b] < 0) return -1;
+  int err = 0;
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+  for (int b = 0; b < B; ++b) {
+    for (int g = 0; g < Hkv; ++g) {
+      const int64_t p = pos[b];
+      double* Sg = S + ((size_t)b * Hkv + g) * Df * d;
+      double* zg = z + ((size_t)b * Hkv + g) * Df;
+      double* Wk = wk + ((size_t)b * Hkv + g) * (size_t)W * d;
+      double* Wv = wv + ((size_t)b * Hkv + g) * (size_t)W * d;
+      const double* kn = k + ((size_t)b * Hkv + g) * d;
+      const double* vn = v + ((size_t)b * Hkv + g) * d;
+      double* pk = (double*)malloc(sizeof(double) * Df);
+      double* pq = (double*)malloc(sizeof(double) * Df);
+      double* A = (double*)malloc(sizeof(double) * d);
+      double* num = (double*)malloc(sizeof(double) * d);
+      if (!pk || !pq || !A || !num) {
+#pragma omp atomic write
+        err = 1;
+        free(pk); free(pq); free(A); free(num);
+        continue;
+      }
+      /* 1. fold the token that leaves the softmax window */
+      const double* fk = NULL;
+      const double* fv = NULL;
+      int64_t nwin = p < W ? p : W;            /* window tokens before this step */
+#if ORACLE_MUTANT == 5
+      if (L->linear && (W == 0 || nwin == W)) { fk = kn; fv = vn; }   /* mutant: folds the new token */
+#else
+      if (L->linear) {
+        if (W == 0) { fk = kn; fv = vn; }
+        else if (nwin == W) { fk = Wk; fv = Wv; }                      /* oldest = token p - W */
+      }
+#endif
+      if (fk) {
+        phi_row(d, Df, Wf, fk, pk);
+        for (int f = 0; f < Df; ++f) {
+          for (int c = 0; c < d; ++c) Sg[(size_t)f * d + c] += pk[f] * fv[c];
+          zg[f] += pk[f];
+        }
+      }
+      /* 2. append the new token (drop the oldest when full) */
+      if (W > 0) {
+        if (nwin == W) {
+          memmove(Wk, Wk + d, sizeof(double) * (size_t)(W - 1) * d);
+          memmove(Wv, Wv + d, sizeof(double) * (size_t)(W - 1) * d);
+          nwin = W - 1;
+        }
+        memcpy(Wk + (size_t)nwin * d, kn, sizeof(double) * d);
+        memcpy(Wv + (size_t)nwin * d, vn, sizeof(double) * d);
+        nwin += 1;
+      }
+      /* 3. read out every query head of the group */
+      for (int hh = 0; hh < G; ++hh) {
+        const int h = g * G + hh;
+        const double* qt = q + ((size_t)b * Hq + h) * d;
+        double a = 0.0;
+        for (int c = 0; c < d; ++c) A[c] = 0.0;
+        if (L->linear) {
+          phi_row(d, Df, Wf, qt, pq);
+          for (int f = 0; f < Df; ++f) {
+            for (int c = 0; c < d; ++c) A[c] += pq[f] * Sg[(size_t)f * d + c];
+            a += pq[f] * zg[f];
+          }
+        }
+        double m = -INFINITY, den = 0.0;
+        for (int c = 0; c < d; ++c) num[c] = 0.0;
+        for (int64_t j = 0; j < nwin; ++j) {
+          const double s = L->tau * dot(d, qt, Wk + (size_t)j * d);
+          if (s > m) m = s;
+        }
+        for (int64_t j = 0; j < nwin; ++j) {
+          const double e = exp(L->tau * dot(d, qt, Wk + (size_t)j * d) - m);
+          for (int c = 0; c < d; ++c) num[c] += e * Wv[(size_t)j * d + c];
+          den += e;
+        }
+        merge(d, nwin > 0, num, den, m, A, a, out + ((size_t)b * Hq + h) * d);
+      }
+      free(pk); free(pq); free(A); free(num);
+    }
+  }
+  for (int b = 0; b < B; ++b) pos[b] += 1;
+  return err ? -1 : 0;
+}

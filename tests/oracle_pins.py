@@ -1,0 +1,313 @@
+"""Pins that tie the CPU oracle to facts fixed outside the oracle itself.
+
+Each check returns None on success or a short failure message.  They are run
+by ``test_oracle_pins.py`` against the real oracle, and by the mutation test
+against oracle builds with one planted mistake each, to show that a plausible
+slip anywhere in the oracle fails at least one pin.
+
+What pins what:
+  * worked example (tests/golden): hand-derived closed forms of the layer
+    definition (GLIDE Sec. III-B) on a 3-token, d = 1 sequence;
+  * full window, linear off == causal softmax attention computed by torch's
+    scaled_dot_product_attention (the first boundary condition of Sec. III-B,
+    "w -> infinity gives causal softmax");
+  * window W, linear off == SDPA with an explicit band mask (Sec. II-C);
+  * W = 0 == causal linear attention as a masked matrix product (the second
+    boundary condition, "w = 0 gives pure linear attention"; Appendix, linear
+    attention before the rearrangement);
+  * W = 1 == closed form built from the W = 0 numerator and denominator at
+    t - 1 plus the diagonal score;
+  * recurrent decode from empty == definition form at every position, and the
+    decoded state == direct sums (Appendix rearrangement to S and Z);
+  * invariants: V == 1 gives O == 1 (shared denominator), outputs in the convex
+    hull of the seen values, linearity in V, GQA == MHA with repeated K/V,
+    0/0 -> 0.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import torch
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "worked_example.json")
+
+
+def _eval_closed_form(expr):
+    return float(eval(expr, {"__builtins__": {}}, {"e": math.e, "exp": math.exp}))
+
+
+def _rand_case(seed, n, Hq, Hkv, d, Df, scale=1.0):
+    g = np.random.default_rng(seed)
+    q = g.standard_normal((n, Hq, d)) * scale
+    k = g.standard_normal((n, Hkv, d)) * scale
+    v = g.standard_normal((n, Hkv, d))
+    Wf = g.standard_normal((d, Df)) / np.sqrt(d)
+    return q, k, v, Wf
+
+
+def _sdpa(q, k, v, tau, mask):
+    """torch SDPA in float64 on CPU; q [n][Hq][d], k/v [n][Hkv][d] (GQA by repeat)."""
+    G = q.shape[1] // k.shape[1]
+    qt = torch.from_numpy(q).permute(1, 0, 2).contiguous()
+    kt = torch.from_numpy(np.repeat(k, G, axis=1)).permute(1, 0, 2).contiguous()
+    vt = torch.from_numpy(np.repeat(v, G, axis=1)).permute(1, 0, 2).contiguous()
+    m = torch.from_numpy(mask)
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=m, scale=tau)
+    return o.permute(1, 0, 2).numpy()
+
+
+def _causal_linear(q, k, v, Wf):
+    """Causal linear attention, masked-matrix form, with numpy matmuls."""
+    G = q.shape[1] // k.shape[1]
+    n = q.shape[0]
+    pq = np.maximum(q @ Wf, 0.0)                       # [n][Hq][Df]
+    pk = np.maximum(np.repeat(k, G, axis=1) @ Wf, 0.0)
+    vv = np.repeat(v, G, axis=1)
+    num = np.zeros(q.shape)
+    den = np.zeros(q.shape[:2])
+    tril = np.tril(np.ones((n, n)))
+    for h in range(q.shape[1]):
+        M = (pq[:, h] @ pk[:, h].T) * tril
+        num[:, h] = M @ vv[:, h]
+        den[:, h] = M.sum(-1)
+    return num, den
+
+
+def pin_worked_example(lib):
+    ex = json.load(open(GOLDEN))
+    s = ex["setup"]
+    q = np.array(s["q"]).reshape(3, 1, 1)
+    k = np.array(s["k"]).reshape(3, 1, 1)
+    v = np.array(s["v"]).reshape(3, 1, 1)
+    Wf = np.array(s["Wf"])
+    for case in ex["cases"]:
+        o = oracle.Oracle(1, 1, 1, 1, case["window"], linear=case["linear"], tau=s["tau"], lib=lib)
+        got = o.attend(Wf, q, k, v).ravel()
+        want = np.array([_eval_closed_form(x) for x in case["out"]])
+        if not np.allclose(got, want, rtol=1e-12, atol=1e-12):
+            return f"worked example W={case['window']}: {got} != {want}"
+        S, z = o.state(Wf, k, v)
+        if not (abs(S.item() - _eval_closed_form(case["S"])) < 1e-12
+                and abs(z.item() - _eval_closed_form(case["z"])) < 1e-12):
+            return f"worked example state W={case['window']}: S={S.item()} z={z.item()}"
+        # recurrent form on the same example
+        st = o.empty_state(1)
+        outs = [o.decode(Wf, st, q[t:t + 1], k[t:t + 1], v[t:t + 1]).item() for t in range(3)]
+        if not np.allclose(outs, want, rtol=1e-12, atol=1e-12):
+            return f"worked example recurrent W={case['window']}: {outs} != {want}"
+        if not (abs(st["S"].item() - _eval_closed_form(case["S"])) < 1e-12):
+            return f"worked example recurrent state W={case['window']}"
+    return None
+
+
+def pin_full_window_is_causal_softmax(lib):
+    n, Hq, Hkv, d, Df = 23, 4, 2, 8, 6
+    q, k, v, Wf = _rand_case(1, n, Hq, Hkv, d, Df)
+    tau = 0.7
+    mask = np.tril(np.ones((n, n), bool))
+    want = _sdpa(q, k, v, tau, mask)
+    for W, lin in ((n, False), (n + 5, False), (n, True), (10 ** 6, True)):
+        got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=lin, tau=tau, lib=lib).attend(Wf, q, k, v)
+        if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
+            return f"full window W={W} linear={lin} != causal SDPA (max err {np.abs(got - want).max()})"
+    return None
+
+
+def pin_band_is_masked_sdpa(lib):
+    n, Hq, Hkv, d, Df = 29, 4, 4, 8, 8
+    q, k, v, Wf = _rand_case(2, n, Hq, Hkv, d, Df)
+    tau = 0.5
+    t = np.arange(n)[:, None]
+    j = np.arange(n)[None, :]
+    for W in (1, 2, 5, 17):
+        mask = (j <= t) & (j >= t - W + 1)
+        want = _sdpa(q, k, v, tau, mask)
+        got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=False, tau=tau, lib=lib).attend(Wf, q, k, v)
+        if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
+            return f"band W={W} != masked SDPA (max err {np.abs(got - want).max()})"
+    return None
+
+
+def pin_w0_is_causal_linear(lib):
+    n, Hq, Hkv, d, Df = 19, 4, 2, 6, 9
+    q, k, v, Wf = _rand_case(3, n, Hq, Hkv, d, Df)
+    num, den = _causal_linear(q, k, v, Wf)
+    safe = np.where(den > 0, den, 1.0)
+    want = np.where((den > 0)[..., None], num / safe[..., None], 0.0)   # 0/0 -> 0
+    if not (den > 0).sum() > 0.9 * den.size:
+        return "W=0 pin degenerate: too many empty linear sets"
+    got = oracle.Oracle(Hq, Hkv, d, Df, 0, linear=True, lib=lib).attend(Wf, q, k, v)
+    if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
+        return f"W=0 != causal linear attention (max err {np.abs(got - want).max()})"
+    return None
+
+
+def pin_w1_closed_form(lib):
+    n, Hq, Hkv, d, Df = 17, 2, 2, 5, 7
+    q, k, v, Wf = _rand_case(4, n, Hq, Hkv, d, Df)
+    tau = 0.9
+    num, den = _causal_linear(q[:], k, v, Wf)
+    # W = 1: linear set [0, t) -> the W=0 sums with the diagonal term removed
+    pq = np.maximum(q @ Wf, 0.0)
+    pk = np.maximum(k @ Wf, 0.0)
+    want = np.zeros(q.shape)
+    for t in range(n):
+        for h in range(Hq):
+            diag = pq[t, h] @ pk[t, h]
+            A = num[t, h] - diag * v[t, h]
+            a = den[t, h] - diag
+            e = math.exp(tau * (q[t, h] @ k[t, h]))
+            want[t, h] = (e * v[t, h] + A) / (e + a)
+    got = oracle.Oracle(Hq, Hkv, d, Df, 1, linear=True, tau=tau, lib=lib).attend(Wf, q, k, v)
+    if not np.allclose(got, want, rtol=1e-9, atol=1e-12):
+        return f"W=1 closed form mismatch (max err {np.abs(got - want).max()})"
+    return None
+
+
+def pin_recurrent_equals_definition(lib):
+    n, Hq, Hkv, d, Df = 21, 4, 2, 6, 5
+    q, k, v, Wf = _rand_case(5, n, Hq, Hkv, d, Df, scale=1.5)
+    for W in (0, 1, 2, 3, 7, n - 1, n, n + 4):
+        for lin in (True, False):
+            if W == 0 and not lin:
+                continue
+            o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=lin, tau=0.6, lib=lib)
+            want = o.attend(Wf, q, k, v)
+            st = o.empty_state(1)
+            got = np.stack([o.decode(Wf, st, q[t:t + 1], k[t:t + 1], v[t:t + 1])[0] for t in range(n)])
+            if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
+                return f"recurrent != definition at W={W} linear={lin} (max err {np.abs(got - want).max()})"
+            S, z = o.state(Wf, k, v)
+            if not (np.allclose(st["S"][0], S, rtol=1e-12, atol=1e-12) and np.allclose(st["z"][0], z)):
+                return f"recurrent state != direct sums at W={W} linear={lin}"
+    return None
+
+
+def pin_state_direct_sums(lib):
+    n, Hkv, d, Df = 15, 3, 4, 6
+    _, k, v, Wf = _rand_case(6, n, Hkv, Hkv, d, Df)
+    for W in (0, 1, 4, n, n + 2):
+        o = oracle.Oracle(Hkv, Hkv, d, Df, W, linear=True, lib=lib)
+        for p in (0, 1, 7, n):
+            S, z = o.state(Wf, k, v, p)
+            m = max(p - W, 0)
+            pk = np.maximum(k[:m] @ Wf, 0.0)              # [m][Hkv][Df]
+            Sw = np.einsum("jgf,jgc->gfc", pk, v[:m])
+            zw = pk.sum(0)
+            if not (np.allclose(S, Sw, atol=1e-12) and np.allclose(z, zw, atol=1e-12)):
+                return f"state != einsum direct sums at W={W} p={p}"
+    return None
+
+
+def pin_v_ones(lib):
+    n, Hq, Hkv, d, Df = 16, 4, 2, 6, 6
+    q, k, _, Wf = _rand_case(7, n, Hq, Hkv, d, Df, scale=2.0)
+    v = np.ones((n, Hkv, d))
+    for W in (0, 1, 3, 9, n):
+        got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib).attend(Wf, q, k, v)
+        if W == 0:   # 0/0 -> 0 where phi(q_t) . sum_{j<=t} phi(k_j) == 0
+            G = Hq // Hkv
+            pq = np.maximum(q @ Wf, 0.0)
+            pk = np.maximum(np.repeat(k, G, 1) @ Wf, 0.0)
+            a = np.einsum("thf,thf->th", pq, np.cumsum(pk, 0))
+            got = np.where((a > 0)[..., None], got, 1.0)
+        if not np.allclose(got, 1.0, rtol=1e-12, atol=1e-12):
+            return f"V==1 does not give O==1 at W={W} (got range {got.min()}..{got.max()})"
+    return None
+
+
+def pin_convex_hull(lib):
+    n, Hq, Hkv, d, Df = 18, 2, 1, 5, 4
+    q, k, v, Wf = _rand_case(8, n, Hq, Hkv, d, Df, scale=1.3)
+    for W in (0, 1, 4, n):
+        got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib).attend(Wf, q, k, v)
+        for t in range(n):
+            lo = v[: t + 1, 0].min(0) - 1e-12
+            hi = v[: t + 1, 0].max(0) + 1e-12
+            for h in range(Hq):
+                o = got[t, h]
+                if W == 0 and np.all(o == 0.0):
+                    continue   # 0/0 rule (empty weight mass, W == 0 only)
+                if np.any(o < lo) or np.any(o > hi):
+                    return f"output outside the convex hull at W={W} t={t} h={h}"
+    return None
+
+
+def pin_linearity(lib):
+    n, Hq, Hkv, d, Df = 12, 2, 2, 4, 4
+    q, k, v, Wf = _rand_case(9, n, Hq, Hkv, d, Df)
+    for W in (0, 2, 5):
+        o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib)
+        a = o.attend(Wf, q, k, v)
+        b = o.attend(Wf, q, k, -2.5 * v)
+        if not np.allclose(b, -2.5 * a, rtol=1e-12, atol=1e-12):
+            return f"O(cV) != c O(V) at W={W}"
+        S1, z1 = o.state(Wf, k, v)
+        S2, z2 = o.state(Wf, k, -2.5 * v)
+        if not (np.allclose(S2, -2.5 * S1) and np.allclose(z1, z2)):
+            return f"S(cV) != c S(V) or z changed at W={W}"
+    return None
+
+
+def pin_gqa_is_repeated_mha(lib):
+    n, Hq, Hkv, d, Df = 14, 6, 2, 5, 5
+    q, k, v, Wf = _rand_case(10, n, Hq, Hkv, d, Df)
+    G = Hq // Hkv
+    for W in (0, 3, n):
+        a = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib).attend(Wf, q, k, v)
+        b = oracle.Oracle(Hq, Hq, d, Df, W, linear=True, lib=lib).attend(
+            Wf, q, np.repeat(k, G, 1), np.repeat(v, G, 1))
+        if not np.allclose(a, b, rtol=1e-12, atol=1e-12):
+            return f"GQA != MHA with repeated K/V at W={W}"
+    return None
+
+
+def pin_zero_over_zero(lib):
+    d = Df = 2
+    Wf = np.eye(2)
+    q = np.array([[[-1.0, -1.0]], [[1.0, 0.0]]])     # phi(q_0) = 0
+    k = np.array([[[1.0, 1.0]], [[0.0, 1.0]]])
+    v = np.array([[[3.0, 4.0]], [[5.0, 6.0]]])
+    got = oracle.Oracle(1, 1, d, Df, 0, linear=True, lib=lib).attend(Wf, q, k, v)
+    # t = 0: phi(q).phi(k_0) = 0 -> 0/0 -> 0.  t = 1: phi(q_1)=(1,0): a_0 = 1, a_1 = 0 -> v_0
+    want = np.array([[[0.0, 0.0]], [[3.0, 4.0]]])
+    if not np.allclose(got, want, atol=1e-15):
+        return f"0/0 rule: {got.ravel()} != {want.ravel()}"
+    return None
+
+
+def pin_continue_from_state(lib):
+    """Decode continuing from a state built by direct sums == definition."""
+    n, Hq, Hkv, d, Df = 20, 4, 2, 5, 6
+    q, k, v, Wf = _rand_case(11, n, Hq, Hkv, d, Df)
+    for W in (0, 3, 8):
+        o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib)
+        want = o.attend(Wf, q, k, v)
+        p0 = 11
+        S, z, wk, wv = o.state_from_history(Wf, k, v, p0)
+        st = {"S": S[None], "z": z[None], "wk": wk[None], "wv": wv[None], "pos": np.array([p0])}
+        got = np.stack([o.decode(Wf, st, q[t:t + 1], k[t:t + 1], v[t:t + 1])[0] for t in range(p0, n)])
+        if not np.allclose(got, want[p0:], rtol=1e-10, atol=1e-12):
+            return f"decode continued from a direct-sum state != definition at W={W}"
+    return None
+
+
+ALL_PINS = [pin_worked_example, pin_full_window_is_causal_softmax, pin_band_is_masked_sdpa,
+            pin_w0_is_causal_linear, pin_w1_closed_form, pin_recurrent_equals_definition,
+            pin_state_direct_sums, pin_v_ones, pin_convex_hull, pin_linearity,
+            pin_gqa_is_repeated_mha, pin_zero_over_zero, pin_continue_from_state]
+
+
+def run_all(lib):
+    fails = []
+    for p in ALL_PINS:
+        try:
+            msg = p(lib)
+        except Exception as e:  # a crash is a failure too
+            msg = f"{p.__name__} raised {type(e).__name__}: {e}"
+        if msg:
+            fails.append(f"{p.__name__}: {msg}")
+    return fails
