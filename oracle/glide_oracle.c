@@ -120,8 +120,12 @@ static void merge(int d, int has_sm, const double* sm_num, double sm_den, double
   (void)m;
   return;
 #else
+  if (!(a > 0.0)) {   /* empty linear mass: A = 0 and a = 0 add nothing */
+    for (int c = 0; c < d; ++c) out[c] = sm_num[c] / sm_den;
+    return;
+  }
   double cst = m;
-  if (a > 0.0 && log(a) > cst) cst = log(a);
+  if (log(a) > cst) cst = log(a);
   const double ws = exp(m - cst), wl = exp(-cst);
   const double den = sm_den * ws + a * wl;
   for (int c = 0; c < d; ++c) out[c] = (sm_num[c] * ws + A[c] * wl) / den;
