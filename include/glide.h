@@ -1,0 +1,166 @@
+/*
+ * glide.h -- C ABI of the GLIDE hybrid-attention step on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * One layer of GLIDE attention (GLIDE, Sec. III-B: the first displayed
+ * equation of the section and the two that expand it, with the split point
+ * read as the effective softmax window W = w - delta; the merge weighted by
+ * the two normalising denominators described in Sec. II-A and III-B):
+ *
+ *   for query head h (KV head g = h / G, G = Hq / Hkv) at 0-indexed position t
+ *     beta      = max(0, t + 1 - W)
+ *     phi(x)    = max(0, x . Wf)                (Wf: d x Df, one per layer)
+ *     A, a      = sum_{j < beta} (phi(q_t).phi(k_j)) v_j ,  sum_{j < beta} phi(q_t).phi(k_j)
+ *               = phi(q_t) . S ,  phi(q_t) . z  with  S = sum phi(k_j)^T v_j,
+ *                 z = sum phi(k_j)              (Sec. II-B recurrence)
+ *     O_t       = (sum_{j=beta..t} e^{tau q_t.k_j} v_j + A) / (sum_{j=beta..t} e^{tau q_t.k_j} + a)
+ *
+ * W = 0 gives pure linear attention (the current token is folded before the
+ * read-out); W >= context gives causal softmax attention (the two boundary
+ * conditions stated in Sec. III-B).  0/0 (W = 0 and phi(q).z = 0) yields 0.
+ *
+ * Threading, memory and errors
+ *   - Every device buffer is allocated and owned by the caller.  The library
+ *     never allocates, frees or synchronises; all work is enqueued on the
+ *     caller's stream (a hipStream_t passed as void*, NULL = default stream).
+ *   - Host arrays (glide_config.windows, cu_seqlens_host) are read during the
+ *     call only and never retained.  The library has no mutable global state.
+ *   - Every argument is validated on the host before the first HIP call; on
+ *     any error nothing is enqueued and the state is untouched.
+ *   - A failed kernel launch returns GLIDE_ERR_HIP and leaves the state
+ *     undefined (re-initialise it).  Asynchronous device faults surface at the
+ *     caller's next synchronisation.  No C++ exception crosses this ABI.
+ *   - Calls that mutate one state blob must not overlap; calls on different
+ *     state blobs may run concurrently on different streams.
+ */
+#ifndef GLIDE_H_
+#define GLIDE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GLIDE_OK = 0,
+  GLIDE_ERR_NULL = -1,        /* a required pointer is NULL */
+  GLIDE_ERR_INVALID = -2,     /* inconsistent or out-of-range argument */
+  GLIDE_ERR_UNSUPPORTED = -3, /* valid per the definition, not built here (d, Df, G, dtype) */
+  GLIDE_ERR_ALIGN = -4,       /* a device pointer is not 16-byte aligned (state: 256) */
+  GLIDE_ERR_SIZE = -5,        /* state or workspace smaller than required */
+  GLIDE_ERR_HIP = -6          /* a HIP launch failed */
+} glide_status;
+
+/* Element type of q, k, v, out, the window ring and phi_w.  S and z are fp32. */
+enum { GLIDE_F32 = 0, GLIDE_BF16 = 1 };
+
+/* Feature map: phi(x) = max(0, x . Wf) (the ReLU kernel of the Appendix's
+ * feature-map list; Wf is non-learnable, one d x Df matrix per layer shared by
+ * every head, applied to queries and keys alike). */
+enum { GLIDE_PHI_RELU = 0 };
+
+/* flags: GLIDE_NO_LINEAR turns the linear part off (plain sliding-window
+ * softmax attention, the "Hybrid" preset with nothing kept beyond the
+ * window); W = 0 is then rejected because the attention set is empty. */
+enum { GLIDE_NO_LINEAR = 1 };
+
+typedef struct {
+  int32_t n_layers;    /* layers held by one state blob (>= 1) */
+  int32_t batch;       /* sequences B (>= 1) */
+  int32_t n_q_heads;   /* Hq */
+  int32_t n_kv_heads;  /* Hkv; Hq % Hkv == 0, G = Hq / Hkv in [1, 16] */
+  int32_t head_dim;    /* d: 64 or 128 */
+  int32_t feat_dim;    /* Df: 64 or 128 */
+  int32_t dtype;       /* GLIDE_F32 or GLIDE_BF16 */
+  int32_t phi;         /* GLIDE_PHI_RELU */
+  int32_t flags;       /* 0 or GLIDE_NO_LINEAR */
+  float sm_scale;      /* tau, the softmax scale (1/sqrt(d) in the Appendix's attention) */
+  const int32_t* windows; /* HOST array [n_layers]: W_l = w - delta_l, 0 <= W_l <= 2^20 */
+} glide_config;
+
+/* Position of the sections of one layer inside the state blob (bytes from the
+ * blob's start).  Layout per layer l, every section 256-byte aligned:
+ *   pos   int64 [B][Hkv]          tokens consumed by sequence b (equal over Hkv)
+ *   S     fp32  [B][Hkv][Df][d]   sum of phi(k_j)^T v_j over tokens left of the window
+ *   z     fp32  [B][Hkv][Df]      sum of phi(k_j) over the same tokens
+ *   kring dtype [B][Hkv][R][d]    key of token j in slot j mod R
+ *   vring dtype [B][Hkv][R/8][d][8]  value of token j: element
+ *                                  [(j mod R)/8][c][(j mod R) % 8]
+ * R = ring_slots = round_up(W + 1, 8) for W > 0, 0 for W = 0.  After p tokens
+ * the ring holds tokens [max(0, p - W), p - 1]; other slots are stale. */
+typedef struct {
+  int64_t pos_offset, s_offset, z_offset, kring_offset, vring_offset;
+  int64_t layer_offset, layer_bytes;
+  int32_t window;      /* W_l */
+  int32_t ring_slots;  /* R_l */
+} glide_layer_layout;
+
+/* Bytes of the state blob for cfg (sum of all layers), 0 if cfg is invalid. */
+size_t glide_state_bytes(const glide_config* cfg);
+
+/* Fills *out with the layout of layer `layer` (0 <= layer < cfg->n_layers). */
+glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_layer_layout* out);
+
+/* Workspace bytes needed by glide_prefill for calls with at most
+ * max_total_tokens packed tokens (any chunk size), and by glide_decode_step
+ * (which needs none).  0 if cfg is invalid. */
+size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens);
+
+/* Zeroes the whole state: S = 0, z = 0 (S_0, Z_0 of the Sec. II-B
+ * recurrence), pos = 0, ring contents 0.  state: device, 256-byte aligned,
+ * state_bytes >= glide_state_bytes(cfg). */
+glide_status glide_state_init(const glide_config* cfg, void* state, size_t state_bytes, void* stream);
+
+/* Prefill (KV-cache population stage, Appendix "KV Cache"): appends
+ * T_b = cu_seqlens[b+1] - cu_seqlens[b] >= 0 tokens to every sequence b,
+ * starting at that sequence's current position (a continuing prefill is
+ * legal), for layers [layer0, layer0 + n_layers), and writes one output per
+ * appended token.  Within a layer the work is chunked: chunk C query tokens
+ * share one softmax band pass and one state read-out (chunk = 0 -> 64; any
+ * C in [16, 256] that is a multiple of 16 gives the same result up to
+ * rounding).
+ *   phi_w  device [n_layers][d][Df]        (layer layer0 first)
+ *   q      device [n_layers][T][Hq][d]     T = total_tokens, packed by sequence
+ *   k, v   device [n_layers][T][Hkv][d]
+ *   cu_seqlens_host  HOST [B+1], cu[0] = 0, non-decreasing, cu[B] = T
+ *   out    device [n_layers][T][Hq][d]
+ *   workspace device, >= glide_workspace_bytes(cfg, T)
+ * Element types follow cfg->dtype; device pointers 16-byte aligned. */
+glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_bytes,
+                           int32_t layer0, int32_t n_layers, const void* phi_w,
+                           const void* q, const void* k, const void* v,
+                           const int32_t* cu_seqlens_host, int64_t total_tokens, int32_t chunk,
+                           void* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Decode (Appendix "KV Cache", decode stage): appends exactly one token to
+ * every sequence for layers [layer0, layer0 + n_layers).  Per (layer,
+ * sequence, KV head), in this order: fold the token leaving the window into
+ * S and z (token p - W when p >= W; the new token itself when W = 0), write
+ * the new key/value into its ring slot, read out O for the G query heads of
+ * the group from the window and the updated state, pos += 1.  Sequences may
+ * sit at different positions (pos lives in the state).
+ *   phi_w  device [n_layers][d][Df]
+ *   q      device [n_layers][B][Hq][d];  k, v device [n_layers][B][Hkv][d]
+ *   out    device [n_layers][B][Hq][d]
+ * workspace may be NULL (decode needs none). */
+glide_status glide_decode_step(const glide_config* cfg, void* state, size_t state_bytes,
+                               int32_t layer0, int32_t n_layers, const void* phi_w,
+                               const void* q, const void* k, const void* v, void* out,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* The feature map alone (kernel (d)): out[r][f] = max(0, sum_c x[r][c] Wf[c][f])
+ * for r < rows, accumulated in fp32.  x device [rows][d], phi_w device [d][Df]
+ * (both cfg->dtype), out device [rows][Df] in cfg->dtype. */
+glide_status glide_feature_map(const glide_config* cfg, const void* phi_w, const void* x,
+                               int64_t rows, void* out, void* stream);
+
+/* Static description of a status code. */
+const char* glide_status_string(glide_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GLIDE_H_ */

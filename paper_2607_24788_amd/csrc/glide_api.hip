@@ -1,0 +1,207 @@
+// C ABI of the GLIDE hybrid-attention library: argument validation (always
+// on the host, before the first HIP call), state layout, and kernel dispatch.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "glide_internal.h"
+
+using namespace glide;
+
+namespace {
+
+constexpr int32_t kMaxWindow = 1 << 20;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+glide_status check_cfg(const glide_config* c) {
+  if (!c || !c->windows) return GLIDE_ERR_NULL;
+  if (c->n_layers < 1 || c->n_layers > (1 << 16)) return GLIDE_ERR_INVALID;
+  if (c->batch < 1 || c->batch > (1 << 20)) return GLIDE_ERR_INVALID;
+  if (c->n_q_heads < 1 || c->n_kv_heads < 1 || c->n_q_heads > 4096) return GLIDE_ERR_INVALID;
+  if (c->n_q_heads % c->n_kv_heads) return GLIDE_ERR_INVALID;
+  if (c->head_dim < 1 || c->feat_dim < 1) return GLIDE_ERR_INVALID;
+  if (c->dtype != GLIDE_F32 && c->dtype != GLIDE_BF16) return GLIDE_ERR_INVALID;
+  if (c->phi != GLIDE_PHI_RELU) return GLIDE_ERR_INVALID;
+  if (c->flags & ~int32_t(GLIDE_NO_LINEAR)) return GLIDE_ERR_INVALID;
+  if (!isfinite(c->sm_scale)) return GLIDE_ERR_INVALID;
+  for (int32_t l = 0; l < c->n_layers; ++l) {
+    const int32_t W = c->windows[l];
+    if (W < 0 || W > kMaxWindow) return GLIDE_ERR_INVALID;
+    if (W == 0 && (c->flags & GLIDE_NO_LINEAR)) return GLIDE_ERR_INVALID;
+  }
+  if (c->n_q_heads / c->n_kv_heads > kMaxG) return GLIDE_ERR_UNSUPPORTED;
+  if (c->head_dim != 64 && c->head_dim != 128) return GLIDE_ERR_UNSUPPORTED;
+  if (c->feat_dim != 64 && c->feat_dim != 128) return GLIDE_ERR_UNSUPPORTED;
+  return GLIDE_OK;
+}
+
+int esize(const glide_config* c) { return c->dtype == GLIDE_BF16 ? 2 : 4; }
+
+LayerSections sections(const glide_config* c, int32_t l) {
+  return layer_sections(c->batch, c->n_kv_heads, c->head_dim, c->feat_dim, ring_slots(c->windows[l]),
+                        esize(c));
+}
+
+int64_t layer_base(const glide_config* c, int32_t l) {
+  int64_t off = 0;
+  for (int32_t i = 0; i < l; ++i) off += sections(c, i).bytes;
+  return off;
+}
+
+int64_t state_bytes_i(const glide_config* c) { return layer_base(c, c->n_layers); }
+
+glide_status check_call(const glide_config* c, void* state, size_t state_bytes, int32_t layer0,
+                        int32_t n_layers) {
+  glide_status s = check_cfg(c);
+  if (s != GLIDE_OK) return s;
+  if (!state) return GLIDE_ERR_NULL;
+  if (!aligned(state, 256)) return GLIDE_ERR_ALIGN;
+  if (state_bytes < size_t(state_bytes_i(c))) return GLIDE_ERR_SIZE;
+  if (layer0 < 0 || n_layers < 1 || int64_t(layer0) + n_layers > c->n_layers) return GLIDE_ERR_INVALID;
+  return GLIDE_OK;
+}
+
+glide_status hip_status(hipError_t e) { return e == hipSuccess ? GLIDE_OK : GLIDE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* glide_status_string(glide_status s) {
+  switch (s) {
+    case GLIDE_OK: return "ok";
+    case GLIDE_ERR_NULL: return "required pointer is NULL";
+    case GLIDE_ERR_INVALID: return "invalid argument";
+    case GLIDE_ERR_UNSUPPORTED: return "unsupported configuration (head_dim/feat_dim in {64,128}, Hq/Hkv <= 16)";
+    case GLIDE_ERR_ALIGN: return "misaligned device pointer (16 bytes; state 256 bytes)";
+    case GLIDE_ERR_SIZE: return "state or workspace too small";
+    case GLIDE_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+size_t glide_state_bytes(const glide_config* cfg) {
+  if (check_cfg(cfg) != GLIDE_OK) return 0;
+  return size_t(state_bytes_i(cfg));
+}
+
+glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_layer_layout* out) {
+  glide_status s = check_cfg(cfg);
+  if (s != GLIDE_OK) return s;
+  if (!out) return GLIDE_ERR_NULL;
+  if (layer < 0 || layer >= cfg->n_layers) return GLIDE_ERR_INVALID;
+  const int64_t base = layer_base(cfg, layer);
+  const LayerSections sec = sections(cfg, layer);
+  out->layer_offset = base;
+  out->layer_bytes = sec.bytes;
+  out->pos_offset = base + sec.pos;
+  out->s_offset = base + sec.S;
+  out->z_offset = base + sec.z;
+  out->kring_offset = base + sec.K;
+  out->vring_offset = base + sec.V;
+  out->window = cfg->windows[layer];
+  out->ring_slots = ring_slots(cfg->windows[layer]);
+  return GLIDE_OK;
+}
+
+size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens) {
+  if (check_cfg(cfg) != GLIDE_OK || max_total_tokens < 0) return 0;
+  (void)max_total_tokens;
+  return 256;
+}
+
+glide_status glide_state_init(const glide_config* cfg, void* state, size_t state_bytes, void* stream) {
+  glide_status s = check_call(cfg, state, state_bytes, 0, cfg ? cfg->n_layers : 0);
+  if (s != GLIDE_OK) return s;
+  return hip_status(hipMemsetAsync(state, 0, size_t(state_bytes_i(cfg)), hipStream_t(stream)));
+}
+
+glide_status glide_decode_step(const glide_config* cfg, void* state, size_t state_bytes, int32_t layer0,
+                               int32_t n_layers, const void* phi_w, const void* q, const void* k,
+                               const void* v, void* out, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  glide_status s = check_call(cfg, state, state_bytes, layer0, n_layers);
+  if (s != GLIDE_OK) return s;
+  if (!phi_w || !q || !k || !v || !out) return GLIDE_ERR_NULL;
+  if (!aligned(phi_w, 16) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
+    return GLIDE_ERR_ALIGN;
+
+  // Longest windows first: the hardware dispatcher then hands out the
+  // longest streams before the short ones (list scheduling).
+  std::vector<int32_t> order(n_layers);
+  for (int32_t i = 0; i < n_layers; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
+    return cfg->windows[layer0 + x] > cfg->windows[layer0 + y];
+  });
+
+  DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.state = static_cast<char*>(state);
+  a.phi_w = phi_w;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.B = cfg->batch;
+  a.Hq = cfg->n_q_heads;
+  a.Hkv = cfg->n_kv_heads;
+  a.G = cfg->n_q_heads / cfg->n_kv_heads;
+  a.linear = (cfg->flags & GLIDE_NO_LINEAR) ? 0 : 1;
+  a.tau = cfg->sm_scale;
+  for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
+    const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
+    a.n_layers = cnt;
+    for (int32_t i = 0; i < cnt; ++i) {
+      const int32_t slot = order[first + i];
+      const int32_t l = layer0 + slot;
+      a.layers[i].base = layer_base(cfg, l);
+      a.layers[i].W = cfg->windows[l];
+      a.layers[i].R = ring_slots(cfg->windows[l]);
+      a.layers[i].slot = slot;
+    }
+    s = hip_status(launch_decode(a, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream)));
+    if (s != GLIDE_OK) return s;
+  }
+  return GLIDE_OK;
+}
+
+glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_bytes, int32_t layer0,
+                           int32_t n_layers, const void* phi_w, const void* q, const void* k, const void* v,
+                           const int32_t* cu_seqlens_host, int64_t total_tokens, int32_t chunk, void* out,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  glide_status s = check_call(cfg, state, state_bytes, layer0, n_layers);
+  if (s != GLIDE_OK) return s;
+  if (!phi_w || !q || !k || !v || !out || !cu_seqlens_host) return GLIDE_ERR_NULL;
+  if (!aligned(phi_w, 16) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
+    return GLIDE_ERR_ALIGN;
+  if (total_tokens < 0) return GLIDE_ERR_INVALID;
+  if (cu_seqlens_host[0] != 0 || cu_seqlens_host[cfg->batch] != total_tokens) return GLIDE_ERR_INVALID;
+  for (int32_t b = 0; b < cfg->batch; ++b)
+    if (cu_seqlens_host[b + 1] < cu_seqlens_host[b]) return GLIDE_ERR_INVALID;
+  if (chunk == 0) chunk = 64;
+  if (chunk < 16 || chunk > 256 || chunk % 16) return GLIDE_ERR_INVALID;
+  const size_t need = glide_workspace_bytes(cfg, total_tokens);
+  if (workspace_bytes < need) return GLIDE_ERR_SIZE;
+  if (need && !workspace) return GLIDE_ERR_NULL;
+  if (workspace && !aligned(workspace, 256)) return GLIDE_ERR_ALIGN;
+  (void)stream;
+  return GLIDE_ERR_UNSUPPORTED;
+}
+
+glide_status glide_feature_map(const glide_config* cfg, const void* phi_w, const void* x, int64_t rows,
+                               void* out, void* stream) {
+  glide_status s = check_cfg(cfg);
+  if (s != GLIDE_OK) return s;
+  if (!phi_w || !x || !out) return GLIDE_ERR_NULL;
+  if (rows < 0) return GLIDE_ERR_INVALID;
+  if (!aligned(phi_w, 16) || !aligned(x, 16) || !aligned(out, 16)) return GLIDE_ERR_ALIGN;
+  (void)stream;
+  return GLIDE_ERR_UNSUPPORTED;
+}
+
+}  // extern "C"

@@ -1,0 +1,199 @@
+"""Thin ctypes binding of ``libglide.so`` (declared in include/glide.h).
+
+Argument marshalling only: every step of the hybrid-attention layer runs in
+the HIP kernels behind the C ABI.  Tensors are torch device tensors; their
+data pointers and the current HIP stream are handed to the library.  If the
+compiled library is missing, loading fails loudly -- there is no fallback.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libglide.so")
+
+F32 = 0
+BF16 = 1
+PHI_RELU = 0
+NO_LINEAR = 1
+
+STATUS = {0: "GLIDE_OK", -1: "GLIDE_ERR_NULL", -2: "GLIDE_ERR_INVALID", -3: "GLIDE_ERR_UNSUPPORTED",
+          -4: "GLIDE_ERR_ALIGN", -5: "GLIDE_ERR_SIZE", -6: "GLIDE_ERR_HIP"}
+
+EXPORTS = ["glide_state_bytes", "glide_state_layout", "glide_workspace_bytes", "glide_state_init",
+           "glide_prefill", "glide_decode_step", "glide_feature_map", "glide_status_string"]
+
+
+class GlideError(RuntimeError):
+    def __init__(self, status, where, lib=None):
+        msg = STATUS.get(status, str(status))
+        if lib is not None:
+            msg += ": " + lib.glide_status_string(status).decode()
+        super().__init__(f"{where} failed with {msg}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("batch", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("feat_dim", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("phi", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("sm_scale", ctypes.c_float), ("windows", ctypes.POINTER(ctypes.c_int32))]
+
+
+class LayerLayout(ctypes.Structure):
+    _fields_ = [("pos_offset", ctypes.c_int64), ("s_offset", ctypes.c_int64),
+                ("z_offset", ctypes.c_int64), ("kring_offset", ctypes.c_int64),
+                ("vring_offset", ctypes.c_int64), ("layer_offset", ctypes.c_int64),
+                ("layer_bytes", ctypes.c_int64), ("window", ctypes.c_int32),
+                ("ring_slots", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path=None):
+    """Load libglide.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it with paper_2607_24788_amd/build.py "
+                           "(or __graft_entry__.build()); there is no fallback path")
+    lib = ctypes.CDLL(p)
+    cfgp = ctypes.POINTER(Config)
+    vp = ctypes.c_void_p
+    lib.glide_state_bytes.argtypes = [cfgp]
+    lib.glide_state_bytes.restype = ctypes.c_size_t
+    lib.glide_state_layout.argtypes = [cfgp, ctypes.c_int32, ctypes.POINTER(LayerLayout)]
+    lib.glide_state_layout.restype = ctypes.c_int
+    lib.glide_workspace_bytes.argtypes = [cfgp, ctypes.c_int64]
+    lib.glide_workspace_bytes.restype = ctypes.c_size_t
+    lib.glide_state_init.argtypes = [cfgp, vp, ctypes.c_size_t, vp]
+    lib.glide_state_init.restype = ctypes.c_int
+    lib.glide_prefill.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp,
+                                  ctypes.POINTER(ctypes.c_int32), ctypes.c_int64, ctypes.c_int32, vp, vp,
+                                  ctypes.c_size_t, vp]
+    lib.glide_prefill.restype = ctypes.c_int
+    lib.glide_decode_step.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp, vp,
+                                      vp, vp, vp, ctypes.c_size_t, vp]
+    lib.glide_decode_step.restype = ctypes.c_int
+    lib.glide_feature_map.argtypes = [cfgp, vp, vp, ctypes.c_int64, vp, vp]
+    lib.glide_feature_map.restype = ctypes.c_int
+    lib.glide_status_string.argtypes = [ctypes.c_int]
+    lib.glide_status_string.restype = ctypes.c_char_p
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+class Glide:
+    """A configured GLIDE layer stack (mirrors ``glide_config``)."""
+
+    def __init__(self, n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, windows,
+                 dtype=torch.bfloat16, sm_scale=None, linear=True, lib=None):
+        self.lib = lib if lib is not None else load_library()
+        self.windows = [int(w) for w in windows]
+        if len(self.windows) != n_layers:
+            raise ValueError("need one window per layer")
+        self._win = (ctypes.c_int32 * n_layers)(*self.windows)
+        self.torch_dtype = dtype
+        code = {torch.float32: F32, torch.bfloat16: BF16}.get(dtype, 99)
+        if sm_scale is None:
+            sm_scale = head_dim ** -0.5
+        self.cfg = Config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, code, PHI_RELU,
+                          0 if linear else NO_LINEAR, float(sm_scale), self._win)
+        self.n_layers, self.batch = n_layers, batch
+        self.n_q_heads, self.n_kv_heads = n_q_heads, n_kv_heads
+        self.head_dim, self.feat_dim = head_dim, feat_dim
+        self.sm_scale = float(sm_scale)
+        self.linear = linear
+
+    # -- sizes and layout ----------------------------------------------------
+    def state_bytes(self):
+        return self.lib.glide_state_bytes(ctypes.byref(self.cfg))
+
+    def workspace_bytes(self, max_total_tokens):
+        return self.lib.glide_workspace_bytes(ctypes.byref(self.cfg), int(max_total_tokens))
+
+    def layout(self, layer):
+        out = LayerLayout()
+        s = self.lib.glide_state_layout(ctypes.byref(self.cfg), int(layer), ctypes.byref(out))
+        if s:
+            raise GlideError(s, "glide_state_layout", self.lib)
+        return out
+
+    def new_state(self, device="cuda"):
+        n = self.state_bytes()
+        if n == 0:
+            raise GlideError(-2, "glide_state_bytes", self.lib)
+        return torch.empty(n, dtype=torch.uint8, device=device)
+
+    def layer_views(self, state, layer):
+        """Typed views (pos, S, z, kring, vring) of one layer inside ``state``."""
+        lay = self.layout(layer)
+        B, H, d, Df, R = self.batch, self.n_kv_heads, self.head_dim, self.feat_dim, lay.ring_slots
+        es = 2 if self.torch_dtype == torch.bfloat16 else 4
+
+        def view(off, n, dt, shape, esz):
+            return state[off:off + n * esz].view(dt).view(*shape)
+
+        return {
+            "pos": view(lay.pos_offset, B * H, torch.int64, (B, H), 8),
+            "S": view(lay.s_offset, B * H * Df * d, torch.float32, (B, H, Df, d), 4),
+            "z": view(lay.z_offset, B * H * Df, torch.float32, (B, H, Df), 4),
+            "kring": view(lay.kring_offset, B * H * R * d, self.torch_dtype, (B, H, R, d), es),
+            "vring": view(lay.vring_offset, B * H * R * d, self.torch_dtype, (B, H, R // 8, d, 8), es),
+            "window": lay.window, "ring_slots": R,
+        }
+
+    # -- calls ---------------------------------------------------------------
+    def state_init(self, state, stream=None):
+        s = self.lib.glide_state_init(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
+                                      _stream(stream))
+        if s:
+            raise GlideError(s, "glide_state_init", self.lib)
+
+    def decode_step(self, state, phi_w, q, k, v, out, layer0=0, n_layers=None, stream=None):
+        if n_layers is None:
+            n_layers = self.n_layers - layer0
+        s = self.lib.glide_decode_step(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
+                                       int(layer0), int(n_layers), _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v),
+                                       _ptr(out), None, 0, _stream(stream))
+        if s:
+            raise GlideError(s, "glide_decode_step", self.lib)
+
+    def prefill(self, state, phi_w, q, k, v, cu_seqlens, out, workspace, layer0=0, n_layers=None, chunk=0,
+                stream=None):
+        if n_layers is None:
+            n_layers = self.n_layers - layer0
+        cu = [int(x) for x in cu_seqlens]
+        if len(cu) != self.batch + 1:
+            raise ValueError("cu_seqlens needs batch + 1 entries")
+        cu_arr = (ctypes.c_int32 * len(cu))(*cu)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        s = self.lib.glide_prefill(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
+                                   int(layer0), int(n_layers), _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v), cu_arr,
+                                   int(cu[-1]), int(chunk), _ptr(out), _ptr(workspace), ws_bytes,
+                                   _stream(stream))
+        if s:
+            raise GlideError(s, "glide_prefill", self.lib)
+
+    def feature_map(self, phi_w, x, out, stream=None):
+        rows = x.numel() // self.head_dim
+        s = self.lib.glide_feature_map(ctypes.byref(self.cfg), _ptr(phi_w), _ptr(x), int(rows), _ptr(out),
+                                       _stream(stream))
+        if s:
+            raise GlideError(s, "glide_feature_map", self.lib)

@@ -1,0 +1,142 @@
+"""Helpers for the GPU parity tests: run the HIP path through the C ABI and
+compare with the CPU oracle on the same seeded inputs.
+
+Tolerances (applied per tensor X, err = max |X_gpu - X_oracle|):
+  fp32 I/O : err <= 1e-5 * max |X_oracle|         for O, S and z
+  bf16 I/O : err(O) <= 2e-2 absolute and err(O) <= 1e-2 * max |O_oracle|,
+             err(S), err(z) <= 1e-2 * max |X_oracle|
+  ring     : bit-exact (it is a copy of the inputs); pos exact.
+"""
+import numpy as np
+import torch
+
+import oracle
+from paper_2607_24788_amd import glide
+
+TOL = {torch.float32: dict(rel=1e-5, abs=None, state_rel=1e-5),
+       torch.bfloat16: dict(rel=1e-2, abs=2e-2, state_rel=1e-2)}
+
+
+def f64(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def check(name, got, want, dtype, kind="out"):
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    assert got.shape == want.shape, f"{name}: shape {got.shape} != {want.shape}"
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    err = float(np.max(np.abs(got - want))) if got.size else 0.0
+    scale = float(np.max(np.abs(want))) if want.size else 0.0
+    t = TOL[dtype]
+    rel = t["rel"] if kind == "out" else t["state_rel"]
+    bound = rel * max(scale, 1e-30)
+    assert err <= bound + 1e-30, f"{name}: max err {err:.3e} > {rel} x max|ref| ({scale:.3e})"
+    if kind == "out" and t["abs"] is not None:
+        assert err <= t["abs"], f"{name}: max err {err:.3e} > {t['abs']}"
+    return err, scale
+
+
+class Case:
+    """A decode/prefill test case on a small synthetic stack."""
+
+    def __init__(self, windows, batch=1, Hq=4, Hkv=4, d=64, Df=64, dtype=torch.float32, linear=True,
+                 tau=None, seed=0, qkv_scale=None, v_scale=None):
+        self.windows = list(windows)
+        self.L = len(windows)
+        self.B, self.Hq, self.Hkv, self.d, self.Df = batch, Hq, Hkv, d, Df
+        self.dtype, self.linear = dtype, linear
+        self.tau = d ** -0.5 if tau is None else tau
+        self.seed = seed
+        self.qkv_scale = d ** -0.5 if qkv_scale is None else qkv_scale
+        self.v_scale = self.qkv_scale if v_scale is None else v_scale
+        self.g = glide.Glide(self.L, batch, Hq, Hkv, d, Df, self.windows, dtype=dtype, sm_scale=self.tau,
+                             linear=linear)
+        gen = torch.Generator().manual_seed(seed * 7919 + 17)
+        self.phi_w = (torch.randn((self.L, d, Df), generator=gen) * d ** -0.5).to(dtype)
+        self._gen = gen
+
+    def tokens(self, n):
+        """History tensors per layer: q [L][B][n][Hq][d], k/v [L][B][n][Hkv][d]."""
+        gen = self._gen
+        q = (torch.randn((self.L, self.B, n, self.Hq, self.d), generator=gen) * self.qkv_scale).to(self.dtype)
+        k = (torch.randn((self.L, self.B, n, self.Hkv, self.d), generator=gen) * self.qkv_scale).to(self.dtype)
+        v = (torch.randn((self.L, self.B, n, self.Hkv, self.d), generator=gen) * self.v_scale).to(self.dtype)
+        return q, k, v
+
+    def oracle(self, l):
+        return oracle.Oracle(self.Hq, self.Hkv, self.d, self.Df, self.windows[l], linear=self.linear,
+                             tau=self.tau)
+
+    def new_state(self):
+        st = self.g.new_state()
+        self.g.state_init(st)
+        return st
+
+    def decode_steps(self, state, q, k, v, t0, t1):
+        """Decode positions [t0, t1) of the history tensors; returns out [L][B][t1-t0][Hq][d] (CPU)."""
+        outs = []
+        phi = self.phi_w.cuda()
+        for t in range(t0, t1):
+            qs = q[:, :, t].contiguous().cuda()
+            ks = k[:, :, t].contiguous().cuda()
+            vs = v[:, :, t].contiguous().cuda()
+            o = torch.empty_like(qs)
+            self.g.decode_step(state, phi, qs, ks, vs, o)
+            outs.append(o)
+        torch.cuda.synchronize()
+        return torch.stack(outs, 2).cpu()
+
+    def load_state_from_oracle(self, state, q, k, v, positions):
+        """Write the state after positions[b] tokens of sequence b, built by the
+        oracle's direct sums plus the literal window, into the GPU state."""
+        for l in range(self.L):
+            views = self.g.layer_views(state, l)
+            o = self.oracle(l)
+            W, R = self.windows[l], views["ring_slots"]
+            for b, p in enumerate(positions):
+                S, z = o.state(f64(self.phi_w[l]), f64(k[l, b]), f64(v[l, b]), p)
+                views["S"][b] = torch.from_numpy(S).float().cuda()
+                views["z"][b] = torch.from_numpy(z).float().cuda()
+                views["pos"][b] = p
+                for j in range(max(0, p - W), p):
+                    s = j % R
+                    views["kring"][b, :, s] = k[l, b, j].cuda()
+                    views["vring"][b, :, s // 8, :, s % 8] = v[l, b, j].cuda()
+        torch.cuda.synchronize()
+
+    def check_decode(self, out, q, k, v, positions, t_steps, label=""):
+        """out [L][B][n][Hq][d] for positions[b] .. positions[b]+n-1."""
+        n = out.shape[2]
+        worst = 0.0
+        for l in range(self.L):
+            o = self.oracle(l)
+            for b, p0 in enumerate(positions):
+                hist = slice(0, p0 + n)
+                want = o.attend(f64(self.phi_w[l]), f64(q[l, b, hist]), f64(k[l, b, hist]), f64(v[l, b, hist]),
+                                positions=np.arange(p0, p0 + n))
+                e, _ = check(f"{label} O layer {l} (W={self.windows[l]}) seq {b}", f64(out[l, b]), want,
+                             self.dtype)
+                worst = max(worst, e)
+        return worst
+
+    def check_state(self, state, k, v, positions, label=""):
+        """S, z, pos and the ring after positions[b] tokens of sequence b."""
+        for l in range(self.L):
+            views = self.g.layer_views(state, l)
+            o = self.oracle(l)
+            W, R = self.windows[l], views["ring_slots"]
+            for b, p in enumerate(positions):
+                assert int(views["pos"][b].min()) == p and int(views["pos"][b].max()) == p, \
+                    f"{label} pos layer {l} seq {b}"
+                if self.linear:
+                    S, z = o.state(f64(self.phi_w[l]), f64(k[l, b]), f64(v[l, b]), p)
+                    check(f"{label} S layer {l} seq {b}", f64(views["S"][b]), S, self.dtype, "state")
+                    check(f"{label} z layer {l} seq {b}", f64(views["z"][b]), z, self.dtype, "state")
+                kr = views["kring"][b].cpu()
+                vr = views["vring"][b].cpu()
+                for j in range(max(0, p - W), p):
+                    s = j % R
+                    assert torch.equal(kr[:, s], k[l, b, j]), f"{label} key ring layer {l} seq {b} token {j}"
+                    assert torch.equal(vr[:, s // 8, :, s % 8], v[l, b, j]), \
+                        f"{label} value ring layer {l} seq {b} token {j}"
