@@ -85,11 +85,15 @@ typedef struct {
  *   pos   int64 [B][Hkv]          tokens consumed by sequence b (equal over Hkv)
  *   S     fp32  [B][Hkv][Df][d]   sum of phi(k_j)^T v_j over tokens left of the window
  *   z     fp32  [B][Hkv][Df]      sum of phi(k_j) over the same tokens
- *   kring dtype [B][Hkv][R][d]    key of token j in slot j mod R
- *   vring dtype [B][Hkv][R/8][d][8]  value of token j: element
- *                                  [(j mod R)/8][c][(j mod R) % 8]
- * R = ring_slots = round_up(W + 1, 8) for W > 0, 0 for W = 0.  After p tokens
- * the ring holds tokens [max(0, p - W), p - 1]; other slots are stale. */
+ *   kring dtype [B][Hkv][R*d]     keys, token j in slot s = j mod R
+ *   vring dtype [B][Hkv][R*d]     values, token j in slot s = j mod R
+ * R = ring_slots = round_up(W + 1, 32) for W > 0, 0 for W = 0.  After p tokens
+ * the ring holds tokens [max(0, p - W), p - 1]; other slots are stale.
+ * Both rings are stored in 32-slot blocks of 32*d elements, in the fragment
+ * order of the decode kernel's matrix-core loads; with o = s % 32, block
+ * s / 32, element c of the slot is at (within the block)
+ *   kring: [(o/4)%2][c/32][(c/8)%4][4*(o/8) + o%4][c%8]
+ *   vring: [c/16][o/8][c%16][o%8]                                          */
 typedef struct {
   int64_t pos_offset, s_offset, z_offset, kring_offset, vring_offset;
   int64_t layer_offset, layer_bytes;
@@ -105,7 +109,9 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
 
 /* Workspace bytes needed by glide_prefill for calls with at most
  * max_total_tokens packed tokens (any chunk size), and by glide_decode_step
- * (which needs none).  0 if cfg is invalid. */
+ * for any layer range (the feature-map rows of every (layer, sequence, KV
+ * head): n_layers * B * Hkv * (G+1) * Df * 4 bytes, or nothing without the
+ * linear part).  0 if cfg is invalid. */
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens);
 
 /* Zeroes the whole state: S = 0, z = 0 (S_0, Z_0 of the Sec. II-B
@@ -144,7 +150,10 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
  *   phi_w  device [n_layers][d][Df]
  *   q      device [n_layers][B][Hq][d];  k, v device [n_layers][B][Hkv][d]
  *   out    device [n_layers][B][Hq][d]
- * workspace may be NULL (decode needs none). */
+ *   workspace device, 256-byte aligned, >= glide_workspace_bytes(cfg, 0)
+ *             (may be NULL when the linear part is off)
+ * Two kernels are enqueued: the feature map of the G query heads and of the
+ * key leaving the window, then the fused window/state pass. */
 glide_status glide_decode_step(const glide_config* cfg, void* state, size_t state_bytes,
                                int32_t layer0, int32_t n_layers, const void* phi_w,
                                const void* q, const void* k, const void* v, void* out,
@@ -152,7 +161,8 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
 
 /* The feature map alone (kernel (d)): out[r][f] = max(0, sum_c x[r][c] Wf[c][f])
  * for r < rows, accumulated in fp32.  x device [rows][d], phi_w device [d][Df]
- * (both cfg->dtype), out device [rows][Df] in cfg->dtype. */
+ * (both cfg->dtype), out device [rows][Df] in cfg->dtype; x and out may be NULL
+ * when rows == 0. */
 glide_status glide_feature_map(const glide_config* cfg, const void* phi_w, const void* x,
                                int64_t rows, void* out, void* stream);
 

@@ -66,6 +66,15 @@ glide_status check_call(const glide_config* c, void* state, size_t state_bytes, 
 
 glide_status hip_status(hipError_t e) { return e == hipSuccess ? GLIDE_OK : GLIDE_ERR_HIP; }
 
+bool linear_on(const glide_config* c) { return (c->flags & GLIDE_NO_LINEAR) == 0; }
+
+// Decode needs the feature-map rows of every unit of every layer of the call.
+size_t decode_ws(const glide_config* c) {
+  if (!linear_on(c)) return 0;
+  return decode_workspace_bytes(c->n_layers, c->batch, c->n_kv_heads, c->n_q_heads / c->n_kv_heads,
+                                c->feat_dim);
+}
+
 }  // namespace
 
 extern "C" {
@@ -110,7 +119,7 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens) {
   if (check_cfg(cfg) != GLIDE_OK || max_total_tokens < 0) return 0;
   (void)max_total_tokens;
-  return 256;
+  return std::max(size_t(256), decode_ws(cfg));
 }
 
 glide_status glide_state_init(const glide_config* cfg, void* state, size_t state_bytes, void* stream) {
@@ -123,13 +132,17 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
                                int32_t n_layers, const void* phi_w, const void* q, const void* k,
                                const void* v, void* out, void* workspace, size_t workspace_bytes,
                                void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   glide_status s = check_call(cfg, state, state_bytes, layer0, n_layers);
   if (s != GLIDE_OK) return s;
   if (!phi_w || !q || !k || !v || !out) return GLIDE_ERR_NULL;
   if (!aligned(phi_w, 16) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
     return GLIDE_ERR_ALIGN;
+  const size_t need = decode_ws(cfg);
+  if (need) {
+    if (!workspace) return GLIDE_ERR_NULL;
+    if (!aligned(workspace, 256)) return GLIDE_ERR_ALIGN;
+    if (workspace_bytes < need) return GLIDE_ERR_SIZE;
+  }
 
   // Longest windows first: the hardware dispatcher then hands out the
   // longest streams before the short ones (list scheduling).
@@ -151,7 +164,8 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
   a.Hq = cfg->n_q_heads;
   a.Hkv = cfg->n_kv_heads;
   a.G = cfg->n_q_heads / cfg->n_kv_heads;
-  a.linear = (cfg->flags & GLIDE_NO_LINEAR) ? 0 : 1;
+  a.phi_ws = static_cast<float*>(workspace);
+  a.linear = linear_on(cfg) ? 1 : 0;
   a.tau = cfg->sm_scale;
   for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
@@ -163,6 +177,10 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
       a.layers[i].W = cfg->windows[l];
       a.layers[i].R = ring_slots(cfg->windows[l]);
       a.layers[i].slot = slot;
+    }
+    if (a.linear) {
+      s = hip_status(launch_phi_decode(a, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream)));
+      if (s != GLIDE_OK) return s;
     }
     s = hip_status(launch_decode(a, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream)));
     if (s != GLIDE_OK) return s;
@@ -197,11 +215,11 @@ glide_status glide_feature_map(const glide_config* cfg, const void* phi_w, const
                                void* out, void* stream) {
   glide_status s = check_cfg(cfg);
   if (s != GLIDE_OK) return s;
-  if (!phi_w || !x || !out) return GLIDE_ERR_NULL;
   if (rows < 0) return GLIDE_ERR_INVALID;
+  if (!phi_w || (rows > 0 && (!x || !out))) return GLIDE_ERR_NULL;
   if (!aligned(phi_w, 16) || !aligned(x, 16) || !aligned(out, 16)) return GLIDE_ERR_ALIGN;
-  (void)stream;
-  return GLIDE_ERR_UNSUPPORTED;
+  return hip_status(launch_phi_rows(phi_w, x, rows, out, cfg->head_dim, cfg->feat_dim, cfg->dtype,
+                                    cfg->dtype == GLIDE_F32, hipStream_t(stream)));
 }
 
 }  // extern "C"

@@ -16,9 +16,35 @@ __host__ __device__ inline int64_t align256(int64_t x) { return (x + 255) & ~int
 
 // Ring slots of a layer with softmax window W: R > W keeps the slot of the
 // token leaving the window distinct from the slot the new token is written
-// to, so both can be touched in one decode pass.  Multiple of 8 so that an
-// 8-token block of the transposed value ring never wraps.
-__host__ __device__ inline int32_t ring_slots(int32_t W) { return W > 0 ? ((W + 1 + 7) & ~7) : 0; }
+// to, so both can be touched in one decode pass.  A multiple of 32 so that a
+// 32-token tile (token j0 = 0 mod 32) is one contiguous 32-slot ring block.
+__host__ __device__ inline int32_t ring_slots(int32_t W) { return W > 0 ? ((W + 1 + 31) & ~31) : 0; }
+
+// (x mod R) for 0 <= x < 2R.
+__device__ __forceinline__ uint32_t wrap_once(uint32_t x, uint32_t R) { return x >= R ? x - R : x; }
+
+// Ring layouts, per (sequence, KV head), in 32-slot blocks of 32*D elements.
+// Both are the MFMA fragment order of the decode kernel, so every fragment
+// load of a wave reads 1 KB (bf16) of consecutive memory.
+//  key   : block [t][D/32][4][16][8] -- slot offset o = 8*(m/4) + 4*t + m%4
+//          (row m of 16-key sub-tile t), element c = 32*kk + 8*g + e
+//  value : block [D/16][4][16][8]    -- slot offset o = 8*g + e, element
+//          c = 16*ct + n
+__host__ __device__ inline int64_t kring_elem(int32_t slot, int c, int D) {
+  const int blk = slot >> 5, o = slot & 31;
+  const int t = (o >> 2) & 1, m = ((o >> 3) << 2) | (o & 3);
+  const int kk = c >> 5, g = (c >> 3) & 3, e = c & 7;
+  return int64_t(blk) * 32 * D + ((((t * (D / 32) + kk) * 4 + g) * 16 + m) * 8 + e);
+}
+__host__ __device__ inline int64_t vring_elem(int32_t slot, int c, int D) {
+  const int blk = slot >> 5, o = slot & 31;
+  const int ct = c >> 4, n = c & 15, g = o >> 3, e = o & 7;
+  return int64_t(blk) * 32 * D + (((ct * 4 + g) * 16 + n) * 8 + e);
+}
+// First element of the 8-element key chunk (k-slab kk, lane group g) of slot s.
+__host__ __device__ inline int64_t kring_chunk(int32_t slot, int kk, int g, int D) {
+  return kring_elem(slot, 32 * kk + 8 * g, D);
+}
 
 // Byte offsets of the sections of one layer, relative to the layer's start.
 struct LayerSections {
@@ -63,6 +89,13 @@ template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) {
   return bf16_t(u >> 16);
 }
 
+// Two floats to a packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t h = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, h);
+}
+
 // ---------------------------------------------------------------------------
 // MFMA fragments.  Every contraction is issued as 16x16 output tiles with a
 // 32-wide slab of the reduction index k.  For both element types, lane l
@@ -80,18 +113,39 @@ template <> struct Frag<bf16_t> {
   uint4 v;  // 8 packed bf16
   __device__ __forceinline__ void zero() { v = make_uint4(0, 0, 0, 0); }
   __device__ __forceinline__ void load(const bf16_t* p) { v = *reinterpret_cast<const uint4*>(p); }
-  __device__ __forceinline__ float get(int i) const {
-    const uint32_t w = (&v.x)[i >> 1];
-    return __uint_as_float((i & 1) ? (w & 0xffff0000u) : (w << 16));
+  // Elements k, k+stride, ..., k+7*stride of a strided row (e.g. a column
+  // of a row-major matrix).
+  __device__ __forceinline__ void load_strided(const bf16_t* p, int stride) {
+    v.x = uint32_t(p[0]) | (uint32_t(p[stride]) << 16);
+    v.y = uint32_t(p[2 * stride]) | (uint32_t(p[3 * stride]) << 16);
+    v.z = uint32_t(p[4 * stride]) | (uint32_t(p[5 * stride]) << 16);
+    v.w = uint32_t(p[6 * stride]) | (uint32_t(p[7 * stride]) << 16);
   }
-  __device__ __forceinline__ void set(int i, float x) {
-    uint32_t& w = (&v.x)[i >> 1];
-    const uint32_t b = from_f32<bf16_t>(x);
-    w = (i & 1) ? ((w & 0xffffu) | (b << 16)) : ((w & 0xffff0000u) | b);
+  // Sum of the 8 elements as fp32.
+  __device__ __forceinline__ float sum() const {
+    float s = 0.f;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s += __uint_as_float(w[i] << 16) + __uint_as_float(w[i] & 0xffff0000u);
+    return s;
   }
-  __device__ __forceinline__ void set_raw(int i, bf16_t b) {
-    uint32_t& w = (&v.x)[i >> 1];
-    w = (i & 1) ? ((w & 0xffffu) | (uint32_t(b) << 16)) : ((w & 0xffff0000u) | b);
+  // 8 floats -> 8 bf16 (compile-time positions only)
+  __device__ __forceinline__ void set8(const float* x) {
+    v.x = pack_bf16x2(x[0], x[1]);
+    v.y = pack_bf16x2(x[2], x[3]);
+    v.z = pack_bf16x2(x[4], x[5]);
+    v.w = pack_bf16x2(x[6], x[7]);
+  }
+  // Replace element i (runtime, 0..7) by b without indexing registers
+  // dynamically (a dynamic index would force the fragment to scratch).
+  __device__ __forceinline__ void patch(int i, bf16_t b) {
+    const uint32_t sh = (i & 1) * 16;
+    const uint32_t keep = ~(0xffffu << sh), put = uint32_t(b) << sh;
+    const int wi = i >> 1;
+    v.x = wi == 0 ? ((v.x & keep) | put) : v.x;
+    v.y = wi == 1 ? ((v.y & keep) | put) : v.y;
+    v.z = wi == 2 ? ((v.z & keep) | put) : v.z;
+    v.w = wi == 3 ? ((v.w & keep) | put) : v.w;
   }
 };
 template <> struct Frag<float> {
@@ -106,9 +160,24 @@ template <> struct Frag<float> {
     v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
     v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
   }
-  __device__ __forceinline__ float get(int i) const { return v[i]; }
-  __device__ __forceinline__ void set(int i, float x) { v[i] = x; }
-  __device__ __forceinline__ void set_raw(int i, float x) { v[i] = x; }
+  __device__ __forceinline__ void load_strided(const float* p, int stride) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = p[i * stride];
+  }
+  __device__ __forceinline__ float sum() const {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += v[i];
+    return s;
+  }
+  __device__ __forceinline__ void set8(const float* x) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = x[i];
+  }
+  __device__ __forceinline__ void patch(int i, float b) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (e == i) ? b : v[e];
+  }
 };
 
 __device__ __forceinline__ f32x4_t mma(const Frag<bf16_t>& a, const Frag<bf16_t>& b, f32x4_t c) {
@@ -123,6 +192,11 @@ __device__ __forceinline__ f32x4_t mma(const Frag<float>& a, const Frag<float>& 
 
 __device__ __forceinline__ f32x4_t zero4() { return f32x4_t{0.f, 0.f, 0.f, 0.f}; }
 
+// Streaming 16-byte store (non-temporal: the line is not kept in the caches).
+__device__ __forceinline__ void store_nt(float* p, float4 v) {
+  __builtin_nontemporal_store(f32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<f32x4_t*>(p));
+}
+
 // ---------------------------------------------------------------------------
 // Launch descriptors.
 
@@ -133,6 +207,7 @@ struct DecodeArgs {
   const void* k;
   const void* v;
   void* out;
+  float* phi_ws;     // [n_layers][B*Hkv][G+1][Df]: phi(q_h) of the group, then phi(k_e)
   int32_t B, Hq, Hkv, G;
   int32_t linear;
   float tau;
@@ -143,5 +218,13 @@ struct DecodeArgs {
 
 // Host-side launchers (one translation unit per kernel family).
 hipError_t launch_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
+hipError_t launch_phi_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
+hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* out, int d, int Df, int dtype,
+                           bool out_f32, hipStream_t stream);
+
+// Workspace of a decode call: phi rows of every unit of every layer.
+inline size_t decode_workspace_bytes(int n_layers, int B, int Hkv, int G, int Df) {
+  return size_t(align256(int64_t(n_layers) * B * Hkv * (G + 1) * Df * 4));
+}
 
 }  // namespace glide

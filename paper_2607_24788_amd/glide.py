@@ -99,6 +99,38 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def kring_logical(raw, R, d):
+    """Key ring [..., R*d] (32-slot blocks [t][d/32][4][16][8]) -> [..., R, d] by slot."""
+    lead = raw.shape[:-1]
+    n = len(lead)
+    x = raw.reshape(*lead, R // 32, 2, d // 32, 4, 4, 4, 8)        # blk t kk g mh ml e
+    return x.permute(*range(n), *(n + i for i in (0, 4, 1, 5, 2, 3, 6))).reshape(*lead, R, d)
+
+
+def kring_raw(logical, R, d):
+    """Inverse of kring_logical."""
+    lead = logical.shape[:-2]
+    n = len(lead)
+    x = logical.reshape(*lead, R // 32, 4, 2, 4, d // 32, 4, 8)    # blk mh t ml kk g e
+    return x.permute(*range(n), *(n + i for i in (0, 2, 4, 5, 1, 3, 6))).reshape(*lead, R * d)
+
+
+def vring_logical(raw, R, d):
+    """Value ring [..., R*d] (32-slot blocks [d/16][4][16][8]) -> [..., R, d] by slot."""
+    lead = raw.shape[:-1]
+    n = len(lead)
+    x = raw.reshape(*lead, R // 32, d // 16, 4, 16, 8)              # blk ct g n e
+    return x.permute(*range(n), *(n + i for i in (0, 2, 4, 1, 3))).reshape(*lead, R, d)
+
+
+def vring_raw(logical, R, d):
+    """Inverse of vring_logical."""
+    lead = logical.shape[:-2]
+    n = len(lead)
+    x = logical.reshape(*lead, R // 32, 4, 8, d // 16, 16)          # blk g e ct n
+    return x.permute(*range(n), *(n + i for i in (0, 3, 1, 4, 2))).reshape(*lead, R * d)
+
+
 class Glide:
     """A configured GLIDE layer stack (mirrors ``glide_config``)."""
 
@@ -142,7 +174,9 @@ class Glide:
         return torch.empty(n, dtype=torch.uint8, device=device)
 
     def layer_views(self, state, layer):
-        """Typed views (pos, S, z, kring, vring) of one layer inside ``state``."""
+        """Typed views of one layer inside ``state``: pos, S, z, and the raw
+        rings kring_raw / vring_raw [B][Hkv][R*d] (fragment-major layout, see
+        include/glide.h; convert with kring_logical / vring_logical)."""
         lay = self.layout(layer)
         B, H, d, Df, R = self.batch, self.n_kv_heads, self.head_dim, self.feat_dim, lay.ring_slots
         es = 2 if self.torch_dtype == torch.bfloat16 else 4
@@ -154,8 +188,8 @@ class Glide:
             "pos": view(lay.pos_offset, B * H, torch.int64, (B, H), 8),
             "S": view(lay.s_offset, B * H * Df * d, torch.float32, (B, H, Df, d), 4),
             "z": view(lay.z_offset, B * H * Df, torch.float32, (B, H, Df), 4),
-            "kring": view(lay.kring_offset, B * H * R * d, self.torch_dtype, (B, H, R, d), es),
-            "vring": view(lay.vring_offset, B * H * R * d, self.torch_dtype, (B, H, R // 8, d, 8), es),
+            "kring_raw": view(lay.kring_offset, B * H * R * d, self.torch_dtype, (B, H, R * d), es),
+            "vring_raw": view(lay.vring_offset, B * H * R * d, self.torch_dtype, (B, H, R * d), es),
             "window": lay.window, "ring_slots": R,
         }
 
@@ -166,12 +200,16 @@ class Glide:
         if s:
             raise GlideError(s, "glide_state_init", self.lib)
 
-    def decode_step(self, state, phi_w, q, k, v, out, layer0=0, n_layers=None, stream=None):
+    def new_workspace(self, max_total_tokens=0, device="cuda"):
+        return torch.empty(max(self.workspace_bytes(max_total_tokens), 256), dtype=torch.uint8, device=device)
+
+    def decode_step(self, state, phi_w, q, k, v, out, workspace, layer0=0, n_layers=None, stream=None):
         if n_layers is None:
             n_layers = self.n_layers - layer0
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         s = self.lib.glide_decode_step(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
                                        int(layer0), int(n_layers), _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v),
-                                       _ptr(out), None, 0, _stream(stream))
+                                       _ptr(out), _ptr(workspace), ws_bytes, _stream(stream))
         if s:
             raise GlideError(s, "glide_decode_step", self.lib)
 
@@ -192,7 +230,7 @@ class Glide:
             raise GlideError(s, "glide_prefill", self.lib)
 
     def feature_map(self, phi_w, x, out, stream=None):
-        rows = x.numel() // self.head_dim
+        rows = out.numel() // self.feat_dim
         s = self.lib.glide_feature_map(ctypes.byref(self.cfg), _ptr(phi_w), _ptr(x), int(rows), _ptr(out),
                                        _stream(stream))
         if s:

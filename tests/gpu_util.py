@@ -73,6 +73,12 @@ class Case:
         self.g.state_init(st)
         return st
 
+    @property
+    def ws(self):
+        if not hasattr(self, "_ws"):
+            self._ws = self.g.new_workspace(4096)
+        return self._ws
+
     def decode_steps(self, state, q, k, v, t0, t1):
         """Decode positions [t0, t1) of the history tensors; returns out [L][B][t1-t0][Hq][d] (CPU)."""
         outs = []
@@ -82,7 +88,7 @@ class Case:
             ks = k[:, :, t].contiguous().cuda()
             vs = v[:, :, t].contiguous().cuda()
             o = torch.empty_like(qs)
-            self.g.decode_step(state, phi, qs, ks, vs, o)
+            self.g.decode_step(state, phi, qs, ks, vs, o, self.ws)
             outs.append(o)
         torch.cuda.synchronize()
         return torch.stack(outs, 2).cpu()
@@ -99,10 +105,14 @@ class Case:
                 views["S"][b] = torch.from_numpy(S).float().cuda()
                 views["z"][b] = torch.from_numpy(z).float().cuda()
                 views["pos"][b] = p
-                for j in range(max(0, p - W), p):
-                    s = j % R
-                    views["kring"][b, :, s] = k[l, b, j].cuda()
-                    views["vring"][b, :, s // 8, :, s % 8] = v[l, b, j].cuda()
+                if R:
+                    kl = glide.kring_logical(views["kring_raw"][b].cpu(), R, self.d)
+                    vl = glide.vring_logical(views["vring_raw"][b].cpu(), R, self.d)
+                    for j in range(max(0, p - W), p):
+                        kl[:, j % R] = k[l, b, j]
+                        vl[:, j % R] = v[l, b, j]
+                    views["kring_raw"][b] = glide.kring_raw(kl, R, self.d).cuda()
+                    views["vring_raw"][b] = glide.vring_raw(vl, R, self.d).cuda()
         torch.cuda.synchronize()
 
     def check_decode(self, out, q, k, v, positions, t_steps, label=""):
@@ -133,10 +143,11 @@ class Case:
                     S, z = o.state(f64(self.phi_w[l]), f64(k[l, b]), f64(v[l, b]), p)
                     check(f"{label} S layer {l} seq {b}", f64(views["S"][b]), S, self.dtype, "state")
                     check(f"{label} z layer {l} seq {b}", f64(views["z"][b]), z, self.dtype, "state")
-                kr = views["kring"][b].cpu()
-                vr = views["vring"][b].cpu()
+                if not R:
+                    continue
+                kr = glide.kring_logical(views["kring_raw"][b].cpu(), R, self.d)
+                vr = glide.vring_logical(views["vring_raw"][b].cpu(), R, self.d)
                 for j in range(max(0, p - W), p):
                     s = j % R
                     assert torch.equal(kr[:, s], k[l, b, j]), f"{label} key ring layer {l} seq {b} token {j}"
-                    assert torch.equal(vr[:, s // 8, :, s % 8], v[l, b, j]), \
-                        f"{label} value ring layer {l} seq {b} token {j}"
+                    assert torch.equal(vr[:, s], v[l, b, j]), f"{label} value ring layer {l} seq {b} token {j}"

@@ -55,7 +55,7 @@ def expected_layout(B, Hkv, d, Df, windows, es):
     off = 0
     out = []
     for W in windows:
-        R = ((W + 1 + 7) // 8) * 8 if W > 0 else 0
+        R = ((W + 1 + 31) // 32) * 32 if W > 0 else 0
         units = B * Hkv
         pos = off
         S = pos + align(units * 8)
@@ -79,15 +79,33 @@ def test_layout_matches_documentation(dtype, es):
             (e["pos"], e["S"], e["z"], e["K"], e["V"])
         assert lay.ring_slots == e["R"] and lay.window == g.windows[l]
         assert lay.layer_bytes == e["bytes"]
-        assert lay.ring_slots == 0 or (lay.ring_slots % 8 == 0 and lay.ring_slots > lay.window)
+        assert lay.ring_slots == 0 or (lay.ring_slots % 32 == 0 and lay.ring_slots > lay.window)
 
 
 def test_layer_views_cover_state():
     g = mk()
     st = torch.zeros(g.state_bytes(), dtype=torch.uint8)
     v = g.layer_views(st, 2)
-    assert v["S"].shape == (2, 2, 64, 128) and v["kring"].shape == (2, 2, 72, 128)
-    assert v["vring"].shape == (2, 2, 9, 128, 8)
+    assert v["S"].shape == (2, 2, 64, 128) and v["kring_raw"].shape == (2, 2, 96 * 128)
+    assert g.layer_views(st, 1)["ring_slots"] == 32      # W = 5: one 32-token block
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_ring_layout_helpers(d):
+    """The logical <-> fragment-major ring conversions follow the documented
+    element positions and are inverses of each other."""
+    R = 64
+    logical = torch.arange(R * d, dtype=torch.float64).view(R, d)
+    kr, vr = glide.kring_raw(logical, R, d), glide.vring_raw(logical, R, d)
+    for s_ in (0, 1, 5, 31, 32, 45, 63):
+        blk, o = divmod(s_, 32)
+        for c in (0, 7, 8, 31, 33, d - 1):
+            kpos = blk * 32 * d + ((((o // 4) % 2 * (d // 32) + c // 32) * 4 + (c // 8) % 4) * 16
+                                   + 4 * (o // 8) + o % 4) * 8 + c % 8
+            vpos = blk * 32 * d + ((c // 16 * 4 + o // 8) * 16 + c % 16) * 8 + o % 8
+            assert kr[kpos] == logical[s_, c] and vr[vpos] == logical[s_, c]
+    assert torch.equal(glide.kring_logical(kr, R, d), logical)
+    assert torch.equal(glide.vring_logical(vr, R, d), logical)
 
 
 BAD_CFGS = [
@@ -127,11 +145,13 @@ def test_null_arguments(lib):
     assert lib.glide_state_layout(ctypes.byref(g.cfg), -1, ctypes.byref(out)) == -2
 
 
-def _decode(g, state=256, size=None, layer0=0, n=1, ptrs=(4096,) * 5):
+def _decode(g, state=256, size=None, layer0=0, n=1, ptrs=(4096,) * 5, ws=1 << 20, ws_bytes=None):
     size = g.state_bytes() if size is None else size
+    ws_bytes = g.workspace_bytes(0) if ws_bytes is None else ws_bytes
     P = [ctypes.c_void_p(x) if x is not None else None for x in ptrs]
     return g.lib.glide_decode_step(ctypes.byref(g.cfg), ctypes.c_void_p(state) if state else None, size,
-                                   layer0, n, P[0], P[1], P[2], P[3], P[4], None, 0, None)
+                                   layer0, n, P[0], P[1], P[2], P[3], P[4],
+                                   ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
 
 
 def test_decode_argument_errors():
@@ -147,6 +167,16 @@ def test_decode_argument_errors():
     assert _decode(g, ptrs=(4096, None, 4096, 4096, 4096)) == -1
     assert _decode(g, ptrs=(4096, 4096, 4096 + 2, 4096, 4096)) == -4   # q misaligned
     assert _decode(g, ptrs=(4096, 4096, 4096, 4096, 4104)) == -4       # out misaligned
+    assert _decode(g, ws=None) == -1                                   # decode needs its workspace
+    assert _decode(g, ws=(1 << 20) + 16) == -4
+    assert _decode(g, ws_bytes=g.workspace_bytes(0) - 1) == -5
+
+
+def test_decode_workspace_size():
+    g = mk(n_layers=3, batch=2, n_q_heads=8, n_kv_heads=2, feat_dim=64)
+    assert g.workspace_bytes(0) >= 3 * 2 * 2 * (4 + 1) * 64 * 4
+    g2 = mk(linear=False, windows=[1, 5, 64])
+    assert g2.workspace_bytes(0) == 256      # nothing but the minimum without the linear part
 
 
 def _prefill(g, cu, total, chunk=0, ws_bytes=None, state=256, ptrs=(4096,) * 6):

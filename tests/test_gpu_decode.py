@@ -61,7 +61,7 @@ def test_ragged_positions_from_built_state(dtype):
         ks = torch.stack([k[:, b, pos[b] + step] for b in range(3)], 1).contiguous()
         vs = torch.stack([v[:, b, pos[b] + step] for b in range(3)], 1).contiguous()
         o = torch.empty_like(qs).cuda()
-        case.g.decode_step(st, case.phi_w.cuda(), qs.cuda(), ks.cuda(), vs.cuda(), o)
+        case.g.decode_step(st, case.phi_w.cuda(), qs.cuda(), ks.cuda(), vs.cuda(), o, case.ws)
         outs.append(o)
     out = torch.stack(outs, 2).cpu()
     case.check_decode(out, q, k, v, pos, n, "ragged")
@@ -85,10 +85,10 @@ def test_layer_subsets_match_full_call():
     for t in range(30):
         qs, ks, vs = (x[:, :, t].contiguous().cuda() for x in (q, k, v))
         oa, ob = torch.empty_like(qs), torch.empty_like(qs)
-        case.g.decode_step(st_a, phi, qs, ks, vs, oa)
+        case.g.decode_step(st_a, phi, qs, ks, vs, oa, case.ws)
         for l in range(case.L):
             case.g.decode_step(st_b, phi[l:l + 1], qs[l:l + 1], ks[l:l + 1], vs[l:l + 1], ob[l:l + 1],
-                               layer0=l, n_layers=1)
+                               case.ws, layer0=l, n_layers=1)
         assert torch.equal(oa, ob), f"step {t}"
     assert torch.equal(st_a, st_b)
 
