@@ -68,6 +68,17 @@ glide_status hip_status(hipError_t e) { return e == hipSuccess ? GLIDE_OK : GLID
 
 bool linear_on(const glide_config* c) { return (c->flags & GLIDE_NO_LINEAR) == 0; }
 
+int32_t max_window(const glide_config* c) {
+  int32_t w = 0;
+  for (int32_t l = 0; l < c->n_layers; ++l) w = std::max(w, c->windows[l]);
+  return w;
+}
+
+PrefillWorkspace prefill_ws(const glide_config* c, int64_t T) {
+  return prefill_workspace(T, c->batch, c->n_q_heads, c->n_kv_heads, c->head_dim, c->feat_dim, esize(c),
+                           max_window(c), linear_on(c));
+}
+
 // Decode needs the feature-map rows of every unit of every layer of the call.
 size_t decode_ws(const glide_config* c) {
   if (!linear_on(c)) return 0;
@@ -118,8 +129,8 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
 
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens) {
   if (check_cfg(cfg) != GLIDE_OK || max_total_tokens < 0) return 0;
-  (void)max_total_tokens;
-  return std::max(size_t(256), decode_ws(cfg));
+  const size_t pre = max_total_tokens > 0 ? prefill_ws(cfg, max_total_tokens).total : 0;
+  return std::max(size_t(256), std::max(pre, decode_ws(cfg)));
 }
 
 glide_status glide_state_init(const glide_config* cfg, void* state, size_t state_bytes, void* stream) {
@@ -202,13 +213,99 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   for (int32_t b = 0; b < cfg->batch; ++b)
     if (cu_seqlens_host[b + 1] < cu_seqlens_host[b]) return GLIDE_ERR_INVALID;
   if (chunk == 0) chunk = 64;
-  if (chunk < 16 || chunk > 256 || chunk % 16) return GLIDE_ERR_INVALID;
+  if (chunk < 32 || chunk > 256 || chunk % 32) return GLIDE_ERR_INVALID;
   const size_t need = glide_workspace_bytes(cfg, total_tokens);
   if (workspace_bytes < need) return GLIDE_ERR_SIZE;
-  if (need && !workspace) return GLIDE_ERR_NULL;
-  if (workspace && !aligned(workspace, 256)) return GLIDE_ERR_ALIGN;
-  (void)stream;
-  return GLIDE_ERR_UNSUPPORTED;
+  if (!workspace) return GLIDE_ERR_NULL;
+  if (!aligned(workspace, 256)) return GLIDE_ERR_ALIGN;
+  if (total_tokens == 0) return GLIDE_OK;
+
+  const int64_t T = total_tokens;
+  const int B = cfg->batch, Hq = cfg->n_q_heads, Hkv = cfg->n_kv_heads, d = cfg->head_dim, Df = cfg->feat_dim;
+  const int es = esize(cfg);
+  const bool lin = linear_on(cfg);
+  const PrefillWorkspace w = prefill_ws(cfg, T);
+  char* ws = static_cast<char*>(workspace);
+  const int64_t per_seg = (T * Hkv + kSegTargetWorkgroups - 1) / kSegTargetWorkgroups;
+  const int32_t seg_len = int32_t(((std::max<int64_t>(chunk, per_seg) + chunk - 1) / chunk) * chunk);
+  hipStream_t st = hipStream_t(stream);
+
+  PrefillArgs a;
+  memset(&a, 0, sizeof(a));
+  a.state = static_cast<char*>(state);
+  a.phq = ws + w.phq;
+  a.phk = ws + w.phk;
+  a.hk = ws + w.hk;
+  a.hv = ws + w.hv;
+  a.hphk = ws + w.hphk;
+  a.seg = reinterpret_cast<float*>(ws + w.seg);
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.G = Hq / Hkv;
+  a.linear = lin ? 1 : 0;
+  a.tau = cfg->sm_scale;
+  a.C = chunk;
+  a.seg_len = seg_len;
+  a.Wcap = max_window(cfg);
+
+  // fill the per-group tables of sequences [g0, g0 + n)
+  auto group = [&](int g0, int32_t seg0) {
+    const int n = std::min(kMaxSeqPerLaunch, B - g0);
+    a.seq0 = g0;
+    a.nseq = n;
+    a.seg0 = seg0;
+    int32_t nseg = 0;
+    for (int i = 0; i < n; ++i) {
+      a.seq_start[i] = cu_seqlens_host[g0 + i];
+      a.seq_len[i] = cu_seqlens_host[g0 + i + 1] - cu_seqlens_host[g0 + i];
+      a.seg_base[i] = nseg;
+      nseg += (a.seq_len[i] + seg_len - 1) / seg_len;
+    }
+    a.seg_base[n] = nseg;
+    a.nseg = nseg;
+    return nseg;
+  };
+
+  for (int32_t i = 0; i < n_layers; ++i) {
+    const int32_t l = layer0 + i;
+    const int32_t W = cfg->windows[l];
+    a.layer_base = layer_base(cfg, l);
+    a.W = W;
+    a.R = ring_slots(W);
+    a.q = static_cast<const char*>(q) + size_t(i) * T * Hq * d * es;
+    a.k = static_cast<const char*>(k) + size_t(i) * T * Hkv * d * es;
+    a.v = static_cast<const char*>(v) + size_t(i) * T * Hkv * d * es;
+    a.out = static_cast<char*>(out) + size_t(i) * T * Hq * d * es;
+    const void* wf = static_cast<const char*>(phi_w) + size_t(i) * d * Df * es;
+    if (lin) {
+      s = hip_status(launch_phi_rows(wf, a.q, T * Hq, ws + w.phq, d, Df, cfg->dtype, cfg->dtype == GLIDE_F32, st));
+      if (s != GLIDE_OK) return s;
+      s = hip_status(launch_phi_rows(wf, a.k, T * Hkv, ws + w.phk, d, Df, cfg->dtype, cfg->dtype == GLIDE_F32, st));
+      if (s != GLIDE_OK) return s;
+    }
+    if (W > 0) {
+      // history of a continuing prefill (nothing to copy when pos == 0)
+      for (int g0 = 0; g0 < B; g0 += kMaxSeqPerLaunch) {
+        group(g0, 0);
+        s = hip_status(launch_prefill_gather(a, d, Df, cfg->dtype, st));
+        if (s != GLIDE_OK) return s;
+      }
+      if (lin) {
+        s = hip_status(launch_phi_rows(wf, a.hk, int64_t(B) * Hkv * W, ws + w.hphk, d, Df, cfg->dtype,
+                                       cfg->dtype == GLIDE_F32, st));
+        if (s != GLIDE_OK) return s;
+      }
+    }
+    int32_t seg0 = 0;
+    for (int g0 = 0; g0 < B; g0 += kMaxSeqPerLaunch) {
+      const int32_t nseg = group(g0, seg0);
+      s = hip_status(launch_prefill_layer(a, d, Df, cfg->dtype, st));
+      if (s != GLIDE_OK) return s;
+      seg0 += nseg;
+    }
+  }
+  return GLIDE_OK;
 }
 
 glide_status glide_feature_map(const glide_config* cfg, const void* phi_w, const void* x, int64_t rows,

@@ -121,6 +121,14 @@ template <> struct Frag<bf16_t> {
     v.z = uint32_t(p[4 * stride]) | (uint32_t(p[5 * stride]) << 16);
     v.w = uint32_t(p[6 * stride]) | (uint32_t(p[7 * stride]) << 16);
   }
+  __device__ __forceinline__ void to_floats(float* x) const {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
   // Sum of the 8 elements as fp32.
   __device__ __forceinline__ float sum() const {
     float s = 0.f;
@@ -159,6 +167,10 @@ template <> struct Frag<float> {
     const float4 b = reinterpret_cast<const float4*>(p)[1];
     v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
     v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+  __device__ __forceinline__ void to_floats(float* x) const {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = v[i];
   }
   __device__ __forceinline__ void load_strided(const float* p, int stride) {
 #pragma unroll
@@ -221,6 +233,71 @@ hipError_t launch_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStrea
 hipError_t launch_phi_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
 hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* out, int d, int Df, int dtype,
                            bool out_f32, hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// Prefill.  Sequences are processed in groups of at most kMaxSeqPerLaunch so
+// the per-sequence tables travel in the kernel arguments.
+constexpr int kMaxSeqPerLaunch = 128;
+constexpr int kSegTargetWorkgroups = 1024;  // segments x KV heads per layer (bound)
+
+struct PrefillArgs {
+  char* state;
+  int64_t layer_base;   // byte offset of the layer in the state blob
+  int32_t W, R;
+  const void* q;        // [T][Hq][d]   this layer's inputs, packed by sequence
+  const void* k;        // [T][Hkv][d]
+  const void* v;        // [T][Hkv][d]
+  void* out;            // [T][Hq][d]
+  const void* phq;      // workspace: phi(q)  [T][Hq][Df]   (element type T)
+  const void* phk;      // workspace: phi(k)  [T][Hkv][Df]
+  void* hk;             // workspace: history keys    [B][Hkv][Wcap][d]
+  void* hv;             // workspace: history values  [B][Hkv][Wcap][d]
+  void* hphk;           // workspace: phi(history)    [B][Hkv][Wcap][Df]
+  float* seg;           // workspace: per (segment, KV head) S [Df][d] then z [Df]
+  int32_t B, Hq, Hkv, G;
+  int32_t linear;
+  float tau;
+  int32_t C;            // chunk tokens (multiple of 32)
+  int32_t seg_len;      // segment tokens (multiple of C)
+  int32_t Wcap;         // history capacity per (sequence, KV head)
+  int32_t nseq;         // sequences in this group
+  int32_t seq0;         // first sequence of the group
+  int32_t seg0;         // first segment record of the group
+  int32_t nseg;         // segments in this group
+  int32_t pad;
+  int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token
+  int32_t seq_len[kMaxSeqPerLaunch];       // new tokens of the sequence
+  int32_t seg_base[kMaxSeqPerLaunch + 1];  // first segment (within the group) of the sequence
+};
+
+struct PrefillWorkspace {
+  size_t phq, phk, hk, hv, hphk, seg, total;
+};
+
+inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hq, int Hkv, int d, int Df, int esize, int Wcap,
+                                          bool linear) {
+  PrefillWorkspace w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += size_t(align256(int64_t(bytes)));
+    return o;
+  };
+  w.phq = take(linear ? size_t(T) * Hq * Df * esize : 0);
+  w.phk = take(linear ? size_t(T) * Hkv * Df * esize : 0);
+  w.hk = take(size_t(B) * Hkv * Wcap * d * esize);
+  w.hv = take(size_t(B) * Hkv * Wcap * d * esize);
+  w.hphk = take(linear ? size_t(B) * Hkv * Wcap * Df * esize : 0);
+  // segments: seg_len >= T*Hkv/kSegTargetWorkgroups, so there are at most
+  // kSegTargetWorkgroups/Hkv + B of them
+  w.seg = take(linear ? (size_t(kSegTargetWorkgroups) + size_t(B) * Hkv) * (size_t(Df) * d + Df) * 4 : 0);
+  w.total = off;
+  return w;
+}
+
+hipError_t launch_prefill_layer(const PrefillArgs& a, int d, int Df, int dtype, hipStream_t stream);
+hipError_t launch_prefill_gather(const PrefillArgs& a, int d, int Df, int dtype, hipStream_t stream);
+hipError_t launch_prefill_ringfill(const PrefillArgs& a, int d, int Df, int dtype, hipStream_t stream);
 
 // Workspace of a decode call: phi rows of every unit of every layer.
 inline size_t decode_workspace_bytes(int n_layers, int B, int Hkv, int G, int Df) {

@@ -93,6 +93,37 @@ class Case:
         torch.cuda.synchronize()
         return torch.stack(outs, 2).cpu()
 
+    def prefill(self, state, q, k, v, starts, lens, chunk=0):
+        """Prefill tokens [starts[b], starts[b] + lens[b]) of every sequence (one
+        call over all layers); returns out [L][B] list of [lens[b]][Hq][d] (CPU)."""
+        cu = [0]
+        for n in lens:
+            cu.append(cu[-1] + n)
+        T = cu[-1]
+        qp = torch.cat([q[:, b, s:s + n] for b, (s, n) in enumerate(zip(starts, lens))], 1).contiguous()
+        kp = torch.cat([k[:, b, s:s + n] for b, (s, n) in enumerate(zip(starts, lens))], 1).contiguous()
+        vp = torch.cat([v[:, b, s:s + n] for b, (s, n) in enumerate(zip(starts, lens))], 1).contiguous()
+        out = torch.full((self.L, T, self.Hq, self.d), float("nan"), dtype=self.dtype, device="cuda")
+        ws = self.g.new_workspace(max(T, 1))
+        self.g.prefill(state, self.phi_w.cuda(), qp.cuda(), kp.cuda(), vp.cuda(), cu, out, ws, chunk=chunk)
+        torch.cuda.synchronize()
+        out = out.cpu()
+        return [[out[l, cu[b]:cu[b + 1]] for b in range(self.B)] for l in range(self.L)]
+
+    def check_prefill(self, outs, q, k, v, starts, lens, label="", positions=None):
+        """outs from prefill(); compares every (or the listed) output position."""
+        for l in range(self.L):
+            o = self.oracle(l)
+            for b, (s, n) in enumerate(zip(starts, lens)):
+                if n == 0:
+                    continue
+                pos = np.arange(s, s + n) if positions is None else np.asarray(positions[b])
+                hist = slice(0, int(pos.max()) + 1)
+                want = o.attend(f64(self.phi_w[l]), f64(q[l, b, hist]), f64(k[l, b, hist]), f64(v[l, b, hist]),
+                                positions=pos)
+                check(f"{label} prefill O layer {l} (W={self.windows[l]}) seq {b}", f64(outs[l][b][pos - s]),
+                      want, self.dtype)
+
     def load_state_from_oracle(self, state, q, k, v, positions):
         """Write the state after positions[b] tokens of sequence b, built by the
         oracle's direct sums plus the literal window, into the GPU state."""

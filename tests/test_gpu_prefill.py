@@ -1,0 +1,99 @@
+"""GPU parity of glide_prefill against the CPU oracle (through the C ABI)."""
+import pytest
+import torch
+
+from .gpu_util import Case
+
+pytestmark = pytest.mark.gpu
+
+
+def _prefill_from_empty(case, lens, chunk=0, label=""):
+    n = max(lens)
+    q, k, v = case.tokens(n)
+    st = case.new_state()
+    outs = case.prefill(st, q, k, v, [0] * case.B, lens, chunk=chunk)
+    case.check_prefill(outs, q, k, v, [0] * case.B, lens, label)
+    case.check_state(st, k, v, lens, label)
+    return st, (q, k, v)
+
+
+def test_single_layer_fp32_prefill_then_decode():
+    """Single fp32 layer (4 = 4 heads, d = Df = 64, W = 64): 512 tokens
+    prefilled, every output checked, then 16 decode steps."""
+    case = Case([64], batch=1, Hq=4, Hkv=4, d=64, Df=64, dtype=torch.float32, seed=0)
+    q, k, v = case.tokens(528)
+    st = case.new_state()
+    outs = case.prefill(st, q, k, v, [0], [512])
+    case.check_prefill(outs, q, k, v, [0], [512], "fp32 prefill")
+    case.check_state(st, k, v, [512], "fp32 prefill")
+    out = case.decode_steps(st, q, k, v, 512, 528)
+    case.check_decode(out, q, k, v, [512], 16, "fp32 decode after prefill")
+    case.check_state(st, k, v, [528], "fp32 after decode")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("d,Df", [(128, 128), (64, 64), (128, 64), (64, 128)])
+def test_window_sweep_ragged(dtype, d, Df):
+    """Windows around tile and chunk edges, three ragged sequences (one empty),
+    GQA 4:1, all layers in one call."""
+    wins = [0, 1, 2, 31, 32, 33, 65, 200]
+    case = Case(wins, batch=3, Hq=8, Hkv=2, d=d, Df=Df, dtype=dtype, seed=11)
+    _prefill_from_empty(case, [0, 37, 300], label=f"sweep {dtype} d={d} Df={Df}")
+
+
+@pytest.mark.parametrize("chunk", [32, 96, 256])
+def test_chunk_sizes(chunk):
+    case = Case([0, 7, 64, 130], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=12)
+    _prefill_from_empty(case, [257, 130], chunk=chunk, label=f"chunk {chunk}")
+
+
+@pytest.mark.parametrize("G", [1, 8, 16])
+def test_group_sizes(G):
+    case = Case([0, 5, 70], batch=2, Hq=2 * G, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=13)
+    _prefill_from_empty(case, [90, 161], label=f"G={G}")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_no_linear(dtype):
+    case = Case([1, 9, 100], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=dtype, linear=False, seed=14)
+    _prefill_from_empty(case, [150, 33], label="no-linear")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_continuing_prefill(dtype):
+    """prefill(n1) then prefill(n2) from the reached state == the definition over
+    n1 + n2 tokens (history from the ring feeds the band and the fold)."""
+    case = Case([0, 3, 40, 129], batch=3, Hq=8, Hkv=2, d=128, Df=128, dtype=dtype, seed=15)
+    n1 = [20, 0, 150]
+    n2 = [70, 45, 9]
+    q, k, v = case.tokens(max(a + b for a, b in zip(n1, n2)))
+    st = case.new_state()
+    case.prefill(st, q, k, v, [0] * 3, n1)
+    outs = case.prefill(st, q, k, v, n1, n2)
+    case.check_prefill(outs, q, k, v, n1, n2, "continued")
+    case.check_state(st, k, v, [a + b for a, b in zip(n1, n2)], "continued")
+
+
+def test_prefill_then_decode_bf16():
+    case = Case([0, 16, 48, 100], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=16)
+    q, k, v = case.tokens(230)
+    st = case.new_state()
+    case.prefill(st, q, k, v, [0, 0], [200, 140])
+    # decode both sequences from their (different) positions
+    outs = []
+    for step in range(30):
+        qs = torch.stack([q[:, 0, 200 + step], q[:, 1, 140 + step]], 1).contiguous()
+        ks = torch.stack([k[:, 0, 200 + step], k[:, 1, 140 + step]], 1).contiguous()
+        vs = torch.stack([v[:, 0, 200 + step], v[:, 1, 140 + step]], 1).contiguous()
+        o = torch.empty_like(qs).cuda()
+        case.g.decode_step(st, case.phi_w.cuda(), qs.cuda(), ks.cuda(), vs.cuda(), o, case.ws)
+        outs.append(o)
+    out = torch.stack(outs, 2).cpu()
+    case.check_decode(out, q, k, v, [200, 140], 30, "decode after prefill")
+    case.check_state(st, k, v, [230, 170], "decode after prefill")
+
+
+def test_sharp_logits_prefill():
+    case = Case([0, 6, 50], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=17, qkv_scale=0.5,
+                v_scale=1.0)
+    _prefill_from_empty(case, [120, 77], label="sharp")
