@@ -226,8 +226,7 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   const bool lin = linear_on(cfg);
   const PrefillWorkspace w = prefill_ws(cfg, T);
   char* ws = static_cast<char*>(workspace);
-  const int64_t per_seg = (T * Hkv + kSegTargetWorkgroups - 1) / kSegTargetWorkgroups;
-  const int32_t seg_len = int32_t(((std::max<int64_t>(chunk, per_seg) + chunk - 1) / chunk) * chunk);
+  const int32_t seg_len = chunk * kSegChunks;
   hipStream_t st = hipStream_t(stream);
 
   PrefillArgs a;
@@ -247,6 +246,7 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   a.tau = cfg->sm_scale;
   a.C = chunk;
   a.seg_len = seg_len;
+  a.npass = (chunk * (Hq / Hkv) + 127) / 128;
   a.Wcap = max_window(cfg);
 
   // fill the per-group tables of sequences [g0, g0 + n)
@@ -255,14 +255,17 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
     a.seq0 = g0;
     a.nseq = n;
     a.seg0 = seg0;
-    int32_t nseg = 0;
+    int32_t nseg = 0, nwg = 0;
     for (int i = 0; i < n; ++i) {
       a.seq_start[i] = cu_seqlens_host[g0 + i];
       a.seq_len[i] = cu_seqlens_host[g0 + i + 1] - cu_seqlens_host[g0 + i];
       a.seg_base[i] = nseg;
+      a.wg_base[i] = nwg;
       nseg += (a.seq_len[i] + seg_len - 1) / seg_len;
+      nwg += (a.seq_len[i] + chunk - 1) / chunk * a.npass;
     }
     a.seg_base[n] = nseg;
+    a.wg_base[n] = nwg;
     a.nseg = nseg;
     return nseg;
   };

@@ -204,6 +204,38 @@ __device__ __forceinline__ f32x4_t mma(const Frag<float>& a, const Frag<float>& 
 
 __device__ __forceinline__ f32x4_t zero4() { return f32x4_t{0.f, 0.f, 0.f, 0.f}; }
 
+// Fragment of 8 consecutive ROWS of one column from a row-major LDS tile M
+// (row stride rs elements): lane (n = lane%16, g = lane/16) receives
+// M[row0 + e][col0 + n], e = 0..7, where row0 must be equal across each group
+// of 16 lanes (here row0 = 8*g + const).  This is the operand layout of a
+// contraction over rows (keys) with the tile stored naturally.
+//   bf16: two ds_read_b64_tr_b16.  Within a 16-lane group, source lane i
+//   supplies 4 consecutive 16-bit values and output lane j receives, in slot
+//   s, element j%4 of source lane 4s + j/4; pointing source lane i at
+//   M[row0 + i/4][col0 + 4*(i%4)] therefore hands lane j the column
+//   M[row0 .. row0+3][col0 + j].
+//   fp32: eight scalar LDS reads.
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+
+__device__ __forceinline__ void load_colfrag(Frag<bf16_t>& f, const bf16_t* M, int rs, int row0, int col0) {
+  const int n = threadIdx.x & 15;
+  const bf16_t* p = M + (row0 + (n >> 2)) * rs + col0 + 4 * (n & 3);
+  const auto* p1 = (lds_i16x4_t*)(__attribute__((address_space(3))) bf16_t*)(p);
+  const auto* p2 = (lds_i16x4_t*)(__attribute__((address_space(3))) bf16_t*)(p + 4 * rs);
+  const i16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)p1);
+  const i16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)p2);
+  f.v.x = uint32_t(uint16_t(a[0])) | (uint32_t(uint16_t(a[1])) << 16);
+  f.v.y = uint32_t(uint16_t(a[2])) | (uint32_t(uint16_t(a[3])) << 16);
+  f.v.z = uint32_t(uint16_t(b[0])) | (uint32_t(uint16_t(b[1])) << 16);
+  f.v.w = uint32_t(uint16_t(b[2])) | (uint32_t(uint16_t(b[3])) << 16);
+}
+__device__ __forceinline__ void load_colfrag(Frag<float>& f, const float* M, int rs, int row0, int col0) {
+  const int n = threadIdx.x & 15;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f.v[e] = M[(row0 + e) * rs + col0 + n];
+}
+
 // Streaming 16-byte store (non-temporal: the line is not kept in the caches).
 __device__ __forceinline__ void store_nt(float* p, float4 v) {
   __builtin_nontemporal_store(f32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<f32x4_t*>(p));
@@ -238,7 +270,7 @@ hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* ou
 // Prefill.  Sequences are processed in groups of at most kMaxSeqPerLaunch so
 // the per-sequence tables travel in the kernel arguments.
 constexpr int kMaxSeqPerLaunch = 128;
-constexpr int kSegTargetWorkgroups = 1024;  // segments x KV heads per layer (bound)
+constexpr int kSegChunks = 4;  // chunks per segment of the state scan
 
 struct PrefillArgs {
   char* state;
@@ -265,9 +297,12 @@ struct PrefillArgs {
   int32_t seg0;         // first segment record of the group
   int32_t nseg;         // segments in this group
   int32_t pad;
+  int32_t npass;        // 128-row passes per chunk: ceil(C * G / 128)
+  int32_t pad2;
   int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token
   int32_t seq_len[kMaxSeqPerLaunch];       // new tokens of the sequence
   int32_t seg_base[kMaxSeqPerLaunch + 1];  // first segment (within the group) of the sequence
+  int32_t wg_base[kMaxSeqPerLaunch + 1];   // first (chunk, pass) workgroup of the sequence
 };
 
 struct PrefillWorkspace {
@@ -288,9 +323,8 @@ inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hq, int Hkv, int
   w.hk = take(size_t(B) * Hkv * Wcap * d * esize);
   w.hv = take(size_t(B) * Hkv * Wcap * d * esize);
   w.hphk = take(linear ? size_t(B) * Hkv * Wcap * Df * esize : 0);
-  // segments: seg_len >= T*Hkv/kSegTargetWorkgroups, so there are at most
-  // kSegTargetWorkgroups/Hkv + B of them
-  w.seg = take(linear ? (size_t(kSegTargetWorkgroups) + size_t(B) * Hkv) * (size_t(Df) * d + Df) * 4 : 0);
+  // segments of kSegChunks chunks of at least 32 tokens: at most T/128 + B of them
+  w.seg = take(linear ? (size_t(T) / (32 * kSegChunks) + B) * Hkv * (size_t(Df) * d + Df) * 4 : 0);
   w.total = off;
   return w;
 }

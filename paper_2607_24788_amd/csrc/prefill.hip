@@ -32,7 +32,6 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kPad = 8;  // LDS row padding (elements)
 constexpr float kLog2e = 1.4426950408889634f;
 
 // Rows of one (sequence, KV head) of a layer: new tokens come from the
@@ -97,23 +96,12 @@ __device__ __forceinline__ void store8(float* dst, const Frag<float>& f) {
   reinterpret_cast<float4*>(dst)[0] = make_float4(f.v[0], f.v[1], f.v[2], f.v[3]);
   reinterpret_cast<float4*>(dst)[1] = make_float4(f.v[4], f.v[5], f.v[6], f.v[7]);
 }
-__device__ __forceinline__ void store_t8(bf16_t* dst, int stride, const Frag<bf16_t>& f) {
-  const uint32_t w[4] = {f.v.x, f.v.y, f.v.z, f.v.w};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    dst[(2 * e) * stride] = bf16_t(w[e] & 0xffffu);
-    dst[(2 * e + 1) * stride] = bf16_t(w[e] >> 16);
-  }
-}
-__device__ __forceinline__ void store_t8(float* dst, int stride, const Frag<float>& f) {
-#pragma unroll
-  for (int e = 0; e < 8; ++e) dst[e * stride] = f.v[e];
-}
-
-// Stage 32 token rows of NC elements into LDS: natural [32][NC + kPad] and/or
-// transposed [NC][32 + kPad].  row(r) gives the row pointer, nullptr = zeros.
+// Stage 32 token rows of NC elements into LDS, natural layout [32][rs].
+// row(r) gives the row pointer, nullptr = zeros.  Contractions over the rows
+// read them back with load_colfrag (transposing reads), so no transposed copy
+// is ever written.
 template <typename T, int NC, typename RowFn>
-__device__ __forceinline__ void stage32(T* nat, T* trans, RowFn row) {
+__device__ __forceinline__ void stage32(T* nat, int rs, RowFn row) {
   constexpr int CPR = NC / 8;
   for (int id = threadIdx.x; id < 32 * CPR; id += kThreads) {
     const int r = id / CPR, ch = id - r * CPR;
@@ -121,10 +109,15 @@ __device__ __forceinline__ void stage32(T* nat, T* trans, RowFn row) {
     Frag<T> f;
     if (src) f.load(src + 8 * ch);
     else f.zero();
-    if (nat) store8(nat + r * (NC + kPad) + 8 * ch, f);
-    if (trans) store_t8(trans + (8 * ch) * (32 + kPad) + r, 32 + kPad, f);
+    store8(nat + r * rs + 8 * ch, f);
   }
 }
+
+// LDS row strides (elements): tiles read with 16-byte fragment loads use a
+// padding of 8; tiles read with load_colfrag use 16 so the four rows a
+// 16-lane group touches fall on distinct banks.
+template <int N> constexpr int row_a() { return N + 8; }
+template <int N> constexpr int row_t() { return N + 16; }
 
 // ---------------------------------------------------------------------------
 // gather: history tokens [h0, p0) of a continuing prefill, ring -> [b][g][W][d]
@@ -156,9 +149,10 @@ template <typename T, int D, int DF>
 __global__ __launch_bounds__(kThreads) void prefill_segsum(PrefillArgs a) {
   constexpr int CT = D / 16;
   constexpr int FTW = DF / 16 / kWaves;  // feature tiles per wave
+  constexpr int PROW = row_t<DF>(), VROW = row_t<D>();
   extern __shared__ __align__(16) char smem[];
-  T* pkT = reinterpret_cast<T*>(smem);      // [DF][32 + kPad]
-  T* vT = pkT + DF * (32 + kPad);           // [D][32 + kPad]
+  T* pk = reinterpret_cast<T*>(smem);       // [32][PROW]  phi(k) of 32 delayed keys
+  T* vs = pk + 32 * PROW;                   // [32][VROW]  their values
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hq = lane & 15, lg = lane >> 4;
   const int sg = blockIdx.x, g = blockIdx.y;
   const int bl = find_seq(a, sg);
@@ -176,23 +170,23 @@ __global__ __launch_bounds__(kThreads) void prefill_segsum(PrefillArgs a) {
   float zinc = 0.f;
   for (int64_t j0 = jlo; j0 < jhi; j0 += 32) {
     __syncthreads();
-    stage32<T, DF>(nullptr, pkT, [&](int r) { return j0 + r < jhi ? sr.phk(j0 + r) : nullptr; });
-    stage32<T, D>(nullptr, vT, [&](int r) { return j0 + r < jhi ? sr.v(j0 + r) : nullptr; });
+    stage32<T, DF>(pk, PROW, [&](int r) { return j0 + r < jhi ? sr.phk(j0 + r) : nullptr; });
+    stage32<T, D>(vs, VROW, [&](int r) { return j0 + r < jhi ? sr.v(j0 + r) : nullptr; });
     __syncthreads();
 #pragma unroll
     for (int x = 0; x < FTW; ++x) {
       Frag<T> fa;
-      fa.load(pkT + (16 * (wave * FTW + x) + hq) * (32 + kPad) + 8 * lg);
+      load_colfrag(fa, pk, PROW, 8 * lg, 16 * (wave * FTW + x));
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct) {
         Frag<T> fb;
-        fb.load(vT + (16 * ct + hq) * (32 + kPad) + 8 * lg);
+        load_colfrag(fb, vs, VROW, 8 * lg, 16 * ct);
         sacc[x][ct] = mma(fa, fb, sacc[x][ct]);
       }
     }
     if (tid < DF) {
 #pragma unroll 8
-      for (int r = 0; r < 32; ++r) zinc += to_f32(pkT[tid * (32 + kPad) + r]);
+      for (int r = 0; r < 32; ++r) zinc += to_f32(pk[r * PROW + tid]);
     }
   }
   float* rec = a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
@@ -228,49 +222,90 @@ __global__ __launch_bounds__(kThreads) void prefill_scan(PrefillArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// main: outputs of one segment
+// main: the outputs of one (chunk, 128-row pass) of one (sequence, KV head)
+//
+//   1. S_c, z_c: the segment-start record plus the delayed keys of the
+//      segment's earlier chunks (MFMA), kept in LDS in the element type as
+//      S^T for the read-out;
+//   2. linear part of each query row: phi(q).S_c plus the masked block of the
+//      chunk's own delayed keys; it becomes the row's online-softmax start
+//      (pseudo-key of weight a, value A/a);
+//   3. banded window attention over 32-key tiles staged in LDS, the next
+//      tile's global loads in flight while the current one computes;
+//   4. O = acc / l.
 template <typename T, int D, int DF>
-__global__ __launch_bounds__(kThreads) void prefill_main(PrefillArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void prefill_main(PrefillArgs a) {
   constexpr int KS = D / 32, KSF = DF / 32, CT = D / 16;
   constexpr int FTW = DF / 16 / kWaves;
-  constexpr int SROW = DF + kPad;  // sT row stride
+  constexpr int SROW = row_a<DF>();           // sT row stride
+  constexpr int KROW = row_a<D>(), VROW = row_t<D>(), PROW = row_t<DF>();
+  constexpr int BAND = 32 * KROW + 32 * VROW;  // one band buffer (elements)
+  constexpr int CPR = D / 8;                  // 8-element chunks per K/V row
+  constexpr int NLD = 32 * CPR / kThreads;    // chunks per thread per tile (K and V each)
+  static_assert(NLD * kThreads == 32 * CPR, "tile staging must divide evenly");
   extern __shared__ __align__(16) char smem[];
-  T* sT = reinterpret_cast<T*>(smem);                                        // [D][DF + kPad]: S^T
+  T* sT = reinterpret_cast<T*>(smem);                                        // [D][SROW]
   float* zs = reinterpret_cast<float*>(smem + size_t(D) * SROW * sizeof(T));  // [DF]
   T* reg = reinterpret_cast<T*>(smem + size_t(D) * SROW * sizeof(T) + DF * 4);
-  // band tiles
-  T* kt = reg;                        // [32][D + kPad]
-  T* vt = kt + 32 * (D + kPad);       // [D][32 + kPad]
-  // chunk slab (aliases the band tiles)
-  T* pk = reg;                        // [32][DF + kPad]
-  T* pkT = pk + 32 * (DF + kPad);     // [DF][32 + kPad]
-  T* vT = pkT + DF * (32 + kPad);     // [D][32 + kPad]
+  T* pk = reg;                        // slab: phi(k) of 32 delayed keys [32][PROW]
+  T* vs = pk + 32 * PROW;             //       their values               [32][VROW]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hq = lane & 15, lg = lane >> 4;
-  const int sg = blockIdx.x, g = blockIdx.y;
-  const int bl = find_seq(a, sg);
-  const SeqRows<T, D, DF> sr = seq_rows<T, D, DF>(a, bl, g);
-  const int sigma = sg - a.seg_base[bl];
-  const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
+  const int wgi = blockIdx.x, g = blockIdx.y;
+  int bl = 0;
+  while (bl + 1 < a.nseq && a.wg_base[bl + 1] <= wgi) ++bl;
+  const int local = wgi - a.wg_base[bl];
+  const int chunk = local / a.npass, pass = local - chunk * a.npass;
+  const int Tb = a.seq_len[bl];
+  const int c0 = chunk * a.C, c1 = min(Tb, c0 + a.C);
   const int G = a.G, W = a.W;
+  const int rows = (c1 - c0) * G;
+  if (128 * pass >= rows) return;
+  const SeqRows<T, D, DF> sr = seq_rows<T, D, DF>(a, bl, g);
   const bool linear = a.linear != 0;
   const float sc2 = a.tau * kLog2e;
-  const T* Q = static_cast<const T*>(a.q);
-  const T* PQ = static_cast<const T*>(a.phq);
-  T* O = static_cast<T*>(a.out);
+  const int64_t t0 = sr.p0 + c0;  // absolute position of the chunk's first token
+  const int r_end = min(rows, 128 * (pass + 1));
+  const int ti_min = (128 * pass) / G, ti_max = (r_end - 1) / G;  // chunk-relative tokens of the pass
 
-  // S carried across the segment's chunks: wave w owns feature tiles
-  // w*FTW .. w*FTW+FTW-1 (rows f), all column tiles (c).
-  f32x4_t sacc[FTW][CT];
+  // ---- 1. S_c and z_c
   if (linear) {
-    const float* S0 = a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
+    const int sigma = c0 / a.seg_len;
+    const float* S0 = a.seg + (int64_t(a.seg0 + a.seg_base[bl] + sigma) * a.Hkv + g) * (int64_t(DF) * D + DF);
+    f32x4_t sacc[FTW][CT];
 #pragma unroll
     for (int x = 0; x < FTW; ++x)
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
         for (int i = 0; i < 4; ++i) sacc[x][ct][i] = S0[(16 * (wave * FTW + x) + 4 * lg + i) * D + 16 * ct + hq];
-    for (int f = tid; f < DF; f += kThreads) zs[f] = S0[DF * D + f];
+    float zacc = tid < DF ? S0[DF * D + tid] : 0.f;
+    // delayed keys of the segment's earlier chunks: j in [p0 + sigma*seg_len - W, t0 - W)
+    int64_t jlo = sr.p0 + int64_t(sigma) * a.seg_len - W;
+    const int64_t jhi = t0 - W;
+    if (jlo < 0) jlo = 0;
+    for (int64_t j0 = jlo; j0 < jhi; j0 += 32) {
+      __syncthreads();
+      stage32<T, DF>(pk, PROW, [&](int r) { return j0 + r < jhi ? sr.phk(j0 + r) : nullptr; });
+      stage32<T, D>(vs, VROW, [&](int r) { return j0 + r < jhi ? sr.v(j0 + r) : nullptr; });
+      __syncthreads();
+#pragma unroll
+      for (int x = 0; x < FTW; ++x) {
+        Frag<T> fa;
+        load_colfrag(fa, pk, PROW, 8 * lg, 16 * (wave * FTW + x));
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          Frag<T> fb;
+          load_colfrag(fb, vs, VROW, 8 * lg, 16 * ct);
+          sacc[x][ct] = mma(fa, fb, sacc[x][ct]);
+        }
+      }
+      if (tid < DF) {
+#pragma unroll 8
+        for (int r = 0; r < 32; ++r) zacc += to_f32(pk[r * PROW + tid]);
+      }
+    }
 #pragma unroll
     for (int x = 0; x < FTW; ++x)
 #pragma unroll
@@ -278,251 +313,249 @@ __global__ __launch_bounds__(kThreads) void prefill_main(PrefillArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           sT[(16 * ct + hq) * SROW + 16 * (wave * FTW + x) + 4 * lg + i] = from_f32<T>(sacc[x][ct][i]);
+    if (tid < DF) zs[tid] = zacc;
   }
   __syncthreads();
 
-  for (int c0 = s_lo; c0 < s_hi; c0 += a.C) {
-    const int c1 = min(s_hi, c0 + a.C);
-    const int64_t t0 = sr.p0 + c0;  // absolute position of the chunk's first token
-    const int rows = (c1 - c0) * G;
-    const int npass = (rows + 127) / 128;
-    float zinc = 0.f;
-    for (int pass = 0; pass < npass; ++pass) {
-      const bool last = pass == npass - 1;
-      const int r_end = min(rows, 128 * (pass + 1));
-      const int ti_min = (128 * pass) / G, ti_max = (r_end - 1) / G;  // chunk-relative tokens of the pass
-      // this lane's query row in the score layout, per q-tile
-      int ti[2], hh[2];
-      bool rv[2];
+  // this lane's query rows (score layout: row = hq of each 16-row q-tile)
+  int ti[2], hh[2];
+  bool rv[2];
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        const int r = 128 * pass + 32 * wave + 16 * qt + hq;
-        rv[qt] = r < rows;
-        const int rr = rv[qt] ? r : 128 * pass;
-        ti[qt] = rr / G;
-        hh[qt] = rr - ti[qt] * G;
-      }
-      f32x4_t acc[2][CT];
+  for (int qt = 0; qt < 2; ++qt) {
+    const int r = 128 * pass + 32 * wave + 16 * qt + hq;
+    rv[qt] = r < rows;
+    const int rr = rv[qt] ? r : 128 * pass;
+    ti[qt] = rr / G;
+    hh[qt] = rr - ti[qt] * G;
+  }
+  f32x4_t acc[2][CT];
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
+  for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[qt][ct] = zero4();
-      float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    for (int ct = 0; ct < CT; ++ct) acc[qt][ct] = zero4();
+  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
 
-      if (linear) {
-        Frag<T> pqf[2][KSF];
+  // ---- 2. linear part
+  if (linear) {
+    const T* PQ = static_cast<const T*>(a.phq);
+    Frag<T> pqf[2][KSF];
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
+    for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-          for (int kk = 0; kk < KSF; ++kk) pqf[qt][kk].load(PQ + sr.qrow(c0 + ti[qt], hh[qt]) * DF + 32 * kk + 8 * lg);
-        // read-out phi(q) . S_c
+      for (int kk = 0; kk < KSF; ++kk) pqf[qt][kk].load(PQ + sr.qrow(c0 + ti[qt], hh[qt]) * DF + 32 * kk + 8 * lg);
 #pragma unroll
-        for (int kk = 0; kk < KSF; ++kk) {
+    for (int kk = 0; kk < KSF; ++kk) {
 #pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            Frag<T> fb;
-            fb.load(sT + (16 * ct + hq) * SROW + 32 * kk + 8 * lg);
+      for (int ct = 0; ct < CT; ++ct) {
+        Frag<T> fb;
+        fb.load(sT + (16 * ct + hq) * SROW + 32 * kk + 8 * lg);
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pqf[qt][kk], fb, acc[qt][ct]);
-          }
-        }
-        float den[2];
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          float dz = 0.f;
-#pragma unroll
-          for (int kk = 0; kk < KSF; ++kk) {
-            // phi(q)_f * z_f over this lane's 8 features of the slab
-            float qv[8];
-            pqf[qt][kk].to_floats(qv);
-            const float* zz = zs + 32 * kk + 8 * lg;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) dz = fmaf(qv[e], zz[e], dz);
-          }
-          den[qt] = dz;
-        }
-        // intra-chunk block: delayed keys i' in [0, ti], j = t0 - W + i'
-        for (int s0 = 0; s0 <= ti_max; s0 += 32) {
-          __syncthreads();
-          const int nk = c1 - c0;
-          auto key = [&](int r) -> int64_t { return t0 - W + s0 + r; };
-          stage32<T, DF>(pk, last ? pkT : nullptr, [&](int r) {
-            return (s0 + r < nk && key(r) >= 0) ? sr.phk(key(r)) : nullptr;
-          });
-          stage32<T, D>(nullptr, vT, [&](int r) { return (s0 + r < nk && key(r) >= 0) ? sr.v(key(r)) : nullptr; });
-          __syncthreads();
-          f32x4_t sc[2][2];
-#pragma unroll
-          for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
-#pragma unroll
-          for (int t = 0; t < 2; ++t) {
-#pragma unroll
-            for (int kk = 0; kk < KSF; ++kk) {
-              Frag<T> fa;
-              fa.load(pk + (8 * (hq >> 2) + 4 * t + (hq & 3)) * (DF + kPad) + 32 * kk + 8 * lg);
-#pragma unroll
-              for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, pqf[qt][kk], sc[qt][t]);
-            }
-          }
-          Frag<T> pf[2];
-#pragma unroll
-          for (int qt = 0; qt < 2; ++qt) {
-            float pv[8];
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) pv[4 * t + i] = (s0 + 8 * lg + 4 * t + i <= ti[qt]) ? sc[qt][t][i] : 0.f;
-            pf[qt].set8(pv);
-            den[qt] += pf[qt].sum();
-          }
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            Frag<T> fb;
-            fb.load(vT + (16 * ct + hq) * (32 + kPad) + 8 * lg);
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pf[qt], fb, acc[qt][ct]);
-          }
-          if (last) {
-            // the chunk's state increment (all delayed keys are covered by the last pass)
-#pragma unroll
-            for (int x = 0; x < FTW; ++x) {
-              Frag<T> fa;
-              fa.load(pkT + (16 * (wave * FTW + x) + hq) * (32 + kPad) + 8 * lg);
-#pragma unroll
-              for (int ct = 0; ct < CT; ++ct) {
-                Frag<T> fb;
-                fb.load(vT + (16 * ct + hq) * (32 + kPad) + 8 * lg);
-                sacc[x][ct] = mma(fa, fb, sacc[x][ct]);
-              }
-            }
-            if (tid < DF) {
-#pragma unroll 8
-              for (int r = 0; r < 32; ++r) zinc += to_f32(pkT[tid * (32 + kPad) + r]);
-            }
-          }
-        }
-        // the linear part as the starting state of the online softmax
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          float dn = den[qt];
-          dn += __shfl_xor(dn, 16);
-          dn += __shfl_xor(dn, 32);
-          m_run[qt] = dn > 0.f ? log2f(dn) : -INFINITY;
-          l_run[qt] = (dn > 0.f && lg == 0) ? 1.f : 0.f;
-          const float inv = dn > 0.f ? 1.f / dn : 0.f;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float ir = __shfl(inv, 4 * lg + i);
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct) acc[qt][ct][i] *= ir;
-          }
-        }
-      }
-
-      // banded window attention, keys [t0 + ti_min - W + 1, t0 + ti_max]
-      if (W > 0) {
-        Frag<T> qf[2][KS];
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-          for (int kk = 0; kk < KS; ++kk) qf[qt][kk].load(Q + sr.qrow(c0 + ti[qt], hh[qt]) * D + 32 * kk + 8 * lg);
-        int64_t klo = t0 + ti_min - W + 1;
-        if (klo < 0) klo = 0;
-        const int64_t khi = t0 + ti_max;
-        for (int64_t kb = klo & ~int64_t(31); kb <= khi; kb += 32) {
-          __syncthreads();
-          stage32<T, D>(kt, nullptr, [&](int r) { return (kb + r >= klo && kb + r <= khi) ? sr.k(kb + r) : nullptr; });
-          stage32<T, D>(nullptr, vt, [&](int r) { return (kb + r >= klo && kb + r <= khi) ? sr.v(kb + r) : nullptr; });
-          __syncthreads();
-          f32x4_t sc[2][2];
-#pragma unroll
-          for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
-#pragma unroll
-          for (int t = 0; t < 2; ++t) {
-#pragma unroll
-            for (int kk = 0; kk < KS; ++kk) {
-              Frag<T> fa;
-              fa.load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * (D + kPad) + 32 * kk + 8 * lg);
-#pragma unroll
-              for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
-            }
-          }
-          Frag<T> pf[2];
-#pragma unroll
-          for (int qt = 0; qt < 2; ++qt) {
-            const int64_t tq = t0 + ti[qt];
-            float s[8];
-            float mx = -INFINITY;
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const int64_t j = kb + 8 * lg + 4 * t + i;
-                const bool ok = rv[qt] && j >= klo && j <= tq && j > tq - W;
-                const float v = ok ? sc[qt][t][i] * sc2 : -INFINITY;
-                s[4 * t + i] = v;
-                mx = fmaxf(mx, v);
-              }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run[qt], mx);
-            const float m_use = m_new == -INFINITY ? 0.f : m_new;
-            const float alpha = exp2f(m_run[qt] - m_use);
-            float pv[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) pv[i] = exp2f(s[i] - m_use);
-            pf[qt].set8(pv);
-            l_run[qt] = l_run[qt] * alpha + pf[qt].sum();
-            m_run[qt] = m_new;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const float al = __shfl(alpha, 4 * lg + i);
-#pragma unroll
-              for (int ct = 0; ct < CT; ++ct) acc[qt][ct][i] *= al;
-            }
-          }
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            Frag<T> fb;
-            fb.load(vt + (16 * ct + hq) * (32 + kPad) + 8 * lg);
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pf[qt], fb, acc[qt][ct]);
-          }
-        }
-      }
-
-      // outputs of this pass
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        float ls = l_run[qt];
-        ls += __shfl_xor(ls, 16);
-        ls += __shfl_xor(ls, 32);
-        const float inv = ls > 0.f ? 1.f / ls : 0.f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float ir = __shfl(inv, 4 * lg + i);
-          const int r = 128 * pass + 32 * wave + 16 * qt + 4 * lg + i;
-          if (r < rows) {
-            const int tr = r / G, hr = r - tr * G;
-            T* orow = O + sr.qrow(c0 + tr, hr) * D;
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct) orow[16 * ct + hq] = from_f32<T>(acc[qt][ct][i] * ir);
-          }
-        }
+        for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pqf[qt][kk], fb, acc[qt][ct]);
       }
     }
-    // next chunk's state: S^T copy and z
-    if (linear) {
+    float den[2];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float dz = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < KSF; ++kk) {
+        float qv[8];
+        pqf[qt][kk].to_floats(qv);
+        const float* zz = zs + 32 * kk + 8 * lg;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dz = fmaf(qv[e], zz[e], dz);
+      }
+      den[qt] = dz;
+    }
+    // the chunk's own delayed keys i' in [0, ti], key j = t0 - W + i'
+    const int nk = c1 - c0;
+    for (int s0 = 0; s0 <= ti_max; s0 += 32) {
       __syncthreads();
-      if (tid < DF) zs[tid] += zinc;
-#pragma unroll
-      for (int x = 0; x < FTW; ++x)
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            sT[(16 * ct + hq) * SROW + 16 * (wave * FTW + x) + 4 * lg + i] = from_f32<T>(sacc[x][ct][i]);
+      stage32<T, DF>(pk, PROW, [&](int r) {
+        const int64_t j = t0 - W + s0 + r;
+        return (s0 + r < nk && j >= 0) ? sr.phk(j) : nullptr;
+      });
+      stage32<T, D>(vs, VROW, [&](int r) {
+        const int64_t j = t0 - W + s0 + r;
+        return (s0 + r < nk && j >= 0) ? sr.v(j) : nullptr;
+      });
       __syncthreads();
+      f32x4_t sc[2][2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+#pragma unroll
+        for (int kk = 0; kk < KSF; ++kk) {
+          Frag<T> fa;
+          fa.load(pk + (8 * (hq >> 2) + 4 * t + (hq & 3)) * PROW + 32 * kk + 8 * lg);
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, pqf[qt][kk], sc[qt][t]);
+        }
+      }
+      Frag<T> pf[2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        float pv[8];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) pv[4 * t + i] = (s0 + 8 * lg + 4 * t + i <= ti[qt]) ? sc[qt][t][i] : 0.f;
+        pf[qt].set8(pv);
+        den[qt] += pf[qt].sum();
+      }
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        Frag<T> fb;
+        load_colfrag(fb, vs, VROW, 8 * lg, 16 * ct);
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pf[qt], fb, acc[qt][ct]);
+      }
+    }
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float dn = den[qt];
+      dn += __shfl_xor(dn, 16);
+      dn += __shfl_xor(dn, 32);
+      m_run[qt] = dn > 0.f ? log2f(dn) : -INFINITY;
+      l_run[qt] = (dn > 0.f && lg == 0) ? 1.f : 0.f;
+      const float inv = dn > 0.f ? 1.f / dn : 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float ir = __shfl(inv, 4 * lg + i);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[qt][ct][i] *= ir;
+      }
+    }
+  }
+
+  // ---- 3. banded window attention, keys [t0 + ti_min - W + 1, t0 + ti_max]
+  if (W > 0) {
+    const T* Q = static_cast<const T*>(a.q);
+    Frag<T> qf[2][KS];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) qf[qt][kk].load(Q + sr.qrow(c0 + ti[qt], hh[qt]) * D + 32 * kk + 8 * lg);
+    int64_t klo = t0 + ti_min - W + 1;
+    if (klo < 0) klo = 0;
+    const int64_t khi = t0 + ti_max;
+    const int64_t kb0 = klo & ~int64_t(31);
+    const int ntile = int((khi - kb0) / 32) + 1;
+    // staging registers: this thread's chunks of the next tile
+    Frag<T> sk[NLD], sv[NLD];
+    auto fetch = [&](int n) {
+      const int64_t kb = kb0 + 32 * int64_t(n);
+#pragma unroll
+      for (int u = 0; u < NLD; ++u) {
+        const int id = tid + u * kThreads, r = id / CPR, ch = id - r * CPR;
+        const int64_t j = kb + r;
+        const bool ok = j >= klo && j <= khi;
+        if (ok) {
+          sk[u].load(sr.k(j) + 8 * ch);
+          sv[u].load(sr.v(j) + 8 * ch);
+        } else {
+          sk[u].zero();
+          sv[u].zero();
+        }
+      }
+    };
+    auto store = [&](int buf) {
+      T* kt = reg + buf * BAND;
+      T* vt = kt + 32 * KROW;
+#pragma unroll
+      for (int u = 0; u < NLD; ++u) {
+        const int id = tid + u * kThreads, r = id / CPR, ch = id - r * CPR;
+        store8(kt + r * KROW + 8 * ch, sk[u]);
+        store8(vt + r * VROW + 8 * ch, sv[u]);
+      }
+    };
+    __syncthreads();  // the slab region is free again
+    fetch(0);
+    store(0);
+    __syncthreads();
+    for (int n = 0; n < ntile; ++n) {
+      if (n + 1 < ntile) fetch(n + 1);
+      const T* kt = reg + (n & 1) * BAND;
+      const T* vt = kt + 32 * KROW;
+      const int64_t kb = kb0 + 32 * int64_t(n);
+      f32x4_t sc[2][2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          Frag<T> fa;
+          fa.load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * KROW + 32 * kk + 8 * lg);
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
+        }
+      }
+      Frag<T> pf[2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const int64_t tq = t0 + ti[qt];
+        float sv8[8];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int64_t j = kb + 8 * lg + 4 * t + i;
+            const bool ok = rv[qt] && j >= klo && j <= tq && j > tq - W;
+            const float v = ok ? sc[qt][t][i] * sc2 : -INFINITY;
+            sv8[4 * t + i] = v;
+            mx = fmaxf(mx, v);
+          }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run[qt], mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = exp2f(m_run[qt] - m_use);
+        float pv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pv[i] = exp2f(sv8[i] - m_use);
+        pf[qt].set8(pv);
+        l_run[qt] = l_run[qt] * alpha + pf[qt].sum();
+        m_run[qt] = m_new;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float al = __shfl(alpha, 4 * lg + i);
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) acc[qt][ct][i] *= al;
+        }
+      }
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        Frag<T> fb;
+        load_colfrag(fb, vt, VROW, 8 * lg, 16 * ct);
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pf[qt], fb, acc[qt][ct]);
+      }
+      if (n + 1 < ntile) store((n + 1) & 1);
+      __syncthreads();
+    }
+  }
+
+  // ---- 4. outputs
+  T* O = static_cast<T*>(a.out);
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    float ls = l_run[qt];
+    ls += __shfl_xor(ls, 16);
+    ls += __shfl_xor(ls, 32);
+    const float inv = ls > 0.f ? 1.f / ls : 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float ir = __shfl(inv, 4 * lg + i);
+      const int r = 128 * pass + 32 * wave + 16 * qt + 4 * lg + i;
+      if (r < rows) {
+        const int tr = r / G, hr = r - tr * G;
+        T* orow = O + sr.qrow(c0 + tr, hr) * D;
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) orow[16 * ct + hq] = from_f32<T>(acc[qt][ct][i] * ir);
+      }
     }
   }
 }
@@ -565,9 +598,9 @@ __global__ void prefill_advance(PrefillArgs a) {
 
 template <typename T, int D, int DF>
 size_t main_lds() {
-  const size_t band = (size_t(32) * (D + kPad) + size_t(D) * (32 + kPad)) * sizeof(T);
-  const size_t slab = (size_t(32) * (DF + kPad) + size_t(DF) * (32 + kPad) + size_t(D) * (32 + kPad)) * sizeof(T);
-  return size_t(D) * (DF + kPad) * sizeof(T) + DF * 4 + (band > slab ? band : slab);
+  const size_t band = 2 * (size_t(32) * row_a<D>() + size_t(32) * row_t<D>()) * sizeof(T);
+  const size_t slab = (size_t(32) * row_t<DF>() + size_t(32) * row_t<D>()) * sizeof(T);
+  return size_t(D) * row_a<DF>() * sizeof(T) + DF * 4 + (band > slab ? band : slab);
 }
 
 template <typename K>
@@ -581,7 +614,7 @@ template <typename T, int D, int DF>
 hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
   hipError_t e;
   if (a.linear && a.nseg > 0) {
-    const size_t lds_seg = (size_t(DF) * (32 + kPad) + size_t(D) * (32 + kPad)) * sizeof(T);
+    const size_t lds_seg = (size_t(32) * row_t<DF>() + size_t(32) * row_t<D>()) * sizeof(T);
     hipLaunchKernelGGL((prefill_segsum<T, D, DF>), dim3(a.nseg, a.Hkv), dim3(kThreads), lds_seg, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int E = DF * D + DF;
@@ -589,10 +622,10 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
                        dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if (a.nseg > 0) {
+  if (a.wg_base[a.nseq] > 0) {
     const size_t lds = main_lds<T, D, DF>();
     if ((e = set_lds(&prefill_main<T, D, DF>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv), dim3(kThreads), lds, s, a);
+    hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.wg_base[a.nseq], a.Hkv), dim3(kThreads), lds, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (a.W > 0) {
