@@ -77,24 +77,48 @@ __device__ __forceinline__ void phi_tile16(const T* wt, const T* row, int skk, i
   }
 }
 
+// Dense rows: persistent workgroups.  Wave w owns features
+// [w*DF/4, (w+1)*DF/4) and keeps their Wf fragments in registers for the
+// whole launch; the workgroup walks 64-row tiles (every wave reads the same
+// rows, so three of the four reads hit the L1).
 template <typename T, int D, int DF, typename OutT>
 __global__ __launch_bounds__(kThreads) void phi_rows_kernel(const T* __restrict__ Wf, const T* __restrict__ x,
                                                             int64_t rows, OutT* __restrict__ out) {
-  extern __shared__ __align__(16) char smem[];
-  T* wt = reinterpret_cast<T*>(smem);
-  stage_wf_transposed<T, D, DF>(Wf, wt);
-  __syncthreads();
+  constexpr int KS = D / 32, NTW = DF / 16 / 4;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
-  const int64_t r0 = int64_t(blockIdx.x) * 64 + 16 * wave;
-  const int64_t r = r0 + hq;
-  f32x4_t acc[DF / 16];
-  phi_tile16<T, D, DF>(wt, r < rows ? x + r * D : nullptr, 32, 8, acc);
+  const int f0 = wave * NTW * 16;
+  Frag<T> wb[KS][NTW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t ro = r0 + 4 * lg + i;
-    if (ro < rows) {
+  for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
-      for (int nt = 0; nt < DF / 16; ++nt) out[ro * DF + 16 * nt + hq] = from_f32<OutT>(fmaxf(acc[nt][i], 0.f));
+    for (int nt = 0; nt < NTW; ++nt) wb[kk][nt].load_strided(Wf + int64_t(32 * kk + 8 * lg) * DF + f0 + 16 * nt + hq, DF);
+  const int64_t ntile = (rows + 63) / 64;
+  for (int64_t tile = blockIdx.x; tile < ntile; tile += gridDim.x) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      const int64_t r0 = tile * 64 + 16 * rt;
+      const int64_t r = r0 + hq;
+      Frag<T> fa[KS];
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        if (r < rows) fa[kk].load(x + r * D + 32 * kk + 8 * lg);
+        else fa[kk].zero();
+      }
+      f32x4_t acc[NTW];
+#pragma unroll
+      for (int nt = 0; nt < NTW; ++nt) {
+        acc[nt] = zero4();
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) acc[nt] = mma(fa[kk], wb[kk][nt], acc[nt]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t ro = r0 + 4 * lg + i;
+        if (ro < rows) {
+#pragma unroll
+          for (int nt = 0; nt < NTW; ++nt) out[ro * DF + f0 + 16 * nt + hq] = from_f32<OutT>(fmaxf(acc[nt][i], 0.f));
+        }
+      }
     }
   }
 }
@@ -156,15 +180,10 @@ size_t wt_bytes() { return size_t(DF) * wt_stride<D>() * sizeof(T); }
 template <typename T, int D, int DF, typename OutT>
 hipError_t launch_rows_t(const void* Wf, const void* x, int64_t rows, void* out, hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  const dim3 grid(unsigned((rows + 63) / 64));
-  const size_t lds = wt_bytes<T, D, DF>();
-  if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&phi_rows_kernel<T, D, DF, OutT>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL((phi_rows_kernel<T, D, DF, OutT>), grid, dim3(kThreads), lds, s,
-                     static_cast<const T*>(Wf), static_cast<const T*>(x), rows, static_cast<OutT*>(out));
+  const int64_t ntile = (rows + 63) / 64;
+  const dim3 grid(unsigned(ntile < 1024 ? ntile : 1024));
+  hipLaunchKernelGGL((phi_rows_kernel<T, D, DF, OutT>), grid, dim3(kThreads), 0, s, static_cast<const T*>(Wf),
+                     static_cast<const T*>(x), rows, static_cast<OutT*>(out));
   return hipGetLastError();
 }
 

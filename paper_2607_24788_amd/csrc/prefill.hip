@@ -492,39 +492,60 @@ void prefill_main(PrefillArgs a) {
           for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
         }
       }
+      // keys [kb, kb+31] lie inside the band of every row of the pass
+      // (tokens t0+ti_min .. t0+ti_max) for all but the edge tiles
+      const bool interior = kb >= t0 + ti_max - W + 1 && kb + 31 <= t0 + ti_min;
       Frag<T> pf[2];
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
-        const int64_t tq = t0 + ti[qt];
         float sv8[8];
-        float mx = -INFINITY;
+        if (interior) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+          for (int t = 0; t < 2; ++t)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int64_t j = kb + 8 * lg + 4 * t + i;
-            const bool ok = rv[qt] && j >= klo && j <= tq && j > tq - W;
-            const float v = ok ? sc[qt][t][i] * sc2 : -INFINITY;
-            sv8[4 * t + i] = v;
-            mx = fmaxf(mx, v);
-          }
+            for (int i = 0; i < 4; ++i) sv8[4 * t + i] = sc[qt][t][i] * sc2;
+        } else {
+          // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row exists
+          const int base = int(kb - (t0 + ti[qt]));
+          const int64_t offlo = klo - kb;  // first in-band offset of the tile (<= 31)
+          const int lo = offlo < -1 ? -1 : int(offlo);
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int off = 8 * lg + 4 * t + i;
+              const bool ok = rv[qt] && off >= lo && base + off <= 0 && base + off > -W;
+              sv8[4 * t + i] = ok ? sc[qt][t][i] * sc2 : -INFINITY;
+            }
+        }
+        float mx = sv8[0];
+#pragma unroll
+        for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv8[i]);
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run[qt], mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m_run[qt] - m_use);
-        float pv[8];
+        // lazy rescale: the running max moves only when a score exceeds it by
+        // more than 2^8, so p = 2^(s - m) <= 256 and acc, l stay in range
+        if (__any(mx > m_run[qt] + 8.f)) {
+          const float m_new = fmaxf(m_run[qt], mx);
+          const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
+          l_run[qt] *= alpha;
+          m_run[qt] = m_new;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) pv[i] = exp2f(sv8[i] - m_use);
-        pf[qt].set8(pv);
-        l_run[qt] = l_run[qt] * alpha + pf[qt].sum();
-        m_run[qt] = m_new;
+          for (int i = 0; i < 4; ++i) {
+            const float al = __shfl(alpha, 4 * lg + i);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float al = __shfl(alpha, 4 * lg + i);
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) acc[qt][ct][i] *= al;
+            for (int ct = 0; ct < CT; ++ct) acc[qt][ct][i] *= al;
+          }
         }
+        const float m_use = m_run[qt] == -INFINITY ? 0.f : m_run[qt];
+        float pv[8], ps = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          pv[i] = __builtin_amdgcn_exp2f(sv8[i] - m_use);
+          ps += pv[i];
+        }
+        pf[qt].set8(pv);
+        l_run[qt] += ps;
       }
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct) {
