@@ -82,20 +82,27 @@ typedef struct {
 
 /* Position of the sections of one layer inside the state blob (bytes from the
  * blob's start).  Layout per layer l, every section 256-byte aligned:
- *   pos   int64 [B][Hkv]          tokens consumed by sequence b (equal over Hkv)
- *   S     fp32  [B][Hkv][Df][d]   sum of phi(k_j)^T v_j over tokens left of the window
+ *   pos   int64 [B][Hkv]          p: tokens consumed by sequence b (equal over Hkv)
+ *   nf    int64 [B][Hkv]          tokens folded into S and z (see below)
+ *   S     fp32  [B][Hkv][Df][d]   sum of phi(k_j)^T v_j over tokens j < nf
  *   z     fp32  [B][Hkv][Df]      sum of phi(k_j) over the same tokens
  *   kring dtype [B][Hkv][R*d]     keys, token j in slot s = j mod R
  *   vring dtype [B][Hkv][R*d]     values, token j in slot s = j mod R
- * R = ring_slots = round_up(W + 1, 32) for W > 0, 0 for W = 0.  After p tokens
- * the ring holds tokens [max(0, p - W), p - 1]; other slots are stale.
+ * Deferred folding: the linear part of the next read-out covers tokens
+ * [0, beta), beta = max(0, p - W).  Decode steps fold the tokens leaving the
+ * window in batches of up to 8 (staggered over units), so nf lies in
+ * [beta - 8, beta] (W = 0: nf = beta); tokens [nf, beta) are "pending": kept
+ * in the ring and added to the read-out from there.  glide_prefill and
+ * glide_state_flush leave nf = beta.  R = ring_slots = round_up(W + 8, 32)
+ * for W > 0, 0 for W = 0.  After p tokens the ring holds tokens [nf, p - 1]
+ * (W > 0); other slots are stale.
  * Both rings are stored in 32-slot blocks of 32*d elements, in the fragment
  * order of the decode kernel's matrix-core loads; with o = s % 32, block
  * s / 32, element c of the slot is at (within the block)
  *   kring: [(o/4)%2][c/32][(c/8)%4][4*(o/8) + o%4][c%8]
  *   vring: [c/16][o/8][c%16][o%8]                                          */
 typedef struct {
-  int64_t pos_offset, s_offset, z_offset, kring_offset, vring_offset;
+  int64_t pos_offset, nf_offset, s_offset, z_offset, kring_offset, vring_offset;
   int64_t layer_offset, layer_bytes;
   int32_t window;      /* W_l */
   int32_t ring_slots;  /* R_l */
@@ -108,15 +115,13 @@ size_t glide_state_bytes(const glide_config* cfg);
 glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_layer_layout* out);
 
 /* Workspace bytes needed by glide_prefill for calls with at most
- * max_total_tokens packed tokens (any chunk size), and by glide_decode_step
- * for any layer range (the feature-map rows of every (layer, sequence, KV
- * head): n_layers * B * Hkv * (G+1) * Df * 4 bytes, or nothing without the
- * linear part).  0 if cfg is invalid. */
+ * max_total_tokens packed tokens (any chunk size); at least 256.
+ * glide_decode_step needs none.  0 if cfg is invalid. */
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens);
 
 /* Zeroes the whole state: S = 0, z = 0 (S_0, Z_0 of the Sec. II-B
- * recurrence), pos = 0, ring contents 0.  state: device, 256-byte aligned,
- * state_bytes >= glide_state_bytes(cfg). */
+ * recurrence), pos = nf = 0, ring contents 0.  state: device, 256-byte
+ * aligned, state_bytes >= glide_state_bytes(cfg). */
 glide_status glide_state_init(const glide_config* cfg, void* state, size_t state_bytes, void* stream);
 
 /* Prefill (KV-cache population stage, Appendix "KV Cache"): appends
@@ -125,8 +130,9 @@ glide_status glide_state_init(const glide_config* cfg, void* state, size_t state
  * legal), for layers [layer0, layer0 + n_layers), and writes one output per
  * appended token.  Within a layer the work is chunked: chunk C query tokens
  * share one softmax band pass and one state read-out (chunk = 0 -> 64; any
- * C in [16, 256] that is a multiple of 16 gives the same result up to
- * rounding).
+ * C in [32, 256] that is a multiple of 32 gives the same result up to
+ * rounding).  Pending tokens are folded first (as glide_state_flush); on
+ * return nf = max(0, p - W).
  *   phi_w  device [n_layers][d][Df]        (layer layer0 first)
  *   q      device [n_layers][T][Hq][d]     T = total_tokens, packed by sequence
  *   k, v   device [n_layers][T][Hkv][d]
@@ -142,22 +148,29 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
 
 /* Decode (Appendix "KV Cache", decode stage): appends exactly one token to
  * every sequence for layers [layer0, layer0 + n_layers).  Per (layer,
- * sequence, KV head), in this order: fold the token leaving the window into
- * S and z (token p - W when p >= W; the new token itself when W = 0), write
- * the new key/value into its ring slot, read out O for the G query heads of
- * the group from the window and the updated state, pos += 1.  Sequences may
- * sit at different positions (pos lives in the state).
+ * sequence, KV head): the token leaving the window (token p - W when p >= W;
+ * the new token itself when W = 0) joins the linear part, the new key/value
+ * is written into its ring slot, O is read out for the G query heads of the
+ * group from the window and from S + the pending tokens, pos += 1; on the
+ * unit's fold step (one in 8; every step when W = 0) the pending tokens are
+ * folded into S and z.  Sequences may sit at different positions (pos lives
+ * in the state).  One kernel is enqueued.
  *   phi_w  device [n_layers][d][Df]
  *   q      device [n_layers][B][Hq][d];  k, v device [n_layers][B][Hkv][d]
  *   out    device [n_layers][B][Hq][d]
- *   workspace device, 256-byte aligned, >= glide_workspace_bytes(cfg, 0)
- *             (may be NULL when the linear part is off)
- * Two kernels are enqueued: the feature map of the G query heads and of the
- * key leaving the window, then the fused window/state pass. */
+ *   workspace  unused (may be NULL; kept for future use) */
 glide_status glide_decode_step(const glide_config* cfg, void* state, size_t state_bytes,
                                int32_t layer0, int32_t n_layers, const void* phi_w,
                                const void* q, const void* k, const void* v, void* out,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Folds every pending token of layers [layer0, layer0 + n_layers) into S and
+ * z (nf := max(0, p - W)), so that S and z hold exactly the Sec. II-B sums
+ * over the linear part of the next token.  Outputs of later steps are
+ * unchanged up to rounding.  phi_w device [n_layers][d][Df] (layer layer0
+ * first).  Nothing to do without the linear part. */
+glide_status glide_state_flush(const glide_config* cfg, void* state, size_t state_bytes,
+                               int32_t layer0, int32_t n_layers, const void* phi_w, void* stream);
 
 /* The feature map alone (kernel (d)): out[r][f] = max(0, sum_c x[r][c] Wf[c][f])
  * for r < rows, accumulated in fp32.  x device [rows][d], phi_w device [d][Df]

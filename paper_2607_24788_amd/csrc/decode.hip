@@ -1,19 +1,21 @@
 // GLIDE decode step: one fused pass per (layer, sequence, KV head).
 //
-// Per unit, in the order of the layer definition (GLIDE Sec. III-B; state
-// recurrence of Sec. II-B applied to the token leaving the window):
+// Per unit (GLIDE Sec. III-B; the state recurrence of Sec. II-B applied to
+// the tokens that have left the window):
 //   1. the new key/value is written to ring slot p mod R;
-//   2. state: the token leaving the window (token p - W, or the new token when
-//      W = 0) is folded, S += phi(k_e)^T v_e, z += phi(k_e), in place, and the
-//      read-out phi(q_h).S, phi(q_h).z is taken from the updated rows in the
-//      same pass over S.  phi of the G query heads and of k_e comes from the
-//      feature-map kernel that runs just before (decode workspace);
-//   3. window: the W most recent tokens (ring tokens p-W+1 .. p-1 plus the new
+//   2. phi of the G query heads and of the pending keys (tokens that have
+//      left the window but are not yet folded into S, z) on MFMA against Wf,
+//      each wave producing the features of the state rows it owns;
+//   3. state: S' = S + sum_pending phi(k_j)^T v_j (and z') in registers, the
+//      read-out phi(q_h).S', phi(q_h).z' from the same pass over S; on the
+//      unit's fold step S', z' are written back (deferred folding: at most
+//      one write of the state per kFoldPeriod steps);
+//   4. window: the W most recent tokens (ring tokens p-W+1 .. p-1 plus the new
 //      token taken straight from the input) are streamed in 32-token tiles,
 //      the next tile's loads in flight while the current one is computed;
 //      QK^T and PV run on MFMA with the G query heads of the group as the
 //      16-wide tile dimension; online softmax in the log2 domain;
-//   4. merge of the two parts over one shared denominator, output, pos += 1.
+//   5. merge of the two parts over one shared denominator, output, pos += 1.
 //
 // One workgroup of 4 waves handles one unit; units of the call are ordered by
 // decreasing window so the longest streams start first.
@@ -58,11 +60,12 @@ void decode_kernel(DecodeArgs a) {
   constexpr int KS = D / 32;       // 32-wide k slabs over the head dim
   constexpr int CT = D / 16;       // 16-wide column tiles of the output
   constexpr int RW = DF / kWaves;  // state rows (features) per wave
+  constexpr int NTW = RW / 16;     // 16-feature tiles per wave
   constexpr int LPR = D / 4;       // lanes per state row (4 floats each)
   constexpr int RPS = 64 / LPR;    // state rows per wave step
   constexpr int STEPS = RW / RPS;
   constexpr bool kTwoStages = sizeof(T) == 2 && GLIDE_DECODE_STAGES == 2;
-  static_assert(STEPS * RPS == RW, "state rows must tile the wave");
+  static_assert(STEPS * RPS == RW && NTW * 16 == RW, "state rows must tile the wave");
 
   extern __shared__ __align__(16) char smem[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -78,6 +81,7 @@ void decode_kernel(DecodeArgs a) {
   char* lay = a.state + L.base;
   const int64_t unit = int64_t(b) * Hkv + g;
   int64_t* pos_ptr = reinterpret_cast<int64_t*>(lay + sec.pos) + unit;
+  int64_t* nf_ptr = reinterpret_cast<int64_t*>(lay + sec.nf) + unit;
   float* S = reinterpret_cast<float*>(lay + sec.S) + unit * DF * D;
   float* z = reinterpret_cast<float*>(lay + sec.z) + unit * DF;
   T* Kr = reinterpret_cast<T*>(lay + sec.K) + unit * int64_t(R) * D;
@@ -87,23 +91,34 @@ void decode_kernel(DecodeArgs a) {
   const T* kn = reinterpret_cast<const T*>(a.k) + (tok * Hkv + g) * D;
   const T* vn = reinterpret_cast<const T*>(a.v) + (tok * Hkv + g) * D;
   T* og = reinterpret_cast<T*>(a.out) + (tok * Hq + int64_t(g) * G) * D;
-  const float* phw = a.phi_ws + ((int64_t(L.slot) * B * Hkv) + unit) * (G + 1) * DF;
+  const T* Wf = reinterpret_cast<const T*>(a.phi_w) + int64_t(L.slot) * D * DF;
 
   const int64_t p = *pos_ptr;
 
-  float* ve = reinterpret_cast<float*>(smem);  // [D]           folded value
-  float* ph = ve + D;                          // [G+1][DF]     phi(q_h), then phi(k_e)
-  float* lnum = ph + (G + 1) * DF;             // [waves][G][D] linear numerator partials phi(q).S
+  float* ph = reinterpret_cast<float*>(smem);  // [G + kFoldPeriod][DF] phi(q_h), then phi(k_j) of pending j
+  float* pv = ph + (G + kFoldPeriod) * DF;     // [kFoldPeriod][D]      values of the pending tokens
+  float* lnum = pv + kFoldPeriod * D;          // [waves][G][D] linear numerator partials phi(q).S
   float* lden = lnum + kWaves * G * D;         // [waves][G]    linear denominator partials phi(q).z
   float* wacc = lden + kWaves * G;             // [waves][G][D] window partials sum e^s v
   float* wm = wacc + kWaves * G * D;           // [waves][G]    window running max (log2 units)
   float* wl = wm + kWaves * G;                 // [waves][G]    window sum e^s
 
-  const bool linear = a.linear != 0;
-  // Something is folded in this step exactly when the state is non-empty
-  // after it, so the fold and the linear read-out go together.
-  const bool fold = linear && (W == 0 || p >= W);
-  const bool s_nonzero = linear && (p - W > 0);  // state non-empty before the fold
+  // Linear set after this step: tokens [0, beta).  S, z hold tokens [0, nf);
+  // tokens [nf, beta) are pending (in the ring, or the new token when W = 0)
+  // and enter the read-out through phi(k_j) v_j.  They are folded for good on
+  // this step when the unit's turn comes (every step when W = 0).
+  const int64_t beta = p + 1 - W > 0 ? p + 1 - W : 0;
+  const bool lin = a.linear != 0 && beta > 0;
+  const int fper = W > 0 ? kFoldPeriod : 1;
+  // nf of a well-formed state lies in [beta - fper, beta]; the clamp keeps
+  // every access in bounds whatever the blob holds.
+  int64_t nf = *nf_ptr;
+  nf = nf < beta ? nf : beta;
+  nf = nf > beta - fper ? nf : beta - fper;
+  nf = nf > 0 ? nf : 0;
+  const int npend = lin ? int(beta - nf) : 0;  // 0 .. fper
+  const bool fold = npend > 0 && (npend >= fper || (beta + int64_t(unit % fper)) % fper == 0);
+  const bool s_nonzero = lin && nf > 0;  // S, z hold something
 
   // ---- loads issued up front: this wave's S rows, and its first window tile
   const int f0 = wave * RW;
@@ -119,7 +134,6 @@ void decode_kernel(DecodeArgs a) {
 #if !GLIDE_DECODE_STATE_LAST
   load_state();
 #endif
-
   // window: tokens [tlo, p] in 32-token tiles; wave w takes tiles w, w+4, ...
   const int64_t tlo = p - W + 1 > 0 ? p - W + 1 : 0;
   const int64_t tile0 = tlo >> 5;
@@ -171,8 +185,7 @@ void decode_kernel(DecodeArgs a) {
     else qf[kk].zero();
   }
 
-  // ---- 1. new token into its ring slot (no reader of that slot this step);
-  //         stage phi rows and the folded value
+  // ---- 1. new token into its ring slot (no token this step reads that slot)
   if (W > 0) {
     const int32_t sn = int32_t(p % R);
     for (int c = tid; c < D; c += kThreads) {
@@ -180,47 +193,87 @@ void decode_kernel(DecodeArgs a) {
       Vr[vring_elem(sn, c, D)] = vn[c];
     }
   }
-  if (fold) {
-    for (int i = tid; i < (G + 1) * DF / 4; i += kThreads)
-      reinterpret_cast<float4*>(ph)[i] = reinterpret_cast<const float4*>(phw)[i];
-    if (W == 0) {
-      for (int c = tid; c < D; c += kThreads) ve[c] = to_f32(vn[c]);
-    } else {
-      const int32_t se = int32_t((p - W) % R);
-      for (int c = tid; c < D; c += kThreads) ve[c] = to_f32(Vr[vring_elem(se, c, D)]);
+
+  // ---- 2. feature map of the G query heads and the pending keys, on MFMA:
+  //         rows [q_0 .. q_{G-1}, k_nf .. k_{beta-1}] x Wf, each wave computing
+  //         its own RW features (the state rows it owns); fp32 into LDS.
+  if (lin) {
+    const int nrows = G + npend;
+    for (int rt = 0; 16 * rt < nrows; ++rt) {
+      const int r = 16 * rt + hq;
+      f32x4_t acc[NTW];
+#pragma unroll
+      for (int nt = 0; nt < NTW; ++nt) acc[nt] = zero4();
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        Frag<T> xa;
+        if (r < G) {
+          xa.load(qg + r * D + 32 * kk + 8 * lg);
+        } else if (r < nrows) {
+          const int64_t j = nf + (r - G);
+          if (W == 0) xa.load(kn + 32 * kk + 8 * lg);  // the pending token is the new one
+          else xa.load(Kr + kring_chunk(int32_t(j % R), kk, lg, D));
+        } else {
+          xa.zero();
+        }
+#pragma unroll
+        for (int nt = 0; nt < NTW; ++nt) {
+          Frag<T> wb;
+          wb.load_strided(Wf + int64_t(32 * kk + 8 * lg) * DF + f0 + 16 * nt + hq, DF);
+          acc[nt] = mma(xa, wb, acc[nt]);
+        }
+      }
+#pragma unroll
+      for (int nt = 0; nt < NTW; ++nt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 16 * rt + 4 * lg + i;
+          if (row < nrows) ph[row * DF + f0 + 16 * nt + hq] = fmaxf(acc[nt][i], 0.f);
+        }
+      }
+    }
+    for (int e = tid; e < npend * D; e += kThreads) {
+      const int i = e / D, c = e - i * D;
+      pv[e] = W == 0 ? to_f32(vn[c]) : to_f32(Vr[vring_elem(int32_t((nf + i) % R), c, D)]);
     }
   }
   __syncthreads();
 
   auto state_phase = [&]() {
-  // ---- 2. state: fold + read-out, one read and one write of S; the
-  //         per-wave read-out partials are summed in the merge
-  if (fold) {
+  // ---- 3. state: the pending tokens are added to this wave's S rows in
+  //         registers (S' = S + sum_j phi(k_j)^T v_j, z' likewise), the
+  //         read-out phi(q_h).S', phi(q_h).z' is taken from them, and on a
+  //         fold step S', z' are written back (rows no pending token touches
+  //         are unchanged and skipped).  Per-wave partials are summed in the
+  //         merge.
+  if (lin) {
     const float* pk = ph + G * DF;
-    const float4 vv = *reinterpret_cast<const float4*>(ve + c4);
-    // Row f changes only where phi(k_e)_f != 0; with the ReLU feature map
-    // about half of the rows are untouched and are not written back (on the
-    // first fold every row is written, whatever the memory held).
+    uint32_t touched = 0;
+    for (int i = 0; i < npend; ++i) {
+      const float4 vv = *reinterpret_cast<const float4*>(pv + i * D + c4);
 #pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      const int f = f0 + s * RPS + lr;
-      const float w = pk[f];
-      if (w != 0.f || !s_nonzero) {
+      for (int s = 0; s < STEPS; ++s) {
+        const float w = pk[i * DF + f0 + s * RPS + lr];
+        touched |= uint32_t(w != 0.f) << s;
         sr[s].x = fmaf(w, vv.x, sr[s].x);
         sr[s].y = fmaf(w, vv.y, sr[s].y);
         sr[s].z = fmaf(w, vv.z, sr[s].z);
         sr[s].w = fmaf(w, vv.w, sr[s].w);
-        store_nt(S + f * D + c4, sr[s]);
       }
+    }
+    if (fold) {
+      // On the first fold every row is written, whatever the memory held.
+#pragma unroll
+      for (int s = 0; s < STEPS; ++s)
+        if (!s_nonzero || ((touched >> s) & 1u)) store_nt(S + (f0 + s * RPS + lr) * D + c4, sr[s]);
     }
     float zf = 0.f;
     if (lane < RW) {
       zf = s_nonzero ? z[f0 + lane] : 0.f;
-      const float w = pk[f0 + lane];
-      if (w != 0.f || !s_nonzero) {
-        zf += w;
-        z[f0 + lane] = zf;
-      }
+      float dz = 0.f;
+      for (int i = 0; i < npend; ++i) dz += pk[i * DF + f0 + lane];
+      zf += dz;
+      if (fold && (dz != 0.f || !s_nonzero)) z[f0 + lane] = zf;
     }
     for (int hh = 0; hh < G; ++hh) {
       const float* pq = ph + hh * DF;
@@ -359,7 +412,7 @@ void decode_kernel(DecodeArgs a) {
   for (int i = tid; i < G * D; i += kThreads) {
     const int hh = i / D, c = i - hh * D;
     float nm = 0.f, dn = 0.f;
-    if (fold) {
+    if (lin) {
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
         nm += lnum[(w * G + hh) * D + c];
@@ -393,13 +446,88 @@ void decode_kernel(DecodeArgs a) {
     }
     og[i] = from_f32<T>(o);
   }
-  if (tid == 0) *pos_ptr = p + 1;
+  if (tid == 0) {
+    *pos_ptr = p + 1;
+    if (fold) *nf_ptr = beta;
+  }
+}
+
+// Fold every pending token of a unit into S and z (nf := beta = max(0, p-W)),
+// leaving the state in its direct form S = sum_{j < beta} phi(k_j)^T v_j.
+// Plain fp32 arithmetic: it runs once per prefill call, not per token.
+template <typename T, int D, int DF>
+__global__ __launch_bounds__(kThreads) void flush_kernel(DecodeArgs a) {
+  __shared__ float kx[kFoldPeriod][D], vx[kFoldPeriod][D], pk[kFoldPeriod][DF];
+  const int tid = threadIdx.x;
+  const int per_layer = a.B * a.Hkv;
+  const int li = blockIdx.x / per_layer;
+  const int64_t unit = blockIdx.x - int64_t(li) * per_layer;
+  const LayerArg L = a.layers[li];
+  const int W = L.W, R = L.R;
+  if (W == 0) return;  // W = 0 units fold on every step
+  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, R, sizeof(T));
+  char* lay = a.state + L.base;
+  const int64_t p = reinterpret_cast<const int64_t*>(lay + sec.pos)[unit];
+  int64_t* nf_ptr = reinterpret_cast<int64_t*>(lay + sec.nf) + unit;
+  const int64_t beta = p - W > 0 ? p - W : 0;
+  int64_t nf = *nf_ptr;
+  nf = nf < beta ? nf : beta;
+  nf = nf > beta - kFoldPeriod ? nf : beta - kFoldPeriod;
+  nf = nf > 0 ? nf : 0;
+  const int n = int(beta - nf);
+  if (n == 0) return;
+  float* S = reinterpret_cast<float*>(lay + sec.S) + unit * DF * D;
+  float* z = reinterpret_cast<float*>(lay + sec.z) + unit * DF;
+  const T* Kr = reinterpret_cast<const T*>(lay + sec.K) + unit * int64_t(R) * D;
+  const T* Vr = reinterpret_cast<const T*>(lay + sec.V) + unit * int64_t(R) * D;
+  const T* Wf = reinterpret_cast<const T*>(a.phi_w) + int64_t(L.slot) * D * DF;
+  for (int e = tid; e < n * D; e += kThreads) {
+    const int i = e / D, c = e - i * D;
+    const int32_t slot = int32_t((nf + i) % R);
+    kx[i][c] = to_f32(Kr[kring_elem(slot, c, D)]);
+    vx[i][c] = to_f32(Vr[vring_elem(slot, c, D)]);
+  }
+  __syncthreads();
+  for (int e = tid; e < n * DF; e += kThreads) {
+    const int i = e / DF, f = e - i * DF;
+    float acc = 0.f;
+    for (int c = 0; c < D; ++c) acc = fmaf(kx[i][c], to_f32(Wf[c * DF + f]), acc);
+    pk[i][f] = fmaxf(acc, 0.f);
+  }
+  __syncthreads();
+  const bool s_nonzero = nf > 0;
+  for (int e = tid; e < DF * D / 4; e += kThreads) {
+    const int f = e / (D / 4), c4 = (e - f * (D / 4)) * 4;
+    float4 sv = s_nonzero ? *reinterpret_cast<const float4*>(S + f * D + c4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = 0; i < n; ++i) {
+      const float w = pk[i][f];
+      sv.x = fmaf(w, vx[i][c4], sv.x);
+      sv.y = fmaf(w, vx[i][c4 + 1], sv.y);
+      sv.z = fmaf(w, vx[i][c4 + 2], sv.z);
+      sv.w = fmaf(w, vx[i][c4 + 3], sv.w);
+    }
+    *reinterpret_cast<float4*>(S + f * D + c4) = sv;
+  }
+  for (int f = tid; f < DF; f += kThreads) {
+    float zf = s_nonzero ? z[f] : 0.f;
+    for (int i = 0; i < n; ++i) zf += pk[i][f];
+    z[f] = zf;
+  }
+  if (tid == 0) *nf_ptr = beta;
+}
+
+template <typename T, int D, int DF>
+hipError_t flush_t(const DecodeArgs& a, hipStream_t stream) {
+  const dim3 grid(unsigned(a.n_layers) * unsigned(a.B) * unsigned(a.Hkv));
+  hipLaunchKernelGGL((flush_kernel<T, D, DF>), grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
 }
 
 template <typename T, int D, int DF>
 hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
   const int G = a.G;
-  const size_t floats = D + size_t(G + 1) * DF + 2 * (size_t(kWaves) * G * D + kWaves * G) + kWaves * G;
+  const size_t floats = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D +
+                        2 * (size_t(kWaves) * G * D + kWaves * G) + kWaves * G;
   const dim3 grid(unsigned(a.n_layers) * unsigned(a.B) * unsigned(a.Hkv));
   hipLaunchKernelGGL((decode_kernel<T, D, DF>), grid, dim3(kThreads), floats * sizeof(float), stream, a);
   return hipGetLastError();
@@ -418,6 +546,21 @@ hipError_t launch_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStrea
     if (d == 128 && Df == 64) return launch_t<float, 128, 64>(a, stream);
     if (d == 64 && Df == 128) return launch_t<float, 64, 128>(a, stream);
     if (d == 64 && Df == 64) return launch_t<float, 64, 64>(a, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_flush(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream) {
+  if (dtype == GLIDE_BF16) {
+    if (d == 128 && Df == 128) return flush_t<bf16_t, 128, 128>(a, stream);
+    if (d == 128 && Df == 64) return flush_t<bf16_t, 128, 64>(a, stream);
+    if (d == 64 && Df == 128) return flush_t<bf16_t, 64, 128>(a, stream);
+    if (d == 64 && Df == 64) return flush_t<bf16_t, 64, 64>(a, stream);
+  } else {
+    if (d == 128 && Df == 128) return flush_t<float, 128, 128>(a, stream);
+    if (d == 128 && Df == 64) return flush_t<float, 128, 64>(a, stream);
+    if (d == 64 && Df == 128) return flush_t<float, 64, 128>(a, stream);
+    if (d == 64 && Df == 64) return flush_t<float, 64, 64>(a, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -79,11 +79,40 @@ PrefillWorkspace prefill_ws(const glide_config* c, int64_t T) {
                            max_window(c), linear_on(c));
 }
 
-// Decode needs the feature-map rows of every unit of every layer of the call.
-size_t decode_ws(const glide_config* c) {
-  if (!linear_on(c)) return 0;
-  return decode_workspace_bytes(c->n_layers, c->batch, c->n_kv_heads, c->n_q_heads / c->n_kv_heads,
-                                c->feat_dim);
+// Decode needs no workspace.
+size_t decode_ws(const glide_config*) { return 0; }
+
+// Decode-style launch descriptor of layers [layer0, layer0 + n): per launch
+// group of at most kMaxLayersPerLaunch layers, ordered by decreasing window
+// (the hardware dispatcher then hands out the longest streams first).
+template <typename Fn>
+glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n_layers, DecodeArgs& a, Fn fn) {
+  std::vector<int32_t> order(n_layers);
+  for (int32_t i = 0; i < n_layers; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
+    return cfg->windows[layer0 + x] > cfg->windows[layer0 + y];
+  });
+  a.B = cfg->batch;
+  a.Hq = cfg->n_q_heads;
+  a.Hkv = cfg->n_kv_heads;
+  a.G = cfg->n_q_heads / cfg->n_kv_heads;
+  a.linear = linear_on(cfg) ? 1 : 0;
+  a.tau = cfg->sm_scale;
+  for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
+    const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
+    a.n_layers = cnt;
+    for (int32_t i = 0; i < cnt; ++i) {
+      const int32_t slot = order[first + i];
+      const int32_t l = layer0 + slot;
+      a.layers[i].base = layer_base(cfg, l);
+      a.layers[i].W = cfg->windows[l];
+      a.layers[i].R = ring_slots(cfg->windows[l]);
+      a.layers[i].slot = slot;
+    }
+    const glide_status s = hip_status(fn(a));
+    if (s != GLIDE_OK) return s;
+  }
+  return GLIDE_OK;
 }
 
 }  // namespace
@@ -118,6 +147,7 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
   out->layer_offset = base;
   out->layer_bytes = sec.bytes;
   out->pos_offset = base + sec.pos;
+  out->nf_offset = base + sec.nf;
   out->s_offset = base + sec.S;
   out->z_offset = base + sec.z;
   out->kring_offset = base + sec.K;
@@ -154,15 +184,6 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
     if (!aligned(workspace, 256)) return GLIDE_ERR_ALIGN;
     if (workspace_bytes < need) return GLIDE_ERR_SIZE;
   }
-
-  // Longest windows first: the hardware dispatcher then hands out the
-  // longest streams before the short ones (list scheduling).
-  std::vector<int32_t> order(n_layers);
-  for (int32_t i = 0; i < n_layers; ++i) order[i] = i;
-  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
-    return cfg->windows[layer0 + x] > cfg->windows[layer0 + y];
-  });
-
   DecodeArgs a;
   memset(&a, 0, sizeof(a));
   a.state = static_cast<char*>(state);
@@ -171,32 +192,25 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
   a.k = k;
   a.v = v;
   a.out = out;
-  a.B = cfg->batch;
-  a.Hq = cfg->n_q_heads;
-  a.Hkv = cfg->n_kv_heads;
-  a.G = cfg->n_q_heads / cfg->n_kv_heads;
-  a.phi_ws = static_cast<float*>(workspace);
-  a.linear = linear_on(cfg) ? 1 : 0;
-  a.tau = cfg->sm_scale;
-  for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
-    const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
-    a.n_layers = cnt;
-    for (int32_t i = 0; i < cnt; ++i) {
-      const int32_t slot = order[first + i];
-      const int32_t l = layer0 + slot;
-      a.layers[i].base = layer_base(cfg, l);
-      a.layers[i].W = cfg->windows[l];
-      a.layers[i].R = ring_slots(cfg->windows[l]);
-      a.layers[i].slot = slot;
-    }
-    if (a.linear) {
-      s = hip_status(launch_phi_decode(a, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream)));
-      if (s != GLIDE_OK) return s;
-    }
-    s = hip_status(launch_decode(a, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream)));
-    if (s != GLIDE_OK) return s;
-  }
-  return GLIDE_OK;
+  return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g) {
+    return launch_decode(g, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
+  });
+}
+
+glide_status glide_state_flush(const glide_config* cfg, void* state, size_t state_bytes, int32_t layer0,
+                               int32_t n_layers, const void* phi_w, void* stream) {
+  glide_status s = check_call(cfg, state, state_bytes, layer0, n_layers);
+  if (s != GLIDE_OK) return s;
+  if (!phi_w) return GLIDE_ERR_NULL;
+  if (!aligned(phi_w, 16)) return GLIDE_ERR_ALIGN;
+  if (!linear_on(cfg)) return GLIDE_OK;
+  DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.state = static_cast<char*>(state);
+  a.phi_w = phi_w;
+  return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g) {
+    return launch_flush(g, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
+  });
 }
 
 glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_bytes, int32_t layer0,
@@ -219,6 +233,11 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   if (!workspace) return GLIDE_ERR_NULL;
   if (!aligned(workspace, 256)) return GLIDE_ERR_ALIGN;
   if (total_tokens == 0) return GLIDE_OK;
+
+  // Tokens still pending from decode steps are folded first, so the state
+  // the chunked pass starts from is S = sum_{j < max(0, p - W)}.
+  s = glide_state_flush(cfg, state, state_bytes, layer0, n_layers, phi_w, stream);
+  if (s != GLIDE_OK) return s;
 
   const int64_t T = total_tokens;
   const int B = cfg->batch, Hq = cfg->n_q_heads, Hkv = cfg->n_kv_heads, d = cfg->head_dim, Df = cfg->feat_dim;

@@ -14,11 +14,19 @@ constexpr int kMaxG = 16;  // query heads per KV head: one MFMA row tile
 
 __host__ __device__ inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
-// Ring slots of a layer with softmax window W: R > W keeps the slot of the
-// token leaving the window distinct from the slot the new token is written
-// to, so both can be touched in one decode pass.  A multiple of 32 so that a
-// 32-token tile (token j0 = 0 mod 32) is one contiguous 32-slot ring block.
-__host__ __device__ inline int32_t ring_slots(int32_t W) { return W > 0 ? ((W + 1 + 31) & ~31) : 0; }
+// Deferred folding.  Decode folds the tokens that have left the window into
+// S and z in batches: a unit keeps up to kFoldPeriod of them "pending" in its
+// ring (their contribution to the read-out is added from the ring), and folds
+// them all at once on one step out of kFoldPeriod.  The step is staggered over
+// units, so on every step about 1/kFoldPeriod of the state is written back
+// instead of all of it.  W = 0 layers (no ring) fold every step.
+constexpr int kFoldPeriod = 8;
+
+// Ring slots of a layer with softmax window W: R >= W + kFoldPeriod holds the
+// window, the pending tokens and keeps the new token's slot distinct from
+// both.  A multiple of 32 so that a 32-token tile (token j0 = 0 mod 32) is one
+// contiguous 32-slot ring block.
+__host__ __device__ inline int32_t ring_slots(int32_t W) { return W > 0 ? ((W + kFoldPeriod + 31) & ~31) : 0; }
 
 // (x mod R) for 0 <= x < 2R.
 __device__ __forceinline__ uint32_t wrap_once(uint32_t x, uint32_t R) { return x >= R ? x - R : x; }
@@ -48,14 +56,15 @@ __host__ __device__ inline int64_t kring_chunk(int32_t slot, int kk, int g, int 
 
 // Byte offsets of the sections of one layer, relative to the layer's start.
 struct LayerSections {
-  int64_t pos, S, z, K, V, bytes;
+  int64_t pos, nf, S, z, K, V, bytes;
 };
 
 __host__ __device__ inline LayerSections layer_sections(int B, int Hkv, int d, int Df, int R, int esize) {
   LayerSections s;
   const int64_t units = int64_t(B) * Hkv;
   s.pos = 0;
-  s.S = align256(units * 8);
+  s.nf = align256(units * 8);
+  s.S = s.nf + align256(units * 8);
   s.z = s.S + align256(units * Df * d * 4);
   s.K = s.z + align256(units * Df * 4);
   s.V = s.K + align256(units * int64_t(R) * d * esize);
@@ -251,7 +260,6 @@ struct DecodeArgs {
   const void* k;
   const void* v;
   void* out;
-  float* phi_ws;     // [n_layers][B*Hkv][G+1][Df]: phi(q_h) of the group, then phi(k_e)
   int32_t B, Hq, Hkv, G;
   int32_t linear;
   float tau;
@@ -262,7 +270,7 @@ struct DecodeArgs {
 
 // Host-side launchers (one translation unit per kernel family).
 hipError_t launch_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
-hipError_t launch_phi_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
+hipError_t launch_flush(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
 hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* out, int d, int Df, int dtype,
                            bool out_f32, hipStream_t stream);
 
@@ -332,10 +340,5 @@ inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hq, int Hkv, int
 hipError_t launch_prefill_layer(const PrefillArgs& a, int d, int Df, int dtype, hipStream_t stream);
 hipError_t launch_prefill_gather(const PrefillArgs& a, int d, int Df, int dtype, hipStream_t stream);
 hipError_t launch_prefill_ringfill(const PrefillArgs& a, int d, int Df, int dtype, hipStream_t stream);
-
-// Workspace of a decode call: phi rows of every unit of every layer.
-inline size_t decode_workspace_bytes(int n_layers, int B, int Hkv, int G, int Df) {
-  return size_t(align256(int64_t(n_layers) * B * Hkv * (G + 1) * Df * 4));
-}
 
 }  // namespace glide

@@ -22,6 +22,8 @@
 //            and value A/a (exactly the shared-denominator merge); then the
 //            banded window attention over LDS-staged key tiles on MFMA;
 //   ringfill the last W tokens into the ring;   advance: pos += T_b.
+// Tokens a decode step left pending are folded (glide_state_flush) before the
+// first of these kernels runs, so the incoming state is S = sum_{j < p0-W}.
 #include <math.h>
 
 #include "glide_internal.h"
@@ -606,15 +608,20 @@ __global__ __launch_bounds__(kThreads) void prefill_ringfill(PrefillArgs a) {
   }
 }
 
-// advance: pos += T_b (after every other kernel of the layer read pos)
+// advance: pos += T_b (after every other kernel of the layer read pos); the
+// scan left S, z = the sums over tokens [0, max(0, pos - W)), nothing pending.
 template <typename T, int D, int DF>
 __global__ void prefill_advance(PrefillArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.nseq * a.Hkv) return;
   const int bl = i / a.Hkv, g = i - bl * a.Hkv;
   const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, a.R, sizeof(T));
-  int64_t* pos = reinterpret_cast<int64_t*>(a.state + a.layer_base + sec.pos) + int64_t(a.seq0 + bl) * a.Hkv + g;
-  *pos += a.seq_len[bl];
+  const int64_t unit = int64_t(a.seq0 + bl) * a.Hkv + g;
+  int64_t* pos = reinterpret_cast<int64_t*>(a.state + a.layer_base + sec.pos) + unit;
+  int64_t* nf = reinterpret_cast<int64_t*>(a.state + a.layer_base + sec.nf) + unit;
+  const int64_t p = *pos + a.seq_len[bl];
+  *pos = p;
+  *nf = p - a.W > 0 ? p - a.W : 0;
 }
 
 template <typename T, int D, int DF>

@@ -22,7 +22,8 @@ STATUS = {0: "GLIDE_OK", -1: "GLIDE_ERR_NULL", -2: "GLIDE_ERR_INVALID", -3: "GLI
           -4: "GLIDE_ERR_ALIGN", -5: "GLIDE_ERR_SIZE", -6: "GLIDE_ERR_HIP"}
 
 EXPORTS = ["glide_state_bytes", "glide_state_layout", "glide_workspace_bytes", "glide_state_init",
-           "glide_prefill", "glide_decode_step", "glide_feature_map", "glide_status_string"]
+           "glide_prefill", "glide_decode_step", "glide_state_flush", "glide_feature_map",
+           "glide_status_string"]
 
 
 class GlideError(RuntimeError):
@@ -43,7 +44,7 @@ class Config(ctypes.Structure):
 
 
 class LayerLayout(ctypes.Structure):
-    _fields_ = [("pos_offset", ctypes.c_int64), ("s_offset", ctypes.c_int64),
+    _fields_ = [("pos_offset", ctypes.c_int64), ("nf_offset", ctypes.c_int64), ("s_offset", ctypes.c_int64),
                 ("z_offset", ctypes.c_int64), ("kring_offset", ctypes.c_int64),
                 ("vring_offset", ctypes.c_int64), ("layer_offset", ctypes.c_int64),
                 ("layer_bytes", ctypes.c_int64), ("window", ctypes.c_int32),
@@ -80,6 +81,8 @@ def load_library(path=None):
     lib.glide_decode_step.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp, vp,
                                       vp, vp, vp, ctypes.c_size_t, vp]
     lib.glide_decode_step.restype = ctypes.c_int
+    lib.glide_state_flush.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp]
+    lib.glide_state_flush.restype = ctypes.c_int
     lib.glide_feature_map.argtypes = [cfgp, vp, vp, ctypes.c_int64, vp, vp]
     lib.glide_feature_map.restype = ctypes.c_int
     lib.glide_status_string.argtypes = [ctypes.c_int]
@@ -186,6 +189,7 @@ class Glide:
 
         return {
             "pos": view(lay.pos_offset, B * H, torch.int64, (B, H), 8),
+            "nf": view(lay.nf_offset, B * H, torch.int64, (B, H), 8),
             "S": view(lay.s_offset, B * H * Df * d, torch.float32, (B, H, Df, d), 4),
             "z": view(lay.z_offset, B * H * Df, torch.float32, (B, H, Df), 4),
             "kring_raw": view(lay.kring_offset, B * H * R * d, self.torch_dtype, (B, H, R * d), es),
@@ -203,7 +207,16 @@ class Glide:
     def new_workspace(self, max_total_tokens=0, device="cuda"):
         return torch.empty(max(self.workspace_bytes(max_total_tokens), 256), dtype=torch.uint8, device=device)
 
-    def decode_step(self, state, phi_w, q, k, v, out, workspace, layer0=0, n_layers=None, stream=None):
+    def state_flush(self, state, phi_w, layer0=0, n_layers=None, stream=None):
+        """Fold every pending token into S, z (nf := max(0, pos - W))."""
+        if n_layers is None:
+            n_layers = self.n_layers - layer0
+        s = self.lib.glide_state_flush(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
+                                       int(layer0), int(n_layers), _ptr(phi_w), _stream(stream))
+        if s:
+            raise GlideError(s, "glide_state_flush", self.lib)
+
+    def decode_step(self, state, phi_w, q, k, v, out, workspace=None, layer0=0, n_layers=None, stream=None):
         if n_layers is None:
             n_layers = self.n_layers - layer0
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()

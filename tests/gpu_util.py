@@ -136,6 +136,7 @@ class Case:
                 views["S"][b] = torch.from_numpy(S).float().cuda()
                 views["z"][b] = torch.from_numpy(z).float().cuda()
                 views["pos"][b] = p
+                views["nf"][b] = max(0, p - W)      # nothing pending
                 if R:
                     kl = glide.kring_logical(views["kring_raw"][b].cpu(), R, self.d)
                     vl = glide.vring_logical(views["vring_raw"][b].cpu(), R, self.d)
@@ -161,8 +162,15 @@ class Case:
                 worst = max(worst, e)
         return worst
 
-    def check_state(self, state, k, v, positions, label=""):
-        """S, z, pos and the ring after positions[b] tokens of sequence b."""
+    def check_state(self, state, k, v, positions, label="", flush=True):
+        """S, z, pos, nf and the ring after positions[b] tokens of sequence b.
+        S, z are compared with the oracle's sums over tokens [0, nf) (deferred
+        folding: nf in [beta - 8, beta], beta = max(0, p - W)); with flush, a
+        copy of the state is flushed and must then hold the sums over [0, beta)."""
+        if flush and self.linear:
+            flushed = state.clone()
+            self.g.state_flush(flushed, self.phi_w.cuda())
+            torch.cuda.synchronize()
         for l in range(self.L):
             views = self.g.layer_views(state, l)
             o = self.oracle(l)
@@ -170,15 +178,34 @@ class Case:
             for b, p in enumerate(positions):
                 assert int(views["pos"][b].min()) == p and int(views["pos"][b].max()) == p, \
                     f"{label} pos layer {l} seq {b}"
+                beta = max(0, p - W)
+                first = beta
                 if self.linear:
-                    S, z = o.state(f64(self.phi_w[l]), f64(k[l, b]), f64(v[l, b]), p)
-                    check(f"{label} S layer {l} seq {b}", f64(views["S"][b]), S, self.dtype, "state")
-                    check(f"{label} z layer {l} seq {b}", f64(views["z"][b]), z, self.dtype, "state")
+                    # the fold step is staggered over units: nf is per KV head
+                    nfs = [int(x) for x in views["nf"][b]]
+                    lo = beta if W == 0 else max(0, beta - 8)
+                    assert all(lo <= x <= beta for x in nfs), \
+                        f"{label} nf {nfs} outside [{lo}, {beta}] layer {l} seq {b}"
+                    first = min(nfs)
+                    for nf in sorted(set(nfs)):
+                        hs = [h for h, x in enumerate(nfs) if x == nf]
+                        # the oracle's state after n tokens sums tokens [0, n - W)
+                        S, z = o.state(f64(self.phi_w[l]), f64(k[l, b]), f64(v[l, b]), nf + W)
+                        check(f"{label} S layer {l} seq {b} heads {hs} (nf {nf})", f64(views["S"][b, hs]), S[hs],
+                              self.dtype, "state")
+                        check(f"{label} z layer {l} seq {b} heads {hs} (nf {nf})", f64(views["z"][b, hs]), z[hs],
+                              self.dtype, "state")
+                    if flush:
+                        fv = self.g.layer_views(flushed, l)
+                        assert torch.all(fv["nf"][b] == beta), f"{label} flushed nf layer {l} seq {b}"
+                        S, z = o.state(f64(self.phi_w[l]), f64(k[l, b]), f64(v[l, b]), p)
+                        check(f"{label} flushed S layer {l} seq {b}", f64(fv["S"][b]), S, self.dtype, "state")
+                        check(f"{label} flushed z layer {l} seq {b}", f64(fv["z"][b]), z, self.dtype, "state")
                 if not R:
                     continue
                 kr = glide.kring_logical(views["kring_raw"][b].cpu(), R, self.d)
                 vr = glide.vring_logical(views["vring_raw"][b].cpu(), R, self.d)
-                for j in range(max(0, p - W), p):
+                for j in range(first, p):
                     s = j % R
                     assert torch.equal(kr[:, s], k[l, b, j]), f"{label} key ring layer {l} seq {b} token {j}"
                     assert torch.equal(vr[:, s], v[l, b, j]), f"{label} value ring layer {l} seq {b} token {j}"

@@ -55,15 +55,16 @@ def expected_layout(B, Hkv, d, Df, windows, es):
     off = 0
     out = []
     for W in windows:
-        R = ((W + 1 + 31) // 32) * 32 if W > 0 else 0
+        R = ((W + 8 + 31) // 32) * 32 if W > 0 else 0    # window + up to 8 pending tokens
         units = B * Hkv
         pos = off
-        S = pos + align(units * 8)
+        nf = pos + align(units * 8)
+        S = nf + align(units * 8)
         z = S + align(units * Df * d * 4)
         K = z + align(units * Df * 4)
         V = K + align(units * R * d * es)
         end = V + align(units * R * d * es)
-        out.append(dict(pos=pos, S=S, z=z, K=K, V=V, R=R, bytes=end - off))
+        out.append(dict(pos=pos, nf=nf, S=S, z=z, K=K, V=V, R=R, bytes=end - off))
         off = end
     return out, off
 
@@ -75,11 +76,11 @@ def test_layout_matches_documentation(dtype, es):
     assert g.state_bytes() == total
     for l, e in enumerate(exp):
         lay = g.layout(l)
-        assert (lay.pos_offset, lay.s_offset, lay.z_offset, lay.kring_offset, lay.vring_offset) == \
-            (e["pos"], e["S"], e["z"], e["K"], e["V"])
+        assert (lay.pos_offset, lay.nf_offset, lay.s_offset, lay.z_offset, lay.kring_offset,
+                lay.vring_offset) == (e["pos"], e["nf"], e["S"], e["z"], e["K"], e["V"])
         assert lay.ring_slots == e["R"] and lay.window == g.windows[l]
         assert lay.layer_bytes == e["bytes"]
-        assert lay.ring_slots == 0 or (lay.ring_slots % 32 == 0 and lay.ring_slots > lay.window)
+        assert lay.ring_slots == 0 or (lay.ring_slots % 32 == 0 and lay.ring_slots >= lay.window + 8)
 
 
 def test_layer_views_cover_state():
@@ -167,16 +168,30 @@ def test_decode_argument_errors():
     assert _decode(g, ptrs=(4096, None, 4096, 4096, 4096)) == -1
     assert _decode(g, ptrs=(4096, 4096, 4096 + 2, 4096, 4096)) == -4   # q misaligned
     assert _decode(g, ptrs=(4096, 4096, 4096, 4096, 4104)) == -4       # out misaligned
-    assert _decode(g, ws=None) == -1                                   # decode needs its workspace
-    assert _decode(g, ws=(1 << 20) + 16) == -4
-    assert _decode(g, ws_bytes=g.workspace_bytes(0) - 1) == -5
 
 
-def test_decode_workspace_size():
+
+def _flush(g, state=256, size=None, layer0=0, n=1, phi=4096):
+    size = g.state_bytes() if size is None else size
+    return g.lib.glide_state_flush(ctypes.byref(g.cfg), ctypes.c_void_p(state) if state else None, size, layer0, n,
+                                   ctypes.c_void_p(phi) if phi else None, None)
+
+
+def test_flush_argument_errors():
+    g = mk()
+    assert _flush(g, state=None) == -1
+    assert _flush(g, state=128) == -4
+    assert _flush(g, size=g.state_bytes() - 1) == -5
+    assert _flush(g, layer0=2, n=2) == -2
+    assert _flush(g, phi=None) == -1
+    assert _flush(g, phi=4096 + 4) == -4
+    assert _flush(mk(linear=False, windows=[1, 5, 64])) == 0     # nothing to fold, nothing enqueued
+
+
+def test_workspace_sizes():
     g = mk(n_layers=3, batch=2, n_q_heads=8, n_kv_heads=2, feat_dim=64)
-    assert g.workspace_bytes(0) >= 3 * 2 * 2 * (4 + 1) * 64 * 4
-    g2 = mk(linear=False, windows=[1, 5, 64])
-    assert g2.workspace_bytes(0) == 256      # nothing but the minimum without the linear part
+    assert g.workspace_bytes(0) == 256       # decode needs none: only the documented minimum
+    assert g.workspace_bytes(1000) > g.workspace_bytes(10) > 256
 
 
 def _prefill(g, cu, total, chunk=0, ws_bytes=None, state=256, ptrs=(4096,) * 6):
@@ -192,7 +207,7 @@ def test_prefill_argument_errors():
     assert _prefill(g, [0, 5, 3], 3) == -2              # decreasing
     assert _prefill(g, [1, 2, 3], 3) == -2              # cu[0] != 0
     assert _prefill(g, [0, 2, 3], 4) == -2              # cu[B] != total
-    assert _prefill(g, [0, 2, 3], 3, chunk=24) == -2    # chunk not a multiple of 16
+    assert _prefill(g, [0, 2, 3], 3, chunk=48) == -2    # chunk not a multiple of 32
     assert _prefill(g, [0, 2, 3], 3, chunk=512) == -2   # chunk too large
     assert _prefill(g, [0, 2, 3], 3, ws_bytes=0) == -5  # workspace too small
     assert _prefill(g, [0, 2, 3], 3, ptrs=(4096, 4096, 4096, None, 4096, 4096)) == -1

@@ -105,3 +105,28 @@ def test_checkpoint_restore_is_bit_identical():
     st.copy_(snap)
     b = case.decode_steps(st, q, k, v, 20, 40)
     assert torch.equal(a, b)
+
+
+def test_deferred_folding_state_every_step():
+    """After every decode step: nf stays within [beta - 8, beta] and moves in
+    batches, S and z equal the sums over [0, nf), and a flushed copy holds the
+    sums over the whole linear part [0, beta)."""
+    case = Case([0, 3, 40], batch=2, Hq=8, Hkv=2, d=64, Df=64, dtype=torch.float32, seed=8)
+    q, k, v = case.tokens(70)
+    st = case.new_state()
+    case.prefill(st, q, k, v, [0, 0], [50, 23])
+    phi = case.phi_w.cuda()
+    folds = 0
+    prev = [case.g.layer_views(st, l)["nf"].clone() for l in range(case.L)]
+    for step in range(17):
+        qs = torch.stack([q[:, 0, 50 + step], q[:, 1, 23 + step]], 1).contiguous().cuda()
+        ks = torch.stack([k[:, 0, 50 + step], k[:, 1, 23 + step]], 1).contiguous().cuda()
+        vs = torch.stack([v[:, 0, 50 + step], v[:, 1, 23 + step]], 1).contiguous().cuda()
+        case.g.decode_step(st, phi, qs, ks, vs, torch.empty_like(qs))
+        torch.cuda.synchronize()
+        case.check_state(st, k, v, [51 + step, 24 + step], f"step {step}")
+        for l in range(case.L):
+            nf = case.g.layer_views(st, l)["nf"]
+            folds += int((nf != prev[l]).sum())
+            prev[l] = nf.clone()
+    assert folds > 0

@@ -97,3 +97,29 @@ def test_sharp_logits_prefill():
     case = Case([0, 6, 50], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=17, qkv_scale=0.5,
                 v_scale=1.0)
     _prefill_from_empty(case, [120, 77], label="sharp")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_prefill_after_decode(dtype):
+    """prefill, decode a few steps (tokens left pending by deferred folding),
+    then a continuing prefill: the pending tokens are folded first and the
+    outputs still follow the definition over the whole history."""
+    case = Case([0, 3, 40, 129], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=dtype, seed=18)
+    n1, m, n2 = [150, 61], 5, [40, 77]
+    q, k, v = case.tokens(max(a + m + b for a, b in zip(n1, n2)))
+    st = case.new_state()
+    case.prefill(st, q, k, v, [0, 0], n1)
+    outs = []
+    phi = case.phi_w.cuda()
+    for step in range(m):
+        qs = torch.stack([q[:, b, n1[b] + step] for b in range(2)], 1).contiguous().cuda()
+        ks = torch.stack([k[:, b, n1[b] + step] for b in range(2)], 1).contiguous().cuda()
+        vs = torch.stack([v[:, b, n1[b] + step] for b in range(2)], 1).contiguous().cuda()
+        o = torch.empty_like(qs)
+        case.g.decode_step(st, phi, qs, ks, vs, o)
+        outs.append(o)
+    case.check_decode(torch.stack(outs, 2).cpu(), q, k, v, n1, m, "decode between prefills")
+    starts = [a + m for a in n1]
+    outs = case.prefill(st, q, k, v, starts, n2)
+    case.check_prefill(outs, q, k, v, starts, n2, "prefill after decode")
+    case.check_state(st, k, v, [a + b for a, b in zip(starts, n2)], "prefill after decode")
