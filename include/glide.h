@@ -115,8 +115,11 @@ size_t glide_state_bytes(const glide_config* cfg);
 glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_layer_layout* out);
 
 /* Workspace bytes needed by glide_prefill for calls with at most
- * max_total_tokens packed tokens (any chunk size); at least 256.
- * glide_decode_step needs none.  0 if cfg is invalid. */
+ * max_total_tokens packed tokens (any chunk size) and by glide_decode_step
+ * (any layer range); at least 256.  Decode uses it only when the stack has
+ * fewer than 1024 (layer, sequence, KV head) units: long windows are then
+ * split over several workgroups, whose partial results it holds.  0 if cfg
+ * is invalid. */
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens);
 
 /* Zeroes the whole state: S = 0, z = 0 (S_0, Z_0 of the Sec. II-B
@@ -154,11 +157,13 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
  * group from the window and from S + the pending tokens, pos += 1; on the
  * unit's fold step (one in 8; every step when W = 0) the pending tokens are
  * folded into S and z.  Sequences may sit at different positions (pos lives
- * in the state).  One kernel is enqueued.
+ * in the state).  One kernel is enqueued per 64 layers, plus a merge kernel
+ * when windows are split (see glide_workspace_bytes).
  *   phi_w  device [n_layers][d][Df]
  *   q      device [n_layers][B][Hq][d];  k, v device [n_layers][B][Hkv][d]
  *   out    device [n_layers][B][Hq][d]
- *   workspace  unused (may be NULL; kept for future use) */
+ *   workspace  device, 256-byte aligned, >= glide_workspace_bytes(cfg, 0);
+ *              may be NULL when that is 256 (nothing is split) */
 glide_status glide_decode_step(const glide_config* cfg, void* state, size_t state_bytes,
                                int32_t layer0, int32_t n_layers, const void* phi_w,
                                const void* q, const void* k, const void* v, void* out,

@@ -43,12 +43,6 @@ struct WindowTile {
   Frag<T> v[D / 16];     // B operand: 8 tokens x 1 column per lane, per column tile
 };
 
-#ifndef GLIDE_DECODE_STAGES
-#define GLIDE_DECODE_STAGES 2   // register stages of the window stream (bf16)
-#endif
-#ifndef GLIDE_DECODE_STATE_LAST
-#define GLIDE_DECODE_STATE_LAST 0  // 1: window stream first, state fold last
-#endif
 #ifndef GLIDE_DECODE_WAVES_PER_SIMD
 #define GLIDE_DECODE_WAVES_PER_SIMD 2
 #endif
@@ -64,18 +58,24 @@ void decode_kernel(DecodeArgs a) {
   constexpr int LPR = D / 4;       // lanes per state row (4 floats each)
   constexpr int RPS = 64 / LPR;    // state rows per wave step
   constexpr int STEPS = RW / RPS;
-  constexpr bool kTwoStages = sizeof(T) == 2 && GLIDE_DECODE_STAGES == 2;
+  constexpr uint32_t ES = sizeof(T);
+  constexpr int PVT = (kFoldPeriod * D + kThreads - 1) / kThreads;  // pending values per thread
   static_assert(STEPS * RPS == RW && NTW * 16 == RW, "state rows must tile the wave");
 
-  extern __shared__ __align__(16) char smem[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  extern __shared__ __align__(16) float smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hq = lane & 15, lg = lane >> 4;
   const int G = a.G, B = a.B, Hkv = a.Hkv, Hq = a.Hq;
   const int per_layer = B * Hkv;
-  const int li = blockIdx.x / per_layer;
-  const int rem = blockIdx.x - li * per_layer;
+  const int prow = __builtin_amdgcn_readfirstlane(int(blockIdx.x) / per_layer);
+  const int rem = int(blockIdx.x) - prow * per_layer;
+  // (the table is read a dword at a time: a scalar load, no vector memory wait)
+  const uint32_t lw = reinterpret_cast<const uint32_t*>(a.piece_layer)[prow >> 2];
+  const LayerArg L = a.layers[(lw >> (8 * (prow & 3))) & 0xffu];
+  const int piece = prow == L.prow0 ? 0 : prow - L.prow1 + 1;
+  const bool split = L.npiece > 1;
   const int b = rem / Hkv, g = rem - b * Hkv;
-  const LayerArg L = a.layers[li];
   const int W = L.W, R = L.R;
   const LayerSections sec = layer_sections(B, Hkv, D, DF, R, sizeof(T));
   char* lay = a.state + L.base;
@@ -95,20 +95,24 @@ void decode_kernel(DecodeArgs a) {
 
   const int64_t p = *pos_ptr;
 
-  float* ph = reinterpret_cast<float*>(smem);  // [G + kFoldPeriod][DF] phi(q_h), then phi(k_j) of pending j
-  float* pv = ph + (G + kFoldPeriod) * DF;     // [kFoldPeriod][D]      values of the pending tokens
-  float* lnum = pv + kFoldPeriod * D;          // [waves][G][D] linear numerator partials phi(q).S
-  float* lden = lnum + kWaves * G * D;         // [waves][G]    linear denominator partials phi(q).z
-  float* wacc = lden + kWaves * G;             // [waves][G][D] window partials sum e^s v
-  float* wm = wacc + kWaves * G * D;           // [waves][G]    window running max (log2 units)
-  float* wl = wm + kWaves * G;                 // [waves][G]    window sum e^s
+  float* ph = smem;                        // [G + kFoldPeriod][DF] phi(q_h), then phi(k_j) of pending j
+  float* pvl = ph + (G + kFoldPeriod) * DF;  // [kFoldPeriod][D]    values of the pending tokens
+  float* kpl = pvl + kFoldPeriod * D;      // [D]           the new key
+  float* vpl = kpl + D;                    // [D]           the new value
+  float* spl = vpl + D;                    // [kMaxG]       the new token's score (log2 units)
+  float* lnum = spl + kMaxG;               // [waves][G][D] linear numerator partials phi(q).S
+  float* lden = lnum + kWaves * G * D;     // [waves][G]    linear denominator partials phi(q).z
+  float* wacc = lden + kWaves * G;         // [waves][G][D] window partials sum e^s v
+  float* wm = wacc + kWaves * G * D;       // [waves][G]    window running max (log2 units)
+  float* wl = wm + kWaves * G;             // [waves][G]    window sum e^s
 
   // Linear set after this step: tokens [0, beta).  S, z hold tokens [0, nf);
   // tokens [nf, beta) are pending (in the ring, or the new token when W = 0)
   // and enter the read-out through phi(k_j) v_j.  They are folded for good on
   // this step when the unit's turn comes (every step when W = 0).
   const int64_t beta = p + 1 - W > 0 ? p + 1 - W : 0;
-  const bool lin = a.linear != 0 && beta > 0;
+  const bool lin_unit = a.linear != 0 && beta > 0;
+  const bool lin = lin_unit && piece == 0;  // the state pass belongs to piece 0
   const int fper = W > 0 ? kFoldPeriod : 1;
   // nf of a well-formed state lies in [beta - fper, beta]; the clamp keeps
   // every access in bounds whatever the blob holds.
@@ -120,127 +124,165 @@ void decode_kernel(DecodeArgs a) {
   const bool fold = npend > 0 && (npend >= fper || (beta + int64_t(unit % fper)) % fper == 0);
   const bool s_nonzero = lin && nf > 0;  // S, z hold something
 
-  // ---- loads issued up front: this wave's S rows, and its first window tile
-  const int f0 = wave * RW;
-  const int lr = lane / LPR, c4 = (lane % LPR) * 4;
-  float4 sr[STEPS];
-  auto load_state = [&]() {
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      const int f = f0 + s * RPS + lr;
-      sr[s] = s_nonzero ? *reinterpret_cast<const float4*>(S + f * D + c4) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-  };
-#if !GLIDE_DECODE_STATE_LAST
-  load_state();
-#endif
-  // window: tokens [tlo, p] in 32-token tiles; wave w takes tiles w, w+4, ...
+  // Window: tokens [tlo, p] in 32-token tiles.  Ring tiles cover [tlo, p-1];
+  // the new token p (not in the ring yet) is a partial of its own.  The
+  // piece takes tiles [t_first, n_tiles) (piece 0 fewer, as it also does the
+  // state); wave w takes tiles t_first + w, t_first + w + 4, ...
   const int64_t tlo = p - W + 1 > 0 ? p - W + 1 : 0;
   const int64_t tile0 = tlo >> 5;
-  const int n_tiles = W > 0 ? int((p >> 5) - tile0 + 1) : 0;
-  int it = wave;
+  const int n_all = W > 0 ? int((p >> 5) - tile0 + 1) : 0;
+  int t_first = 0, n_tiles = n_all;
+  if (split) {
+    const int off = lin_unit ? kStateTiles : 0;
+    const int share = (n_all + off + L.npiece - 1) / L.npiece;
+    t_first = piece * share - off;
+    t_first = t_first > 0 ? t_first : 0;
+    n_tiles = (piece + 1) * share - off;
+    n_tiles = n_tiles < n_all ? n_tiles : n_all;
+  }
+  const bool own_p = W > 0 && t_first <= n_all - 1 && n_all - 1 < n_tiles;  // the new token's partial
+  int it = t_first + wave;
   int64_t j0 = (tile0 + it) << 5;
-  uint32_t s0 = (W > 0 && it < n_tiles) ? uint32_t(j0 % R) : 0u;
+  uint32_t s0 = W > 0 ? uint32_t(j0 % R) : 0u;
   const uint32_t step = W > 0 ? uint32_t((32 * kWaves) % R) : 0u;
 
-  // Loads of one tile.  Key row m of sub-tile t is token j0 + 8(m/4) + 4t + m%4,
-  // so that after QK^T lane group lg holds tokens j0 + 8lg .. j0 + 8lg + 7,
-  // exactly the A-operand layout PV needs.  lo/pn: window bounds relative
-  // to j0 (clamped to [-1, 32]); pn is also where the new token sits.
-  // Tile loads.  s0t = (j0 mod R) is a multiple of 32, so the tile is ring
-  // block s0t/32 and every fragment load is one contiguous 1 KB read.  Rows
-  // outside the window (and the new token, whose key is still in the input)
-  // read the new key instead; masked rows' scores and out-of-window values'
-  // probabilities are exactly 0, so substitute data never matters and the
-  // loads need no branches.
-  auto load_tile = [&](WindowTile<T, D>& tl, uint32_t s0t, int lo, int pn) {
-    const T* Kb = Kr + int64_t(s0t) * D;
-    const T* Vb = Vr + int64_t(s0t) * D;
+  const brsrc_t rq = make_rsrc(qg, uint32_t(G * D) * ES);
+  const brsrc_t rk = make_rsrc(kn, D * ES), rv = make_rsrc(vn, D * ES);
+  const brsrc_t rS = make_rsrc(S, DF * D * 4), rz = make_rsrc(z, DF * 4);
+  const brsrc_t rK = make_rsrc(Kr, uint32_t(R) * D * ES), rV = make_rsrc(Vr, uint32_t(R) * D * ES);
+  const brsrc_t rW = make_rsrc(Wf, D * DF * ES);
+  const brsrc_t rpk = W > 0 ? rK : rk;  // where pending keys / values live
+  const brsrc_t rpv = W > 0 ? rV : rv;
+
+  // Tile loads: s0t = (j0 mod R) is a multiple of 32, so the tile is ring
+  // block s0t/32 and every fragment load is one contiguous 1 KB read.  Key
+  // row m of sub-tile t is token j0 + 8(m/4) + 4t + m%4, so that after QK^T
+  // lane group lg holds tokens j0 + 8lg .. j0 + 8lg + 7, exactly the A-operand
+  // layout PV needs.  A tile that is not needed reads zeros (no traffic).
+  auto load_tile = [&](WindowTile<T, D>& tl, uint32_t s0t, bool valid) {
+    const uint32_t base = valid ? s0t * D * ES : kOOB;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int off = 8 * (hq >> 2) + 4 * t + (hq & 3);
-      const bool ring = off >= lo && off < pn;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        const T* src = ring ? Kb + (((t * KS + kk) * 4 + lg) * 16 + hq) * 8 : kn + 32 * kk + 8 * lg;
-        tl.k[t][kk].load(src);
-      }
-    }
-    const int ob = 8 * lg;
-    const bool bvalid = ob + 7 >= lo && ob <= pn;
+      for (int kk = 0; kk < KS; ++kk)
+        bload_frag(tl.k[t][kk], rK, base + uint32_t((((t * KS + kk) * 4 + lg) * 16 + hq) * 8) * ES);
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) tl.v[ct].load((bvalid ? Vb : Vr) + ((ct * 4 + lg) * 16 + hq) * 8);
-    if (bvalid && pn - ob < 8) {
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct) tl.v[ct].patch(pn - ob, vn[16 * ct + hq]);
-    }
+    for (int ct = 0; ct < CT; ++ct) bload_frag(tl.v[ct], rV, base + uint32_t(((ct * 4 + lg) * 16 + hq) * 8) * ES);
   };
 
-  WindowTile<T, D> ta;
-  if (it < n_tiles) load_tile(ta, s0, clamp_rel(tlo - j0), clamp_rel(p - j0));
-  Frag<T> qf[KS];
+  // ---- 1. prologue: every load up to the first window tile is issued before
+  //         any of them is waited for.
+  // the new token's element tid % D (its own score, and the ring write at the end)
+  const T kraw = bload_elem(rk, uint32_t(tid % D) * ES, T());
+  const T vraw = bload_elem(rv, uint32_t(tid % D) * ES, T());
+  // rows of the feature-map tile, which are also the queries of the window's
+  // QK^T: row hq < G is query head hq, rows G .. G+npend-1 the pending keys
+  // (second tile: rows 16 ..), other rows zero.  Columns of QK^T beyond G are
+  // never read.
+  Frag<T> xa[KS], xb[KS];
+  {
+    const int ia = hq - G, ib = 16 + hq - G;
+    const bool pa = hq >= G && ia < npend, pb = ib >= 0 && ib < npend;
+    const int32_t sa = W > 0 ? int32_t((nf + (pa ? ia : 0)) % R) : 0;
+    const int32_t sb = W > 0 ? int32_t((nf + (pb ? ib : 0)) % R) : 0;
 #pragma unroll
-  for (int kk = 0; kk < KS; ++kk) {
-    if (W > 0 && hq < G) qf[kk].load(qg + hq * D + 32 * kk + 8 * lg);
-    else qf[kk].zero();
-  }
-
-  // ---- 1. new token into its ring slot (no token this step reads that slot)
-  if (W > 0) {
-    const int32_t sn = int32_t(p % R);
-    for (int c = tid; c < D; c += kThreads) {
-      Kr[kring_elem(sn, c, D)] = kn[c];
-      Vr[vring_elem(sn, c, D)] = vn[c];
+    for (int kk = 0; kk < KS; ++kk) {
+      Frag<T> fq, fp;
+      bload_frag(fq, rq, hq < G ? uint32_t(hq * D + 32 * kk + 8 * lg) * ES : kOOB);
+      const uint32_t oa = W > 0 ? uint32_t(kring_chunk(sa, kk, lg, D)) * ES : uint32_t(32 * kk + 8 * lg) * ES;
+      bload_frag(fp, rpk, pa ? oa : kOOB);
+      xa[kk] = frag_or(fq, fp);
+      const uint32_t ob = W > 0 ? uint32_t(kring_chunk(sb, kk, lg, D)) * ES : uint32_t(32 * kk + 8 * lg) * ES;
+      bload_frag(xb[kk], rpk, pb ? ob : kOOB);
     }
   }
-
-  // ---- 2. feature map of the G query heads and the pending keys, on MFMA:
-  //         rows [q_0 .. q_{G-1}, k_nf .. k_{beta-1}] x Wf, each wave computing
-  //         its own RW features (the state rows it owns); fp32 into LDS.
-  if (lin) {
-    const int nrows = G + npend;
-    for (int rt = 0; 16 * rt < nrows; ++rt) {
-      const int r = 16 * rt + hq;
-      f32x4_t acc[NTW];
+  // Wf B fragments of this wave's features (zeros when there is no state pass)
+  const int f0 = wave * RW;
+  Frag<T> wb[KS][NTW];
 #pragma unroll
-      for (int nt = 0; nt < NTW; ++nt) acc[nt] = zero4();
+  for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+    for (int nt = 0; nt < NTW; ++nt)
+      bload_frag_strided(wb[kk][nt], rW, lin ? uint32_t((32 * kk + 8 * lg) * DF + f0 + 16 * nt + hq) * ES : kOOB,
+                         DF * ES);
+  // values of the pending tokens
+  T pvr[PVT];
+#pragma unroll
+  for (int u = 0; u < PVT; ++u) {
+    const int e = tid + u * kThreads, i = e / D, c = e - i * D;
+    const bool ok = i < npend;
+    const uint32_t off = W > 0 ? uint32_t(vring_elem(int32_t((nf + (ok ? i : 0)) % R), c, D)) * ES : uint32_t(c) * ES;
+    pvr[u] = bload_elem(rpv, ok ? off : kOOB, T());
+  }
+  // this wave's S rows and z entries (zeros when S is empty)
+  const int lr = lane / LPR, c4 = (lane % LPR) * 4;
+  float4 sr[STEPS];
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s)
+    sr[s] = bload_f4(rS, s_nonzero ? uint32_t(((f0 + s * RPS + lr) * D + c4) * 4) : kOOB);
+  float zf = bload_f(rz, s_nonzero && lane < RW ? uint32_t((f0 + lane) * 4) : kOOB);
+  // first window tile of this wave
+  WindowTile<T, D> ta, tb;
+  load_tile(ta, s0, W > 0 && it < n_tiles);
+
+  // ---- 2. feature map on MFMA: rows x Wf, this wave's RW features, fp32
+  {
+    const int nrows = G + npend;
+    f32x4_t acc[NTW], acb[NTW];
+#pragma unroll
+    for (int nt = 0; nt < NTW; ++nt) {
+      acc[nt] = zero4();
+      acb[nt] = zero4();
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
-        Frag<T> xa;
-        if (r < G) {
-          xa.load(qg + r * D + 32 * kk + 8 * lg);
-        } else if (r < nrows) {
-          const int64_t j = nf + (r - G);
-          if (W == 0) xa.load(kn + 32 * kk + 8 * lg);  // the pending token is the new one
-          else xa.load(Kr + kring_chunk(int32_t(j % R), kk, lg, D));
-        } else {
-          xa.zero();
-        }
-#pragma unroll
-        for (int nt = 0; nt < NTW; ++nt) {
-          Frag<T> wb;
-          wb.load_strided(Wf + int64_t(32 * kk + 8 * lg) * DF + f0 + 16 * nt + hq, DF);
-          acc[nt] = mma(xa, wb, acc[nt]);
-        }
+        acc[nt] = mma(xa[kk], wb[kk][nt], acc[nt]);
+        acb[nt] = mma(xb[kk], wb[kk][nt], acb[nt]);
       }
+    }
+    if (lin) {
 #pragma unroll
       for (int nt = 0; nt < NTW; ++nt) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int row = 16 * rt + 4 * lg + i;
+          const int row = 4 * lg + i;
           if (row < nrows) ph[row * DF + f0 + 16 * nt + hq] = fmaxf(acc[nt][i], 0.f);
+          if (16 + row < nrows) ph[(16 + row) * DF + f0 + 16 * nt + hq] = fmaxf(acb[nt][i], 0.f);
         }
       }
     }
-    for (int e = tid; e < npend * D; e += kThreads) {
-      const int i = e / D, c = e - i * D;
-      pv[e] = W == 0 ? to_f32(vn[c]) : to_f32(Vr[vring_elem(int32_t((nf + i) % R), c, D)]);
+  }
+
+  if (lin) {
+#pragma unroll
+    for (int u = 0; u < PVT; ++u) {
+      const int e = tid + u * kThreads;
+      if (e < kFoldPeriod * D) pvl[e] = to_f32(pvr[u]);
     }
   }
+  if (own_p && tid < D) {
+    kpl[tid] = to_f32(kraw);
+    vpl[tid] = to_f32(vraw);
+  }
+  if (tid < kMaxG) spl[tid] = -INFINITY;
   __syncthreads();
 
-  auto state_phase = [&]() {
-  // ---- 3. state: the pending tokens are added to this wave's S rows in
+  const float sc2 = a.tau * kLog2e;
+  // ---- 3. the new token's score, one per query head (wave 0)
+  if (own_p && wave == 0) {
+    float d = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      float x[8];
+      xa[kk].to_floats(x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d = fmaf(x[e], kpl[32 * kk + 8 * lg + e], d);
+    }
+    d += __shfl_xor(d, 16);
+    d += __shfl_xor(d, 32);
+    if (lane < G) spl[lane] = d * sc2;
+  }
+
+  // ---- 4. state: the pending tokens are added to this wave's S rows in
   //         registers (S' = S + sum_j phi(k_j)^T v_j, z' likewise), the
   //         read-out phi(q_h).S', phi(q_h).z' is taken from them, and on a
   //         fold step S', z' are written back (rows no pending token touches
@@ -249,8 +291,9 @@ void decode_kernel(DecodeArgs a) {
   if (lin) {
     const float* pk = ph + G * DF;
     uint32_t touched = 0;
+    float dz = 0.f;
     for (int i = 0; i < npend; ++i) {
-      const float4 vv = *reinterpret_cast<const float4*>(pv + i * D + c4);
+      const float4 vv = *reinterpret_cast<const float4*>(pvl + i * D + c4);
 #pragma unroll
       for (int s = 0; s < STEPS; ++s) {
         const float w = pk[i * DF + f0 + s * RPS + lr];
@@ -260,20 +303,15 @@ void decode_kernel(DecodeArgs a) {
         sr[s].z = fmaf(w, vv.z, sr[s].z);
         sr[s].w = fmaf(w, vv.w, sr[s].w);
       }
+      if (lane < RW) dz += pk[i * DF + f0 + lane];
     }
+    zf += dz;
     if (fold) {
       // On the first fold every row is written, whatever the memory held.
 #pragma unroll
       for (int s = 0; s < STEPS; ++s)
         if (!s_nonzero || ((touched >> s) & 1u)) store_nt(S + (f0 + s * RPS + lr) * D + c4, sr[s]);
-    }
-    float zf = 0.f;
-    if (lane < RW) {
-      zf = s_nonzero ? z[f0 + lane] : 0.f;
-      float dz = 0.f;
-      for (int i = 0; i < npend; ++i) dz += pk[i * DF + f0 + lane];
-      zf += dz;
-      if (fold && (dz != 0.f || !s_nonzero)) z[f0 + lane] = zf;
+      if (lane < RW && (dz != 0.f || !s_nonzero)) z[f0 + lane] = zf;
     }
     for (int hh = 0; hh < G; ++hh) {
       const float* pq = ph + hh * DF;
@@ -299,15 +337,13 @@ void decode_kernel(DecodeArgs a) {
     }
   }
 
-  };
-
-  auto window_phase = [&]() {
-  // ---- 3. window: softmax over tokens [tlo, p]
+  // ---- 5. window: softmax over the ring tokens [tlo, p-1]
   if (W > 0) {
-    const float sc2 = a.tau * kLog2e;
     f32x4_t acc[CT];
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) acc[ct] = zero4();
+    // running max (log2 units) and per-lane sum; the accumulator is only
+    // rescaled when the max grows by more than 8 (weights stay below 2^8)
     float m_run = -INFINITY, l_run = 0.f;
 
     auto compute_tile = [&](const WindowTile<T, D>& tl, int lo, int pn) {
@@ -316,69 +352,65 @@ void decode_kernel(DecodeArgs a) {
       for (int t = 0; t < 2; ++t) {
         sc[t] = zero4();
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) sc[t] = mma(tl.k[t][kk], qf[kk], sc[t]);
+        for (int kk = 0; kk < KS; ++kk) sc[t] = mma(tl.k[t][kk], xa[kk], sc[t]);
       }
       float s[8];
-      float mx = -INFINITY;
+      if (lo <= 0 && pn >= 32) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int off = 8 * lg + 4 * t + i;
-          const float v = (off >= lo && off <= pn) ? sc[t][i] * sc2 : -INFINITY;
-          s[4 * t + i] = v;
-          mx = fmaxf(mx, v);
-        }
+          for (int i = 0; i < 4; ++i) s[4 * t + i] = sc[t][i] * sc2;
+      } else {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int off = 8 * lg + 4 * t + i;
+            s[4 * t + i] = (off >= lo && off < pn) ? sc[t][i] * sc2 : -INFINITY;
+          }
       }
+      float mx = s[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) mx = fmaxf(mx, s[i]);
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = exp2f(m_run - m_new);
+      if (__any(mx > m_run + 8.f)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = m_run == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+        m_run = m_new;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float al = __shfl(alpha, 4 * lg + i);
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) acc[ct][i] *= al;
+        }
+      }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
       float pv[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pv[i] = exp2f(s[i] - m_new);
+      for (int i = 0; i < 8; ++i) pv[i] = __builtin_amdgcn_exp2f(s[i] - m_use);
       Frag<T> pf;
       pf.set8(pv);
-      l_run = l_run * alpha + pf.sum();
-      m_run = m_new;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float al = __shfl(alpha, 4 * lg + i);
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[ct][i] *= al;
-      }
+      l_run += pf.sum();
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct) acc[ct] = mma(pf, tl.v[ct], acc[ct]);
     };
 
-    if constexpr (kTwoStages) {
-      // two register stages: tile it+4 loads while tile it computes
-      WindowTile<T, D> tb;
-      while (it < n_tiles) {
-        if (it + kWaves < n_tiles)
-          load_tile(tb, wrap_once(s0 + step, R), clamp_rel(tlo - j0 - 32 * kWaves),
-                    clamp_rel(p - j0 - 32 * kWaves));
-        compute_tile(ta, clamp_rel(tlo - j0), clamp_rel(p - j0));
-        it += kWaves;
-        j0 += 32 * kWaves;
-        s0 = wrap_once(s0 + step, R);
-        if (it >= n_tiles) break;
-        if (it + kWaves < n_tiles)
-          load_tile(ta, wrap_once(s0 + step, R), clamp_rel(tlo - j0 - 32 * kWaves),
-                    clamp_rel(p - j0 - 32 * kWaves));
-        compute_tile(tb, clamp_rel(tlo - j0), clamp_rel(p - j0));
-        it += kWaves;
-        j0 += 32 * kWaves;
-        s0 = wrap_once(s0 + step, R);
-      }
-    } else {
-      while (it < n_tiles) {
-        compute_tile(ta, clamp_rel(tlo - j0), clamp_rel(p - j0));
-        it += kWaves;
-        j0 += 32 * kWaves;
-        s0 = wrap_once(s0 + step, R);
-        if (it < n_tiles) load_tile(ta, s0, clamp_rel(tlo - j0), clamp_rel(p - j0));
-      }
+    // two register stages: the next tile's loads are in flight while the
+    // current one is computed (a tile past the range reads zeros)
+    while (it < n_tiles) {
+      load_tile(tb, wrap_once(s0 + step, R), it + kWaves < n_tiles);
+      compute_tile(ta, clamp_rel(tlo - j0), clamp_rel(p - j0));
+      it += kWaves;
+      j0 += 32 * kWaves;
+      s0 = wrap_once(s0 + step, R);
+      if (it >= n_tiles) break;
+      load_tile(ta, wrap_once(s0 + step, R), it + kWaves < n_tiles);
+      compute_tile(tb, clamp_rel(tlo - j0), clamp_rel(p - j0));
+      it += kWaves;
+      j0 += 32 * kWaves;
+      s0 = wrap_once(s0 + step, R);
     }
 
     l_run += __shfl_xor(l_run, 16);
@@ -396,19 +428,10 @@ void decode_kernel(DecodeArgs a) {
       }
     }
   }
-  };
-
-#if GLIDE_DECODE_STATE_LAST
-  window_phase();
-  load_state();
-  state_phase();
-#else
-  state_phase();
-  window_phase();
-#endif
   __syncthreads();
 
-  // ---- 4. shared-denominator merge and output
+  // ---- 6. shared-denominator merge over the waves and the new token (and,
+  //         for a split unit, over the pieces in merge_kernel)
   for (int i = tid; i < G * D; i += kThreads) {
     const int hh = i / D, c = i - hh * D;
     float nm = 0.f, dn = 0.f;
@@ -419,12 +442,12 @@ void decode_kernel(DecodeArgs a) {
         dn += lden[w * G + hh];
       }
     }
-    float o;
+    float M = -INFINITY, Ls = 0.f, Ac = 0.f;
     if (W > 0) {
-      float M = -INFINITY;
+      const float sp = spl[hh];
+      M = sp;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wm[w * G + hh]);
-      float Ls = 0.f, Ac = 0.f;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
         const float mw = wm[w * G + hh];
@@ -434,6 +457,25 @@ void decode_kernel(DecodeArgs a) {
           Ac = fmaf(wacc[(w * G + hh) * D + c], e, Ac);
         }
       }
+      if (sp != -INFINITY) {
+        const float e = exp2f(sp - M);
+        Ls += e;
+        Ac = fmaf(vpl[c], e, Ac);
+      }
+    }
+    if (split) {
+      float* rec = a.part + int64_t(blockIdx.x) * part_floats(G, D) + int64_t(hh) * (2 * D + 3);
+      if (c == 0) {
+        rec[0] = M;
+        rec[1] = Ls;
+        rec[2] = dn;
+      }
+      rec[3 + c] = Ac;
+      if (piece == 0) rec[3 + D + c] = nm;
+      continue;
+    }
+    float o;
+    if (W > 0) {
       if (dn > 0.f) {
         const float c2 = fmaxf(M, log2f(dn));
         const float ws = exp2f(M - c2), wlin = exp2f(-c2);
@@ -446,10 +488,123 @@ void decode_kernel(DecodeArgs a) {
     }
     og[i] = from_f32<T>(o);
   }
-  if (tid == 0) {
-    *pos_ptr = p + 1;
+
+  // ---- 7. the new token into its ring slot (no token of this step reads
+  //         that slot), position and fold count
+  if (W > 0 && piece == 0 && tid < D) {
+    const int32_t sn = int32_t(p % R);
+    Kr[kring_elem(sn, tid, D)] = kraw;
+    Vr[vring_elem(sn, tid, D)] = vraw;
+  }
+  if (tid == 0 && piece == 0) {
+    if (!split) *pos_ptr = p + 1;  // a split unit's position moves in merge_kernel
     if (fold) *nf_ptr = beta;
   }
+}
+
+// Merge of the pieces of split units: the window parts (running max m, sum
+// l, weighted values acc per piece) over one max, plus piece 0's linear
+// part, over the shared denominator; then pos += 1.  Every record load of the
+// workgroup is issued before the first wait (one memory round trip).
+template <typename T, int D, int DF>
+__global__ __launch_bounds__(kThreads) void merge_kernel(DecodeArgs a) {
+  constexpr int EPT = 4;                   // output elements per thread whose loads go first
+  static_assert(kMaxPieces * kMaxG <= kThreads, "one (piece, head) scalar pair per thread");
+  __shared__ float pw[kThreads];  // [piece][G]: m, then its weight e^(m - M)
+  __shared__ float pl[kThreads];  // [piece][G]: l
+  __shared__ float hs[kMaxG][3];            // per head: window weight, linear weight, 1 / denominator
+  const int G = a.G, B = a.B, Hkv = a.Hkv, Hq = a.Hq;
+  const int per_layer = B * Hkv;
+  const int li = blockIdx.x / per_layer;
+  const int rem = blockIdx.x - li * per_layer;
+  const LayerArg L = a.layers[li];
+  const int np = L.npiece;
+  if (np <= 1) return;
+  const int b = rem / Hkv, g = rem - b * Hkv;
+  const int64_t unit = int64_t(b) * Hkv + g;
+  const LayerSections sec = layer_sections(B, Hkv, D, DF, L.R, sizeof(T));
+  int64_t* pos_ptr = reinterpret_cast<int64_t*>(a.state + L.base + sec.pos) + unit;
+  const int64_t tok = int64_t(L.slot) * B + b;
+  T* og = reinterpret_cast<T*>(a.out) + (tok * Hq + int64_t(g) * G) * D;
+  constexpr int RH = 2 * D + 3;  // floats per head in a record
+  const uint32_t rb = uint32_t(part_floats(G, D)) * 4;  // bytes per record
+  // piece 0's record, and those of pieces 1 .. np-1 (consecutive rows)
+  const brsrc_t r0 = make_rsrc(a.part + (int64_t(L.prow0) * per_layer + rem) * part_floats(G, D), rb);
+  const brsrc_t r1 = make_rsrc(a.part + (int64_t(L.prow1) * per_layer + rem) * part_floats(G, D),
+                               uint32_t(np - 1) * uint32_t(per_layer) * rb);
+  const uint32_t rs = uint32_t(per_layer) * rb;  // bytes between pieces 1..
+  const int tid = threadIdx.x;
+  const int n = G * D;
+  // per piece and head: m, l (threads tid < np * G), loaded first
+  const int mpc = tid / G, mh = tid - mpc * G;
+  const bool mok = tid < np * G;
+  const uint32_t mo = uint32_t(mh * RH) * 4;
+  const float m0 = bload_f(r0, mok && mpc == 0 ? mo : kOOB);
+  const float m1 = bload_f(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo : kOOB);
+  const float l0 = bload_f(r0, mok && mpc == 0 ? mo + 4 : kOOB);
+  const float l1 = bload_f(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo + 4 : kOOB);
+  const float dnv = bload_f(r0, tid < G ? uint32_t(tid * RH + 2) * 4 : kOOB);  // linear denominator
+  float v[EPT][kMaxPieces], nmv[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = tid + e * kThreads;
+    const int hh = i / D, c = i - hh * D;
+    const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
+    const bool ok = i < n;
+    v[e][0] = bload_f(r0, ok ? o : kOOB);
+#pragma unroll
+    for (int pc = 1; pc < kMaxPieces; ++pc) v[e][pc] = bload_f(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
+    nmv[e] = bload_f(r0, ok ? o + D * 4 : kOOB);
+  }
+  // every thread writes its slot (kThreads slots; no branch, so the loads
+  // above are not sunk behind the record loads)
+  pw[tid] = m0 + m1;  // at most one of the two is not an OOB zero
+  pl[tid] = l0 + l1;
+  __syncthreads();
+  if (tid < G) {
+    float M = -INFINITY;
+    for (int pc = 0; pc < np; ++pc) M = fmaxf(M, pw[pc * G + tid]);
+    float Ls = 0.f;
+    for (int pc = 0; pc < np; ++pc) {
+      const float e = pw[pc * G + tid] == -INFINITY ? 0.f : exp2f(pw[pc * G + tid] - M);
+      pw[pc * G + tid] = e;
+      Ls = fmaf(pl[pc * G + tid], e, Ls);
+    }
+    const float dn = dnv;
+    if (dn > 0.f) {
+      const float c2 = fmaxf(M, log2f(dn));
+      const float ws = exp2f(M - c2), wlin = exp2f(-c2);
+      hs[tid][0] = ws;
+      hs[tid][1] = wlin;
+      hs[tid][2] = 1.f / (Ls * ws + dn * wlin);
+    } else {
+      hs[tid][0] = 1.f;
+      hs[tid][1] = 0.f;
+      hs[tid][2] = 1.f / Ls;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = tid + e * kThreads;
+    if (i < n) {
+      const int hh = i / D;
+      float Ac = 0.f;
+#pragma unroll
+      for (int pc = 0; pc < kMaxPieces; ++pc) Ac = pc < np ? fmaf(v[e][pc], pw[pc * G + hh], Ac) : Ac;
+      const float nm = hs[hh][1] == 0.f ? 0.f : nmv[e];
+      og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
+    }
+  }
+  for (int i = tid + EPT * kThreads; i < n; i += kThreads) {  // G * D > EPT * 256 (large G)
+    const int hh = i / D, c = i - hh * D;
+    const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
+    float Ac = bload_f(r0, o) * pw[hh];
+    for (int pc = 1; pc < np; ++pc) Ac = fmaf(bload_f(r1, (pc - 1) * rs + o), pw[pc * G + hh], Ac);
+    const float nm = hs[hh][1] == 0.f ? 0.f : bload_f(r0, o + D * 4);
+    og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
+  }
+  if (tid == 0) *pos_ptr += 1;
 }
 
 // Fold every pending token of a unit into S and z (nf := beta = max(0, p-W)),
@@ -524,28 +679,33 @@ hipError_t flush_t(const DecodeArgs& a, hipStream_t stream) {
 }
 
 template <typename T, int D, int DF>
-hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
+hipError_t launch_t(const DecodeArgs& a, int total_wg, bool merge, hipStream_t stream) {
   const int G = a.G;
-  const size_t floats = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D +
+  const size_t floats = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D + 2 * D + kMaxG +
                         2 * (size_t(kWaves) * G * D + kWaves * G) + kWaves * G;
+  hipLaunchKernelGGL((decode_kernel<T, D, DF>), dim3(unsigned(total_wg)), dim3(kThreads), floats * sizeof(float),
+                     stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !merge) return e;
   const dim3 grid(unsigned(a.n_layers) * unsigned(a.B) * unsigned(a.Hkv));
-  hipLaunchKernelGGL((decode_kernel<T, D, DF>), grid, dim3(kThreads), floats * sizeof(float), stream, a);
+  hipLaunchKernelGGL((merge_kernel<T, D, DF>), grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream) {
+hipError_t launch_decode(const DecodeArgs& a, int total_wg, bool merge, int d, int Df, int dtype,
+                         hipStream_t stream) {
   if (dtype == GLIDE_BF16) {
-    if (d == 128 && Df == 128) return launch_t<bf16_t, 128, 128>(a, stream);
-    if (d == 128 && Df == 64) return launch_t<bf16_t, 128, 64>(a, stream);
-    if (d == 64 && Df == 128) return launch_t<bf16_t, 64, 128>(a, stream);
-    if (d == 64 && Df == 64) return launch_t<bf16_t, 64, 64>(a, stream);
+    if (d == 128 && Df == 128) return launch_t<bf16_t, 128, 128>(a, total_wg, merge, stream);
+    if (d == 128 && Df == 64) return launch_t<bf16_t, 128, 64>(a, total_wg, merge, stream);
+    if (d == 64 && Df == 128) return launch_t<bf16_t, 64, 128>(a, total_wg, merge, stream);
+    if (d == 64 && Df == 64) return launch_t<bf16_t, 64, 64>(a, total_wg, merge, stream);
   } else {
-    if (d == 128 && Df == 128) return launch_t<float, 128, 128>(a, stream);
-    if (d == 128 && Df == 64) return launch_t<float, 128, 64>(a, stream);
-    if (d == 64 && Df == 128) return launch_t<float, 64, 128>(a, stream);
-    if (d == 64 && Df == 64) return launch_t<float, 64, 64>(a, stream);
+    if (d == 128 && Df == 128) return launch_t<float, 128, 128>(a, total_wg, merge, stream);
+    if (d == 128 && Df == 64) return launch_t<float, 128, 64>(a, total_wg, merge, stream);
+    if (d == 64 && Df == 128) return launch_t<float, 64, 128>(a, total_wg, merge, stream);
+    if (d == 64 && Df == 64) return launch_t<float, 64, 64>(a, total_wg, merge, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -79,14 +79,63 @@ PrefillWorkspace prefill_ws(const glide_config* c, int64_t T) {
                            max_window(c), linear_on(c));
 }
 
-// Decode needs no workspace.
-size_t decode_ws(const glide_config*) { return 0; }
+// Decode window split (pieces per unit of each layer).  The work of a unit
+// is counted in 32-token window tiles plus kStateTiles for the state pass; a
+// layer whose units have work w gets min(kMaxPieces, ceil(w / q)) pieces, with
+// q the smallest piece size (>= 4 tiles) for which the whole stack fits in
+// kDecodeSlots workgroups.  When the units alone fill the slots, nothing is
+// split.
+std::vector<int32_t> decode_pieces(const glide_config* c) {
+  std::vector<int32_t> np(c->n_layers, 1);
+  const int64_t per_layer = int64_t(c->batch) * c->n_kv_heads;
+  if (per_layer * c->n_layers >= kDecodeSlots) return np;
+  const int st = linear_on(c) ? kStateTiles : 0;
+  std::vector<int64_t> work(c->n_layers);
+  int64_t wmax = 4;
+  for (int32_t l = 0; l < c->n_layers; ++l) {
+    work[l] = c->windows[l] > 0 ? decode_tiles_max(c->windows[l]) + st : 0;
+    wmax = std::max(wmax, work[l]);
+  }
+  auto pieces = [&](int64_t q, int32_t l) {
+    if (work[l] == 0) return int64_t(1);
+    return std::min<int64_t>(kMaxPieces, std::max<int64_t>(1, (work[l] + q - 1) / q));
+  };
+  auto wgs = [&](int64_t q) {
+    int64_t n = 0;
+    for (int32_t l = 0; l < c->n_layers; ++l) n += pieces(q, l) * per_layer;
+    return n;
+  };
+  int64_t lo = 4, hi = wmax;  // wgs(wmax) = units <= slots
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) / 2;
+    if (wgs(mid) <= kDecodeSlots) hi = mid;
+    else lo = mid + 1;
+  }
+  for (int32_t l = 0; l < c->n_layers; ++l) np[l] = int32_t(pieces(lo, l));
+  return np;
+}
+
+// Decode workspace: the partial records of every workgroup of a launch when
+// some layer is split (records are indexed by workgroup).
+size_t decode_ws(const glide_config* c) {
+  const std::vector<int32_t> np = decode_pieces(c);
+  int64_t wgs = 0;
+  bool any = false;
+  for (int32_t l = 0; l < c->n_layers; ++l) {
+    wgs += int64_t(np[l]) * c->batch * c->n_kv_heads;
+    any = any || np[l] > 1;
+  }
+  if (!any) return 0;
+  return size_t(align256(wgs * part_floats(c->n_q_heads / c->n_kv_heads, c->head_dim) * 4));
+}
 
 // Decode-style launch descriptor of layers [layer0, layer0 + n): per launch
 // group of at most kMaxLayersPerLaunch layers, ordered by decreasing window
 // (the hardware dispatcher then hands out the longest streams first).
 template <typename Fn>
 glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n_layers, DecodeArgs& a, Fn fn) {
+  const std::vector<int32_t> np = decode_pieces(cfg);
+  const int32_t per_layer = cfg->batch * cfg->n_kv_heads;
   std::vector<int32_t> order(n_layers);
   for (int32_t i = 0; i < n_layers; ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
@@ -101,15 +150,26 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
   for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
     a.n_layers = cnt;
-    for (int32_t i = 0; i < cnt; ++i) {
+    int32_t rows = 0;
+    bool split = false;
+    for (int32_t i = 0; i < cnt; ++i) {  // piece 0 of every layer first
       const int32_t slot = order[first + i];
       const int32_t l = layer0 + slot;
       a.layers[i].base = layer_base(cfg, l);
       a.layers[i].W = cfg->windows[l];
       a.layers[i].R = ring_slots(cfg->windows[l]);
       a.layers[i].slot = slot;
+      a.layers[i].npiece = np[l];
+      a.layers[i].prow0 = rows;
+      a.piece_layer[rows++] = uint8_t(i);
+      split = split || np[l] > 1;
     }
-    const glide_status s = hip_status(fn(a));
+    for (int32_t i = 0; i < cnt; ++i) {  // then the other pieces
+      const int32_t l = layer0 + order[first + i];
+      a.layers[i].prow1 = rows;
+      for (int32_t r = 1; r < np[l]; ++r) a.piece_layer[rows++] = uint8_t(i);
+    }
+    const glide_status s = hip_status(fn(a, rows * per_layer, split));
     if (s != GLIDE_OK) return s;
   }
   return GLIDE_OK;
@@ -192,8 +252,9 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
   a.k = k;
   a.v = v;
   a.out = out;
-  return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g) {
-    return launch_decode(g, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
+  a.part = static_cast<float*>(workspace);
+  return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g, int32_t wgs, bool split) {
+    return launch_decode(g, wgs, split, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
   });
 }
 
@@ -208,7 +269,7 @@ glide_status glide_state_flush(const glide_config* cfg, void* state, size_t stat
   memset(&a, 0, sizeof(a));
   a.state = static_cast<char*>(state);
   a.phi_w = phi_w;
-  return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g) {
+  return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g, int32_t, bool) {
     return launch_flush(g, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
   });
 }

@@ -78,8 +78,26 @@ struct LayerArg {
   int32_t W;       // softmax window
   int32_t R;       // ring slots
   int32_t slot;    // index of the layer inside the call's q/k/v/out/phi_w arrays
-  int32_t pad;
+  int32_t npiece;  // decode: workgroups per unit (window split), >= 1
+  int32_t prow0;   // decode: piece row (workgroup / (B*Hkv)) of the layer's piece 0
+  int32_t prow1;   // decode: piece row of its piece 1 (pieces 1.. are consecutive)
 };
+
+// Decode window split.  When a call has few units the longest windows would
+// leave most CUs idle, so a unit's window tiles are spread over npiece
+// workgroups ("pieces"); piece 0 also does the ring write and the state.
+// Pieces write partial records (running max, sum and weighted values of the
+// window part per head; piece 0 adds the linear part), and a second kernel
+// merges them.  The split depends on the configuration only: the pieces are
+// made as small as possible while every workgroup of the stack still fits in
+// one round of kDecodeSlots resident workgroups (256 CUs x 2), since a
+// second round would be latency-bound; large batches are never split.
+constexpr int kDecodeSlots = 512;
+constexpr int kMaxPieces = 16;
+constexpr int kStateTiles = 4;      // state pass cost in 32-token window tiles
+__host__ __device__ inline int decode_tiles_max(int32_t W) { return W > 0 ? (W + 31) / 32 + 1 : 0; }
+// floats of one partial record: per head m, l, dn, acc[d], nm[d]
+__host__ __device__ inline int64_t part_floats(int G, int d) { return int64_t(G) * (2 * d + 3); }
 
 // ---------------------------------------------------------------------------
 // Element types.  bf16 is carried as raw 16-bit patterns.
@@ -245,6 +263,62 @@ __device__ __forceinline__ void load_colfrag(Frag<float>& f, const float* M, int
   for (int e = 0; e < 8; ++e) f.v[e] = M[(row0 + e) * rs + col0 + n];
 }
 
+// Raw buffer loads: a descriptor (base, size in bytes) in scalar registers
+// and a 32-bit byte offset per lane.  A read at or beyond the size returns 0
+// without a memory access, so a load that may not be needed is issued
+// unconditionally with offset kOOB: no branch around it, and the compiler's
+// memory-counter waits stay exact.
+typedef __amdgpu_buffer_rsrc_t brsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;
+__device__ __forceinline__ brsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, int(bytes), 0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(brsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float4 bload_f4(brsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float bload_f(brsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ bf16_t bload_elem(brsrc_t r, uint32_t off, bf16_t) {
+  return bf16_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+}
+__device__ __forceinline__ float bload_elem(brsrc_t r, uint32_t off, float) { return bload_f(r, off); }
+// Fragment loads through a descriptor: 8 consecutive elements at byte offset off.
+__device__ __forceinline__ void bload_frag(Frag<bf16_t>& f, brsrc_t r, uint32_t off) { f.v = bload16(r, off); }
+__device__ __forceinline__ void bload_frag(Frag<float>& f, brsrc_t r, uint32_t off) {
+  const float4 a = bload_f4(r, off), b = bload_f4(r, off == kOOB ? kOOB : off + 16);
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+}
+// 8 elements at byte offsets off, off + stride, ...  (kOOB: zeros)
+__device__ __forceinline__ void bload_frag_strided(Frag<bf16_t>& f, brsrc_t r, uint32_t off, uint32_t stride) {
+  uint16_t e[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) e[i] = uint16_t(__builtin_amdgcn_raw_buffer_load_b16(r, off + i * stride, 0, 0));
+  f.v.x = uint32_t(e[0]) | (uint32_t(e[1]) << 16);
+  f.v.y = uint32_t(e[2]) | (uint32_t(e[3]) << 16);
+  f.v.z = uint32_t(e[4]) | (uint32_t(e[5]) << 16);
+  f.v.w = uint32_t(e[6]) | (uint32_t(e[7]) << 16);
+}
+__device__ __forceinline__ void bload_frag_strided(Frag<float>& f, brsrc_t r, uint32_t off, uint32_t stride) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f.v[i] = bload_f(r, off + i * stride);
+}
+__device__ __forceinline__ Frag<bf16_t> frag_or(const Frag<bf16_t>& a, const Frag<bf16_t>& b) {
+  Frag<bf16_t> r;
+  r.v = make_uint4(a.v.x | b.v.x, a.v.y | b.v.y, a.v.z | b.v.z, a.v.w | b.v.w);
+  return r;
+}
+__device__ __forceinline__ Frag<float> frag_or(const Frag<float>& a, const Frag<float>& b) {
+  Frag<float> r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r.v[i] = __uint_as_float(__float_as_uint(a.v[i]) | __float_as_uint(b.v[i]));
+  return r;
+}
+
 // Streaming 16-byte store (non-temporal: the line is not kept in the caches).
 __device__ __forceinline__ void store_nt(float* p, float4 v) {
   __builtin_nontemporal_store(f32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<f32x4_t*>(p));
@@ -255,6 +329,7 @@ __device__ __forceinline__ void store_nt(float* p, float4 v) {
 
 struct DecodeArgs {
   char* state;
+  float* part;       // partial records [workgroup][G][2d+3] (split layers only)
   const void* phi_w;
   const void* q;
   const void* k;
@@ -266,10 +341,17 @@ struct DecodeArgs {
   int32_t n_layers;  // layers in this launch (<= kMaxLayersPerLaunch)
   int32_t pad;
   LayerArg layers[kMaxLayersPerLaunch];  // sorted by decreasing W
+  // layer (index into layers) of every piece row: workgroup w of the main
+  // pass belongs to layer piece_layer[w / (B*Hkv)].  The rows of every
+  // layer's piece 0 (the state pass, the longest chain) come first, so their
+  // loads are issued, and served, first.
+  uint8_t piece_layer[kMaxLayersPerLaunch * kMaxPieces];
 };
 
 // Host-side launchers (one translation unit per kernel family).
-hipError_t launch_decode(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
+// total_wg: workgroups of the main pass; merge: some layer is split.
+hipError_t launch_decode(const DecodeArgs& a, int total_wg, bool merge, int d, int Df, int dtype,
+                         hipStream_t stream);
 hipError_t launch_flush(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
 hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* out, int d, int Df, int dtype,
                            bool out_f32, hipStream_t stream);

@@ -168,6 +168,10 @@ def test_decode_argument_errors():
     assert _decode(g, ptrs=(4096, None, 4096, 4096, 4096)) == -1
     assert _decode(g, ptrs=(4096, 4096, 4096 + 2, 4096, 4096)) == -4   # q misaligned
     assert _decode(g, ptrs=(4096, 4096, 4096, 4096, 4104)) == -4       # out misaligned
+    # few units: the window split needs the workspace for its partial records
+    assert _decode(g, ws=None) == -1
+    assert _decode(g, ws=(1 << 20) + 16) == -4
+    assert _decode(g, ws_bytes=g.workspace_bytes(0) - 1) == -5
 
 
 
@@ -189,9 +193,15 @@ def test_flush_argument_errors():
 
 
 def test_workspace_sizes():
+    # 12 units: split windows, one partial record (G x (2d + 3) floats) per workgroup
     g = mk(n_layers=3, batch=2, n_q_heads=8, n_kv_heads=2, feat_dim=64)
-    assert g.workspace_bytes(0) == 256       # decode needs none: only the documented minimum
-    assert g.workspace_bytes(1000) > g.workspace_bytes(10) > 256
+    rec = 4 * (2 * 128 + 3) * 4
+    assert g.workspace_bytes(0) >= 3 * 2 * 2 * rec
+    assert g.workspace_bytes(0) <= 3 * 2 * 2 * 16 * rec + 256
+    # many units of similar windows: no unit is worth splitting, no decode workspace
+    big = mk(n_layers=4, batch=64, n_q_heads=16, n_kv_heads=8, windows=[0, 5, 64, 100])
+    assert big.workspace_bytes(0) == 256
+    assert g.workspace_bytes(100000) > g.workspace_bytes(10)
 
 
 def _prefill(g, cu, total, chunk=0, ws_bytes=None, state=256, ptrs=(4096,) * 6):

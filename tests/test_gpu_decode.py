@@ -122,7 +122,7 @@ def test_deferred_folding_state_every_step():
         qs = torch.stack([q[:, 0, 50 + step], q[:, 1, 23 + step]], 1).contiguous().cuda()
         ks = torch.stack([k[:, 0, 50 + step], k[:, 1, 23 + step]], 1).contiguous().cuda()
         vs = torch.stack([v[:, 0, 50 + step], v[:, 1, 23 + step]], 1).contiguous().cuda()
-        case.g.decode_step(st, phi, qs, ks, vs, torch.empty_like(qs))
+        case.g.decode_step(st, phi, qs, ks, vs, torch.empty_like(qs), case.ws)
         torch.cuda.synchronize()
         case.check_state(st, k, v, [51 + step, 24 + step], f"step {step}")
         for l in range(case.L):
@@ -130,3 +130,28 @@ def test_deferred_folding_state_every_step():
             folds += int((nf != prev[l]).sum())
             prev[l] = nf.clone()
     assert folds > 0
+
+
+def test_split_and_unsplit_paths():
+    """Few units: long windows are split over several workgroups and merged
+    (the decode workspace holds their partial records); 1024 units and more:
+    one workgroup per unit.  Both follow the definition from a ragged
+    prefilled state."""
+    small = Case([0, 5, 40, 300], batch=1, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=9)
+    big = Case([0, 5, 40, 300], batch=32, Hq=16, Hkv=8, d=64, Df=64, dtype=torch.bfloat16, seed=10)
+    assert small.g.workspace_bytes(0) > 256 and big.g.workspace_bytes(0) == 256
+    for case, lens in ((small, [333]), (big, [(37 * i) % 350 for i in range(32)])):
+        n = 6
+        q, k, v = case.tokens(max(lens) + n)
+        st = case.new_state()
+        case.prefill(st, q, k, v, [0] * case.B, lens)
+        phi = case.phi_w.cuda()
+        outs = []
+        for step in range(n):
+            sel = lambda x: torch.stack([x[:, b, lens[b] + step] for b in range(case.B)], 1).contiguous().cuda()
+            qs, ks, vs = sel(q), sel(k), sel(v)
+            o = torch.empty_like(qs)
+            case.g.decode_step(st, phi, qs, ks, vs, o, case.ws if case is small else None)
+            outs.append(o)
+        case.check_decode(torch.stack(outs, 2).cpu(), q, k, v, lens, n, f"B={case.B}")
+        case.check_state(st, k, v, [x + n for x in lens], f"B={case.B}")

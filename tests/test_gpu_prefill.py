@@ -116,7 +116,7 @@ def test_prefill_after_decode(dtype):
         ks = torch.stack([k[:, b, n1[b] + step] for b in range(2)], 1).contiguous().cuda()
         vs = torch.stack([v[:, b, n1[b] + step] for b in range(2)], 1).contiguous().cuda()
         o = torch.empty_like(qs)
-        case.g.decode_step(st, phi, qs, ks, vs, o)
+        case.g.decode_step(st, phi, qs, ks, vs, o, case.ws)
         outs.append(o)
     case.check_decode(torch.stack(outs, 2).cpu(), q, k, v, n1, m, "decode between prefills")
     starts = [a + m for a in n1]
