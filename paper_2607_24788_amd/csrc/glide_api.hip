@@ -75,8 +75,17 @@ int32_t max_window(const glide_config* c) {
 }
 
 PrefillWorkspace prefill_ws(const glide_config* c, int64_t T) {
-  return prefill_workspace(T, c->batch, c->n_q_heads, c->n_kv_heads, c->head_dim, c->feat_dim, esize(c),
-                           max_window(c), linear_on(c));
+  return prefill_workspace(T, c->batch, c->n_kv_heads, c->head_dim, c->feat_dim, esize(c), max_window(c),
+                           linear_on(c));
+}
+
+// Chunks per prefill segment: at least kMinSegTokens tokens (bounds the
+// records), and about one (segment, KV head) workgroup per CU when the call
+// is large enough; at most 16 chunks walked in order by one workgroup.
+int32_t segment_chunks(int64_t T, int Hkv, int32_t chunk) {
+  const int32_t lo = (kMinSegTokens + chunk - 1) / chunk;
+  const int64_t fill = T * Hkv / (int64_t(chunk) * 256);
+  return int32_t(std::max<int64_t>(lo, std::min<int64_t>(16, fill)));
 }
 
 // Decode window split (pieces per unit of each layer).  The work of a unit
@@ -306,17 +315,14 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   const bool lin = linear_on(cfg);
   const PrefillWorkspace w = prefill_ws(cfg, T);
   char* ws = static_cast<char*>(workspace);
-  const int32_t seg_len = chunk * kSegChunks;
+  const int32_t seg_len = chunk * segment_chunks(T, Hkv, chunk);
   hipStream_t st = hipStream_t(stream);
 
   PrefillArgs a;
   memset(&a, 0, sizeof(a));
   a.state = static_cast<char*>(state);
-  a.phq = ws + w.phq;
-  a.phk = ws + w.phk;
   a.hk = ws + w.hk;
   a.hv = ws + w.hv;
-  a.hphk = ws + w.hphk;
   a.seg = reinterpret_cast<float*>(ws + w.seg);
   a.B = B;
   a.Hq = Hq;
@@ -326,7 +332,6 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   a.tau = cfg->sm_scale;
   a.C = chunk;
   a.seg_len = seg_len;
-  a.npass = (chunk * (Hq / Hkv) + 127) / 128;
   a.Wcap = max_window(cfg);
 
   // fill the per-group tables of sequences [g0, g0 + n)
@@ -335,17 +340,14 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
     a.seq0 = g0;
     a.nseq = n;
     a.seg0 = seg0;
-    int32_t nseg = 0, nwg = 0;
+    int32_t nseg = 0;
     for (int i = 0; i < n; ++i) {
       a.seq_start[i] = cu_seqlens_host[g0 + i];
       a.seq_len[i] = cu_seqlens_host[g0 + i + 1] - cu_seqlens_host[g0 + i];
       a.seg_base[i] = nseg;
-      a.wg_base[i] = nwg;
       nseg += (a.seq_len[i] + seg_len - 1) / seg_len;
-      nwg += (a.seq_len[i] + chunk - 1) / chunk * a.npass;
     }
     a.seg_base[n] = nseg;
-    a.wg_base[n] = nwg;
     a.nseg = nseg;
     return nseg;
   };
@@ -360,23 +362,12 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
     a.k = static_cast<const char*>(k) + size_t(i) * T * Hkv * d * es;
     a.v = static_cast<const char*>(v) + size_t(i) * T * Hkv * d * es;
     a.out = static_cast<char*>(out) + size_t(i) * T * Hq * d * es;
-    const void* wf = static_cast<const char*>(phi_w) + size_t(i) * d * Df * es;
-    if (lin) {
-      s = hip_status(launch_phi_rows(wf, a.q, T * Hq, ws + w.phq, d, Df, cfg->dtype, cfg->dtype == GLIDE_F32, st));
-      if (s != GLIDE_OK) return s;
-      s = hip_status(launch_phi_rows(wf, a.k, T * Hkv, ws + w.phk, d, Df, cfg->dtype, cfg->dtype == GLIDE_F32, st));
-      if (s != GLIDE_OK) return s;
-    }
+    a.wf = static_cast<const char*>(phi_w) + size_t(i) * d * Df * es;
     if (W > 0) {
       // history of a continuing prefill (nothing to copy when pos == 0)
       for (int g0 = 0; g0 < B; g0 += kMaxSeqPerLaunch) {
         group(g0, 0);
         s = hip_status(launch_prefill_gather(a, d, Df, cfg->dtype, st));
-        if (s != GLIDE_OK) return s;
-      }
-      if (lin) {
-        s = hip_status(launch_phi_rows(wf, a.hk, int64_t(B) * Hkv * W, ws + w.hphk, d, Df, cfg->dtype,
-                                       cfg->dtype == GLIDE_F32, st));
         if (s != GLIDE_OK) return s;
       }
     }

@@ -262,6 +262,55 @@ __device__ __forceinline__ void load_colfrag(Frag<float>& f, const float* M, int
 #pragma unroll
   for (int e = 0; e < 8; ++e) f.v[e] = M[(row0 + e) * rs + col0 + n];
 }
+// As load_colfrag, with the 8 rows taken as rows r0 .. r0+3, then r1 .. r1+3
+// (a permuted order of the reduction index, shared with the other operand).
+__device__ __forceinline__ void load_colfrag2(Frag<bf16_t>& f, const bf16_t* M, int rs, int r0, int r1, int col0) {
+  const int n = threadIdx.x & 15;
+  const bf16_t* p = M + (r0 + (n >> 2)) * rs + col0 + 4 * (n & 3);
+  const bf16_t* q = M + (r1 + (n >> 2)) * rs + col0 + 4 * (n & 3);
+  const i16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(__attribute__((address_space(3))) bf16_t*)(p));
+  const i16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(__attribute__((address_space(3))) bf16_t*)(q));
+  f.v.x = uint32_t(uint16_t(a[0])) | (uint32_t(uint16_t(a[1])) << 16);
+  f.v.y = uint32_t(uint16_t(a[2])) | (uint32_t(uint16_t(a[3])) << 16);
+  f.v.z = uint32_t(uint16_t(b[0])) | (uint32_t(uint16_t(b[1])) << 16);
+  f.v.w = uint32_t(uint16_t(b[2])) | (uint32_t(uint16_t(b[3])) << 16);
+}
+__device__ __forceinline__ void load_colfrag2(Frag<float>& f, const float* M, int rs, int r0, int r1, int col0) {
+  const int n = threadIdx.x & 15;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f.v[e] = M[(r0 + e) * rs + col0 + n];
+    f.v[4 + e] = M[(r1 + e) * rs + col0 + n];
+  }
+}
+// From an fp32 LDS tile, converted to the fragment's element type.
+__device__ __forceinline__ void load_colfrag2_f32(Frag<bf16_t>& f, const float* M, int rs, int r0, int r1,
+                                                  int col0) {
+  const int n = threadIdx.x & 15;
+  float x[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[e] = M[(r0 + e) * rs + col0 + n];
+    x[4 + e] = M[(r1 + e) * rs + col0 + n];
+  }
+  f.set8(x);
+}
+__device__ __forceinline__ void load_colfrag2_f32(Frag<float>& f, const float* M, int rs, int r0, int r1, int col0) {
+  load_colfrag2(f, M, rs, r0, r1, col0);
+}
+// 8 elements of one row: 4 at column c0, 4 at column c1 (the same permuted
+// reduction order, for an operand stored row-major).
+__device__ __forceinline__ void load_row2(Frag<bf16_t>& f, const bf16_t* row, int c0, int c1) {
+  const uint2 a = *reinterpret_cast<const uint2*>(row + c0);
+  const uint2 b = *reinterpret_cast<const uint2*>(row + c1);
+  f.v = make_uint4(a.x, a.y, b.x, b.y);
+}
+__device__ __forceinline__ void load_row2(Frag<float>& f, const float* row, int c0, int c1) {
+  const float4 a = *reinterpret_cast<const float4*>(row + c0);
+  const float4 b = *reinterpret_cast<const float4*>(row + c1);
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+}
 
 // Raw buffer loads: a descriptor (base, size in bytes) in scalar registers
 // and a 32-bit byte offset per lane.  A read at or beyond the size returns 0
@@ -360,7 +409,6 @@ hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* ou
 // Prefill.  Sequences are processed in groups of at most kMaxSeqPerLaunch so
 // the per-sequence tables travel in the kernel arguments.
 constexpr int kMaxSeqPerLaunch = 128;
-constexpr int kSegChunks = 4;  // chunks per segment of the state scan
 
 struct PrefillArgs {
   char* state;
@@ -370,11 +418,9 @@ struct PrefillArgs {
   const void* k;        // [T][Hkv][d]
   const void* v;        // [T][Hkv][d]
   void* out;            // [T][Hq][d]
-  const void* phq;      // workspace: phi(q)  [T][Hq][Df]   (element type T)
-  const void* phk;      // workspace: phi(k)  [T][Hkv][Df]
+  const void* wf;       // this layer's feature-map matrix [d][Df]
   void* hk;             // workspace: history keys    [B][Hkv][Wcap][d]
   void* hv;             // workspace: history values  [B][Hkv][Wcap][d]
-  void* hphk;           // workspace: phi(history)    [B][Hkv][Wcap][Df]
   float* seg;           // workspace: per (segment, KV head) S [Df][d] then z [Df]
   int32_t B, Hq, Hkv, G;
   int32_t linear;
@@ -387,19 +433,19 @@ struct PrefillArgs {
   int32_t seg0;         // first segment record of the group
   int32_t nseg;         // segments in this group
   int32_t pad;
-  int32_t npass;        // 128-row passes per chunk: ceil(C * G / 128)
-  int32_t pad2;
   int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token
   int32_t seq_len[kMaxSeqPerLaunch];       // new tokens of the sequence
   int32_t seg_base[kMaxSeqPerLaunch + 1];  // first segment (within the group) of the sequence
-  int32_t wg_base[kMaxSeqPerLaunch + 1];   // first (chunk, pass) workgroup of the sequence
 };
+
+// Segments hold at least kMinSegTokens tokens, which bounds the records.
+constexpr int kMinSegTokens = 128;
 
 struct PrefillWorkspace {
-  size_t phq, phk, hk, hv, hphk, seg, total;
+  size_t hk, hv, seg, total;
 };
 
-inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hq, int Hkv, int d, int Df, int esize, int Wcap,
+inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hkv, int d, int Df, int esize, int Wcap,
                                           bool linear) {
   PrefillWorkspace w;
   size_t off = 0;
@@ -408,13 +454,9 @@ inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hq, int Hkv, int
     off += size_t(align256(int64_t(bytes)));
     return o;
   };
-  w.phq = take(linear ? size_t(T) * Hq * Df * esize : 0);
-  w.phk = take(linear ? size_t(T) * Hkv * Df * esize : 0);
   w.hk = take(size_t(B) * Hkv * Wcap * d * esize);
   w.hv = take(size_t(B) * Hkv * Wcap * d * esize);
-  w.hphk = take(linear ? size_t(B) * Hkv * Wcap * Df * esize : 0);
-  // segments of kSegChunks chunks of at least 32 tokens: at most T/128 + B of them
-  w.seg = take(linear ? (size_t(T) / (32 * kSegChunks) + B) * Hkv * (size_t(Df) * d + Df) * 4 : 0);
+  w.seg = take(linear ? (size_t(T) / kMinSegTokens + B) * Hkv * (size_t(Df) * d + Df) * 4 : 0);
   w.total = off;
   return w;
 }
