@@ -65,11 +65,17 @@ def main():
     ap.add_argument("--workload", default="c2")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run 5 device-to-device copies of MIB MiB (the known-size kernel that "
+                         "calibrates the FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested); the hybrid-attention "
               "step has no multi-GPU path in this build", file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
 
     import torch
     from paper_2607_24788_amd import glide, workload as W
@@ -144,13 +150,17 @@ def main():
     dec_step_s = dec_ms * 1e-3 / max(wl.decode_steps, 1)
     pre_flops = prefill_flops(wl, lens)
     mfma_peak = MFMA_BF16_PEAK if wl.dtype == torch.bfloat16 else MFMA_FP32_PEAK
-    hbm = {"bound": "hbm", "kernel": "decode step (decode_kernel)",
+    traffic = measured_traffic(wl.name)
+    hbm = {"bound": "hbm", "kernel": "decode step (decode_kernel, + merge_kernel when windows are split)",
            "achieved": dec_bytes / dec_step_s / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-           "frac": dec_bytes / dec_step_s / HBM_PEAK, "traffic": None,
+           "frac": dec_bytes / dec_step_s / HBM_PEAK,
+           "traffic": traffic and traffic["decode_step_bytes"],
            "algorithmic_bytes_per_launch": dec_bytes, "avg_launch_us": dec_step_s * 1e6}
-    mfma = {"bound": "mfma", "kernel": "prefill call (all layers)",
+    mfma = {"bound": "mfma", "kernel": "glide_prefill call over the stack (prefill_main + segsum/scan/ringfill/"
+                                      "advance/gather per layer)",
             "achieved": pre_flops / (pre_ms * 1e-3) / 1e12, "peak": mfma_peak / 1e12, "unit": "TFLOP/s",
-            "frac": pre_flops / (pre_ms * 1e-3) / mfma_peak, "traffic": None,
+            "frac": pre_flops / (pre_ms * 1e-3) / mfma_peak,
+            "traffic": traffic and traffic["prefill_call_bytes"],
             "algorithmic_flops_per_launch": pre_flops, "avg_launch_us": pre_ms * 1e3}
     dominant = hbm if dec_ms >= pre_ms else mfma
 
@@ -182,6 +192,53 @@ def main():
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, g, state, phi, dq, dk, dv, args.cpu_baseline_seconds)
     print(json.dumps(line), flush=True)
+
+
+def kernel_sources_hash():
+    """sha256 prefix over the kernel sources (csrc/*.hip, csrc/*.h, include/glide.h)."""
+    import glob
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    files = sorted(glob.glob(os.path.join(root, "paper_2607_24788_amd", "csrc", "*.hip")) +
+                   glob.glob(os.path.join(root, "paper_2607_24788_amd", "csrc", "*.h")))
+    files.append(os.path.join(root, "include", "glide.h"))
+    h = hashlib.sha256()
+    for f in files:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload_name):
+    """HBM-side bytes per prefill call and per decode step from the rocprofv3
+    FETCH_SIZE / WRITE_SIZE runs summarised in profiles/ (copy-calibrated);
+    None when the kernels have changed since the counters were taken."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("sources_sha256_16") != kernel_sources_hash():
+        return None
+    w = t.get("workloads", {}).get(workload_name)
+    if not w:
+        return None
+    return {"decode_step_bytes": round(w["decode_step_bytes"]), "prefill_call_bytes": round(w["prefill_call_bytes"])}
+
+
+def copy_probe(mib):
+    """Plain device-to-device copies of a known size: under rocprofv3 --pmc
+    their FETCH_SIZE / WRITE_SIZE per dispatch give the factor that turns the
+    counters into bytes."""
+    import torch
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "copies": 5}), flush=True)
 
 
 def cpu_baseline(wl, g, state, phi, dq, dk, dv, budget_s):
