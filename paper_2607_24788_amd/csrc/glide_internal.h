@@ -311,6 +311,16 @@ __device__ __forceinline__ void load_row2(Frag<float>& f, const float* row, int 
   f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
   f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
 }
+// The same from an fp32 row, converted to the fragment's element type.
+__device__ __forceinline__ void load_row2_f32(Frag<bf16_t>& f, const float* row, int c0, int c1) {
+  const float4 a = *reinterpret_cast<const float4*>(row + c0);
+  const float4 b = *reinterpret_cast<const float4*>(row + c1);
+  const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  f.set8(x);
+}
+__device__ __forceinline__ void load_row2_f32(Frag<float>& f, const float* row, int c0, int c1) {
+  load_row2(f, row, c0, c1);
+}
 
 // Raw buffer loads: a descriptor (base, size in bytes) in scalar registers
 // and a 32-bit byte offset per lane.  A read at or beyond the size returns 0
@@ -365,6 +375,43 @@ __device__ __forceinline__ Frag<float> frag_or(const Frag<float>& a, const Frag<
   Frag<float> r;
 #pragma unroll
   for (int i = 0; i < 8; ++i) r.v[i] = __uint_as_float(__float_as_uint(a.v[i]) | __float_as_uint(b.v[i]));
+  return r;
+}
+// The same LDS address, opaque to the compiler.  Taken at the start of a
+// phase, it keeps that phase's accesses to one base register per array plus
+// constants carried in the instructions' 16-bit offset field.  (Constants
+// counted from the start of an LDS allocation over 64 KiB do not fit that
+// field: each then takes a register of its own, computed once and kept live,
+// or spilled, across the whole kernel.)
+template <typename P>
+__device__ __forceinline__ P* lds_fresh(P* p) {
+  uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) P*)p));
+  asm volatile("" : "+s"(a));
+  return (P*)((__attribute__((address_space(3))) P*)(uintptr_t)a);
+}
+
+// The same wave-uniform pointer, opaque to the compiler: per-lane addresses
+// derived from it after this point are computed there, not hoisted from a
+// loop and kept live (or spilled) across it.
+template <typename P>
+__device__ __forceinline__ P* sfresh(P* p) {
+  // through the global address space, so that accesses stay global (not flat)
+  auto q = (__attribute__((address_space(1))) P*)p;
+  asm volatile("" : "+s"(q));
+  return (P*)q;
+}
+
+// a if keep, else zeros: a select on registers (taken where the value is
+// used), not a branch around the load that produced a.
+__device__ __forceinline__ Frag<bf16_t> frag_keep(const Frag<bf16_t>& a, bool keep) {
+  Frag<bf16_t> r;
+  r.v = make_uint4(keep ? a.v.x : 0u, keep ? a.v.y : 0u, keep ? a.v.z : 0u, keep ? a.v.w : 0u);
+  return r;
+}
+__device__ __forceinline__ Frag<float> frag_keep(const Frag<float>& a, bool keep) {
+  Frag<float> r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r.v[i] = keep ? a.v[i] : 0.f;
   return r;
 }
 

@@ -67,6 +67,13 @@ struct SeqRows {
     if (j >= h0) return vh + (j - h0) * D;
     return nullptr;
   }
+  // A key/value row that always exists (the sequence's first new token):
+  // masked-off lanes load from it, so that every load is unconditional and
+  // the zeros are selected where the value is used.  (A load skipped by a
+  // branch whose other side zeroes the register makes the wave wait for the
+  // loads in flight, serialising the prefetches.)
+  __device__ const T* k_safe() const { return kin + (int64_t(start) * Hkv + g) * D; }
+  __device__ const T* v_safe() const { return vin + (int64_t(start) * Hkv + g) * D; }
   // packed query row of new token i (0-based within the call) and head hh of the group
   __device__ int64_t qrow(int i, int hh) const { return (int64_t(start) + i) * Hq + int64_t(g) * G + hh; }
 };
@@ -104,6 +111,14 @@ __device__ __forceinline__ void store8(float* dst, const Frag<float>& f) {
   reinterpret_cast<float4*>(dst)[1] = make_float4(f.v[4], f.v[5], f.v[6], f.v[7]);
 }
 
+// 4 consecutive outputs (scaled) in one store: 8 bytes (bf16) or 16 (fp32).
+__device__ __forceinline__ void store4(bf16_t* dst, f32x4_t x, float s) {
+  *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(x[0] * s, x[1] * s), pack_bf16x2(x[2] * s, x[3] * s));
+}
+__device__ __forceinline__ void store4(float* dst, f32x4_t x, float s) {
+  *reinterpret_cast<float4*>(dst) = make_float4(x[0] * s, x[1] * s, x[2] * s, x[3] * s);
+}
+
 // LDS row strides (elements): tiles read with 16-byte fragment loads use a
 // padding of 8; tiles read with load_colfrag use 16 so the four rows a
 // 16-lane group touches fall on distinct banks.
@@ -135,33 +150,40 @@ __device__ __forceinline__ void stage_wf(const T* Wf, T* Wn, int nthreads) {
   }
 }
 
-// phi of 32 keys into LDS pk[32][row_t<DF>] (element type, natural layout).
-// The 2 x DF/16 output tiles are spread over the nw waves of the workgroup;
-// every tile of a wave has the same key tile (2*DF/16 is a multiple of nw), so
-// a wave loads the key rows of its tile once (slab_keys), and the loads can be
-// issued well before phi_slab consumes them.
+// phi of NK keys (16 per key tile) into LDS pk[NK][row_t<DF>] (element type,
+// natural layout).  The NK/16 x DF/16 output tiles are spread over the nw
+// waves of the workgroup so that every tile of a wave has the same key tile
+// (slab_key_tile): phi_slab takes that tile's key rows as A fragments x
+// (rows that do not exist are zeros).
+template <int D, int DF, int NK>
+__device__ __forceinline__ int slab_key_tile(int nw) {
+  constexpr int FT = DF / 16;
+  return (int(threadIdx.x >> 6) * ((NK / 16) * FT / nw)) / FT;
+}
 template <typename T, int D, int DF>
 struct SlabKeys {
   Frag<T> x[D / 32];
+  bool ok;  // the lane's key row exists (else it counts as zeros)
 };
-template <typename T, int D, int DF, typename RowFn>
-__device__ __forceinline__ void slab_keys(SlabKeys<T, D, DF>& sk, int nw, RowFn krow) {
+// krow(r) is the address of key row r of the slab, or nullptr (zeros); such
+// rows are loaded from safe and masked in phi_slab.
+template <typename T, int D, int DF, int NK, typename RowFn>
+__device__ __forceinline__ void slab_keys(SlabKeys<T, D, DF>& sk, int nw, RowFn krow, const T* safe) {
   constexpr int FT = DF / 16;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
-  const int kt = (wave * (2 * FT / nw)) / FT;
+  const int kt = slab_key_tile<D, DF, NK>(nw);
   const T* src = krow(16 * kt + hq);
+  sk.ok = src != nullptr;
+  if (!sk.ok) src = safe;
 #pragma unroll
-  for (int kk = 0; kk < D / 32; ++kk) {
-    if (src) sk.x[kk].load(src + 32 * kk + 8 * lg);
-    else sk.x[kk].zero();
-  }
+  for (int kk = 0; kk < D / 32; ++kk) sk.x[kk].load(src + 32 * kk + 8 * lg);
 }
-template <typename T, int D, int DF, bool kLds>
-__device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const SlabKeys<T, D, DF>& sk, T* pk,
+template <typename T, int D, int DF, int NK, bool kLds>
+__device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const Frag<T> (&x)[D / 32], T* pk,
                                          int nw) {
   constexpr int KS = D / 32, FT = DF / 16, PROW = row_t<DF>();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
-  const int per = 2 * FT / nw;  // tiles per wave
+  const int per = (NK / 16) * FT / nw;
   for (int u = 0; u < per; ++u) {
     const int tile = wave * per + u, kt = tile / FT, ft = tile - kt * FT;
     f32x4_t acc = zero4();
@@ -169,7 +191,7 @@ __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const
     for (int kk = 0; kk < KS; ++kk) {
       Frag<T> wb;
       wf.col(wb, kk, 16 * ft);
-      acc = mma(sk.x[kk], wb, acc);
+      acc = mma(x[kk], wb, acc);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) pk[(16 * kt + 4 * lg + i) * PROW + 16 * ft + hq] = from_f32<T>(fmaxf(acc[i], 0.f));
@@ -232,23 +254,29 @@ __global__ __launch_bounds__(kThreads) void prefill_segsum(PrefillArgs a) {
   constexpr int VPT = 32 * D / 8 / kThreads;  // value chunks per thread
   SlabKeys<T, D, DF> kx;
   Frag<T> vx[VPT];
+  bool vok[VPT];
   auto load_slab = [&](int64_t j0) {
-    slab_keys(kx, kWaves, [&](int r) { return j0 + r < jhi ? sr.k(j0 + r) : nullptr; });
+    slab_keys<T, D, DF, 32>(kx, kWaves, [&](int r) { return j0 + r < jhi ? sr.k(j0 + r) : nullptr; }, sr.k_safe());
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
       const int id = tid + u * kThreads, r = id / (D / 8), ch = id - r * (D / 8);
-      if (j0 + r < jhi) vx[u].load(sr.v(j0 + r) + 8 * ch);
-      else vx[u].zero();
+      vok[u] = j0 + r < jhi;
+      vx[u].load((vok[u] ? sr.v(j0 + r) : sr.v_safe()) + 8 * ch);
     }
   };
   if (jlo < jhi) load_slab(jlo);
   for (int64_t j0 = jlo; j0 < jhi; j0 += 32) {
     __syncthreads();
-    phi_slab(wf, kx, pk, kWaves);
+    {
+      Frag<T> x[D / 32];
+#pragma unroll
+      for (int kk = 0; kk < D / 32; ++kk) x[kk] = frag_keep(kx.x[kk], kx.ok);
+      phi_slab<T, D, DF, 32>(wf, x, pk, kWaves);
+    }
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
       const int id = tid + u * kThreads, r = id / (D / 8), ch = id - r * (D / 8);
-      store8(vs + r * VROW + 8 * ch, vx[u]);
+      store8(vs + r * VROW + 8 * ch, frag_keep(vx[u], vok[u]));
     }
     if (j0 + 32 < jhi) load_slab(j0 + 32);
     __syncthreads();
@@ -299,25 +327,40 @@ __global__ __launch_bounds__(kThreads) void prefill_scan(PrefillArgs a) {
 
 // ---------------------------------------------------------------------------
 // main: the outputs of one segment of one (sequence, KV head), chunk by chunk.
+//
+// Accumulators are kept transposed (O^T = V^T P^T): a lane holds 4
+// consecutive output columns of one query row, so the online-softmax rescale
+// and the final normalisation are lane-local and the output leaves in 8-byte
+// (bf16) stores.
+//
+// The walk is software-pipelined over passes (256 query rows of a chunk):
+// the next pass's query rows, first slab of delayed keys and first band tile
+// are loaded before this pass's output stores.  Loads and stores retire in
+// order, so a load issued after the stores could only be waited for together
+// with them.
 template <typename T, int D, int DF>
 struct MainLds {
   static constexpr int NBUF = sizeof(T) == 2 ? 2 : 1;  // band stages (fp32: one, to fit)
+  static constexpr int SLAB = sizeof(T) == 4 && D == 128 ? 32 : 64;  // delayed keys per slab
   static constexpr int WROW = row_t<DF>(), PROW = row_t<DF>(), VROW = row_t<D>();
-  static constexpr int SROW = D + 4;                   // fp32 S: 4 rows of a 16-lane group on distinct banks
+  static constexpr int SROW = DF + 4;                  // fp32 S^T rows: 16 rows of a 16-byte access on distinct banks
   static constexpr int KROW = row_a<D>();
   static constexpr int BAND = 32 * KROW + 32 * VROW;  // one band buffer (elements)
-  static constexpr size_t rest = size_t(DF) * SROW * 4 + size_t(DF) * 4 + size_t(32) * PROW * sizeof(T) +
-                                 size_t(32) * VROW * sizeof(T) + size_t(NBUF) * BAND * sizeof(T);
-  // Wf in LDS when it fits beside the rest (all but fp32 with d = Df = 128,
-  // which reads it from global memory)
+  // the slab (phi(k), values, raw keys) and the band buffers are never live
+  // together
+  static constexpr size_t slab_b = size_t(SLAB) * (PROW + VROW + KROW) * sizeof(T);
+  static constexpr size_t band_b = size_t(NBUF) * BAND * sizeof(T);
+  static constexpr size_t shared_b = slab_b > band_b ? slab_b : band_b;
+  static constexpr size_t rest = size_t(D) * SROW * 4 + size_t(DF) * 4 + shared_b;
+  // Wf in LDS when it fits beside the rest (fp32 with d = 128 reads it from
+  // global memory)
   static constexpr bool kWfLds = size_t(D) * WROW * sizeof(T) + rest <= 160 * 1024;
   static constexpr size_t wn = 0;
   static constexpr size_t sn = wn + (kWfLds ? size_t(D) * WROW * sizeof(T) : 0);
-  static constexpr size_t zs = sn + size_t(DF) * SROW * 4;
-  static constexpr size_t pk = zs + size_t(DF) * 4;
-  static constexpr size_t vs = pk + size_t(32) * PROW * sizeof(T);
-  static constexpr size_t band = vs + size_t(32) * VROW * sizeof(T);
-  static constexpr size_t bytes = band + size_t(NBUF) * BAND * sizeof(T);
+  static constexpr size_t zs = sn + size_t(D) * SROW * 4;
+  static constexpr size_t sh = zs + size_t(DF) * 4;
+  static constexpr size_t bytes = sh + shared_b;
+  static_assert(bytes <= 160 * 1024, "LDS budget");
 };
 
 template <typename T, int D, int DF>
@@ -326,23 +369,27 @@ void prefill_main(PrefillArgs a) {
   using LD = MainLds<T, D, DF>;
   constexpr int KS = D / 32, KSF = DF / 32, CT = D / 16, FT = DF / 16;
   constexpr int NT = FT * CT / kMW;            // S tiles per wave (state update)
+  constexpr int SL = LD::SLAB;
   constexpr int SROW = LD::SROW, PROW = LD::PROW, VROW = LD::VROW, KROW = LD::KROW;
   constexpr int NBUF = LD::NBUF, BAND = LD::BAND;
   constexpr int CPR = D / 8;                   // 8-element chunks per K/V row
+  constexpr int VPT = SL * CPR / kMT;          // slab chunks per thread (keys; values alike)
   static_assert(NT * kMW == FT * CT, "S tiles must spread evenly over the waves");
-  static_assert(32 * CPR <= kMT, "one staging chunk per thread");
-  extern __shared__ __align__(16) char smem[];
-  T* Wn = reinterpret_cast<T*>(smem + LD::wn);    // [D][WROW]   Wf (bf16)
-  float* Sn = reinterpret_cast<float*>(smem + LD::sn);  // [DF][SROW]  S_c, fp32
-  float* zs = reinterpret_cast<float*>(smem + LD::zs);  // [DF] z_c
-  T* pk = reinterpret_cast<T*>(smem + LD::pk);    // [32][PROW]  phi(k) of 32 delayed keys
-  T* vs = reinterpret_cast<T*>(smem + LD::vs);    // [32][VROW]  their values
-  T* bnd = reinterpret_cast<T*>(smem + LD::band); // band tiles: [NBUF] x (K [32][KROW], V [32][VROW])
+  static_assert(32 * CPR <= kMT && VPT >= 1 && VPT * kMT == SL * CPR, "staging must divide evenly");
+  // static LDS: the layout is fixed per instantiation
+  __shared__ __align__(16) char smem[LD::bytes];
+  T* Wn = reinterpret_cast<T*>(smem + LD::wn);          // [D][WROW]    Wf
+  float* St = reinterpret_cast<float*>(smem + LD::sn);  // [D][SROW]    S_c^T, fp32
+  float* zs = reinterpret_cast<float*>(smem + LD::zs);  // [DF]         z_c
+  T* pk = reinterpret_cast<T*>(smem + LD::sh);          // [SL][PROW]   phi(k) of the delayed keys
+  T* vs = pk + SL * PROW;                               // [SL][VROW]   their values
+  T* kr = vs + SL * VROW;                               // [SL][KROW]   their keys
+  T* bnd = reinterpret_cast<T*>(smem + LD::sh);         // band tiles: [NBUF] x (K [32][KROW], V [32][VROW])
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hq = lane & 15, lg = lane >> 4;
   const int sg = blockIdx.x, g = blockIdx.y;
   const int bl = find_seq(a, sg);
-  const SeqRows<T, D> sr = seq_rows<T, D, DF>(a, bl, g);
+  SeqRows<T, D> sr = seq_rows<T, D, DF>(a, bl, g);
   const int sigma = sg - a.seg_base[bl];
   const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
   const int G = a.G, W = a.W, C = a.C;
@@ -350,186 +397,263 @@ void prefill_main(PrefillArgs a) {
   const float sc2 = a.tau * kLog2e;
   const T* Q = static_cast<const T*>(a.q);
   T* O = static_cast<T*>(a.out);
-  const WfCols<T, D, DF, LD::kWfLds> wf{LD::kWfLds ? Wn : static_cast<const T*>(a.wf)};
+  // the global bases, made opaque once per pass: row addresses are then
+  // computed where they are used instead of being kept across the walk
+  auto refresh = [&]() {
+    sr.kin = sfresh(sr.kin);
+    sr.vin = sfresh(sr.vin);
+    sr.kh = sfresh(sr.kh);
+    sr.vh = sfresh(sr.vh);
+    Q = sfresh(Q);
+    O = sfresh(O);
+  };
+  // Wf columns, with a fresh LDS base per phase
+  auto wf_cols = [&]() {
+    if constexpr (LD::kWfLds) return WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))};
+    else return WfCols<T, D, DF, false>{static_cast<const T*>(a.wf)};
+  };
 
   // ---- 0. Wf into LDS; S, z at the segment start (the scan's record), fp32,
-  //         into LDS; they stay there for the whole walk
+  //         into LDS (S transposed); they stay there for the whole walk
   if (linear) {
     if (LD::kWfLds) stage_wf<T, D, DF>(static_cast<const T*>(a.wf), Wn, kMT);
     const float* S0 = a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
     for (int i = tid; i < DF * D / 4; i += kMT) {
       const int f = i / (D / 4), c4 = 4 * (i - f * (D / 4));
-      *reinterpret_cast<float4*>(Sn + f * SROW + c4) = *reinterpret_cast<const float4*>(S0 + f * D + c4);
+      const float4 x = *reinterpret_cast<const float4*>(S0 + f * D + c4);
+      St[(c4 + 0) * SROW + f] = x.x;
+      St[(c4 + 1) * SROW + f] = x.y;
+      St[(c4 + 2) * SROW + f] = x.z;
+      St[(c4 + 3) * SROW + f] = x.w;
     }
     if (tid < DF) zs[tid] = S0[DF * D + tid];
   }
-  __syncthreads();
 
-  for (int c0 = s_lo; c0 < s_hi; c0 += C) {
-    const int nk = min(s_hi, c0 + C) - c0;  // tokens of the chunk
-    const int64_t t0 = sr.p0 + c0;          // absolute position of its first token
-    const int nrow = nk * G;
-    for (int rb = 0; rb < nrow; rb += kRB) {
-      const bool first_pass = rb == 0, last_pass = rb + kRB >= nrow;
-      const int r_end = min(nrow, rb + kRB);
-      const int ti_min = rb / G, ti_max = (r_end - 1) / G;  // chunk-relative tokens of the pass
+  // ---- pass geometry: chunk c0 (nk tokens from absolute position t0), rows
+  //      [rb, rb + kRB) of its nrow = nk * G query rows
+  int c0 = s_lo, rb = 0, nk = 0, nrow = 0, ti_min = 0, ti_max = 0, ntile = 0;
+  bool last_pass = true;
+  int64_t t0 = 0, klo = 0, khi = 0, kb0 = 0;
+  int ti[2], hh[2];  // this lane's query row (row hq) in each of its two 16-row q-tiles
+  bool rv[2];
+  auto geom = [&]() {
+    nk = min(s_hi, c0 + C) - c0;
+    t0 = sr.p0 + c0;
+    nrow = nk * G;
+    last_pass = rb + kRB >= nrow;
+    const int r_end = min(nrow, rb + kRB);
+    ti_min = rb / G;
+    ti_max = (r_end - 1) / G;
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      const int r = rb + 32 * wave + 16 * qt + hq;
+      rv[qt] = r < nrow;
+      const int rr = rv[qt] ? r : rb;
+      ti[qt] = rr / G;
+      hh[qt] = rr - ti[qt] * G;
+    }
+    // band keys [klo, khi]: the window of every row of the pass
+    klo = t0 + ti_min - W + 1;
+    if (klo < 0) klo = 0;
+    khi = t0 + ti_max;
+    kb0 = klo & ~int64_t(31);
+    ntile = int((khi - kb0) / 32) + 1;
+  };
 
-      // this lane's query rows (score layout: row = hq of each 16-row q-tile)
-      int ti[2], hh[2];
-      bool rv[2];
+  // ---- loads into registers (all unconditional; rows that do not exist are
+  //      read from a row that does and replaced by zeros where stored)
+  Frag<T> qf[2][KS];
+  auto load_q = [&]() {
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) qf[qt][kk].load(Q + sr.qrow(c0 + ti[qt], hh[qt]) * D + 32 * kk + 8 * lg);
+  };
+  // delayed keys i' of the chunk (key j = t0 - W + i'), a slab of SL at a time
+  Frag<T> kst[VPT], vst[VPT];
+  bool sok[VPT];
+  auto load_slab = [&](int s0) {
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int id = tid + u * kMT, r = id / CPR, ch = id - r * CPR;
+      const int64_t j = t0 - W + s0 + r;
+      sok[u] = s0 + r < nk && j >= 0;
+      kst[u].load((sok[u] ? sr.k(j) : sr.k_safe()) + 8 * ch);
+      vst[u].load((sok[u] ? sr.v(j) : sr.v_safe()) + 8 * ch);
+    }
+  };
+  auto put_slab = [&]() {
+    T* krw = lds_fresh(kr);
+    T* vsw = lds_fresh(vs);
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int id = tid + u * kMT, r = id / CPR, ch = id - r * CPR;
+      store8(krw + r * KROW + 8 * ch, frag_keep(kst[u], sok[u]));
+      store8(vsw + r * VROW + 8 * ch, frag_keep(vst[u], sok[u]));
+    }
+  };
+  // band tiles: this thread's chunk of the next tile (K and V)
+  Frag<T> sk, sv;
+  bool fok = false;
+  const bool stager = tid < 32 * CPR;  // wave-uniform
+  const int srr = tid / CPR, sch = tid - srr * CPR;
+  auto fetch = [&](int n) {
+    if (stager) {
+      const int64_t j = kb0 + 32 * int64_t(n) + srr;
+      fok = j >= klo && j <= khi;
+      sk.load((fok ? sr.k(j) : sr.k_safe()) + 8 * sch);
+      sv.load((fok ? sr.v(j) : sr.v_safe()) + 8 * sch);
+    }
+  };
+  auto store = [&](int buf) {
+    if (stager) {
+      T* kt = lds_fresh(bnd + buf * BAND);
+      store8(kt + srr * KROW + 8 * sch, frag_keep(sk, fok));
+      store8(kt + 32 * KROW + srr * VROW + 8 * sch, frag_keep(sv, fok));
+    }
+  };
+  auto prefetch = [&]() {
+    if (linear) {
+      load_q();
+      load_slab(0);
+    }
+    if (W > 0) fetch(0);
+  };
+
+  geom();
+  prefetch();
+  __syncthreads();  // Wf, S, z staged
+
+  while (true) {
+    f32x4_t acc[2][CT];  // transposed: value columns 16ct+4lg+i of query row hq
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) acc[qt][ct] = zero4();
+    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+
+    // ---- 1. linear part
+    if (linear) {
+      put_slab();  // the first slab's keys and values (made visible by the slab loop's barrier)
+      // phi(q), transposed: lane (row hq, group lg) gets features
+      // 32kf+4lg+i and 32kf+16+4lg+i of its query row in fragment kf
+      Frag<T> pqf[2][KSF];
+      const auto wf = wf_cols();
+#pragma unroll
+      for (int kf = 0; kf < KSF; ++kf) {
+        float pv[2][8];
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          f32x4_t ph[2] = {zero4(), zero4()};
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) {
+            Frag<T> wa;
+            wf.col(wa, kk, 32 * kf + 16 * half);
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) ph[qt] = mma(wa, qf[qt][kk], ph[qt]);
+          }
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pv[qt][4 * half + i] = fmaxf(ph[qt][i], 0.f);
+        }
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) pqf[qt][kf].set8(pv[qt]);
+      }
+      // read-out (phi(q).S_c)^T = S_c^T phi(q)^T, and phi(q).z_c
+      const float* Sr = lds_fresh(static_cast<const float*>(St)) + hq * SROW;
+#pragma unroll
+      for (int kf = 0; kf < KSF; ++kf) {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          Frag<T> fs;
+          load_row2_f32(fs, Sr + 16 * ct * SROW, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fs, pqf[qt][kf], acc[qt][ct]);
+        }
+      }
+      float den[2];
+      const float* zr = lds_fresh(static_cast<const float*>(zs));
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
-        const int r = rb + 32 * wave + 16 * qt + hq;
-        rv[qt] = r < nrow;
-        const int rr = rv[qt] ? r : rb;
-        ti[qt] = rr / G;
-        hh[qt] = rr - ti[qt] * G;
+        float dz = 0.f;
+#pragma unroll
+        for (int kf = 0; kf < KSF; ++kf) {
+          float qv[8];
+          pqf[qt][kf].to_floats(qv);
+          const float4 za = *reinterpret_cast<const float4*>(zr + 32 * kf + 4 * lg);
+          const float4 zb = *reinterpret_cast<const float4*>(zr + 32 * kf + 16 + 4 * lg);
+          dz = fmaf(qv[0], za.x, dz); dz = fmaf(qv[1], za.y, dz);
+          dz = fmaf(qv[2], za.z, dz); dz = fmaf(qv[3], za.w, dz);
+          dz = fmaf(qv[4], zb.x, dz); dz = fmaf(qv[5], zb.y, dz);
+          dz = fmaf(qv[6], zb.z, dz); dz = fmaf(qv[7], zb.w, dz);
+        }
+        den[qt] = dz;
       }
-      Frag<T> qf[2][KS];
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) qf[qt][kk].load(Q + sr.qrow(c0 + ti[qt], hh[qt]) * D + 32 * kk + 8 * lg);
-      // loads issued now and consumed later: the first slab of delayed keys
-      // (key rows and values) and the first band tile
-      SlabKeys<T, D, DF> kx;
-      Frag<T> vx;
-      auto load_slab = [&](int s0) {
-        slab_keys(kx, kMW, [&](int r) {
-          const int64_t j = t0 - W + s0 + r;
-          return (s0 + r < nk && j >= 0) ? sr.k(j) : nullptr;
-        });
-        const int r = tid / CPR, ch = tid - r * CPR;
-        const int64_t j = t0 - W + s0 + r;
-        if (tid < 32 * CPR && s0 + r < nk && j >= 0) vx.load(sr.v(j) + 8 * ch);
-        else vx.zero();
-      };
-      if (linear) load_slab(0);
-      int64_t klo = t0 + ti_min - W + 1;
-      if (klo < 0) klo = 0;
-      const int64_t khi = t0 + ti_max;
-      const int64_t kb0 = klo & ~int64_t(31);
-      const int ntile = int((khi - kb0) / 32) + 1;
-      Frag<T> sk, sv;  // staging registers: this thread's chunk of the next band tile (K and V)
-      const bool stager = tid < 32 * CPR;
-      const int srr = tid / CPR, sch = tid - srr * CPR;
-      auto fetch = [&](int n) {
-        const int64_t j = kb0 + 32 * int64_t(n) + srr;
-        if (stager && j >= klo && j <= khi) {
-          sk.load(sr.k(j) + 8 * sch);
-          sv.load(sr.v(j) + 8 * sch);
-        } else {
-          sk.zero();
-          sv.zero();
+      // the chunk's delayed keys, SL at a time: phi(k) into LDS, the masked
+      // block i' <= ti of every query row, and (last pass: every read-out of
+      // S_c, z_c is done, and the loop covers all the chunk's keys)
+      // S_{c+1} = S_c + phi(k)^T v, z_{c+1} = z_c + sum phi(k), in place
+      for (int s0 = 0; s0 < nk; s0 += SL) {
+        if (s0 > ti_max) break;
+        if (s0 > 0) {
+          __syncthreads();  // the previous slab's readers are done
+          load_slab(s0);
+          put_slab();
         }
-      };
-      auto store = [&](int buf) {
-        if (stager) {
-          T* kt = bnd + buf * BAND;
-          store8(kt + srr * KROW + 8 * sch, sk);
-          store8(kt + 32 * KROW + srr * VROW + 8 * sch, sv);
+        __syncthreads();  // keys and values staged; the read-outs of S_c, z_c are done
+        {
+          const int kt = slab_key_tile<D, DF, SL>(kMW);
+          const T* krr = lds_fresh(static_cast<const T*>(kr));
+          Frag<T> x[KS];
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) x[kk].load(krr + (16 * kt + hq) * KROW + 32 * kk + 8 * lg);
+          phi_slab<T, D, DF, SL>(wf_cols(), x, lds_fresh(pk), kMW);
         }
-      };
-      if (W > 0) fetch(0);
-      f32x4_t acc[2][CT];
+        __syncthreads();
+        const T* pkr = lds_fresh(static_cast<const T*>(pk));
+        const T* vsr = lds_fresh(static_cast<const T*>(vs));
+        if (last_pass) {
+          // every S tile (and z slice) has one owner wave: plain updates.
+          // Lane (hq, lg) gets features 16ft+4lg.. of value column 16ct+hq,
+          // 4 consecutive floats of S^T
+          float* Sw = lds_fresh(St);
+          float* zw = lds_fresh(zs);
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
+          for (int x = 0; x < NT; ++x) {
+            const int tile = wave * NT + x, ft = tile / CT, ct = tile - ft * CT;
+            f32x4_t d = zero4();
+            float zp = 0.f;
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[qt][ct] = zero4();
-      float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
-
-      // ---- 1. linear part
-      if (linear) {
-        // phi(q), transposed: lane (row hq, group lg) gets features
-        // 32kf+4lg+i and 32kf+16+4lg+i of its query row in fragment kf
-        Frag<T> pqf[2][KSF];
-#pragma unroll
-        for (int kf = 0; kf < KSF; ++kf) {
-          float pv[2][8];
-#pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            f32x4_t ph[2] = {zero4(), zero4()};
-#pragma unroll
-            for (int kk = 0; kk < KS; ++kk) {
-              Frag<T> wa;
-              wf.col(wa, kk, 32 * kf + 16 * half);
-#pragma unroll
-              for (int qt = 0; qt < 2; ++qt) ph[qt] = mma(wa, qf[qt][kk], ph[qt]);
-            }
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) pv[qt][4 * half + i] = fmaxf(ph[qt][i], 0.f);
-          }
-#pragma unroll
-          for (int qt = 0; qt < 2; ++qt) pqf[qt][kf].set8(pv[qt]);
-        }
-        // read-out phi(q).S_c and phi(q).z_c
-#pragma unroll
-        for (int kf = 0; kf < KSF; ++kf) {
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            Frag<T> fb;
-            load_colfrag2_f32(fb, Sn, SROW, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg, 16 * ct);
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pqf[qt][kf], fb, acc[qt][ct]);
-          }
-        }
-        float den[2];
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          float dz = 0.f;
-#pragma unroll
-          for (int kf = 0; kf < KSF; ++kf) {
-            float qv[8];
-            pqf[qt][kf].to_floats(qv);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              dz = fmaf(qv[e], zs[32 * kf + 4 * lg + e], dz);
-              dz = fmaf(qv[4 + e], zs[32 * kf + 16 + 4 * lg + e], dz);
-            }
-          }
-          den[qt] = dz;
-        }
-        // the chunk's delayed keys i' (key j = t0 - W + i'), 32 at a time:
-        // phi(k) and values into LDS, the masked block i' <= ti of every
-        // query row, and (last pass: every read-out of S_c is done, the loop
-        // covers all the chunk's keys) S_{c+1} = S_c + phi(k)^T v in place
-        for (int s0 = 0; s0 < nk; s0 += 32) {
-          if (s0 > ti_max) break;
-          __syncthreads();
-          phi_slab(wf, kx, pk, kMW);
-          if (tid < 32 * CPR) {
-            const int r = tid / CPR, ch = tid - r * CPR;
-            store8(vs + r * VROW + 8 * ch, vx);
-          }
-          if (s0 + 32 < nk && s0 + 32 <= ti_max) load_slab(s0 + 32);
-          __syncthreads();
-          if (last_pass) {
-#pragma unroll
-            for (int x = 0; x < NT; ++x) {
-              const int tile = wave * NT + x, ft = tile / CT, ct = tile - ft * CT;
+            for (int kh = 0; kh < SL / 32; ++kh) {
               Frag<T> fa, fb;
-              load_colfrag(fa, pk, PROW, 8 * lg, 16 * ft);
-              load_colfrag(fb, vs, VROW, 8 * lg, 16 * ct);
-              const f32x4_t d = mma(fa, fb, zero4());
-#pragma unroll
-              for (int i = 0; i < 4; ++i) Sn[(16 * ft + 4 * lg + i) * SROW + 16 * ct + hq] += d[i];
+              load_colfrag(fa, pkr, PROW, 32 * kh + 8 * lg, 16 * ft);
+              load_colfrag(fb, vsr, VROW, 32 * kh + 8 * lg, 16 * ct);
+              d = mma(fa, fb, d);
+              if (ct == 0) zp += fa.sum();  // keys 32kh+8lg.. of feature 16ft+hq
             }
-            if (tid < DF) {
-              float dz = 0.f;
-#pragma unroll 8
-              for (int r = 0; r < 32; ++r) dz += to_f32(pk[r * PROW + tid]);
-              zs[tid] += dz;
+            float4* sp = reinterpret_cast<float4*>(Sw + (16 * ct + hq) * SROW + 16 * ft + 4 * lg);
+            float4 s4 = *sp;
+            s4.x += d[0]; s4.y += d[1]; s4.z += d[2]; s4.w += d[3];
+            *sp = s4;
+            if (ct == 0) {
+              zp += __shfl_xor(zp, 16);
+              zp += __shfl_xor(zp, 32);
+              if (lg == 0) zw[16 * ft + hq] += zp;
             }
           }
-          // scores: key row m of sub-tile t is i' = s0 + 8(m/4) + 4t + m%4
+        }
+        // scores: key row m of sub-tile t of 32-key block kb is
+        // i' = s0 + 32kb + 8(m/4) + 4t + m%4
+#pragma unroll
+        for (int kb = 0; kb < SL / 32; ++kb) {
+          if (s0 + 32 * kb > ti_max) break;
           f32x4_t sc[2][2];
 #pragma unroll
           for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
-            const T* prow = pk + (8 * (hq >> 2) + 4 * t + (hq & 3)) * PROW;
+            const T* prow = pkr + (32 * kb + 8 * (hq >> 2) + 4 * t + (hq & 3)) * PROW;
 #pragma unroll
             for (int kf = 0; kf < KSF; ++kf) {
               Frag<T> fa;
@@ -545,154 +669,163 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
-              for (int i = 0; i < 4; ++i) pv[4 * t + i] = (s0 + 8 * lg + 4 * t + i <= ti[qt]) ? sc[qt][t][i] : 0.f;
+              for (int i = 0; i < 4; ++i)
+                pv[4 * t + i] = (s0 + 32 * kb + 8 * lg + 4 * t + i <= ti[qt]) ? sc[qt][t][i] : 0.f;
             pf[qt].set8(pv);
             den[qt] += pf[qt].sum();
           }
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct) {
-            Frag<T> fb;
-            load_colfrag(fb, vs, VROW, 8 * lg, 16 * ct);
+            Frag<T> fv;
+            load_colfrag(fv, vsr, VROW, 32 * kb + 8 * lg, 16 * ct);
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pf[qt], fb, acc[qt][ct]);
-          }
-        }
-        // the linear part becomes the start of the online softmax: one
-        // pseudo-key of weight den (log2 domain: max = log2 den, sum 1)
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          float dn = den[qt];
-          dn += __shfl_xor(dn, 16);
-          dn += __shfl_xor(dn, 32);
-          m_run[qt] = dn > 0.f ? log2f(dn) : -INFINITY;
-          l_run[qt] = (dn > 0.f && lg == 0) ? 1.f : 0.f;
-          const float inv = dn > 0.f ? 1.f / dn : 0.f;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float ir = __shfl(inv, 4 * lg + i);
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct) acc[qt][ct][i] *= ir;
+            for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
           }
         }
       }
-
-      // ---- 2. banded window attention, keys [t0 + ti_min - W + 1, t0 + ti_max]
-      if (W > 0) {
-        __syncthreads();  // the previous users of the band buffers are done
-        store(0);         // tile 0 was fetched at the start of the pass
-        __syncthreads();
-        for (int n = 0; n < ntile; ++n) {
-          const int buf = NBUF == 2 ? (n & 1) : 0;
-          if (n + 1 < ntile) fetch(n + 1);
-          const T* kt = bnd + buf * BAND;
-          const T* vt = kt + 32 * KROW;
-          const int64_t kb = kb0 + 32 * int64_t(n);
-          f32x4_t sc[2][2];
-#pragma unroll
-          for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
-#pragma unroll
-          for (int t = 0; t < 2; ++t) {
-#pragma unroll
-            for (int kk = 0; kk < KS; ++kk) {
-              Frag<T> fa;
-              fa.load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * KROW + 32 * kk + 8 * lg);
-#pragma unroll
-              for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
-            }
-          }
-          // keys [kb, kb+31] lie inside the band of every row of the pass
-          // (tokens t0+ti_min .. t0+ti_max) for all but the edge tiles
-          const bool interior = kb >= t0 + ti_max - W + 1 && kb + 31 <= t0 + ti_min;
-          Frag<T> pf[2];
-#pragma unroll
-          for (int qt = 0; qt < 2; ++qt) {
-            float sv8[8];
-            if (interior) {
-#pragma unroll
-              for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) sv8[4 * t + i] = sc[qt][t][i] * sc2;
-            } else {
-              // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row exists
-              const int base = int(kb - (t0 + ti[qt]));
-              const int64_t offlo = klo - kb;  // first in-band offset of the tile (<= 31)
-              const int lo = offlo < -1 ? -1 : int(offlo);
-#pragma unroll
-              for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                  const int off = 8 * lg + 4 * t + i;
-                  const bool ok = rv[qt] && off >= lo && base + off <= 0 && base + off > -W;
-                  sv8[4 * t + i] = ok ? sc[qt][t][i] * sc2 : -INFINITY;
-                }
-            }
-            float mx = sv8[0];
-#pragma unroll
-            for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv8[i]);
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            // lazy rescale: the running max moves only when a score exceeds it
-            // by more than 2^8, so p = 2^(s - m) <= 256 and acc, l stay in range
-            if (__any(mx > m_run[qt] + 8.f)) {
-              const float m_new = fmaxf(m_run[qt], mx);
-              const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
-              l_run[qt] *= alpha;
-              m_run[qt] = m_new;
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const float al = __shfl(alpha, 4 * lg + i);
-#pragma unroll
-                for (int ct = 0; ct < CT; ++ct) acc[qt][ct][i] *= al;
-              }
-            }
-            const float m_use = m_run[qt] == -INFINITY ? 0.f : m_run[qt];
-            float pv[8], ps = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              pv[i] = __builtin_amdgcn_exp2f(sv8[i] - m_use);
-              ps += pv[i];
-            }
-            pf[qt].set8(pv);
-            l_run[qt] += ps;
-          }
-#pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            Frag<T> fb;
-            load_colfrag(fb, vt, VROW, 8 * lg, 16 * ct);
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(pf[qt], fb, acc[qt][ct]);
-          }
-          if (n + 1 < ntile) {
-            if (NBUF == 1) __syncthreads();  // every wave is done with the single buffer
-            store(NBUF == 2 ? ((n + 1) & 1) : 0);
-          }
-          __syncthreads();
-        }
-      }
-
-      // ---- 3. outputs
+      // the linear part becomes the start of the online softmax: one
+      // pseudo-key of weight den (log2 domain: max = log2 den, sum 1)
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
-        float ls = l_run[qt];
-        ls += __shfl_xor(ls, 16);
-        ls += __shfl_xor(ls, 32);
-        const float inv = ls > 0.f ? 1.f / ls : 0.f;
+        float dn = den[qt];
+        dn += __shfl_xor(dn, 16);
+        dn += __shfl_xor(dn, 32);
+        m_run[qt] = dn > 0.f ? log2f(dn) : -INFINITY;
+        l_run[qt] = (dn > 0.f && lg == 0) ? 1.f : 0.f;
+        const float inv = dn > 0.f ? 1.f / dn : 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float ir = __shfl(inv, 4 * lg + i);
-          const int r = rb + 32 * wave + 16 * qt + 4 * lg + i;
-          if (r < nrow) {
-            const int tr = r / G, hr = r - tr * G;
-            T* orow = O + sr.qrow(c0 + tr, hr) * D;
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct) orow[16 * ct + hq] = from_f32<T>(acc[qt][ct][i] * ir);
-          }
-        }
+          for (int i = 0; i < 4; ++i) acc[qt][ct][i] *= inv;
       }
     }
 
-    // S_{c+1}, z_{c+1} are in LDS; the next chunk's first read of them comes
-    // after a barrier (its band staging or its first delayed-key slab)
+    // ---- 2. banded window attention, keys [klo, khi]
+    if (W > 0) {
+      refresh();
+      load_q();         // the band's copy of the query rows (recently read: cache-resident)
+      __syncthreads();  // the previous users of the shared region (slab, band) are done
+      store(0);         // tile 0 was fetched with the pass's other prefetches
+      __syncthreads();
+      for (int n = 0; n < ntile; ++n) {
+        const int buf = NBUF == 2 ? (n & 1) : 0;
+        if (n + 1 < ntile) fetch(n + 1);
+        const T* kt = lds_fresh(static_cast<const T*>(bnd) + buf * BAND);
+        const T* vt = kt + 32 * KROW;
+        const int64_t kb = kb0 + 32 * int64_t(n);
+        f32x4_t sc[2][2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) {
+            Frag<T> fa;
+            fa.load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * KROW + 32 * kk + 8 * lg);
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
+          }
+        }
+        // keys [kb, kb+31] lie inside the band of every row of the pass
+        // (tokens t0+ti_min .. t0+ti_max) for all but the edge tiles
+        const bool interior = kb >= t0 + ti_max - W + 1 && kb + 31 <= t0 + ti_min;
+        Frag<T> pf[2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          float sv8[8];
+          if (interior) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) sv8[4 * t + i] = sc[qt][t][i] * sc2;
+          } else {
+            // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row exists
+            const int base = int(kb - (t0 + ti[qt]));
+            const int64_t offlo = klo - kb;  // first in-band offset of the tile (<= 31)
+            const int lo = offlo < -1 ? -1 : int(offlo);
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int off = 8 * lg + 4 * t + i;
+                const bool ok = rv[qt] && off >= lo && base + off <= 0 && base + off > -W;
+                sv8[4 * t + i] = ok ? sc[qt][t][i] * sc2 : -INFINITY;
+              }
+          }
+          float mx = sv8[0];
+#pragma unroll
+          for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv8[i]);
+          mx = fmaxf(mx, __shfl_xor(mx, 16));
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          // lazy rescale: the running max moves only when a score exceeds it
+          // by more than 2^8, so p = 2^(s - m) <= 256 and acc, l stay in range
+          if (__any(mx > m_run[qt] + 8.f)) {
+            const float m_new = fmaxf(m_run[qt], mx);
+            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
+            l_run[qt] *= alpha;
+            m_run[qt] = m_new;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) acc[qt][ct][i] *= alpha;
+          }
+          const float m_use = m_run[qt] == -INFINITY ? 0.f : m_run[qt];
+          float pv[8], ps = 0.f;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            pv[i] = __builtin_amdgcn_exp2f(sv8[i] - m_use);
+            ps += pv[i];
+          }
+          pf[qt].set8(pv);
+          l_run[qt] += ps;
+        }
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          Frag<T> fv;
+          load_colfrag(fv, vt, VROW, 8 * lg, 16 * ct);
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
+        }
+        if (n + 1 < ntile) {
+          if (NBUF == 1) __syncthreads();  // every wave is done with the single buffer
+          store(NBUF == 2 ? ((n + 1) & 1) : 0);
+        }
+        __syncthreads();
+      }
+    }
+
+    // ---- 3. the next pass's loads, then this pass's outputs: value columns
+    //         16ct+4lg .. +3 of query row hq
+    int64_t orow[2];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) orow[qt] = sr.qrow(c0 + ti[qt], hh[qt]) * D + 4 * lg;
+    const bool ov[2] = {rv[0], rv[1]};
+    const bool more = !(last_pass && c0 + C >= s_hi);
+    if (more) {
+      if (last_pass) {
+        c0 += C;
+        rb = 0;
+      } else {
+        rb += kRB;
+      }
+      geom();
+      refresh();
+      prefetch();
+    }
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float ls = l_run[qt];
+      ls += __shfl_xor(ls, 16);
+      ls += __shfl_xor(ls, 32);
+      const float inv = ls > 0.f ? 1.f / ls : 0.f;
+      if (ov[qt]) {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) store4(O + orow[qt] + 16 * ct, acc[qt][ct], inv);
+      }
+    }
+    if (!more) break;
+    // pass boundary: the next pass writes the slab staging (and, at a chunk
+    // boundary, reads S_{c+1}, z_{c+1})
     __syncthreads();
   }
 }
@@ -760,9 +893,7 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
                          dim3(kThreads), 0, s, a);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    const size_t lds = MainLds<T, D, DF>::bytes;
-    if ((e = set_lds(&prefill_main<T, D, DF>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv), dim3(kMT), lds, s, a);
+    hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv), dim3(kMT), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (a.W > 0) {
