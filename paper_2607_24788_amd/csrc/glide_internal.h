@@ -401,6 +401,23 @@ __device__ __forceinline__ P* sfresh(P* p) {
   return (P*)q;
 }
 
+// Max / sum over the 4 lanes that share lane % 16 (the lane groups of an
+// MFMA fragment), with the gfx950 row-swap permutes (no LDS round trip):
+// permlane16_swap pairs rows (0,1), (2,3); permlane32_swap pairs the halves.
+// Wave-uniform control flow only (every lane active).
+__device__ __forceinline__ float lg_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float lg_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // a if keep, else zeros: a select on registers (taken where the value is
 // used), not a branch around the load that produced a.
 __device__ __forceinline__ Frag<bf16_t> frag_keep(const Frag<bf16_t>& a, bool keep) {

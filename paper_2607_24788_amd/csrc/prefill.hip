@@ -138,15 +138,22 @@ struct WfCols {
   }
 };
 
-// Wf [D][DF] into LDS, natural layout (nthreads cooperating).
-template <typename T, int D, int DF>
-__device__ __forceinline__ void stage_wf(const T* Wf, T* Wn, int nthreads) {
-  constexpr int WROW = row_t<DF>();
-  for (int i = threadIdx.x; i < D * DF / 8; i += nthreads) {
-    const int r = i / (DF / 8), ch = i - r * (DF / 8);
-    Frag<T> f;
-    f.load(Wf + r * DF + 8 * ch);
-    store8(Wn + r * WROW + 8 * ch, f);
+// Wf [D][DF] into LDS, natural layout (NTH threads cooperating; every load
+// is issued before the first store).
+template <typename T, int D, int DF, int NTH>
+__device__ __forceinline__ void stage_wf(const T* Wf, T* Wn) {
+  constexpr int WROW = row_t<DF>(), N = D * DF / 8 / NTH;
+  static_assert(N * NTH == D * DF / 8, "even split");
+  Frag<T> f[N];
+#pragma unroll
+  for (int u = 0; u < N; ++u) {
+    const int i = threadIdx.x + u * NTH, r = i / (DF / 8), ch = i - r * (DF / 8);
+    f[u].load(Wf + r * DF + 8 * ch);
+  }
+#pragma unroll
+  for (int u = 0; u < N; ++u) {
+    const int i = threadIdx.x + u * NTH, r = i / (DF / 8), ch = i - r * (DF / 8);
+    store8(Wn + r * WROW + 8 * ch, f[u]);
   }
 }
 
@@ -224,15 +231,31 @@ __global__ __launch_bounds__(kThreads) void prefill_gather(PrefillArgs a) {
 // segsum: state increment of one segment from its delayed keys
 //   dS[f][c] = sum_j phi(k_j)[f] v_j[c],  dz[f] = sum_j phi(k_j)[f],
 //   j in [t_lo - W, t_hi - W) and j >= 0, where [t_lo, t_hi) are the segment's queries.
+// 8 waves, slabs of 64 keys; each wave owns 1/8 of the dS tiles (registers),
+// computed transposed so that a lane holds 4 consecutive columns of one
+// feature row (16-byte stores of the record); dz comes from the same phi(k)
+// fragments.
+constexpr int kSegThreads = 512, kSegWaves = 8, kSegSlab = 64;
+
 template <typename T, int D, int DF>
-__global__ __launch_bounds__(kThreads) void prefill_segsum(PrefillArgs a) {
-  constexpr int CT = D / 16, FT = DF / 16;
-  constexpr int NT = FT * CT / kWaves;  // output tiles per wave
-  constexpr int WROW = row_t<DF>(), PROW = row_t<DF>(), VROW = row_t<D>();
-  extern __shared__ __align__(16) char smem[];
-  T* Wn = reinterpret_cast<T*>(smem);  // [D][WROW]   Wf
-  T* pk = Wn + D * WROW;                // [32][PROW]  phi(k) of 32 delayed keys
-  T* vs = pk + 32 * PROW;               // [32][VROW]  their values
+struct SegLds {
+  static constexpr int WROW = row_t<DF>(), PROW = row_t<DF>(), VROW = row_t<D>();
+  static constexpr size_t bytes = (size_t(D) * WROW + size_t(kSegSlab) * (PROW + VROW)) * sizeof(T);
+};
+
+template <typename T, int D, int DF>
+__global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
+  using LD = SegLds<T, D, DF>;
+  constexpr int CT = D / 16, FT = DF / 16, CPR = D / 8;
+  constexpr int NT = FT * CT / kSegWaves;                  // dS tiles per wave
+  constexpr int VPT = kSegSlab * CPR / kSegThreads;        // value chunks per thread
+  constexpr int WROW = LD::WROW, PROW = LD::PROW, VROW = LD::VROW;
+  static_assert(NT * kSegWaves == FT * CT && VPT * kSegThreads == kSegSlab * CPR, "even split");
+  static_assert(NT <= CT, "at most one ct == 0 tile per wave (it carries dz)");
+  __shared__ __align__(16) char smem[LD::bytes];
+  T* Wn = reinterpret_cast<T*>(smem);  // [D][WROW]      Wf
+  T* pk = Wn + D * WROW;                // [64][PROW]     phi(k) of a slab of delayed keys
+  T* vs = pk + kSegSlab * PROW;         // [64][VROW]     their values
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hq = lane & 15, lg = lane >> 4;
   const int sg = blockIdx.x, g = blockIdx.y;
   const int bl = find_seq(a, sg);
@@ -242,65 +265,76 @@ __global__ __launch_bounds__(kThreads) void prefill_segsum(PrefillArgs a) {
   int64_t jlo = sr.p0 + s_lo - a.W;
   const int64_t jhi = sr.p0 + s_hi - a.W;
   if (jlo < 0) jlo = 0;
-  stage_wf<T, D, DF>(static_cast<const T*>(a.wf), Wn, kThreads);
-  const WfCols<T, D, DF, true> wf{Wn};
 
   f32x4_t sacc[NT];
 #pragma unroll
   for (int x = 0; x < NT; ++x) sacc[x] = zero4();
-  float zinc = 0.f;
+  float zp = 0.f;  // lanes of ct == 0 tiles: keys 8lg.. of feature 16ft+hq
   // the next slab's key rows and values are loaded while the current one is
   // computed
-  constexpr int VPT = 32 * D / 8 / kThreads;  // value chunks per thread
   SlabKeys<T, D, DF> kx;
   Frag<T> vx[VPT];
   bool vok[VPT];
   auto load_slab = [&](int64_t j0) {
-    slab_keys<T, D, DF, 32>(kx, kWaves, [&](int r) { return j0 + r < jhi ? sr.k(j0 + r) : nullptr; }, sr.k_safe());
+    slab_keys<T, D, DF, kSegSlab>(kx, kSegWaves, [&](int r) { return j0 + r < jhi ? sr.k(j0 + r) : nullptr; },
+                                   sr.k_safe());
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
-      const int id = tid + u * kThreads, r = id / (D / 8), ch = id - r * (D / 8);
+      const int id = tid + u * kSegThreads, r = id / CPR, ch = id - r * CPR;
       vok[u] = j0 + r < jhi;
       vx[u].load((vok[u] ? sr.v(j0 + r) : sr.v_safe()) + 8 * ch);
     }
   };
   if (jlo < jhi) load_slab(jlo);
-  for (int64_t j0 = jlo; j0 < jhi; j0 += 32) {
-    __syncthreads();
+  stage_wf<T, D, DF, kSegThreads>(static_cast<const T*>(a.wf), Wn);
+  for (int64_t j0 = jlo; j0 < jhi; j0 += kSegSlab) {
+    __syncthreads();  // Wf staged; the previous slab's readers are done
     {
       Frag<T> x[D / 32];
 #pragma unroll
       for (int kk = 0; kk < D / 32; ++kk) x[kk] = frag_keep(kx.x[kk], kx.ok);
-      phi_slab<T, D, DF, 32>(wf, x, pk, kWaves);
+      phi_slab<T, D, DF, kSegSlab>(WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))}, x, lds_fresh(pk),
+                                   kSegWaves);
     }
+    {
+      T* vw = lds_fresh(vs);
 #pragma unroll
-    for (int u = 0; u < VPT; ++u) {
-      const int id = tid + u * kThreads, r = id / (D / 8), ch = id - r * (D / 8);
-      store8(vs + r * VROW + 8 * ch, frag_keep(vx[u], vok[u]));
+      for (int u = 0; u < VPT; ++u) {
+        const int id = tid + u * kSegThreads, r = id / CPR, ch = id - r * CPR;
+        store8(vw + r * VROW + 8 * ch, frag_keep(vx[u], vok[u]));
+      }
     }
-    if (j0 + 32 < jhi) load_slab(j0 + 32);
+    if (j0 + kSegSlab < jhi) load_slab(j0 + kSegSlab);
     __syncthreads();
+    const T* pr = lds_fresh(static_cast<const T*>(pk));
+    const T* vr = lds_fresh(static_cast<const T*>(vs));
 #pragma unroll
     for (int x = 0; x < NT; ++x) {
       const int tile = wave * NT + x, ft = tile / CT, ct = tile - ft * CT;
-      Frag<T> fa, fb;
-      load_colfrag(fa, pk, PROW, 8 * lg, 16 * ft);
-      load_colfrag(fb, vs, VROW, 8 * lg, 16 * ct);
-      sacc[x] = mma(fa, fb, sacc[x]);
-    }
-    if (tid < DF) {
-#pragma unroll 8
-      for (int r = 0; r < 32; ++r) zinc += to_f32(pk[r * PROW + tid]);
+#pragma unroll
+      for (int kh = 0; kh < kSegSlab / 32; ++kh) {
+        Frag<T> fv, fp;
+        load_colfrag(fv, vr, VROW, 32 * kh + 8 * lg, 16 * ct);
+        load_colfrag(fp, pr, PROW, 32 * kh + 8 * lg, 16 * ft);
+        sacc[x] = mma(fv, fp, sacc[x]);  // rows c = 16ct+4lg+i, column f = 16ft+hq
+        if (ct == 0) zp += fp.sum();
+      }
     }
   }
   float* rec = a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
 #pragma unroll
   for (int x = 0; x < NT; ++x) {
     const int tile = wave * NT + x, ft = tile / CT, ct = tile - ft * CT;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) rec[(16 * ft + 4 * lg + i) * D + 16 * ct + hq] = sacc[x][i];
+    *reinterpret_cast<float4*>(rec + (16 * ft + hq) * D + 16 * ct + 4 * lg) =
+        make_float4(sacc[x][0], sacc[x][1], sacc[x][2], sacc[x][3]);
   }
-  if (tid < DF) rec[DF * D + tid] = zinc;
+  // dz: the owner wave of each feature block's ct == 0 tile
+  zp = lg_sum(zp);
+#pragma unroll
+  for (int x = 0; x < NT; ++x) {
+    const int tile = wave * NT + x, ft = tile / CT, ct = tile - ft * CT;
+    if (ct == 0 && lg == 0) rec[DF * D + 16 * ft + hq] = zp;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -316,10 +350,23 @@ __global__ __launch_bounds__(kThreads) void prefill_scan(PrefillArgs a) {
   float* st = e < DF * D ? reinterpret_cast<float*>(a.state + a.layer_base + sec.S) + unit * DF * D + e
                          : reinterpret_cast<float*>(a.state + a.layer_base + sec.z) + unit * DF + (e - DF * D);
   float4 run = *reinterpret_cast<const float4*>(st);
-  for (int sg = a.seg_base[bl]; sg < a.seg_base[bl + 1]; ++sg) {
-    float4* rec = reinterpret_cast<float4*>(a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * E + e);
-    const float4 d = *rec;
-    *rec = run;
+  auto rec = [&](int sg) { return reinterpret_cast<float4*>(a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * E + e); };
+  const int s1 = a.seg_base[bl + 1];
+  int sg = a.seg_base[bl];
+  // eight records' loads in flight at a time (the sum itself is serial)
+  for (; sg + 8 <= s1; sg += 8) {
+    float4 d[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) d[u] = *rec(sg + u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      *rec(sg + u) = run;
+      run.x += d[u].x; run.y += d[u].y; run.z += d[u].z; run.w += d[u].w;
+    }
+  }
+  for (; sg < s1; ++sg) {
+    const float4 d = *rec(sg);
+    *rec(sg) = run;
     run.x += d.x; run.y += d.y; run.z += d.z; run.w += d.w;
   }
   *reinterpret_cast<float4*>(st) = run;
@@ -413,22 +460,6 @@ void prefill_main(PrefillArgs a) {
     else return WfCols<T, D, DF, false>{static_cast<const T*>(a.wf)};
   };
 
-  // ---- 0. Wf into LDS; S, z at the segment start (the scan's record), fp32,
-  //         into LDS (S transposed); they stay there for the whole walk
-  if (linear) {
-    if (LD::kWfLds) stage_wf<T, D, DF>(static_cast<const T*>(a.wf), Wn, kMT);
-    const float* S0 = a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
-    for (int i = tid; i < DF * D / 4; i += kMT) {
-      const int f = i / (D / 4), c4 = 4 * (i - f * (D / 4));
-      const float4 x = *reinterpret_cast<const float4*>(S0 + f * D + c4);
-      St[(c4 + 0) * SROW + f] = x.x;
-      St[(c4 + 1) * SROW + f] = x.y;
-      St[(c4 + 2) * SROW + f] = x.z;
-      St[(c4 + 3) * SROW + f] = x.w;
-    }
-    if (tid < DF) zs[tid] = S0[DF * D + tid];
-  }
-
   // ---- pass geometry: chunk c0 (nk tokens from absolute position t0), rows
   //      [rb, rb + kRB) of its nrow = nk * G query rows
   int c0 = s_lo, rb = 0, nk = 0, nrow = 0, ti_min = 0, ti_max = 0, ntile = 0;
@@ -505,7 +536,7 @@ void prefill_main(PrefillArgs a) {
       sv.load((fok ? sr.v(j) : sr.v_safe()) + 8 * sch);
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf) {  // buf < NBUF
     if (stager) {
       T* kt = lds_fresh(bnd + buf * BAND);
       store8(kt + srr * KROW + 8 * sch, frag_keep(sk, fok));
@@ -522,6 +553,31 @@ void prefill_main(PrefillArgs a) {
 
   geom();
   prefetch();
+  // ---- 0. (behind the first pass's loads) Wf into LDS; S, z at the
+  //         segment start (the scan's record), fp32, into LDS (S transposed);
+  //         they stay there for the whole walk
+  if (linear) {
+    if constexpr (LD::kWfLds) stage_wf<T, D, DF, kMT>(static_cast<const T*>(a.wf), Wn);
+    const float* S0 = a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
+    constexpr int NS = DF * D / 4 / kMT;
+    static_assert(NS * kMT * 4 == DF * D, "even split");
+    float4 x[NS];
+#pragma unroll
+    for (int u = 0; u < NS; ++u) {
+      const int i = tid + u * kMT, f = i / (D / 4), c4 = 4 * (i - f * (D / 4));
+      x[u] = *reinterpret_cast<const float4*>(S0 + f * D + c4);
+    }
+    const float zv = tid < DF ? S0[DF * D + tid] : 0.f;
+#pragma unroll
+    for (int u = 0; u < NS; ++u) {
+      const int i = tid + u * kMT, f = i / (D / 4), c4 = 4 * (i - f * (D / 4));
+      St[(c4 + 0) * SROW + f] = x[u].x;
+      St[(c4 + 1) * SROW + f] = x[u].y;
+      St[(c4 + 2) * SROW + f] = x[u].z;
+      St[(c4 + 3) * SROW + f] = x[u].w;
+    }
+    if (tid < DF) zs[tid] = zv;
+  }
   __syncthreads();  // Wf, S, z staged
 
   while (true) {
@@ -637,8 +693,7 @@ void prefill_main(PrefillArgs a) {
             s4.x += d[0]; s4.y += d[1]; s4.z += d[2]; s4.w += d[3];
             *sp = s4;
             if (ct == 0) {
-              zp += __shfl_xor(zp, 16);
-              zp += __shfl_xor(zp, 32);
+              zp = lg_sum(zp);
               if (lg == 0) zw[16 * ft + hq] += zp;
             }
           }
@@ -687,9 +742,7 @@ void prefill_main(PrefillArgs a) {
       // pseudo-key of weight den (log2 domain: max = log2 den, sum 1)
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
-        float dn = den[qt];
-        dn += __shfl_xor(dn, 16);
-        dn += __shfl_xor(dn, 32);
+        const float dn = lg_sum(den[qt]);
         m_run[qt] = dn > 0.f ? log2f(dn) : -INFINITY;
         l_run[qt] = (dn > 0.f && lg == 0) ? 1.f : 0.f;
         const float inv = dn > 0.f ? 1.f / dn : 0.f;
@@ -700,19 +753,21 @@ void prefill_main(PrefillArgs a) {
       }
     }
 
-    // ---- 2. banded window attention, keys [klo, khi]
+    // ---- 2. banded window attention, keys [klo, khi], 32-key tiles
     if (W > 0) {
       refresh();
       load_q();         // the band's copy of the query rows (recently read: cache-resident)
       __syncthreads();  // the previous users of the shared region (slab, band) are done
       store(0);         // tile 0 was fetched with the pass's other prefetches
       __syncthreads();
+      const bool pos_scale = sc2 > 0.f;  // (wave-uniform) the usual case: max of raw scores
       for (int n = 0; n < ntile; ++n) {
         const int buf = NBUF == 2 ? (n & 1) : 0;
         if (n + 1 < ntile) fetch(n + 1);
         const T* kt = lds_fresh(static_cast<const T*>(bnd) + buf * BAND);
         const T* vt = kt + 32 * KROW;
         const int64_t kb = kb0 + 32 * int64_t(n);
+        // scores: key row m of sub-tile t is key kb + 8(m/4) + 4t + m%4
         f32x4_t sc[2][2];
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
@@ -732,12 +787,16 @@ void prefill_main(PrefillArgs a) {
         Frag<T> pf[2];
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) {
+          // sv8: the tile's scores, -inf outside the band; scaled by sc2
+          // unless pos_scale (then the max is taken on the raw scores and the
+          // scale joins the exponent's FMA)
+          const float sm = pos_scale ? 1.f : sc2;
           float sv8[8];
           if (interior) {
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
-              for (int i = 0; i < 4; ++i) sv8[4 * t + i] = sc[qt][t][i] * sc2;
+              for (int i = 0; i < 4; ++i) sv8[4 * t + i] = pos_scale ? sc[qt][t][i] : sc[qt][t][i] * sm;
           } else {
             // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row exists
             const int base = int(kb - (t0 + ti[qt]));
@@ -749,14 +808,14 @@ void prefill_main(PrefillArgs a) {
               for (int i = 0; i < 4; ++i) {
                 const int off = 8 * lg + 4 * t + i;
                 const bool ok = rv[qt] && off >= lo && base + off <= 0 && base + off > -W;
-                sv8[4 * t + i] = ok ? sc[qt][t][i] * sc2 : -INFINITY;
+                sv8[4 * t + i] = ok ? sc[qt][t][i] * sm : -INFINITY;
               }
           }
           float mx = sv8[0];
 #pragma unroll
           for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv8[i]);
-          mx = fmaxf(mx, __shfl_xor(mx, 16));
-          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          mx = lg_max(mx);
+          if (pos_scale) mx *= sc2;
           // lazy rescale: the running max moves only when a score exceeds it
           // by more than 2^8, so p = 2^(s - m) <= 256 and acc, l stay in range
           if (__any(mx > m_run[qt] + 8.f)) {
@@ -771,10 +830,18 @@ void prefill_main(PrefillArgs a) {
           }
           const float m_use = m_run[qt] == -INFINITY ? 0.f : m_run[qt];
           float pv[8], ps = 0.f;
+          if (pos_scale) {
 #pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            pv[i] = __builtin_amdgcn_exp2f(sv8[i] - m_use);
-            ps += pv[i];
+            for (int i = 0; i < 8; ++i) {
+              pv[i] = __builtin_amdgcn_exp2f(fmaf(sv8[i], sc2, -m_use));
+              ps += pv[i];
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              pv[i] = __builtin_amdgcn_exp2f(sv8[i] - m_use);
+              ps += pv[i];
+            }
           }
           pf[qt].set8(pv);
           l_run[qt] += ps;
@@ -814,9 +881,7 @@ void prefill_main(PrefillArgs a) {
     }
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-      float ls = l_run[qt];
-      ls += __shfl_xor(ls, 16);
-      ls += __shfl_xor(ls, 32);
+      const float ls = lg_sum(l_run[qt]);
       const float inv = ls > 0.f ? 1.f / ls : 0.f;
       if (ov[qt]) {
 #pragma unroll
@@ -831,7 +896,12 @@ void prefill_main(PrefillArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// ringfill: tokens [max(p0, p_end - W), p_end) into their ring slots
+// ringfill: tokens [max(p0, p_end - W), p_end) into their ring slots.  A key
+// slot takes 16-byte chunks (8 consecutive columns); the value layout keeps 8
+// consecutive slots of one column together, so a thread gathers one column of
+// 8 consecutive tokens (R is a multiple of 8, so such a group never wraps)
+// and stores it at once, or element by element where the group is only partly
+// in range (its other slots may hold live tokens).
 template <typename T, int D, int DF>
 __global__ __launch_bounds__(kThreads) void prefill_ringfill(PrefillArgs a) {
   const int bl = blockIdx.y, g = blockIdx.z;
@@ -846,12 +916,32 @@ __global__ __launch_bounds__(kThreads) void prefill_ringfill(PrefillArgs a) {
   const int64_t unit = int64_t(sr.b) * a.Hkv + g;
   T* Kr = reinterpret_cast<T*>(a.state + a.layer_base + sec.K) + unit * a.R * D;
   T* Vr = reinterpret_cast<T*>(a.state + a.layer_base + sec.V) + unit * a.R * D;
-  for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < n * D; idx += gridDim.x * kThreads) {
-    const int i = idx / D, c = idx - i * D;
+  constexpr int CPR = D / 8;
+  const int stride = gridDim.x * kThreads;
+  for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < n * CPR; idx += stride) {
+    const int i = idx / CPR, ch = idx - i * CPR;
     const int64_t j = jlo + i;
-    const int32_t s = int32_t(j % a.R);
-    Kr[kring_elem(s, c, D)] = sr.k(j)[c];
-    Vr[vring_elem(s, c, D)] = sr.v(j)[c];
+    Frag<T> f;
+    f.load(sr.k(j) + 8 * ch);
+    store8(Kr + kring_elem(int32_t(j % a.R), 8 * ch, D), f);
+  }
+  const int64_t m0 = jlo >> 3;
+  const int ng = int(((pend - 1) >> 3) - m0 + 1);
+  for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < ng * D; idx += stride) {
+    const int gi = idx / D, c = idx - gi * D;
+    const int64_t j0 = (m0 + gi) * 8;
+    T* dst = Vr + vring_elem(int32_t(j0 % a.R), c, D);  // slots s0 .. s0+7 of column c
+    if (j0 >= jlo && j0 + 8 <= pend) {
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = to_f32(sr.v(j0 + e)[c]);
+      Frag<T> f;
+      f.set8(x);
+      store8(dst, f);
+    } else {
+      for (int e = 0; e < 8; ++e)
+        if (j0 + e >= jlo && j0 + e < pend) dst[e] = sr.v(j0 + e)[c];
+    }
   }
 }
 
@@ -883,10 +973,7 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
   hipError_t e;
   if (a.nseg > 0) {
     if (a.linear) {
-      const size_t lds_seg = (size_t(D) * row_t<DF>() + size_t(32) * row_t<DF>() + size_t(32) * row_t<D>()) *
-                             sizeof(T);
-      if ((e = set_lds(&prefill_segsum<T, D, DF>, lds_seg)) != hipSuccess) return e;
-      hipLaunchKernelGGL((prefill_segsum<T, D, DF>), dim3(a.nseg, a.Hkv), dim3(kThreads), lds_seg, s, a);
+      hipLaunchKernelGGL((prefill_segsum<T, D, DF>), dim3(a.nseg, a.Hkv), dim3(kSegThreads), 0, s, a);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       const int E = DF * D + DF;
       hipLaunchKernelGGL((prefill_scan<T, D, DF>), dim3((E / 4 + kThreads - 1) / kThreads, a.nseq, a.Hkv),
@@ -897,7 +984,7 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (a.W > 0) {
-    hipLaunchKernelGGL((prefill_ringfill<T, D, DF>), dim3(16, a.nseq, a.Hkv), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((prefill_ringfill<T, D, DF>), dim3(32, a.nseq, a.Hkv), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   hipLaunchKernelGGL((prefill_advance<T, D, DF>), dim3((a.nseq * a.Hkv + 255) / 256), dim3(256), 0, s, a);
