@@ -197,36 +197,42 @@ void decode_kernel(DecodeArgs a) {
     }
   }
   // Wf B fragments of this wave's features (zeros when there is no state pass)
+  // The state pass's loads (Wf, pending values, S rows, z) are issued only by
+  // the workgroup that does it (lin is uniform over the workgroup): other
+  // pieces go straight to their window tiles.
   const int f0 = wave * RW;
   Frag<T> wb[KS][NTW];
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk)
-#pragma unroll
-    for (int nt = 0; nt < NTW; ++nt)
-      bload_frag_strided(wb[kk][nt], rW, lin ? uint32_t((32 * kk + 8 * lg) * DF + f0 + 16 * nt + hq) * ES : kOOB,
-                         DF * ES);
-  // values of the pending tokens
   T pvr[PVT];
-#pragma unroll
-  for (int u = 0; u < PVT; ++u) {
-    const int e = tid + u * kThreads, i = e / D, c = e - i * D;
-    const bool ok = i < npend;
-    const uint32_t off = W > 0 ? uint32_t(vring_elem(int32_t((nf + (ok ? i : 0)) % R), c, D)) * ES : uint32_t(c) * ES;
-    pvr[u] = bload_elem(rpv, ok ? off : kOOB, T());
-  }
-  // this wave's S rows and z entries (zeros when S is empty)
   const int lr = lane / LPR, c4 = (lane % LPR) * 4;
   float4 sr[STEPS];
+  float zf = 0.f;
+  if (lin) {
 #pragma unroll
-  for (int s = 0; s < STEPS; ++s)
-    sr[s] = bload_f4(rS, s_nonzero ? uint32_t(((f0 + s * RPS + lr) * D + c4) * 4) : kOOB);
-  float zf = bload_f(rz, s_nonzero && lane < RW ? uint32_t((f0 + lane) * 4) : kOOB);
+    for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+      for (int nt = 0; nt < NTW; ++nt)
+        bload_frag_strided(wb[kk][nt], rW, uint32_t((32 * kk + 8 * lg) * DF + f0 + 16 * nt + hq) * ES, DF * ES);
+    // values of the pending tokens
+#pragma unroll
+    for (int u = 0; u < PVT; ++u) {
+      const int e = tid + u * kThreads, i = e / D, c = e - i * D;
+      const bool ok = i < npend;
+      const uint32_t off =
+          W > 0 ? uint32_t(vring_elem(int32_t((nf + (ok ? i : 0)) % R), c, D)) * ES : uint32_t(c) * ES;
+      pvr[u] = bload_elem(rpv, ok ? off : kOOB, T());
+    }
+    // this wave's S rows and z entries (zeros when S is empty)
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s)
+      sr[s] = bload_f4(rS, s_nonzero ? uint32_t(((f0 + s * RPS + lr) * D + c4) * 4) : kOOB);
+    zf = bload_f(rz, s_nonzero && lane < RW ? uint32_t((f0 + lane) * 4) : kOOB);
+  }
   // first window tile of this wave
   WindowTile<T, D> ta, tb;
   load_tile(ta, s0, W > 0 && it < n_tiles);
 
   // ---- 2. feature map on MFMA: rows x Wf, this wave's RW features, fp32
-  {
+  if (lin) {
     const int nrows = G + npend;
     f32x4_t acc[NTW], acb[NTW];
 #pragma unroll
@@ -239,15 +245,13 @@ void decode_kernel(DecodeArgs a) {
         acb[nt] = mma(xb[kk], wb[kk][nt], acb[nt]);
       }
     }
-    if (lin) {
 #pragma unroll
-      for (int nt = 0; nt < NTW; ++nt) {
+    for (int nt = 0; nt < NTW; ++nt) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = 4 * lg + i;
-          if (row < nrows) ph[row * DF + f0 + 16 * nt + hq] = fmaxf(acc[nt][i], 0.f);
-          if (16 + row < nrows) ph[(16 + row) * DF + f0 + 16 * nt + hq] = fmaxf(acb[nt][i], 0.f);
-        }
+      for (int i = 0; i < 4; ++i) {
+        const int row = 4 * lg + i;
+        if (row < nrows) ph[row * DF + f0 + 16 * nt + hq] = fmaxf(acc[nt][i], 0.f);
+        if (16 + row < nrows) ph[(16 + row) * DF + f0 + 16 * nt + hq] = fmaxf(acb[nt][i], 0.f);
       }
     }
   }

@@ -79,15 +79,6 @@ PrefillWorkspace prefill_ws(const glide_config* c, int64_t T) {
                            linear_on(c));
 }
 
-// Chunks per prefill segment: at least kMinSegTokens tokens (bounds the
-// records), and about one (segment, KV head) workgroup per CU when the call
-// is large enough; at most 16 chunks walked in order by one workgroup.
-int32_t segment_chunks(int64_t T, int Hkv, int32_t chunk) {
-  const int32_t lo = (kMinSegTokens + chunk - 1) / chunk;
-  const int64_t fill = T * Hkv / (int64_t(chunk) * 256);
-  return int32_t(std::max<int64_t>(lo, std::min<int64_t>(16, fill)));
-}
-
 // Decode window split (pieces per unit of each layer).  The work of a unit
 // is counted in 32-token window tiles plus kStateTiles for the state pass; a
 // layer whose units have work w gets min(kMaxPieces, ceil(w / q)) pieces, with
@@ -228,7 +219,11 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
 
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens) {
   if (check_cfg(cfg) != GLIDE_OK || max_total_tokens < 0) return 0;
-  const size_t pre = max_total_tokens > 0 ? prefill_ws(cfg, max_total_tokens).total : 0;
+  size_t pre = 0;
+  if (max_total_tokens > 0) {
+    const size_t slot = prefill_ws(cfg, max_total_tokens).slot;
+    pre = slot * size_t(prefill_slots(cfg->n_layers, slot));
+  }
   return std::max(size_t(256), std::max(pre, decode_ws(cfg)));
 }
 
@@ -314,16 +309,27 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   const int es = esize(cfg);
   const bool lin = linear_on(cfg);
   const PrefillWorkspace w = prefill_ws(cfg, T);
-  char* ws = static_cast<char*>(workspace);
   const int32_t seg_len = chunk * segment_chunks(T, Hkv, chunk);
   hipStream_t st = hipStream_t(stream);
+  // layers per launch: as many workspace slots as the caller's workspace holds
+  const int64_t fit = w.slot > 0 ? int64_t(workspace_bytes / w.slot) : n_layers;
+  const int32_t per_launch = int32_t(std::max<int64_t>(1, std::min<int64_t>({fit, n_layers, kMaxLayersPerLaunch})));
 
   PrefillArgs a;
   memset(&a, 0, sizeof(a));
   a.state = static_cast<char*>(state);
-  a.hk = ws + w.hk;
-  a.hv = ws + w.hv;
-  a.seg = reinterpret_cast<float*>(ws + w.seg);
+  a.q = static_cast<const char*>(q);
+  a.k = static_cast<const char*>(k);
+  a.v = static_cast<const char*>(v);
+  a.out = static_cast<char*>(out);
+  a.wf = static_cast<const char*>(phi_w);
+  a.q_stride = T * Hq * d * es;
+  a.kv_stride = T * Hkv * d * es;
+  a.wf_stride = int64_t(d) * Df * es;
+  a.ws = static_cast<char*>(workspace);
+  a.ws_slot = int64_t(w.slot);
+  a.ws_hv = int64_t(w.hv);
+  a.ws_seg = int64_t(w.seg);
   a.B = B;
   a.Hq = Hq;
   a.Hkv = Hkv;
@@ -352,28 +358,38 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
     return nseg;
   };
 
-  for (int32_t i = 0; i < n_layers; ++i) {
-    const int32_t l = layer0 + i;
-    const int32_t W = cfg->windows[l];
-    a.layer_base = layer_base(cfg, l);
-    a.W = W;
-    a.R = ring_slots(W);
-    a.q = static_cast<const char*>(q) + size_t(i) * T * Hq * d * es;
-    a.k = static_cast<const char*>(k) + size_t(i) * T * Hkv * d * es;
-    a.v = static_cast<const char*>(v) + size_t(i) * T * Hkv * d * es;
-    a.out = static_cast<char*>(out) + size_t(i) * T * Hq * d * es;
-    a.wf = static_cast<const char*>(phi_w) + size_t(i) * d * Df * es;
-    if (W > 0) {
-      // history of a continuing prefill (nothing to copy when pos == 0)
-      for (int g0 = 0; g0 < B; g0 += kMaxSeqPerLaunch) {
-        group(g0, 0);
-        s = hip_status(launch_prefill_gather(a, d, Df, cfg->dtype, st));
-        if (s != GLIDE_OK) return s;
-      }
+  // Layers by decreasing window, dealt round-robin over the launches: every
+  // launch gets a like mix of long and short windows, longest first (their
+  // workgroups are dispatched first).
+  std::vector<int32_t> rank(n_layers);
+  for (int32_t j = 0; j < n_layers; ++j) rank[j] = j;
+  std::stable_sort(rank.begin(), rank.end(), [&](int32_t x, int32_t y) {
+    return cfg->windows[layer0 + x] > cfg->windows[layer0 + y];
+  });
+  const int32_t n_launch = (n_layers + per_launch - 1) / per_launch;
+  for (int32_t li = 0; li < n_launch; ++li) {
+    std::vector<int32_t> order;
+    for (int32_t j = li; j < n_layers; j += n_launch) order.push_back(rank[j]);
+    const int32_t nl = int32_t(order.size());
+    bool window = false;
+    for (int32_t j = 0; j < nl; ++j) {
+      const int32_t l = layer0 + order[j];
+      PrefillLayer& L = a.layers[j];
+      L.layer_base = layer_base(cfg, l);
+      L.W = cfg->windows[l];
+      L.R = ring_slots(L.W);
+      L.li = order[j];
+      window = window || L.W > 0;
     }
+    a.nlayer = nl;
     int32_t seg0 = 0;
     for (int g0 = 0; g0 < B; g0 += kMaxSeqPerLaunch) {
       const int32_t nseg = group(g0, seg0);
+      if (window) {
+        // history of a continuing prefill (nothing to copy when pos == 0)
+        s = hip_status(launch_prefill_gather(a, d, Df, cfg->dtype, st));
+        if (s != GLIDE_OK) return s;
+      }
       s = hip_status(launch_prefill_layer(a, d, Df, cfg->dtype, st));
       if (s != GLIDE_OK) return s;
       seg0 += nseg;

@@ -474,18 +474,29 @@ hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* ou
 // the per-sequence tables travel in the kernel arguments.
 constexpr int kMaxSeqPerLaunch = 128;
 
+// Layers are batched: every prefill kernel takes up to kMaxLayersPerLaunch
+// layers in one launch (the grid's last dimension), each with a workspace
+// slot of its own, within kPrefillWsBudget bytes of workspace.
+constexpr size_t kPrefillWsBudget = size_t(1) << 30;
+
+struct PrefillLayer {
+  int64_t layer_base;  // byte offset of the layer in the state blob
+  int32_t W, R;
+  int32_t li;          // position of the layer in the call (inputs, outputs and Wf at li strides)
+  int32_t pad;
+};
+
 struct PrefillArgs {
   char* state;
-  int64_t layer_base;   // byte offset of the layer in the state blob
-  int32_t W, R;
-  const void* q;        // [T][Hq][d]   this layer's inputs, packed by sequence
-  const void* k;        // [T][Hkv][d]
-  const void* v;        // [T][Hkv][d]
-  void* out;            // [T][Hq][d]
-  const void* wf;       // this layer's feature-map matrix [d][Df]
-  void* hk;             // workspace: history keys    [B][Hkv][Wcap][d]
-  void* hv;             // workspace: history values  [B][Hkv][Wcap][d]
-  float* seg;           // workspace: per (segment, KV head) S [Df][d] then z [Df]
+  const char* q;        // [n][T][Hq][d]   the call's inputs (layer li at li * q_stride bytes)
+  const char* k;        // [n][T][Hkv][d]  (kv_stride)
+  const char* v;        // [n][T][Hkv][d]  (kv_stride)
+  char* out;            // [n][T][Hq][d]   (q_stride)
+  const char* wf;       // [n][d][Df]      (wf_stride)
+  int64_t q_stride, kv_stride, wf_stride;
+  char* ws;             // workspace: slot ls at ls * ws_slot bytes; per slot
+  int64_t ws_slot;      //   history keys [B][Hkv][Wcap][d] at 0, history values at ws_hv,
+  int64_t ws_hv, ws_seg;  // per (segment, KV head) S [Df][d] then z [Df] at ws_seg
   int32_t B, Hq, Hkv, G;
   int32_t linear;
   float tau;
@@ -496,19 +507,32 @@ struct PrefillArgs {
   int32_t seq0;         // first sequence of the group
   int32_t seg0;         // first segment record of the group
   int32_t nseg;         // segments in this group
-  int32_t pad;
+  int32_t nlayer;       // layers in this launch
+  PrefillLayer layers[kMaxLayersPerLaunch];  // the launch's layers, by decreasing window
   int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token
   int32_t seq_len[kMaxSeqPerLaunch];       // new tokens of the sequence
   int32_t seg_base[kMaxSeqPerLaunch + 1];  // first segment (within the group) of the sequence
 };
+static_assert(sizeof(PrefillArgs) <= 4096, "kernel argument block");
 
 // Segments hold at least kMinSegTokens tokens, which bounds the records.
 constexpr int kMinSegTokens = 128;
 
+// Chunks per prefill segment: at least kMinSegTokens tokens, and about one
+// (segment, KV head) workgroup per CU when the call is large enough; at most
+// 16 chunks walked in order by one workgroup.
+inline int32_t segment_chunks(int64_t T, int Hkv, int32_t chunk) {
+  const int32_t lo = (kMinSegTokens + chunk - 1) / chunk;
+  const int64_t fill = T * Hkv / (int64_t(chunk) * 256);
+  return int32_t(fill > lo ? (fill < 16 ? fill : 16) : lo);
+}
+
 struct PrefillWorkspace {
-  size_t hk, hv, seg, total;
+  size_t hk, hv, seg, slot;  // offsets within a slot, and the slot's bytes
 };
 
+// One layer's slot for calls of T tokens: the records bound takes the
+// shortest segment any legal chunk gives for T.
 inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hkv, int d, int Df, int esize, int Wcap,
                                           bool linear) {
   PrefillWorkspace w;
@@ -518,11 +542,24 @@ inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hkv, int d, int 
     off += size_t(align256(int64_t(bytes)));
     return o;
   };
+  int64_t seg_min = INT64_MAX;
+  for (int32_t c = 32; c <= 256; c += 32) {
+    const int64_t sl = int64_t(c) * segment_chunks(T, Hkv, c);
+    seg_min = sl < seg_min ? sl : seg_min;
+  }
   w.hk = take(size_t(B) * Hkv * Wcap * d * esize);
   w.hv = take(size_t(B) * Hkv * Wcap * d * esize);
-  w.seg = take(linear ? (size_t(T) / kMinSegTokens + B) * Hkv * (size_t(Df) * d + Df) * 4 : 0);
-  w.total = off;
+  w.seg = take(linear ? (size_t(T / seg_min) + B) * Hkv * (size_t(Df) * d + Df) * 4 : 0);
+  w.slot = off;
   return w;
+}
+
+// Layers per launch the workspace is sized for.
+inline int32_t prefill_slots(int32_t n_layers, size_t slot) {
+  int64_t n = n_layers < kMaxLayersPerLaunch ? n_layers : kMaxLayersPerLaunch;
+  const int64_t fit = slot > 0 ? int64_t(kPrefillWsBudget / slot) : n;
+  n = fit < n ? fit : n;
+  return int32_t(n > 1 ? n : 1);
 }
 
 hipError_t launch_prefill_layer(const PrefillArgs& a, int d, int Df, int dtype, hipStream_t stream);

@@ -78,8 +78,36 @@ struct SeqRows {
   __device__ int64_t qrow(int i, int hh) const { return (int64_t(start) + i) * Hq + int64_t(g) * G + hh; }
 };
 
+// Layer slot ls of the launch: its window, ring, state section, inputs,
+// outputs and workspace slot.
+struct LayerView {
+  char* base;  // the layer's sections in the state blob
+  int32_t W, R;
+  const void *q, *k, *v, *wf;
+  void* out;
+  void *hk, *hv;
+  float* seg;
+};
+__device__ __forceinline__ LayerView layer_view(const PrefillArgs& a, int ls) {
+  const PrefillLayer& L = a.layers[ls];
+  LayerView v;
+  v.base = a.state + L.layer_base;
+  v.W = L.W;
+  v.R = L.R;
+  v.q = a.q + int64_t(L.li) * a.q_stride;
+  v.out = a.out + int64_t(L.li) * a.q_stride;
+  v.k = a.k + int64_t(L.li) * a.kv_stride;
+  v.v = a.v + int64_t(L.li) * a.kv_stride;
+  v.wf = a.wf + int64_t(L.li) * a.wf_stride;
+  char* slot = a.ws + int64_t(ls) * a.ws_slot;
+  v.hk = slot;
+  v.hv = slot + a.ws_hv;
+  v.seg = reinterpret_cast<float*>(slot + a.ws_seg);
+  return v;
+}
+
 template <typename T, int D, int DF>
-__device__ __forceinline__ SeqRows<T, D> seq_rows(const PrefillArgs& a, int bl, int g) {
+__device__ __forceinline__ SeqRows<T, D> seq_rows(const PrefillArgs& a, const LayerView& L, int bl, int g) {
   SeqRows<T, D> r;
   r.b = a.seq0 + bl;
   r.g = g;
@@ -88,13 +116,13 @@ __device__ __forceinline__ SeqRows<T, D> seq_rows(const PrefillArgs& a, int bl, 
   r.Hkv = a.Hkv;
   r.G = a.G;
   const int64_t unit = int64_t(r.b) * a.Hkv + g;
-  r.kin = static_cast<const T*>(a.k);
-  r.vin = static_cast<const T*>(a.v);
-  r.kh = static_cast<const T*>(a.hk) + unit * a.Wcap * D;
-  r.vh = static_cast<const T*>(a.hv) + unit * a.Wcap * D;
-  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, a.R, sizeof(T));
-  r.p0 = reinterpret_cast<const int64_t*>(a.state + a.layer_base + sec.pos)[unit];
-  r.h0 = r.p0 - a.W > 0 ? r.p0 - a.W : 0;
+  r.kin = static_cast<const T*>(L.k);
+  r.vin = static_cast<const T*>(L.v);
+  r.kh = static_cast<const T*>(L.hk) + unit * a.Wcap * D;
+  r.vh = static_cast<const T*>(L.hv) + unit * a.Wcap * D;
+  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T));
+  r.p0 = reinterpret_cast<const int64_t*>(L.base + sec.pos)[unit];
+  r.h0 = r.p0 - L.W > 0 ? r.p0 - L.W : 0;
   return r;
 }
 
@@ -209,19 +237,21 @@ __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const
 // gather: history tokens [h0, p0) of a continuing prefill, ring -> [b][g][Wcap][d]
 template <typename T, int D, int DF>
 __global__ __launch_bounds__(kThreads) void prefill_gather(PrefillArgs a) {
-  const int bl = blockIdx.y, g = blockIdx.z;
-  const SeqRows<T, D> sr = seq_rows<T, D, DF>(a, bl, g);
+  const int bl = blockIdx.y, g = int(blockIdx.z) % a.Hkv;
+  const LayerView L = layer_view(a, int(blockIdx.z) / a.Hkv);
+  if (L.W == 0) return;
+  const SeqRows<T, D> sr = seq_rows<T, D, DF>(a, L, bl, g);
   const int n = int(sr.p0 - sr.h0);
   if (n <= 0) return;
-  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, a.R, sizeof(T));
+  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T));
   const int64_t unit = int64_t(sr.b) * a.Hkv + g;
-  const T* Kr = reinterpret_cast<const T*>(a.state + a.layer_base + sec.K) + unit * a.R * D;
-  const T* Vr = reinterpret_cast<const T*>(a.state + a.layer_base + sec.V) + unit * a.R * D;
-  T* hk = static_cast<T*>(a.hk) + unit * a.Wcap * D;
-  T* hv = static_cast<T*>(a.hv) + unit * a.Wcap * D;
+  const T* Kr = reinterpret_cast<const T*>(L.base + sec.K) + unit * L.R * D;
+  const T* Vr = reinterpret_cast<const T*>(L.base + sec.V) + unit * L.R * D;
+  T* hk = static_cast<T*>(L.hk) + unit * a.Wcap * D;
+  T* hv = static_cast<T*>(L.hv) + unit * a.Wcap * D;
   for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < n * D; idx += gridDim.x * kThreads) {
     const int i = idx / D, c = idx - i * D;
-    const int32_t s = int32_t((sr.h0 + i) % a.R);
+    const int32_t s = int32_t((sr.h0 + i) % L.R);
     hk[int64_t(i) * D + c] = Kr[kring_elem(s, c, D)];
     hv[int64_t(i) * D + c] = Vr[vring_elem(s, c, D)];
   }
@@ -258,12 +288,13 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
   T* vs = pk + kSegSlab * PROW;         // [64][VROW]     their values
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hq = lane & 15, lg = lane >> 4;
   const int sg = blockIdx.x, g = blockIdx.y;
+  const LayerView L = layer_view(a, blockIdx.z);
   const int bl = find_seq(a, sg);
-  const SeqRows<T, D> sr = seq_rows<T, D, DF>(a, bl, g);
+  const SeqRows<T, D> sr = seq_rows<T, D, DF>(a, L, bl, g);
   const int sigma = sg - a.seg_base[bl];
   const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
-  int64_t jlo = sr.p0 + s_lo - a.W;
-  const int64_t jhi = sr.p0 + s_hi - a.W;
+  int64_t jlo = sr.p0 + s_lo - L.W;
+  const int64_t jhi = sr.p0 + s_hi - L.W;
   if (jlo < 0) jlo = 0;
 
   f32x4_t sacc[NT];
@@ -286,7 +317,7 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
     }
   };
   if (jlo < jhi) load_slab(jlo);
-  stage_wf<T, D, DF, kSegThreads>(static_cast<const T*>(a.wf), Wn);
+  stage_wf<T, D, DF, kSegThreads>(static_cast<const T*>(L.wf), Wn);
   for (int64_t j0 = jlo; j0 < jhi; j0 += kSegSlab) {
     __syncthreads();  // Wf staged; the previous slab's readers are done
     {
@@ -321,7 +352,7 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
       }
     }
   }
-  float* rec = a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
+  float* rec = L.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
 #pragma unroll
   for (int x = 0; x < NT; ++x) {
     const int tile = wave * NT + x, ft = tile / CT, ct = tile - ft * CT;
@@ -342,15 +373,16 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
 template <typename T, int D, int DF>
 __global__ __launch_bounds__(kThreads) void prefill_scan(PrefillArgs a) {
   constexpr int E = DF * D + DF;
-  const int bl = blockIdx.y, g = blockIdx.z, b = a.seq0 + bl;
+  const int bl = blockIdx.y, g = int(blockIdx.z) % a.Hkv, b = a.seq0 + bl;
+  const LayerView L = layer_view(a, int(blockIdx.z) / a.Hkv);
   const int e = 4 * (blockIdx.x * kThreads + threadIdx.x);
   if (e >= E) return;
-  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, a.R, sizeof(T));
+  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T));
   const int64_t unit = int64_t(b) * a.Hkv + g;
-  float* st = e < DF * D ? reinterpret_cast<float*>(a.state + a.layer_base + sec.S) + unit * DF * D + e
-                         : reinterpret_cast<float*>(a.state + a.layer_base + sec.z) + unit * DF + (e - DF * D);
+  float* st = e < DF * D ? reinterpret_cast<float*>(L.base + sec.S) + unit * DF * D + e
+                         : reinterpret_cast<float*>(L.base + sec.z) + unit * DF + (e - DF * D);
   float4 run = *reinterpret_cast<const float4*>(st);
-  auto rec = [&](int sg) { return reinterpret_cast<float4*>(a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * E + e); };
+  auto rec = [&](int sg) { return reinterpret_cast<float4*>(L.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * E + e); };
   const int s1 = a.seg_base[bl + 1];
   int sg = a.seg_base[bl];
   // eight records' loads in flight at a time (the sum itself is serial)
@@ -435,15 +467,16 @@ void prefill_main(PrefillArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hq = lane & 15, lg = lane >> 4;
   const int sg = blockIdx.x, g = blockIdx.y;
+  const LayerView L = layer_view(a, blockIdx.z);
   const int bl = find_seq(a, sg);
-  SeqRows<T, D> sr = seq_rows<T, D, DF>(a, bl, g);
+  SeqRows<T, D> sr = seq_rows<T, D, DF>(a, L, bl, g);
   const int sigma = sg - a.seg_base[bl];
   const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
-  const int G = a.G, W = a.W, C = a.C;
+  const int G = a.G, W = L.W, C = a.C;
   const bool linear = a.linear != 0;
   const float sc2 = a.tau * kLog2e;
-  const T* Q = static_cast<const T*>(a.q);
-  T* O = static_cast<T*>(a.out);
+  const T* Q = static_cast<const T*>(L.q);
+  T* O = static_cast<T*>(L.out);
   // the global bases, made opaque once per pass: row addresses are then
   // computed where they are used instead of being kept across the walk
   auto refresh = [&]() {
@@ -457,7 +490,7 @@ void prefill_main(PrefillArgs a) {
   // Wf columns, with a fresh LDS base per phase
   auto wf_cols = [&]() {
     if constexpr (LD::kWfLds) return WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))};
-    else return WfCols<T, D, DF, false>{static_cast<const T*>(a.wf)};
+    else return WfCols<T, D, DF, false>{static_cast<const T*>(L.wf)};
   };
 
   // ---- pass geometry: chunk c0 (nk tokens from absolute position t0), rows
@@ -557,8 +590,8 @@ void prefill_main(PrefillArgs a) {
   //         segment start (the scan's record), fp32, into LDS (S transposed);
   //         they stay there for the whole walk
   if (linear) {
-    if constexpr (LD::kWfLds) stage_wf<T, D, DF, kMT>(static_cast<const T*>(a.wf), Wn);
-    const float* S0 = a.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
+    if constexpr (LD::kWfLds) stage_wf<T, D, DF, kMT>(static_cast<const T*>(L.wf), Wn);
+    const float* S0 = L.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
     constexpr int NS = DF * D / 4 / kMT;
     static_assert(NS * kMT * 4 == DF * D, "even split");
     float4 x[NS];
@@ -904,18 +937,20 @@ void prefill_main(PrefillArgs a) {
 // in range (its other slots may hold live tokens).
 template <typename T, int D, int DF>
 __global__ __launch_bounds__(kThreads) void prefill_ringfill(PrefillArgs a) {
-  const int bl = blockIdx.y, g = blockIdx.z;
-  const SeqRows<T, D> sr = seq_rows<T, D, DF>(a, bl, g);
+  const int bl = blockIdx.y, g = int(blockIdx.z) % a.Hkv;
+  const LayerView L = layer_view(a, int(blockIdx.z) / a.Hkv);
+  if (L.W == 0) return;
+  const SeqRows<T, D> sr = seq_rows<T, D, DF>(a, L, bl, g);
   const int Tb = a.seq_len[bl];
   const int64_t pend = sr.p0 + Tb;
-  int64_t jlo = pend - a.W;
+  int64_t jlo = pend - L.W;
   if (jlo < sr.p0) jlo = sr.p0;
   const int n = int(pend - jlo);
-  if (n <= 0 || a.W == 0) return;
-  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, a.R, sizeof(T));
+  if (n <= 0) return;
+  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T));
   const int64_t unit = int64_t(sr.b) * a.Hkv + g;
-  T* Kr = reinterpret_cast<T*>(a.state + a.layer_base + sec.K) + unit * a.R * D;
-  T* Vr = reinterpret_cast<T*>(a.state + a.layer_base + sec.V) + unit * a.R * D;
+  T* Kr = reinterpret_cast<T*>(L.base + sec.K) + unit * L.R * D;
+  T* Vr = reinterpret_cast<T*>(L.base + sec.V) + unit * L.R * D;
   constexpr int CPR = D / 8;
   const int stride = gridDim.x * kThreads;
   for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < n * CPR; idx += stride) {
@@ -923,14 +958,14 @@ __global__ __launch_bounds__(kThreads) void prefill_ringfill(PrefillArgs a) {
     const int64_t j = jlo + i;
     Frag<T> f;
     f.load(sr.k(j) + 8 * ch);
-    store8(Kr + kring_elem(int32_t(j % a.R), 8 * ch, D), f);
+    store8(Kr + kring_elem(int32_t(j % L.R), 8 * ch, D), f);
   }
   const int64_t m0 = jlo >> 3;
   const int ng = int(((pend - 1) >> 3) - m0 + 1);
   for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < ng * D; idx += stride) {
     const int gi = idx / D, c = idx - gi * D;
     const int64_t j0 = (m0 + gi) * 8;
-    T* dst = Vr + vring_elem(int32_t(j0 % a.R), c, D);  // slots s0 .. s0+7 of column c
+    T* dst = Vr + vring_elem(int32_t(j0 % L.R), c, D);  // slots s0 .. s0+7 of column c
     if (j0 >= jlo && j0 + 8 <= pend) {
       float x[8];
 #pragma unroll
@@ -951,49 +986,49 @@ template <typename T, int D, int DF>
 __global__ void prefill_advance(PrefillArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.nseq * a.Hkv) return;
+  const LayerView L = layer_view(a, blockIdx.y);
   const int bl = i / a.Hkv, g = i - bl * a.Hkv;
-  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, a.R, sizeof(T));
+  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T));
   const int64_t unit = int64_t(a.seq0 + bl) * a.Hkv + g;
-  int64_t* pos = reinterpret_cast<int64_t*>(a.state + a.layer_base + sec.pos) + unit;
-  int64_t* nf = reinterpret_cast<int64_t*>(a.state + a.layer_base + sec.nf) + unit;
+  int64_t* pos = reinterpret_cast<int64_t*>(L.base + sec.pos) + unit;
+  int64_t* nf = reinterpret_cast<int64_t*>(L.base + sec.nf) + unit;
   const int64_t p = *pos + a.seq_len[bl];
   *pos = p;
-  *nf = p - a.W > 0 ? p - a.W : 0;
+  *nf = p - L.W > 0 ? p - L.W : 0;
 }
 
-template <typename K>
-hipError_t set_lds(K* kern, size_t bytes) {
-  if (bytes <= 65536) return hipSuccess;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                             int(bytes));
-}
-
+// The kernels of one prefill launch, for the a.nlayer layers of a.layers
+// (the grid's last dimension runs over them, longest windows first).
 template <typename T, int D, int DF>
 hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
   hipError_t e;
+  const unsigned nl = unsigned(a.nlayer);
+  bool window = false;
+  for (int i = 0; i < a.nlayer; ++i) window = window || a.layers[i].W > 0;
   if (a.nseg > 0) {
     if (a.linear) {
-      hipLaunchKernelGGL((prefill_segsum<T, D, DF>), dim3(a.nseg, a.Hkv), dim3(kSegThreads), 0, s, a);
+      hipLaunchKernelGGL((prefill_segsum<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kSegThreads), 0, s, a);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       const int E = DF * D + DF;
-      hipLaunchKernelGGL((prefill_scan<T, D, DF>), dim3((E / 4 + kThreads - 1) / kThreads, a.nseq, a.Hkv),
+      hipLaunchKernelGGL((prefill_scan<T, D, DF>), dim3((E / 4 + kThreads - 1) / kThreads, a.nseq, a.Hkv * nl),
                          dim3(kThreads), 0, s, a);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv), dim3(kMT), 0, s, a);
+    hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kMT), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if (a.W > 0) {
-    hipLaunchKernelGGL((prefill_ringfill<T, D, DF>), dim3(32, a.nseq, a.Hkv), dim3(kThreads), 0, s, a);
+  if (window) {
+    hipLaunchKernelGGL((prefill_ringfill<T, D, DF>), dim3(32, a.nseq, a.Hkv * nl), dim3(kThreads), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((prefill_advance<T, D, DF>), dim3((a.nseq * a.Hkv + 255) / 256), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((prefill_advance<T, D, DF>), dim3((a.nseq * a.Hkv + 255) / 256, nl), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 template <typename T, int D, int DF>
 hipError_t gather_t(const PrefillArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((prefill_gather<T, D, DF>), dim3(16, a.nseq, a.Hkv), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((prefill_gather<T, D, DF>), dim3(16, a.nseq, a.Hkv * unsigned(a.nlayer)), dim3(kThreads), 0,
+                     s, a);
   return hipGetLastError();
 }
 
