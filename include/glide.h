@@ -114,9 +114,12 @@ size_t glide_state_bytes(const glide_config* cfg);
 /* Fills *out with the layout of layer `layer` (0 <= layer < cfg->n_layers). */
 glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_layer_layout* out);
 
-/* Workspace bytes needed by glide_prefill for calls with at most
- * max_total_tokens packed tokens (any chunk size) and by glide_decode_step
- * (any layer range); at least 256.  Decode uses it only when the stack has
+/* Workspace bytes needed by glide_prefill for calls of max_total_tokens
+ * packed tokens (any chunk size) and by glide_decode_step (any layer range);
+ * at least 256.  Prefill takes one slot per layer of a launch (history rows
+ * and per-segment state records) and batches as many layers per launch as
+ * the given workspace holds, up to 64; this size holds as many as fit in
+ * 1 GiB (at least one).  Decode uses the workspace only when the stack has
  * fewer than 1024 (layer, sequence, KV head) units: long windows are then
  * split over several workgroups, whose partial results it holds.  0 if cfg
  * is invalid. */

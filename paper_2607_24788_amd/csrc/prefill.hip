@@ -577,10 +577,8 @@ void prefill_main(PrefillArgs a) {
     }
   };
   auto prefetch = [&]() {
-    if (linear) {
-      load_q();
-      load_slab(0);
-    }
+    load_q();  // the band's queries, then the feature map's input
+    if (linear) load_slab(0);
     if (W > 0) fetch(0);
   };
 
@@ -621,10 +619,137 @@ void prefill_main(PrefillArgs a) {
       for (int ct = 0; ct < CT; ++ct) acc[qt][ct] = zero4();
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
 
-    // ---- 1. linear part
+    // ---- 1. banded window attention, keys [klo, khi], 32-key tiles (the
+    //         previous pass ended at a barrier: the shared region is free)
+    if (W > 0) {
+      refresh();
+      store(0);  // tile 0 was fetched with the pass's other prefetches
+      __syncthreads();
+      const bool pos_scale = sc2 > 0.f;  // (wave-uniform) the usual case: max of raw scores
+      for (int n = 0; n < ntile; ++n) {
+        const int buf = NBUF == 2 ? (n & 1) : 0;
+        if (n + 1 < ntile) fetch(n + 1);
+        const T* kt = lds_fresh(static_cast<const T*>(bnd) + buf * BAND);
+        const T* vt = kt + 32 * KROW;
+        const int64_t kb = kb0 + 32 * int64_t(n);
+        // scores: key row m of sub-tile t is key kb + 8(m/4) + 4t + m%4
+        f32x4_t sc[2][2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) {
+            Frag<T> fa;
+            fa.load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * KROW + 32 * kk + 8 * lg);
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
+          }
+        }
+        // keys [kb, kb+31] lie inside the band of every row of the pass
+        // (tokens t0+ti_min .. t0+ti_max) for all but the edge tiles
+        const bool interior = kb >= t0 + ti_max - W + 1 && kb + 31 <= t0 + ti_min;
+        Frag<T> pf[2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          // sv8: the tile's scores, -inf outside the band; scaled by sc2
+          // unless pos_scale (then the max is taken on the raw scores and the
+          // scale joins the exponent's FMA)
+          const float sm = pos_scale ? 1.f : sc2;
+          float sv8[8];
+          if (interior) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) sv8[4 * t + i] = pos_scale ? sc[qt][t][i] : sc[qt][t][i] * sm;
+          } else {
+            // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row exists
+            const int base = int(kb - (t0 + ti[qt]));
+            const int64_t offlo = klo - kb;  // first in-band offset of the tile (<= 31)
+            const int lo = offlo < -1 ? -1 : int(offlo);
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int off = 8 * lg + 4 * t + i;
+                const bool ok = rv[qt] && off >= lo && base + off <= 0 && base + off > -W;
+                sv8[4 * t + i] = ok ? sc[qt][t][i] * sm : -INFINITY;
+              }
+          }
+          float mx = sv8[0];
+#pragma unroll
+          for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv8[i]);
+          mx = lg_max(mx);
+          if (pos_scale) mx *= sc2;
+          // lazy rescale: the running max moves only when a score exceeds it
+          // by more than 2^8, so p = 2^(s - m) <= 256 and acc, l stay in range
+          if (__any(mx > m_run[qt] + 8.f)) {
+            const float m_new = fmaxf(m_run[qt], mx);
+            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
+            l_run[qt] *= alpha;
+            m_run[qt] = m_new;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) acc[qt][ct][i] *= alpha;
+          }
+          const float m_use = m_run[qt] == -INFINITY ? 0.f : m_run[qt];
+          float pv[8], ps = 0.f;
+          if (pos_scale) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              pv[i] = __builtin_amdgcn_exp2f(fmaf(sv8[i], sc2, -m_use));
+              ps += pv[i];
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              pv[i] = __builtin_amdgcn_exp2f(sv8[i] - m_use);
+              ps += pv[i];
+            }
+          }
+          pf[qt].set8(pv);
+          l_run[qt] += ps;
+        }
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          Frag<T> fv;
+          load_colfrag(fv, vt, VROW, 8 * lg, 16 * ct);
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
+        }
+        if (n + 1 < ntile) {
+          if (NBUF == 1) __syncthreads();  // every wave is done with the single buffer
+          store(NBUF == 2 ? ((n + 1) & 1) : 0);
+        }
+        __syncthreads();
+      }
+    }
+
+
+    // ---- 2. linear part.  The band's running max m (log2 domain) is the
+    //         row's frame: the linear terms enter scaled by 2^-m, m raised to
+    //         -60 first (the band's terms rescaled to match) so that 2^-m
+    //         stays finite; without a band (W = 0) m = 0.
     if (linear) {
       put_slab();  // the first slab's keys and values (made visible by the slab loop's barrier)
-      // phi(q), transposed: lane (row hq, group lg) gets features
+      float qscale[2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const bool none = m_run[qt] == -INFINITY;
+        const float m0 = none ? 0.f : fmaxf(m_run[qt], -60.f);
+        const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m0);
+        if (__any(alpha != 1.f)) {
+          l_run[qt] *= alpha;
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[qt][ct][i] *= alpha;
+        }
+        m_run[qt] = m0;
+        qscale[qt] = __builtin_amdgcn_exp2f(-m0);
+      }
+      // phi(q) 2^-m, transposed: lane (row hq, group lg) gets features
       // 32kf+4lg+i and 32kf+16+4lg+i of its query row in fragment kf
       Frag<T> pqf[2][KSF];
       const auto wf = wf_cols();
@@ -644,7 +769,7 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
           for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) pv[qt][4 * half + i] = fmaxf(ph[qt][i], 0.f);
+            for (int i = 0; i < 4; ++i) pv[qt][4 * half + i] = fmaxf(ph[qt][i], 0.f) * qscale[qt];
         }
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) pqf[qt][kf].set8(pv[qt]);
@@ -771,127 +896,9 @@ void prefill_main(PrefillArgs a) {
           }
         }
       }
-      // the linear part becomes the start of the online softmax: one
-      // pseudo-key of weight den (log2 domain: max = log2 den, sum 1)
+      // the shared denominator: band sum + linear part (per-lane partials)
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        const float dn = lg_sum(den[qt]);
-        m_run[qt] = dn > 0.f ? log2f(dn) : -INFINITY;
-        l_run[qt] = (dn > 0.f && lg == 0) ? 1.f : 0.f;
-        const float inv = dn > 0.f ? 1.f / dn : 0.f;
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc[qt][ct][i] *= inv;
-      }
-    }
-
-    // ---- 2. banded window attention, keys [klo, khi], 32-key tiles
-    if (W > 0) {
-      refresh();
-      load_q();         // the band's copy of the query rows (recently read: cache-resident)
-      __syncthreads();  // the previous users of the shared region (slab, band) are done
-      store(0);         // tile 0 was fetched with the pass's other prefetches
-      __syncthreads();
-      const bool pos_scale = sc2 > 0.f;  // (wave-uniform) the usual case: max of raw scores
-      for (int n = 0; n < ntile; ++n) {
-        const int buf = NBUF == 2 ? (n & 1) : 0;
-        if (n + 1 < ntile) fetch(n + 1);
-        const T* kt = lds_fresh(static_cast<const T*>(bnd) + buf * BAND);
-        const T* vt = kt + 32 * KROW;
-        const int64_t kb = kb0 + 32 * int64_t(n);
-        // scores: key row m of sub-tile t is key kb + 8(m/4) + 4t + m%4
-        f32x4_t sc[2][2];
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-#pragma unroll
-          for (int kk = 0; kk < KS; ++kk) {
-            Frag<T> fa;
-            fa.load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * KROW + 32 * kk + 8 * lg);
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
-          }
-        }
-        // keys [kb, kb+31] lie inside the band of every row of the pass
-        // (tokens t0+ti_min .. t0+ti_max) for all but the edge tiles
-        const bool interior = kb >= t0 + ti_max - W + 1 && kb + 31 <= t0 + ti_min;
-        Frag<T> pf[2];
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          // sv8: the tile's scores, -inf outside the band; scaled by sc2
-          // unless pos_scale (then the max is taken on the raw scores and the
-          // scale joins the exponent's FMA)
-          const float sm = pos_scale ? 1.f : sc2;
-          float sv8[8];
-          if (interior) {
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) sv8[4 * t + i] = pos_scale ? sc[qt][t][i] : sc[qt][t][i] * sm;
-          } else {
-            // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row exists
-            const int base = int(kb - (t0 + ti[qt]));
-            const int64_t offlo = klo - kb;  // first in-band offset of the tile (<= 31)
-            const int lo = offlo < -1 ? -1 : int(offlo);
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const int off = 8 * lg + 4 * t + i;
-                const bool ok = rv[qt] && off >= lo && base + off <= 0 && base + off > -W;
-                sv8[4 * t + i] = ok ? sc[qt][t][i] * sm : -INFINITY;
-              }
-          }
-          float mx = sv8[0];
-#pragma unroll
-          for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv8[i]);
-          mx = lg_max(mx);
-          if (pos_scale) mx *= sc2;
-          // lazy rescale: the running max moves only when a score exceeds it
-          // by more than 2^8, so p = 2^(s - m) <= 256 and acc, l stay in range
-          if (__any(mx > m_run[qt] + 8.f)) {
-            const float m_new = fmaxf(m_run[qt], mx);
-            const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
-            l_run[qt] *= alpha;
-            m_run[qt] = m_new;
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) acc[qt][ct][i] *= alpha;
-          }
-          const float m_use = m_run[qt] == -INFINITY ? 0.f : m_run[qt];
-          float pv[8], ps = 0.f;
-          if (pos_scale) {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              pv[i] = __builtin_amdgcn_exp2f(fmaf(sv8[i], sc2, -m_use));
-              ps += pv[i];
-            }
-          } else {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              pv[i] = __builtin_amdgcn_exp2f(sv8[i] - m_use);
-              ps += pv[i];
-            }
-          }
-          pf[qt].set8(pv);
-          l_run[qt] += ps;
-        }
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          Frag<T> fv;
-          load_colfrag(fv, vt, VROW, 8 * lg, 16 * ct);
-#pragma unroll
-          for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
-        }
-        if (n + 1 < ntile) {
-          if (NBUF == 1) __syncthreads();  // every wave is done with the single buffer
-          store(NBUF == 2 ? ((n + 1) & 1) : 0);
-        }
-        __syncthreads();
-      }
+      for (int qt = 0; qt < 2; ++qt) l_run[qt] += den[qt];
     }
 
     // ---- 3. the next pass's loads, then this pass's outputs: value columns
@@ -909,9 +916,13 @@ void prefill_main(PrefillArgs a) {
         rb += kRB;
       }
       geom();
-      refresh();
-      prefetch();
     }
+    // Unconditional, so that every path issues the same loads here (the
+    // compiler's wait counts merge paths, and a path without these loads
+    // would make the stores below wait for them).  After the last pass it
+    // reloads that pass's rows: valid addresses, never waited for.
+    refresh();
+    prefetch();
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
       const float ls = lg_sum(l_run[qt]);
