@@ -123,3 +123,56 @@ def test_prefill_after_decode(dtype):
     outs = case.prefill(st, q, k, v, starts, n2)
     case.check_prefill(outs, q, k, v, starts, n2, "prefill after decode")
     case.check_state(st, k, v, [a + b for a, b in zip(starts, n2)], "prefill after decode")
+
+
+def test_many_layers_two_launches():
+    """70 layers, more than one launch takes: the layers are dealt over two
+    launches by decreasing window, and every layer still matches the oracle."""
+    wins = [(i * 37) % 97 for i in range(70)]
+    case = Case(wins, batch=2, Hq=4, Hkv=2, d=64, Df=64, dtype=torch.bfloat16, seed=21)
+    _prefill_from_empty(case, [70, 33], label="70 layers")
+
+
+def _aligned_tokens(case, n, beta, c=4.0):
+    """Keys near one direction u (per layer, sequence, head), queries beta*u:
+    every score of a row has the sign of tau and magnitude ~ beta |u|^2 tau."""
+    gen = torch.Generator().manual_seed(case.seed * 31 + 5)
+    L, B, d = case.L, case.B, case.d
+    u = torch.randn((L, B, 1, case.Hkv, d), generator=gen) * (c / d ** 0.5)
+    k = u + 0.05 * torch.randn((L, B, n, case.Hkv, d), generator=gen) * (c / d ** 0.5)
+    uq = u.repeat_interleave(case.Hq // case.Hkv, dim=3)
+    q = beta * uq + 0.05 * torch.randn((L, B, n, case.Hq, d), generator=gen) * (c / d ** 0.5)
+    v = torch.randn((L, B, n, case.Hkv, d), generator=gen)
+    return q.to(case.dtype), k.to(case.dtype), v.to(case.dtype)
+
+
+@pytest.mark.parametrize("sign", [-1.0, 1.0])
+def test_extreme_score_frames(sign):
+    """tau < 0 with aligned queries: every band score is ~ -140 in log2 units
+    (the linear part's frame clamps at -60, the band's weight underflows
+    against the linear part); tau > 0: the band dominates and the linear part
+    vanishes.  Prefill, then decode steps, against the oracle."""
+    case = Case([0, 1, 9, 70], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16,
+                tau=sign * 128 ** -0.5, seed=22)
+    lens = [100, 61]
+    q, k, v = _aligned_tokens(case, 110, beta=70.0)
+    st = case.new_state()
+    outs = case.prefill(st, q, k, v, [0, 0], lens)
+    case.check_prefill(outs, q, k, v, [0, 0], lens, f"aligned tau sign {sign}")
+    case.check_state(st, k, v, lens, f"aligned tau sign {sign}")
+    phi = case.phi_w.cuda()
+    outs = []
+    for step in range(6):
+        qs = torch.stack([q[:, b, lens[b] + step] for b in range(2)], 1).contiguous().cuda()
+        ks = torch.stack([k[:, b, lens[b] + step] for b in range(2)], 1).contiguous().cuda()
+        vs = torch.stack([v[:, b, lens[b] + step] for b in range(2)], 1).contiguous().cuda()
+        o = torch.empty_like(qs)
+        case.g.decode_step(st, phi, qs, ks, vs, o, case.ws)
+        outs.append(o)
+    case.check_decode(torch.stack(outs, 2).cpu(), q, k, v, lens, 6, f"aligned decode tau sign {sign}")
+
+
+def test_zero_tau():
+    """tau = 0: uniform softmax over the window, merged with the linear part."""
+    case = Case([0, 3, 40], batch=1, Hq=4, Hkv=2, d=64, Df=64, dtype=torch.float32, tau=0.0, seed=23)
+    _prefill_from_empty(case, [90], label="tau 0")
