@@ -84,6 +84,8 @@ typedef struct {
  * blob's start).  Layout per layer l, every section 256-byte aligned:
  *   pos   int64 [B][Hkv]          p: tokens consumed by sequence b (equal over Hkv)
  *   nf    int64 [B][Hkv]          tokens folded into S and z (see below)
+ *   cnt   int32 [B][Hkv]          decode bookkeeping: pieces of a split unit
+ *                                 done in the current step; 0 between calls
  *   S     fp32  [B][Hkv][Df][d]   sum of phi(k_j)^T v_j over tokens j < nf
  *   z     fp32  [B][Hkv][Df]      sum of phi(k_j) over the same tokens
  *   kring dtype [B][Hkv][R*d]     keys, token j in slot s = j mod R
@@ -102,7 +104,7 @@ typedef struct {
  *   kring: [(o/4)%2][c/32][(c/8)%4][4*(o/8) + o%4][c%8]
  *   vring: [c/16][o/8][c%16][o%8]                                          */
 typedef struct {
-  int64_t pos_offset, nf_offset, s_offset, z_offset, kring_offset, vring_offset;
+  int64_t pos_offset, nf_offset, cnt_offset, s_offset, z_offset, kring_offset, vring_offset;
   int64_t layer_offset, layer_bytes;
   int32_t window;      /* W_l */
   int32_t ring_slots;  /* R_l */

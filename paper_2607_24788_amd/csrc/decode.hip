@@ -47,6 +47,110 @@ struct WindowTile {
 #define GLIDE_DECODE_WAVES_PER_SIMD 2
 #endif
 
+// Merge of the pieces of a split unit, run by the last of its workgroups to
+// finish (see the end of decode_kernel): the window parts (running max m, sum
+// l, weighted values acc per piece) over one max, plus piece 0's linear part,
+// over the shared denominator; then pos = p + 1.  The records are read with
+// system-coherent loads (they were written through to memory by workgroups
+// that may sit on other XCDs), every load of the workgroup issued before the
+// first wait.
+template <typename T, int D, int DF>
+__device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& L, int rem, int64_t p) {
+  constexpr int EPT = 4;                   // output elements per thread whose loads go first
+  static_assert(kMaxPieces * kMaxG <= kThreads, "one (piece, head) scalar pair per thread");
+  __shared__ float pw[kThreads];  // [piece][G]: m, then its weight e^(m - M)
+  __shared__ float pl[kThreads];  // [piece][G]: l
+  __shared__ float hs[kMaxG][3];            // per head: window weight, linear weight, 1 / denominator
+  const int G = a.G, B = a.B, Hkv = a.Hkv, Hq = a.Hq;
+  const int per_layer = B * Hkv;
+  const int np = L.npiece;
+  const int b = rem / Hkv, g = rem - b * Hkv;
+  const int64_t unit = int64_t(b) * Hkv + g;
+  const LayerSections sec = layer_sections(B, Hkv, D, DF, L.R, sizeof(T));
+  int64_t* pos_ptr = reinterpret_cast<int64_t*>(a.state + L.base + sec.pos) + unit;
+  const int64_t tok = int64_t(L.slot) * B + b;
+  T* og = reinterpret_cast<T*>(a.out) + (tok * Hq + int64_t(g) * G) * D;
+  constexpr int RH = 2 * D + 3;  // floats per head in a record
+  const uint32_t rb = uint32_t(part_floats(G, D)) * 4;  // bytes per record
+  // piece 0's record, and those of pieces 1 .. np-1 (consecutive rows)
+  const brsrc_t r0 = make_rsrc(a.part + (int64_t(L.prow0) * per_layer + rem) * part_floats(G, D), rb);
+  const brsrc_t r1 = make_rsrc(a.part + (int64_t(L.prow1) * per_layer + rem) * part_floats(G, D),
+                               uint32_t(np - 1) * uint32_t(per_layer) * rb);
+  const uint32_t rs = uint32_t(per_layer) * rb;  // bytes between pieces 1..
+  const int tid = threadIdx.x;
+  const int n = G * D;
+  // per piece and head: m, l (threads tid < np * G), loaded first
+  const int mpc = tid / G, mh = tid - mpc * G;
+  const bool mok = tid < np * G;
+  const uint32_t mo = uint32_t(mh * RH) * 4;
+  const float m0 = bload_f_sys(r0, mok && mpc == 0 ? mo : kOOB);
+  const float m1 = bload_f_sys(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo : kOOB);
+  const float l0 = bload_f_sys(r0, mok && mpc == 0 ? mo + 4 : kOOB);
+  const float l1 = bload_f_sys(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo + 4 : kOOB);
+  const float dnv = bload_f_sys(r0, tid < G ? uint32_t(tid * RH + 2) * 4 : kOOB);  // linear denominator
+  float v[EPT][kMaxPieces], nmv[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = tid + e * kThreads;
+    const int hh = i / D, c = i - hh * D;
+    const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
+    const bool ok = i < n;
+    v[e][0] = bload_f_sys(r0, ok ? o : kOOB);
+#pragma unroll
+    for (int pc = 1; pc < kMaxPieces; ++pc) v[e][pc] = bload_f_sys(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
+    nmv[e] = bload_f_sys(r0, ok ? o + D * 4 : kOOB);
+  }
+  // every thread writes its slot (kThreads slots; no branch, so the loads
+  // above are not sunk behind the record loads)
+  pw[tid] = m0 + m1;  // at most one of the two is not an OOB zero
+  pl[tid] = l0 + l1;
+  __syncthreads();
+  if (tid < G) {
+    float M = -INFINITY;
+    for (int pc = 0; pc < np; ++pc) M = fmaxf(M, pw[pc * G + tid]);
+    float Ls = 0.f;
+    for (int pc = 0; pc < np; ++pc) {
+      const float e = pw[pc * G + tid] == -INFINITY ? 0.f : exp2f(pw[pc * G + tid] - M);
+      pw[pc * G + tid] = e;
+      Ls = fmaf(pl[pc * G + tid], e, Ls);
+    }
+    const float dn = dnv;
+    if (dn > 0.f) {
+      const float c2 = fmaxf(M, log2f(dn));
+      const float ws = exp2f(M - c2), wlin = exp2f(-c2);
+      hs[tid][0] = ws;
+      hs[tid][1] = wlin;
+      hs[tid][2] = 1.f / (Ls * ws + dn * wlin);
+    } else {
+      hs[tid][0] = 1.f;
+      hs[tid][1] = 0.f;
+      hs[tid][2] = 1.f / Ls;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = tid + e * kThreads;
+    if (i < n) {
+      const int hh = i / D;
+      float Ac = 0.f;
+#pragma unroll
+      for (int pc = 0; pc < kMaxPieces; ++pc) Ac = pc < np ? fmaf(v[e][pc], pw[pc * G + hh], Ac) : Ac;
+      const float nm = hs[hh][1] == 0.f ? 0.f : nmv[e];
+      og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
+    }
+  }
+  for (int i = tid + EPT * kThreads; i < n; i += kThreads) {  // G * D > EPT * 256 (large G)
+    const int hh = i / D, c = i - hh * D;
+    const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
+    float Ac = bload_f_sys(r0, o) * pw[hh];
+    for (int pc = 1; pc < np; ++pc) Ac = fmaf(bload_f_sys(r1, (pc - 1) * rs + o), pw[pc * G + hh], Ac);
+    const float nm = hs[hh][1] == 0.f ? 0.f : bload_f_sys(r0, o + D * 4);
+    og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
+  }
+  if (tid == 0) *pos_ptr = p + 1;
+}
+
 template <typename T, int D, int DF>
 __global__ __launch_bounds__(kThreads)
 __attribute__((amdgpu_waves_per_eu(GLIDE_DECODE_WAVES_PER_SIMD, GLIDE_DECODE_WAVES_PER_SIMD)))
@@ -435,7 +539,9 @@ void decode_kernel(DecodeArgs a) {
   __syncthreads();
 
   // ---- 6. shared-denominator merge over the waves and the new token (and,
-  //         for a split unit, over the pieces in merge_kernel)
+  //         for a split unit, over the pieces: each writes a record, the last
+  //         to finish merges them)
+  const brsrc_t rrec = make_rsrc(a.part + int64_t(blockIdx.x) * part_floats(G, D), uint32_t(part_floats(G, D)) * 4);
   for (int i = tid; i < G * D; i += kThreads) {
     const int hh = i / D, c = i - hh * D;
     float nm = 0.f, dn = 0.f;
@@ -468,14 +574,14 @@ void decode_kernel(DecodeArgs a) {
       }
     }
     if (split) {
-      float* rec = a.part + int64_t(blockIdx.x) * part_floats(G, D) + int64_t(hh) * (2 * D + 3);
+      const uint32_t ro = uint32_t(hh * (2 * D + 3)) * 4;
       if (c == 0) {
-        rec[0] = M;
-        rec[1] = Ls;
-        rec[2] = dn;
+        bstore_f_sys(rrec, ro, M);
+        bstore_f_sys(rrec, ro + 4, Ls);
+        bstore_f_sys(rrec, ro + 8, dn);
       }
-      rec[3 + c] = Ac;
-      if (piece == 0) rec[3 + D + c] = nm;
+      bstore_f_sys(rrec, ro + uint32_t(3 + c) * 4, Ac);
+      if (piece == 0) bstore_f_sys(rrec, ro + uint32_t(3 + D + c) * 4, nm);
       continue;
     }
     float o;
@@ -492,6 +598,21 @@ void decode_kernel(DecodeArgs a) {
     }
     og[i] = from_f32<T>(o);
   }
+  if (split) {
+    // Every record store of the workgroup has reached memory before the
+    // unit's count moves (relaxed device-scope add: no cache write-back);
+    // the workgroup that brings it to npiece merges, then resets it.
+    __shared__ int last;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+      int* cnt = reinterpret_cast<int*>(lay + sec.cnt) + unit;
+      last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == L.npiece - 1;
+      if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (last) merge_unit<T, D, DF>(a, L, rem, p);
+  }
 
   // ---- 7. the new token into its ring slot (no token of this step reads
   //         that slot), position and fold count
@@ -501,114 +622,9 @@ void decode_kernel(DecodeArgs a) {
     Vr[vring_elem(sn, tid, D)] = vraw;
   }
   if (tid == 0 && piece == 0) {
-    if (!split) *pos_ptr = p + 1;  // a split unit's position moves in merge_kernel
+    if (!split) *pos_ptr = p + 1;  // a split unit's position moves in merge_unit
     if (fold) *nf_ptr = beta;
   }
-}
-
-// Merge of the pieces of split units: the window parts (running max m, sum
-// l, weighted values acc per piece) over one max, plus piece 0's linear
-// part, over the shared denominator; then pos += 1.  Every record load of the
-// workgroup is issued before the first wait (one memory round trip).
-template <typename T, int D, int DF>
-__global__ __launch_bounds__(kThreads) void merge_kernel(DecodeArgs a) {
-  constexpr int EPT = 4;                   // output elements per thread whose loads go first
-  static_assert(kMaxPieces * kMaxG <= kThreads, "one (piece, head) scalar pair per thread");
-  __shared__ float pw[kThreads];  // [piece][G]: m, then its weight e^(m - M)
-  __shared__ float pl[kThreads];  // [piece][G]: l
-  __shared__ float hs[kMaxG][3];            // per head: window weight, linear weight, 1 / denominator
-  const int G = a.G, B = a.B, Hkv = a.Hkv, Hq = a.Hq;
-  const int per_layer = B * Hkv;
-  const int li = blockIdx.x / per_layer;
-  const int rem = blockIdx.x - li * per_layer;
-  const LayerArg L = a.layers[li];
-  const int np = L.npiece;
-  if (np <= 1) return;
-  const int b = rem / Hkv, g = rem - b * Hkv;
-  const int64_t unit = int64_t(b) * Hkv + g;
-  const LayerSections sec = layer_sections(B, Hkv, D, DF, L.R, sizeof(T));
-  int64_t* pos_ptr = reinterpret_cast<int64_t*>(a.state + L.base + sec.pos) + unit;
-  const int64_t tok = int64_t(L.slot) * B + b;
-  T* og = reinterpret_cast<T*>(a.out) + (tok * Hq + int64_t(g) * G) * D;
-  constexpr int RH = 2 * D + 3;  // floats per head in a record
-  const uint32_t rb = uint32_t(part_floats(G, D)) * 4;  // bytes per record
-  // piece 0's record, and those of pieces 1 .. np-1 (consecutive rows)
-  const brsrc_t r0 = make_rsrc(a.part + (int64_t(L.prow0) * per_layer + rem) * part_floats(G, D), rb);
-  const brsrc_t r1 = make_rsrc(a.part + (int64_t(L.prow1) * per_layer + rem) * part_floats(G, D),
-                               uint32_t(np - 1) * uint32_t(per_layer) * rb);
-  const uint32_t rs = uint32_t(per_layer) * rb;  // bytes between pieces 1..
-  const int tid = threadIdx.x;
-  const int n = G * D;
-  // per piece and head: m, l (threads tid < np * G), loaded first
-  const int mpc = tid / G, mh = tid - mpc * G;
-  const bool mok = tid < np * G;
-  const uint32_t mo = uint32_t(mh * RH) * 4;
-  const float m0 = bload_f(r0, mok && mpc == 0 ? mo : kOOB);
-  const float m1 = bload_f(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo : kOOB);
-  const float l0 = bload_f(r0, mok && mpc == 0 ? mo + 4 : kOOB);
-  const float l1 = bload_f(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo + 4 : kOOB);
-  const float dnv = bload_f(r0, tid < G ? uint32_t(tid * RH + 2) * 4 : kOOB);  // linear denominator
-  float v[EPT][kMaxPieces], nmv[EPT];
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const int i = tid + e * kThreads;
-    const int hh = i / D, c = i - hh * D;
-    const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
-    const bool ok = i < n;
-    v[e][0] = bload_f(r0, ok ? o : kOOB);
-#pragma unroll
-    for (int pc = 1; pc < kMaxPieces; ++pc) v[e][pc] = bload_f(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
-    nmv[e] = bload_f(r0, ok ? o + D * 4 : kOOB);
-  }
-  // every thread writes its slot (kThreads slots; no branch, so the loads
-  // above are not sunk behind the record loads)
-  pw[tid] = m0 + m1;  // at most one of the two is not an OOB zero
-  pl[tid] = l0 + l1;
-  __syncthreads();
-  if (tid < G) {
-    float M = -INFINITY;
-    for (int pc = 0; pc < np; ++pc) M = fmaxf(M, pw[pc * G + tid]);
-    float Ls = 0.f;
-    for (int pc = 0; pc < np; ++pc) {
-      const float e = pw[pc * G + tid] == -INFINITY ? 0.f : exp2f(pw[pc * G + tid] - M);
-      pw[pc * G + tid] = e;
-      Ls = fmaf(pl[pc * G + tid], e, Ls);
-    }
-    const float dn = dnv;
-    if (dn > 0.f) {
-      const float c2 = fmaxf(M, log2f(dn));
-      const float ws = exp2f(M - c2), wlin = exp2f(-c2);
-      hs[tid][0] = ws;
-      hs[tid][1] = wlin;
-      hs[tid][2] = 1.f / (Ls * ws + dn * wlin);
-    } else {
-      hs[tid][0] = 1.f;
-      hs[tid][1] = 0.f;
-      hs[tid][2] = 1.f / Ls;
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const int i = tid + e * kThreads;
-    if (i < n) {
-      const int hh = i / D;
-      float Ac = 0.f;
-#pragma unroll
-      for (int pc = 0; pc < kMaxPieces; ++pc) Ac = pc < np ? fmaf(v[e][pc], pw[pc * G + hh], Ac) : Ac;
-      const float nm = hs[hh][1] == 0.f ? 0.f : nmv[e];
-      og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
-    }
-  }
-  for (int i = tid + EPT * kThreads; i < n; i += kThreads) {  // G * D > EPT * 256 (large G)
-    const int hh = i / D, c = i - hh * D;
-    const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
-    float Ac = bload_f(r0, o) * pw[hh];
-    for (int pc = 1; pc < np; ++pc) Ac = fmaf(bload_f(r1, (pc - 1) * rs + o), pw[pc * G + hh], Ac);
-    const float nm = hs[hh][1] == 0.f ? 0.f : bload_f(r0, o + D * 4);
-    og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
-  }
-  if (tid == 0) *pos_ptr += 1;
 }
 
 // Fold every pending token of a unit into S and z (nf := beta = max(0, p-W)),
@@ -683,33 +699,28 @@ hipError_t flush_t(const DecodeArgs& a, hipStream_t stream) {
 }
 
 template <typename T, int D, int DF>
-hipError_t launch_t(const DecodeArgs& a, int total_wg, bool merge, hipStream_t stream) {
+hipError_t launch_t(const DecodeArgs& a, int total_wg, hipStream_t stream) {
   const int G = a.G;
   const size_t floats = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D + 2 * D + kMaxG +
                         2 * (size_t(kWaves) * G * D + kWaves * G) + kWaves * G;
   hipLaunchKernelGGL((decode_kernel<T, D, DF>), dim3(unsigned(total_wg)), dim3(kThreads), floats * sizeof(float),
                      stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !merge) return e;
-  const dim3 grid(unsigned(a.n_layers) * unsigned(a.B) * unsigned(a.Hkv));
-  hipLaunchKernelGGL((merge_kernel<T, D, DF>), grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_decode(const DecodeArgs& a, int total_wg, bool merge, int d, int Df, int dtype,
-                         hipStream_t stream) {
+hipError_t launch_decode(const DecodeArgs& a, int total_wg, int d, int Df, int dtype, hipStream_t stream) {
   if (dtype == GLIDE_BF16) {
-    if (d == 128 && Df == 128) return launch_t<bf16_t, 128, 128>(a, total_wg, merge, stream);
-    if (d == 128 && Df == 64) return launch_t<bf16_t, 128, 64>(a, total_wg, merge, stream);
-    if (d == 64 && Df == 128) return launch_t<bf16_t, 64, 128>(a, total_wg, merge, stream);
-    if (d == 64 && Df == 64) return launch_t<bf16_t, 64, 64>(a, total_wg, merge, stream);
+    if (d == 128 && Df == 128) return launch_t<bf16_t, 128, 128>(a, total_wg, stream);
+    if (d == 128 && Df == 64) return launch_t<bf16_t, 128, 64>(a, total_wg, stream);
+    if (d == 64 && Df == 128) return launch_t<bf16_t, 64, 128>(a, total_wg, stream);
+    if (d == 64 && Df == 64) return launch_t<bf16_t, 64, 64>(a, total_wg, stream);
   } else {
-    if (d == 128 && Df == 128) return launch_t<float, 128, 128>(a, total_wg, merge, stream);
-    if (d == 128 && Df == 64) return launch_t<float, 128, 64>(a, total_wg, merge, stream);
-    if (d == 64 && Df == 128) return launch_t<float, 64, 128>(a, total_wg, merge, stream);
-    if (d == 64 && Df == 64) return launch_t<float, 64, 64>(a, total_wg, merge, stream);
+    if (d == 128 && Df == 128) return launch_t<float, 128, 128>(a, total_wg, stream);
+    if (d == 128 && Df == 64) return launch_t<float, 128, 64>(a, total_wg, stream);
+    if (d == 64 && Df == 128) return launch_t<float, 64, 128>(a, total_wg, stream);
+    if (d == 64 && Df == 64) return launch_t<float, 64, 64>(a, total_wg, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -208,6 +208,7 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
   out->layer_bytes = sec.bytes;
   out->pos_offset = base + sec.pos;
   out->nf_offset = base + sec.nf;
+  out->cnt_offset = base + sec.cnt;
   out->s_offset = base + sec.S;
   out->z_offset = base + sec.z;
   out->kring_offset = base + sec.K;
@@ -258,7 +259,7 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
   a.out = out;
   a.part = static_cast<float*>(workspace);
   return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g, int32_t wgs, bool split) {
-    return launch_decode(g, wgs, split, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
+    return launch_decode(g, wgs, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
   });
 }
 

@@ -56,7 +56,7 @@ __host__ __device__ inline int64_t kring_chunk(int32_t slot, int kk, int g, int 
 
 // Byte offsets of the sections of one layer, relative to the layer's start.
 struct LayerSections {
-  int64_t pos, nf, S, z, K, V, bytes;
+  int64_t pos, nf, cnt, S, z, K, V, bytes;
 };
 
 __host__ __device__ inline LayerSections layer_sections(int B, int Hkv, int d, int Df, int R, int esize) {
@@ -64,7 +64,8 @@ __host__ __device__ inline LayerSections layer_sections(int B, int Hkv, int d, i
   const int64_t units = int64_t(B) * Hkv;
   s.pos = 0;
   s.nf = align256(units * 8);
-  s.S = s.nf + align256(units * 8);
+  s.cnt = s.nf + align256(units * 8);
+  s.S = s.cnt + align256(units * 4);
   s.z = s.S + align256(units * Df * d * 4);
   s.K = s.z + align256(units * Df * 4);
   s.V = s.K + align256(units * int64_t(R) * d * esize);
@@ -341,6 +342,17 @@ __device__ __forceinline__ float4 bload_f4(brsrc_t r, uint32_t off) {
 __device__ __forceinline__ float bload_f(brsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
+// System-coherent access (cache policy sc0 sc1): stores are written through
+// to memory and loads are served from memory, not from a cache that may hold
+// an older copy.  For data one workgroup writes and another, possibly on
+// another XCD, reads within the same kernel.
+constexpr int kSysCoherent = 1 | 16;
+__device__ __forceinline__ float bload_f_sys(brsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSysCoherent));
+}
+__device__ __forceinline__ void bstore_f_sys(brsrc_t r, uint32_t off, float x) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, off, 0, kSysCoherent);
+}
 __device__ __forceinline__ bf16_t bload_elem(brsrc_t r, uint32_t off, bf16_t) {
   return bf16_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
 }
@@ -463,7 +475,7 @@ struct DecodeArgs {
 
 // Host-side launchers (one translation unit per kernel family).
 // total_wg: workgroups of the main pass; merge: some layer is split.
-hipError_t launch_decode(const DecodeArgs& a, int total_wg, bool merge, int d, int Df, int dtype,
+hipError_t launch_decode(const DecodeArgs& a, int total_wg, int d, int Df, int dtype,
                          hipStream_t stream);
 hipError_t launch_flush(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
 hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* out, int d, int Df, int dtype,

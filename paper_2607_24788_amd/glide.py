@@ -44,7 +44,8 @@ class Config(ctypes.Structure):
 
 
 class LayerLayout(ctypes.Structure):
-    _fields_ = [("pos_offset", ctypes.c_int64), ("nf_offset", ctypes.c_int64), ("s_offset", ctypes.c_int64),
+    _fields_ = [("pos_offset", ctypes.c_int64), ("nf_offset", ctypes.c_int64), ("cnt_offset", ctypes.c_int64),
+                ("s_offset", ctypes.c_int64),
                 ("z_offset", ctypes.c_int64), ("kring_offset", ctypes.c_int64),
                 ("vring_offset", ctypes.c_int64), ("layer_offset", ctypes.c_int64),
                 ("layer_bytes", ctypes.c_int64), ("window", ctypes.c_int32),
@@ -190,6 +191,7 @@ class Glide:
         return {
             "pos": view(lay.pos_offset, B * H, torch.int64, (B, H), 8),
             "nf": view(lay.nf_offset, B * H, torch.int64, (B, H), 8),
+            "cnt": view(lay.cnt_offset, B * H, torch.int32, (B, H), 4),
             "S": view(lay.s_offset, B * H * Df * d, torch.float32, (B, H, Df, d), 4),
             "z": view(lay.z_offset, B * H * Df, torch.float32, (B, H, Df), 4),
             "kring_raw": view(lay.kring_offset, B * H * R * d, self.torch_dtype, (B, H, R * d), es),

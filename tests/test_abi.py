@@ -59,12 +59,13 @@ def expected_layout(B, Hkv, d, Df, windows, es):
         units = B * Hkv
         pos = off
         nf = pos + align(units * 8)
-        S = nf + align(units * 8)
+        cnt = nf + align(units * 8)
+        S = cnt + align(units * 4)
         z = S + align(units * Df * d * 4)
         K = z + align(units * Df * 4)
         V = K + align(units * R * d * es)
         end = V + align(units * R * d * es)
-        out.append(dict(pos=pos, nf=nf, S=S, z=z, K=K, V=V, R=R, bytes=end - off))
+        out.append(dict(pos=pos, nf=nf, cnt=cnt, S=S, z=z, K=K, V=V, R=R, bytes=end - off))
         off = end
     return out, off
 
@@ -76,8 +77,8 @@ def test_layout_matches_documentation(dtype, es):
     assert g.state_bytes() == total
     for l, e in enumerate(exp):
         lay = g.layout(l)
-        assert (lay.pos_offset, lay.nf_offset, lay.s_offset, lay.z_offset, lay.kring_offset,
-                lay.vring_offset) == (e["pos"], e["nf"], e["S"], e["z"], e["K"], e["V"])
+        assert (lay.pos_offset, lay.nf_offset, lay.cnt_offset, lay.s_offset, lay.z_offset, lay.kring_offset,
+                lay.vring_offset) == (e["pos"], e["nf"], e["cnt"], e["S"], e["z"], e["K"], e["V"])
         assert lay.ring_slots == e["R"] and lay.window == g.windows[l]
         assert lay.layer_bytes == e["bytes"]
         assert lay.ring_slots == 0 or (lay.ring_slots % 32 == 0 and lay.ring_slots >= lay.window + 8)
