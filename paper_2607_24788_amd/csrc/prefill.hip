@@ -139,13 +139,6 @@ __device__ __forceinline__ void store8(float* dst, const Frag<float>& f) {
   reinterpret_cast<float4*>(dst)[1] = make_float4(f.v[4], f.v[5], f.v[6], f.v[7]);
 }
 
-// 4 consecutive outputs (scaled) in one store: 8 bytes (bf16) or 16 (fp32).
-__device__ __forceinline__ void store4(bf16_t* dst, f32x4_t x, float s) {
-  *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(x[0] * s, x[1] * s), pack_bf16x2(x[2] * s, x[3] * s));
-}
-__device__ __forceinline__ void store4(float* dst, f32x4_t x, float s) {
-  *reinterpret_cast<float4*>(dst) = make_float4(x[0] * s, x[1] * s, x[2] * s, x[3] * s);
-}
 
 // LDS row strides (elements): tiles read with 16-byte fragment loads use a
 // padding of 8; tiles read with load_colfrag use 16 so the four rows a
@@ -165,6 +158,17 @@ struct WfCols {
     else f.load_strided(src + (32 * kk + 8 * lg) * DF + col0 + hq, DF);
   }
 };
+
+// 4 consecutive outputs (scaled) in one store: 8 bytes (bf16) or 16 (fp32).
+__device__ __forceinline__ void store4(bf16_t* dst, f32x4_t x, float s) {
+  *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(x[0] * s, x[1] * s), pack_bf16x2(x[2] * s, x[3] * s));
+}
+__device__ __forceinline__ void store4(float* dst, f32x4_t x, float s) {
+  *reinterpret_cast<float4*>(dst) = make_float4(x[0] * s, x[1] * s, x[2] * s, x[3] * s);
+}
+__device__ __forceinline__ f32x4_t relu4(f32x4_t x) {
+  return f32x4_t{fmaxf(x[0], 0.f), fmaxf(x[1], 0.f), fmaxf(x[2], 0.f), fmaxf(x[3], 0.f)};
+}
 
 // Wf [D][DF] into LDS, natural layout (NTH threads cooperating; every load
 // is issued before the first store).
@@ -221,15 +225,16 @@ __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const
   const int per = (NK / 16) * FT / nw;
   for (int u = 0; u < per; ++u) {
     const int tile = wave * per + u, kt = tile / FT, ft = tile - kt * FT;
+    // transposed (Wf^T K^T): lane (hq, lg) gets features 16ft+4lg .. +3 of
+    // key 16kt+hq, one 4-element store
     f32x4_t acc = zero4();
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       Frag<T> wb;
       wf.col(wb, kk, 16 * ft);
-      acc = mma(x[kk], wb, acc);
+      acc = mma(wb, x[kk], acc);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pk[(16 * kt + 4 * lg + i) * PROW + 16 * ft + hq] = from_f32<T>(fmaxf(acc[i], 0.f));
+    store4(pk + (16 * kt + hq) * PROW + 16 * ft + 4 * lg, relu4(acc), 1.f);
   }
 }
 
