@@ -176,3 +176,40 @@ def test_zero_tau():
     """tau = 0: uniform softmax over the window, merged with the linear part."""
     case = Case([0, 3, 40], batch=1, Hq=4, Hkv=2, d=64, Df=64, dtype=torch.float32, tau=0.0, seed=23)
     _prefill_from_empty(case, [90], label="tau 0")
+
+
+def test_batch_over_one_launch():
+    """130 sequences (one launch takes 128): ragged lengths, empty ones among
+    them, prefill then decode steps."""
+    case = Case([0, 3, 40], batch=130, Hq=4, Hkv=2, d=64, Df=64, dtype=torch.bfloat16, seed=24)
+    gen = torch.Generator().manual_seed(24)
+    lens = [int(x) for x in torch.randint(0, 50, (130,), generator=gen)]
+    lens[0], lens[129] = 0, 49
+    q, k, v = case.tokens(max(lens) + 3)
+    st = case.new_state()
+    outs = case.prefill(st, q, k, v, [0] * 130, lens)
+    case.check_prefill(outs, q, k, v, [0] * 130, lens, "B=130")
+    case.check_state(st, k, v, lens, "B=130")
+    phi = case.phi_w.cuda()
+    step_out = []
+    for step in range(3):
+        qs = torch.stack([q[:, b, lens[b] + step] for b in range(130)], 1).contiguous().cuda()
+        ks = torch.stack([k[:, b, lens[b] + step] for b in range(130)], 1).contiguous().cuda()
+        vs = torch.stack([v[:, b, lens[b] + step] for b in range(130)], 1).contiguous().cuda()
+        o = torch.empty_like(qs)
+        case.g.decode_step(st, phi, qs, ks, vs, o, case.ws)
+        step_out.append(o)
+    case.check_decode(torch.stack(step_out, 2).cpu(), q, k, v, lens, 3, "B=130 decode")
+
+
+def test_max_window():
+    """W = 2^20, the largest window (ring and history buffers of 2^20 + 32
+    slots): a short prefill is plain causal softmax, then decode steps."""
+    case = Case([1 << 20, 0], batch=1, Hq=4, Hkv=2, d=64, Df=64, dtype=torch.bfloat16, seed=25)
+    q, k, v = case.tokens(140)
+    st = case.new_state()
+    outs = case.prefill(st, q, k, v, [0], [130])
+    case.check_prefill(outs, q, k, v, [0], [130], "W=2^20")
+    out = case.decode_steps(st, q, k, v, 130, 140)
+    case.check_decode(out, q, k, v, [130], 10, "W=2^20 decode")
+    case.check_state(st, k, v, [140], "W=2^20")
