@@ -151,7 +151,7 @@ def main():
     pre_flops = prefill_flops(wl, lens)
     mfma_peak = MFMA_BF16_PEAK if wl.dtype == torch.bfloat16 else MFMA_FP32_PEAK
     traffic = measured_traffic(wl.name)
-    hbm = {"bound": "hbm", "kernel": "decode step (decode_kernel, + merge_kernel when windows are split)",
+    hbm = {"bound": "hbm", "kernel": "decode step (decode_kernel; split windows merged by their last piece)",
            "achieved": dec_bytes / dec_step_s / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
            "frac": dec_bytes / dec_step_s / HBM_PEAK,
            "traffic": traffic and traffic["decode_step_bytes"],

@@ -162,8 +162,9 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
  * group from the window and from S + the pending tokens, pos += 1; on the
  * unit's fold step (one in 8; every step when W = 0) the pending tokens are
  * folded into S and z.  Sequences may sit at different positions (pos lives
- * in the state).  One kernel is enqueued per 64 layers, plus a merge kernel
- * when windows are split (see glide_workspace_bytes).
+ * in the state).  One kernel is enqueued per 64 layers; when windows are
+ * split (see glide_workspace_bytes) the workgroup that finishes a unit's last
+ * piece merges the pieces' partial results.
  *   phi_w  device [n_layers][d][Df]
  *   q      device [n_layers][B][Hq][d];  k, v device [n_layers][B][Hkv][d]
  *   out    device [n_layers][B][Hq][d]

@@ -88,8 +88,8 @@ struct LayerArg {
 // leave most CUs idle, so a unit's window tiles are spread over npiece
 // workgroups ("pieces"); piece 0 also does the ring write and the state.
 // Pieces write partial records (running max, sum and weighted values of the
-// window part per head; piece 0 adds the linear part), and a second kernel
-// merges them.  The split depends on the configuration only: the pieces are
+// window part per head; piece 0 adds the linear part); the piece that
+// finishes last (a per-unit counter in the state) merges them.  The split depends on the configuration only: the pieces are
 // made as small as possible while every workgroup of the stack still fits in
 // one round of kDecodeSlots resident workgroups (256 CUs x 2), since a
 // second round would be latency-bound; large batches are never split.

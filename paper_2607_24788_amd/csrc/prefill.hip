@@ -15,14 +15,15 @@
 //            increment from its delayed keys (MFMA, keys as the reduction);
 //   scan     exclusive prefix over segments on top of the incoming state;
 //            its end is the new S, z;
-//   main     per (segment, KV head): the segment's chunks in order, S carried
-//            in fp32 MFMA accumulators.  Per chunk: phi(q) on MFMA from the
-//            query rows; the linear read-out phi(Q)S_c plus the masked block
-//            of the chunk's delayed keys (whose phi(k) is computed once and
-//            also feeds S_{c+1}) start every query row's online softmax as one
-//            pseudo-key of weight a = phi(q).z_c + the block's weights and
-//            value A/a (exactly the shared-denominator merge); then the banded
-//            window attention over LDS-staged key tiles on MFMA;
+//   main     per (segment, KV head): the segment's chunks in order, S_c kept
+//            in LDS in fp32.  Per pass of 256 query rows: first the banded
+//            window attention over LDS-staged key tiles on MFMA (online
+//            softmax, running max m per row); then the linear part, phi(q) on
+//            MFMA, the read-out phi(Q)S_c, phi(q).z_c and the masked block of
+//            the chunk's delayed keys (whose phi(k) is computed once and also
+//            feeds S_{c+1}), all scaled by 2^-m so that they add straight
+//            onto the band's numerator and denominator (the shared-denominator
+//            merge, in the band's frame);
 //   ringfill the last W tokens into the ring;   advance: pos += T_b.
 // Tokens a decode step left pending are folded (glide_state_flush) before the
 // first of these kernels runs, so the incoming state is S = sum_{j < p0-W}.
