@@ -74,9 +74,9 @@ int32_t max_window(const glide_config* c) {
   return w;
 }
 
-PrefillWorkspace prefill_ws(const glide_config* c, int64_t T) {
+PrefillWorkspace prefill_ws(const glide_config* c, int64_t T, int32_t nl) {
   return prefill_workspace(T, c->batch, c->n_kv_heads, c->head_dim, c->feat_dim, esize(c), max_window(c),
-                           linear_on(c));
+                           linear_on(c), nl);
 }
 
 // Decode window split (pieces per unit of each layer).  The work of a unit
@@ -222,8 +222,10 @@ size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens) 
   if (check_cfg(cfg) != GLIDE_OK || max_total_tokens < 0) return 0;
   size_t pre = 0;
   if (max_total_tokens > 0) {
-    const size_t slot = prefill_ws(cfg, max_total_tokens).slot;
-    pre = slot * size_t(prefill_slots(cfg->n_layers, slot));
+    // as many layers per launch as fit in the budget (at least one)
+    auto slot_of = [&](int32_t nl) { return prefill_ws(cfg, max_total_tokens, nl).slot; };
+    const int32_t nl = prefill_layers_per_launch(cfg->n_layers, kPrefillWsBudget, slot_of);
+    pre = std::max(slot_of(1), size_t(nl) * (nl > 0 ? slot_of(nl) : 0));
   }
   return std::max(size_t(256), std::max(pre, decode_ws(cfg)));
 }
@@ -309,12 +311,13 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   const int B = cfg->batch, Hq = cfg->n_q_heads, Hkv = cfg->n_kv_heads, d = cfg->head_dim, Df = cfg->feat_dim;
   const int es = esize(cfg);
   const bool lin = linear_on(cfg);
-  const PrefillWorkspace w = prefill_ws(cfg, T);
-  const int32_t seg_len = chunk * segment_chunks(T, Hkv, chunk);
   hipStream_t st = hipStream_t(stream);
-  // layers per launch: as many workspace slots as the caller's workspace holds
-  const int64_t fit = w.slot > 0 ? int64_t(workspace_bytes / w.slot) : n_layers;
-  const int32_t per_launch = int32_t(std::max<int64_t>(1, std::min<int64_t>({fit, n_layers, kMaxLayersPerLaunch})));
+  // layers per launch: as many workspace slots (each sized for launches of
+  // that many layers) as the caller's workspace holds
+  auto slot_of = [&](int32_t nl) { return prefill_ws(cfg, T, nl).slot; };
+  const int32_t per_launch = std::max(1, prefill_layers_per_launch(n_layers, workspace_bytes, slot_of));
+  const PrefillWorkspace w = prefill_ws(cfg, T, per_launch);
+  const int32_t seg_len = chunk * segment_chunks(T, Hkv, chunk, per_launch);
 
   PrefillArgs a;
   memset(&a, 0, sizeof(a));

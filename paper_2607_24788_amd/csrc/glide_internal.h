@@ -172,6 +172,13 @@ template <> struct Frag<bf16_t> {
     v.z = pack_bf16x2(x[4], x[5]);
     v.w = pack_bf16x2(x[6], x[7]);
   }
+  // Every element's sign flipped (exact).
+  __device__ __forceinline__ void negate() {
+    v.x ^= 0x80008000u;
+    v.y ^= 0x80008000u;
+    v.z ^= 0x80008000u;
+    v.w ^= 0x80008000u;
+  }
   // Replace element i (runtime, 0..7) by b without indexing registers
   // dynamically (a dynamic index would force the fragment to scratch).
   __device__ __forceinline__ void patch(int i, bf16_t b) {
@@ -213,6 +220,10 @@ template <> struct Frag<float> {
   __device__ __forceinline__ void set8(const float* x) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = x[i];
+  }
+  __device__ __forceinline__ void negate() {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = -v[i];
   }
   __device__ __forceinline__ void patch(int i, float b) {
 #pragma unroll
@@ -530,12 +541,18 @@ static_assert(sizeof(PrefillArgs) <= 4096, "kernel argument block");
 // Segments hold at least kMinSegTokens tokens, which bounds the records.
 constexpr int kMinSegTokens = 128;
 
-// Chunks per prefill segment: at least kMinSegTokens tokens, and about one
-// (segment, KV head) workgroup per CU when the call is large enough; at most
-// 16 chunks walked in order by one workgroup.
-inline int32_t segment_chunks(int64_t T, int Hkv, int32_t chunk) {
+// Chunks per prefill segment, for a launch of nl layers: at least
+// kMinSegTokens tokens, and about kSegRounds workgroups per CU over the
+// launch's (segment, KV head, layer) grid when the call is large enough
+// (longer segments amortise each workgroup's start, the state load, over
+// more chunks; several rounds keep the CUs evenly loaded across layers of
+// different windows); at most 16 chunks walked in order by one workgroup.
+// More layers per launch never give shorter segments, so the workspace's
+// record bound, taken at nl = 1, holds for every launch.
+constexpr int kSegRounds = 8;
+inline int32_t segment_chunks(int64_t T, int Hkv, int32_t chunk, int32_t nl) {
   const int32_t lo = (kMinSegTokens + chunk - 1) / chunk;
-  const int64_t fill = T * Hkv / (int64_t(chunk) * 256);
+  const int64_t fill = T * Hkv * nl / (int64_t(chunk) * 256 * kSegRounds);
   return int32_t(fill > lo ? (fill < 16 ? fill : 16) : lo);
 }
 
@@ -543,10 +560,10 @@ struct PrefillWorkspace {
   size_t hk, hv, seg, slot;  // offsets within a slot, and the slot's bytes
 };
 
-// One layer's slot for calls of T tokens: the records bound takes the
-// shortest segment any legal chunk gives for T.
+// One layer's slot for calls of T tokens in launches of nl layers: the
+// records bound takes the shortest segment any legal chunk gives for T.
 inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hkv, int d, int Df, int esize, int Wcap,
-                                          bool linear) {
+                                          bool linear, int32_t nl) {
   PrefillWorkspace w;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -556,7 +573,7 @@ inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hkv, int d, int 
   };
   int64_t seg_min = INT64_MAX;
   for (int32_t c = 32; c <= 256; c += 32) {
-    const int64_t sl = int64_t(c) * segment_chunks(T, Hkv, c);
+    const int64_t sl = int64_t(c) * segment_chunks(T, Hkv, c, nl);
     seg_min = sl < seg_min ? sl : seg_min;
   }
   w.hk = take(size_t(B) * Hkv * Wcap * d * esize);
@@ -566,12 +583,15 @@ inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hkv, int d, int 
   return w;
 }
 
-// Layers per launch the workspace is sized for.
-inline int32_t prefill_slots(int32_t n_layers, size_t slot) {
-  int64_t n = n_layers < kMaxLayersPerLaunch ? n_layers : kMaxLayersPerLaunch;
-  const int64_t fit = slot > 0 ? int64_t(kPrefillWsBudget / slot) : n;
-  n = fit < n ? fit : n;
-  return int32_t(n > 1 ? n : 1);
+// Layers per launch for a workspace of `bytes`: the most layers nl (up to
+// kMaxLayersPerLaunch and n_layers) whose nl slots, sized for launches of nl
+// layers, fit; 0 if not even one layer's slot fits.
+template <typename SlotFn>
+inline int32_t prefill_layers_per_launch(int32_t n_layers, size_t bytes, SlotFn slot_of) {
+  int32_t n = n_layers < kMaxLayersPerLaunch ? n_layers : kMaxLayersPerLaunch;
+  for (; n >= 1; --n)
+    if (size_t(n) * slot_of(n) <= bytes) return n;
+  return 0;
 }
 
 hipError_t launch_prefill_layer(const PrefillArgs& a, int d, int Df, int dtype, hipStream_t stream);

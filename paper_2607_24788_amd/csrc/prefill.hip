@@ -425,7 +425,7 @@ __global__ __launch_bounds__(kThreads) void prefill_scan(PrefillArgs a) {
 // with them.
 template <typename T, int D, int DF>
 struct MainLds {
-  static constexpr int NBUF = sizeof(T) == 2 ? 2 : 1;  // band stages (fp32: one, to fit)
+  static constexpr int NBUF = 2;  // band stages
   static constexpr int SLAB = sizeof(T) == 4 && D == 128 ? 32 : 64;  // delayed keys per slab
   static constexpr int WROW = row_t<DF>(), PROW = row_t<DF>(), VROW = row_t<D>();
   static constexpr int SROW = DF + 4;                  // fp32 S^T rows: 16 rows of a 16-byte access on distinct banks
@@ -456,7 +456,7 @@ void prefill_main(PrefillArgs a) {
   constexpr int NT = FT * CT / kMW;            // S tiles per wave (state update)
   constexpr int SL = LD::SLAB;
   constexpr int SROW = LD::SROW, PROW = LD::PROW, VROW = LD::VROW, KROW = LD::KROW;
-  constexpr int NBUF = LD::NBUF, BAND = LD::BAND;
+  constexpr int BAND = LD::BAND;
   constexpr int CPR = D / 8;                   // 8-element chunks per K/V row
   constexpr int VPT = SL * CPR / kMT;          // slab chunks per thread (keys; values alike)
   static_assert(NT * kMW == FT * CT, "S tiles must spread evenly over the waves");
@@ -469,7 +469,7 @@ void prefill_main(PrefillArgs a) {
   T* pk = reinterpret_cast<T*>(smem + LD::sh);          // [SL][PROW]   phi(k) of the delayed keys
   T* vs = pk + SL * PROW;                               // [SL][VROW]   their values
   T* kr = vs + SL * VROW;                               // [SL][KROW]   their keys
-  T* bnd = reinterpret_cast<T*>(smem + LD::sh);         // band tiles: [NBUF] x (K [32][KROW], V [32][VROW])
+  T* bnd = reinterpret_cast<T*>(smem + LD::sh);         // band tiles: [2] x (K [32][KROW], V [32][VROW])
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hq = lane & 15, lg = lane >> 4;
   const int sg = blockIdx.x, g = blockIdx.y;
@@ -480,7 +480,13 @@ void prefill_main(PrefillArgs a) {
   const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
   const int G = a.G, W = L.W, C = a.C;
   const bool linear = a.linear != 0;
-  const float sc2 = a.tau * kLog2e;
+  // The band works on raw scores q.k scaled by sc2 >= 0 inside the exponent:
+  // a negative tau is carried by the queries' sign (negated in registers for
+  // the band, undone in the feature map), and a zero tau is raised to 1e-30,
+  // whose products with any finite score are far below fp32 resolution
+  // around the running max (every weight still comes out as exactly 1).
+  const bool qneg = a.tau < 0.f;
+  const float sc2 = fmaxf(fabsf(a.tau) * kLog2e, 1e-30f);
   const T* Q = static_cast<const T*>(L.q);
   T* O = static_cast<T*>(L.out);
   // the global bases, made opaque once per pass: row addresses are then
@@ -562,7 +568,7 @@ void prefill_main(PrefillArgs a) {
       store8(vsw + r * VROW + 8 * ch, frag_keep(vst[u], sok[u]));
     }
   };
-  // band tiles: this thread's chunk of the next tile (K and V)
+  // band tiles: this thread's chunk of tile n (K and V), for buffer n % 2
   Frag<T> sk, sv;
   bool fok = false;
   const bool stager = tid < 32 * CPR;  // wave-uniform
@@ -575,16 +581,18 @@ void prefill_main(PrefillArgs a) {
       sv.load((fok ? sr.v(j) : sr.v_safe()) + 8 * sch);
     }
   };
-  auto store = [&](int buf) {  // buf < NBUF
+  auto store = [&](int n) {
     if (stager) {
-      T* kt = lds_fresh(bnd + buf * BAND);
+      T* kt = lds_fresh(bnd + (n & 1) * BAND);
       store8(kt + srr * KROW + 8 * sch, frag_keep(sk, fok));
       store8(kt + 32 * KROW + srr * VROW + 8 * sch, frag_keep(sv, fok));
     }
   };
+  // (with a band, the first slab of delayed keys is loaded only after it:
+  // its registers are not held through the band loop)
   auto prefetch = [&]() {
     load_q();  // the band's queries, then the feature map's input
-    if (linear) load_slab(0);
+    if (linear && W == 0) load_slab(0);
     if (W > 0) fetch(0);
   };
 
@@ -625,19 +633,24 @@ void prefill_main(PrefillArgs a) {
       for (int ct = 0; ct < CT; ++ct) acc[qt][ct] = zero4();
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
 
-    // ---- 1. banded window attention, keys [klo, khi], 32-key tiles (the
-    //         previous pass ended at a barrier: the shared region is free)
+    // ---- 1. banded window attention, keys [klo, khi], 32-key tiles, two
+    //         LDS stages (the previous pass ended at a barrier: the shared
+    //         region is free)
+    float m_use[2] = {0.f, 0.f};  // m_run, or 0 while it is -inf
     if (W > 0) {
       refresh();
       store(0);  // tile 0 was fetched with the pass's other prefetches
+      if (qneg) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) qf[qt][kk].negate();
+      }
       __syncthreads();
-      const bool pos_scale = sc2 > 0.f;  // (wave-uniform) the usual case: max of raw scores
       for (int n = 0; n < ntile; ++n) {
-        const int buf = NBUF == 2 ? (n & 1) : 0;
         if (n + 1 < ntile) fetch(n + 1);
-        const T* kt = lds_fresh(static_cast<const T*>(bnd) + buf * BAND);
+        const T* kt = lds_fresh(static_cast<const T*>(bnd) + (n & 1) * BAND);
         const T* vt = kt + 32 * KROW;
-        const int64_t kb = kb0 + 32 * int64_t(n);
         // scores: key row m of sub-tile t is key kb + 8(m/4) + 4t + m%4
         f32x4_t sc[2][2];
 #pragma unroll
@@ -652,23 +665,18 @@ void prefill_main(PrefillArgs a) {
             for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
           }
         }
+        const int64_t kb = kb0 + 32 * int64_t(n);
         // keys [kb, kb+31] lie inside the band of every row of the pass
         // (tokens t0+ti_min .. t0+ti_max) for all but the edge tiles
         const bool interior = kb >= t0 + ti_max - W + 1 && kb + 31 <= t0 + ti_min;
+        // raw scores, -inf outside the band (edge tiles; set in place), and
+        // each row's tile max (the scale sc2 > 0 joins the exponent's FMA;
+        // the max is taken raw)
+        float mx[2];
         Frag<T> pf[2];
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) {
-          // sv8: the tile's scores, -inf outside the band; scaled by sc2
-          // unless pos_scale (then the max is taken on the raw scores and the
-          // scale joins the exponent's FMA)
-          const float sm = pos_scale ? 1.f : sc2;
-          float sv8[8];
-          if (interior) {
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) sv8[4 * t + i] = pos_scale ? sc[qt][t][i] : sc[qt][t][i] * sm;
-          } else {
+          if (!interior) {
             // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row exists
             const int base = int(kb - (t0 + ti[qt]));
             const int64_t offlo = klo - kb;  // first in-band offset of the tile (<= 31)
@@ -679,40 +687,40 @@ void prefill_main(PrefillArgs a) {
               for (int i = 0; i < 4; ++i) {
                 const int off = 8 * lg + 4 * t + i;
                 const bool ok = rv[qt] && off >= lo && base + off <= 0 && base + off > -W;
-                sv8[4 * t + i] = ok ? sc[qt][t][i] * sm : -INFINITY;
+                sc[qt][t][i] = ok ? sc[qt][t][i] : -INFINITY;
               }
           }
-          float mx = sv8[0];
+          float x = fmaxf(sc[qt][0][0], sc[qt][1][0]);
 #pragma unroll
-          for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv8[i]);
-          mx = lg_max(mx);
-          if (pos_scale) mx *= sc2;
-          // lazy rescale: the running max moves only when a score exceeds it
-          // by more than 2^8, so p = 2^(s - m) <= 256 and acc, l stay in range
-          if (__any(mx > m_run[qt] + 8.f)) {
-            const float m_new = fmaxf(m_run[qt], mx);
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 1; i < 4; ++i) x = fmaxf(x, sc[qt][t][i]);
+          mx[qt] = lg_max(x) * sc2;
+        }
+        // lazy rescale (one test for both row tiles): the running max moves
+        // only when a score exceeds it by more than 2^8, so p = 2^(s - m) <=
+        // 256 and acc, l stay in range
+        if (__any(mx[0] > m_run[0] + 8.f || mx[1] > m_run[1] + 8.f)) {
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) {
+            const float m_new = fmaxf(m_run[qt], mx[qt]);
             const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
             l_run[qt] *= alpha;
             m_run[qt] = m_new;
+            m_use[qt] = m_new == -INFINITY ? 0.f : m_new;
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
               for (int i = 0; i < 4; ++i) acc[qt][ct][i] *= alpha;
           }
-          const float m_use = m_run[qt] == -INFINITY ? 0.f : m_run[qt];
+        }
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
           float pv[8], ps = 0.f;
-          if (pos_scale) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              pv[i] = __builtin_amdgcn_exp2f(fmaf(sv8[i], sc2, -m_use));
-              ps += pv[i];
-            }
-          } else {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-              pv[i] = __builtin_amdgcn_exp2f(sv8[i] - m_use);
-              ps += pv[i];
-            }
+          for (int i = 0; i < 8; ++i) {
+            pv[i] = __builtin_amdgcn_exp2f(fmaf(sc[qt][i >> 2][i & 3], sc2, -m_use[qt]));
+            ps += pv[i];
           }
           pf[qt].set8(pv);
           l_run[qt] += ps;
@@ -724,10 +732,7 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
           for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
         }
-        if (n + 1 < ntile) {
-          if (NBUF == 1) __syncthreads();  // every wave is done with the single buffer
-          store(NBUF == 2 ? ((n + 1) & 1) : 0);
-        }
+        if (n + 1 < ntile) store(n + 1);
         __syncthreads();
       }
     }
@@ -738,7 +743,7 @@ void prefill_main(PrefillArgs a) {
     //         -60 first (the band's terms rescaled to match) so that 2^-m
     //         stays finite; without a band (W = 0) m = 0.
     if (linear) {
-      put_slab();  // the first slab's keys and values (made visible by the slab loop's barrier)
+      if (W > 0) load_slab(0);  // behind the feature map and the read-out
       float qscale[2];
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
@@ -753,7 +758,8 @@ void prefill_main(PrefillArgs a) {
             for (int i = 0; i < 4; ++i) acc[qt][ct][i] *= alpha;
         }
         m_run[qt] = m0;
-        qscale[qt] = __builtin_amdgcn_exp2f(-m0);
+        // (with the band's queries negated, phi takes them back: -(-q) Wf)
+        qscale[qt] = (W > 0 && qneg) ? -__builtin_amdgcn_exp2f(-m0) : __builtin_amdgcn_exp2f(-m0);
       }
       // phi(q) 2^-m, transposed: lane (row hq, group lg) gets features
       // 32kf+4lg+i and 32kf+16+4lg+i of its query row in fragment kf
@@ -775,7 +781,7 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
           for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) pv[qt][4 * half + i] = fmaxf(ph[qt][i], 0.f) * qscale[qt];
+            for (int i = 0; i < 4; ++i) pv[qt][4 * half + i] = fmaxf(ph[qt][i] * qscale[qt], 0.f);
         }
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) pqf[qt][kf].set8(pv[qt]);
@@ -814,6 +820,7 @@ void prefill_main(PrefillArgs a) {
       // block i' <= ti of every query row, and (last pass: every read-out of
       // S_c, z_c is done, and the loop covers all the chunk's keys)
       // S_{c+1} = S_c + phi(k)^T v, z_{c+1} = z_c + sum phi(k), in place
+      put_slab();  // the first slab's keys and values (made visible by the slab loop's barrier)
       for (int s0 = 0; s0 < nk; s0 += SL) {
         if (s0 > ti_max) break;
         if (s0 > 0) {
