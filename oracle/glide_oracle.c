@@ -37,6 +37,20 @@
  *   (token p - W when p >= W; the current token when W = 0), then appends the
  *   new token to the window, then reads out with the updated S and z.
  *
+ * The Appendix's two hybrid-attention equations (retention-based sliding
+ * window) add two separately normalised outputs instead, and the paper states
+ * that GLIDE adapts both through its merge operator.  They are selected by
+ * oracle_layer.form:
+ *   form 0  GLIDE: the shared denominator above, linear set [0, beta);
+ *   form 1  hybrid form 1: O_t = A / a + sum_X e^{s_j} v_j / sum_X e^{s_j},
+ *           linear set [0, beta) (the tokens evicted from the window);
+ *   form 2  hybrid form 2: the same sum, linear set [0, t] (the state holds
+ *           every token, those still in the window included).
+ * Each term of a sum is 0 when its set is empty (and A / a is 0 when a = 0).
+ * The state after p tokens covers the linear set of the next position:
+ * [0, p - W) in forms 0 and 1, [0, p) in form 2; a decode step in form 2
+ * folds the new token itself (as W = 0 does in form 0).
+ *
  * Two independent evaluations are provided: oracle_attend() evaluates the
  * definition directly (the quadratic form, Appendix eq. for O^Linear before
  * the rearrangement), oracle_decode_batch() runs the recurrence.  The tests
@@ -54,6 +68,7 @@ typedef struct {
   int32_t feat_dim;    /* Df */
   int32_t window;      /* W >= 0 */
   int32_t linear;      /* 1: linear part on (GLIDE), 0: pure sliding window */
+  int32_t form;        /* 0: shared denominator; 1, 2: the Appendix hybrid forms */
   double  tau;         /* softmax scale */
 } oracle_layer;
 
@@ -68,6 +83,8 @@ static int valid(const oracle_layer* L) {
   if (L->n_q_heads <= 0 || L->n_kv_heads <= 0 || L->n_q_heads % L->n_kv_heads) return 0;
   if (L->head_dim <= 0 || L->feat_dim <= 0 || L->window < 0) return 0;
   if (L->window == 0 && !L->linear) return 0;   /* empty attention set */
+  if (L->form < 0 || L->form > 2) return 0;
+  if (L->form != 0 && !L->linear) return 0;     /* the forms differ only in the linear part */
   return 1;
 }
 
@@ -99,13 +116,25 @@ static double dot(int n, const double* a, const double* b) {
 }
 
 /*
- * Shared-denominator merge of the two parts for one query head.
+ * Merge of the two parts for one query head (form 0: one shared denominator;
+ * forms 1, 2: two separately normalised outputs added).
  *   sm_num[d], sm_den, m : softmax part as sum e^{s_j - m} v_j, sum e^{s_j - m}
  *                          (has_sm == 0 when the softmax set is empty)
  *   A[d], a              : linear part, unscaled
  */
-static void merge(int d, int has_sm, const double* sm_num, double sm_den, double m,
+static void merge(int form, int d, int has_sm, const double* sm_num, double sm_den, double m,
                   const double* A, double a, double* out) {
+  if (form != 0) {
+#if ORACLE_MUTANT == 10
+    /* mutant: the linear term divided by both denominators */
+    for (int c = 0; c < d; ++c)
+      out[c] = (has_sm ? sm_num[c] / sm_den : 0.0) + (a > 0.0 ? A[c] / (a + (has_sm ? sm_den : 0.0)) : 0.0);
+#else
+    for (int c = 0; c < d; ++c)
+      out[c] = (has_sm ? sm_num[c] / sm_den : 0.0) + (a > 0.0 ? A[c] / a : 0.0);
+#endif
+    return;
+  }
   if (!has_sm) {
     for (int c = 0; c < d; ++c) out[c] = a > 0.0 ? A[c] / a : 0.0;
     return;
@@ -178,13 +207,18 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
           int64_t beta = t + 1 - W;
 #endif
           if (beta < 0) beta = 0;
-          /* linear part over [0, beta) */
+          /* linear part over [0, lend): [0, beta), or [0, t] in form 2 */
+#if ORACLE_MUTANT == 8
+          const int64_t lend = L->form == 2 ? t : beta;        /* mutant: form 2 misses the current token */
+#else
+          const int64_t lend = L->form == 2 ? t + 1 : beta;
+#endif
           double a = 0.0;
           for (int c = 0; c < d; ++c) A[c] = 0.0;
 #if ORACLE_MUTANT != 2
-          if (L->linear && beta > 0) {
+          if (L->linear && lend > 0) {
             phi_row(d, Df, Wf, qt, phq);
-            for (int64_t j = 0; j < beta; ++j) {
+            for (int64_t j = 0; j < lend; ++j) {
               const double aj = dot(Df, phq, phik + ((size_t)j * Hkv + g) * Df);
               const double* vj = v + ((size_t)j * Hkv + g) * d;
               for (int c = 0; c < d; ++c) A[c] += aj * vj[c];
@@ -218,7 +252,7 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
               den += e;
             }
           }
-          merge(d, has_sm, num, den, m, A, a, out + ((size_t)i * Hq + h) * d);
+          merge(L->form, d, has_sm, num, den, m, A, a, out + ((size_t)i * Hq + h) * d);
         }
       }
     }
@@ -230,8 +264,9 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
 
 /*
  * Recurrent state after consuming p tokens of one sequence, by direct sums:
- * S [Hkv][Df][d] = sum_{j < p-W} phi(k_j)^T v_j,  z [Hkv][Df] = sum phi(k_j).
- * Both zero when p <= W or when the linear part is off.
+ * S [Hkv][Df][d] = sum_{j < p-W} phi(k_j)^T v_j,  z [Hkv][Df] = sum phi(k_j)
+ * (j < p in form 2).  Both zero when p <= W (forms 0, 1) or when the linear
+ * part is off.
  */
 int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
                  const double* k, const double* v, double* S, double* z) {
@@ -239,7 +274,7 @@ int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
   const int Hkv = L->n_kv_heads, d = L->head_dim, Df = L->feat_dim, W = L->window;
   memset(S, 0, sizeof(double) * (size_t)Hkv * Df * d);
   memset(z, 0, sizeof(double) * (size_t)Hkv * Df);
-  const int64_t nfold = L->linear ? (p - W > 0 ? p - W : 0) : 0;
+  const int64_t nfold = !L->linear ? 0 : L->form == 2 ? p : (p - W > 0 ? p - W : 0);
   int err = 0;
 #pragma omp parallel for schedule(static)
   for (int g = 0; g < Hkv; ++g) {
@@ -268,8 +303,8 @@ int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
  *   q [B][Hq][d], k, v [B][Hkv][d]: the new token;  out [B][Hq][d]
  * Order per (sequence, KV head): fold the token leaving the window into S, z
  * (the oldest window token when the window is full; the new token itself
- * when W = 0), append the new token, then read out every query head of the
- * group from the updated state and window.
+ * when W = 0, and always in form 2), append the new token, then read out
+ * every query head of the group from the updated state and window.
  */
 int oracle_decode_batch(const oracle_layer* L, const double* Wf, int32_t B,
                         double* S, double* z, double* wk, double* wv, int64_t* pos,
@@ -307,7 +342,11 @@ int oracle_decode_batch(const oracle_layer* L, const double* Wf, int32_t B,
       if (L->linear && (W == 0 || nwin == W)) { fk = kn; fv = vn; }   /* mutant: folds the new token */
 #else
       if (L->linear) {
-        if (W == 0) { fk = kn; fv = vn; }
+#if ORACLE_MUTANT == 9
+        if (W == 0) { fk = kn; fv = vn; }                               /* mutant: form 2 folds like form 1 */
+#else
+        if (W == 0 || L->form == 2) { fk = kn; fv = vn; }
+#endif
         else if (nwin == W) { fk = Wk; fv = Wv; }                      /* oldest = token p - W */
       }
 #endif
@@ -353,7 +392,7 @@ int oracle_decode_batch(const oracle_layer* L, const double* Wf, int32_t B,
           for (int c = 0; c < d; ++c) num[c] += e * Wv[(size_t)j * d + c];
           den += e;
         }
-        merge(d, nwin > 0, num, den, m, A, a, out + ((size_t)b * Hq + h) * d);
+        merge(L->form, d, nwin > 0, num, den, m, A, a, out + ((size_t)b * Hq + h) * d);
       }
       free(pk); free(pq); free(A); free(num);
     }

@@ -21,7 +21,11 @@ What pins what:
     decoded state == direct sums (Appendix rearrangement to S and Z);
   * invariants: V == 1 gives O == 1 (shared denominator), outputs in the convex
     hull of the seen values, linearity in V, GQA == MHA with repeated K/V,
-    0/0 -> 0.
+    0/0 -> 0;
+  * the Appendix's two hybrid forms (forms 1, 2): hand-derived worked-example
+    values, O == band SDPA + causal linear attention (delayed by W in form 1,
+    undelayed in form 2), V == 1 giving one per non-empty part, and the
+    recurrent, direct-sum and continued-decode checks above in both forms.
 """
 import json
 import math
@@ -84,20 +88,21 @@ def pin_worked_example(lib):
     v = np.array(s["v"]).reshape(3, 1, 1)
     Wf = np.array(s["Wf"])
     for case in ex["cases"]:
-        o = oracle.Oracle(1, 1, 1, 1, case["window"], linear=case["linear"], tau=s["tau"], lib=lib)
+        o = oracle.Oracle(1, 1, 1, 1, case["window"], linear=case["linear"], tau=s["tau"], lib=lib,
+                          form=case.get("form", 0))
         got = o.attend(Wf, q, k, v).ravel()
         want = np.array([_eval_closed_form(x) for x in case["out"]])
         if not np.allclose(got, want, rtol=1e-12, atol=1e-12):
-            return f"worked example W={case['window']}: {got} != {want}"
+            return f"worked example form {case.get('form', 0)} W={case['window']}: {got} != {want}"
         S, z = o.state(Wf, k, v)
         if not (abs(S.item() - _eval_closed_form(case["S"])) < 1e-12
                 and abs(z.item() - _eval_closed_form(case["z"])) < 1e-12):
-            return f"worked example state W={case['window']}: S={S.item()} z={z.item()}"
+            return f"worked example state form {case.get('form', 0)} W={case['window']}: S={S.item()} z={z.item()}"
         # recurrent form on the same example
         st = o.empty_state(1)
         outs = [o.decode(Wf, st, q[t:t + 1], k[t:t + 1], v[t:t + 1]).item() for t in range(3)]
         if not np.allclose(outs, want, rtol=1e-12, atol=1e-12):
-            return f"worked example recurrent W={case['window']}: {outs} != {want}"
+            return f"worked example recurrent form {case.get('form', 0)} W={case['window']}: {outs} != {want}"
         if not (abs(st["S"].item() - _eval_closed_form(case["S"])) < 1e-12):
             return f"worked example recurrent state W={case['window']}"
     return None
@@ -171,34 +176,34 @@ def pin_recurrent_equals_definition(lib):
     n, Hq, Hkv, d, Df = 21, 4, 2, 6, 5
     q, k, v, Wf = _rand_case(5, n, Hq, Hkv, d, Df, scale=1.5)
     for W in (0, 1, 2, 3, 7, n - 1, n, n + 4):
-        for lin in (True, False):
+        for lin, form in ((True, 0), (False, 0), (True, 1), (True, 2)):
             if W == 0 and not lin:
                 continue
-            o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=lin, tau=0.6, lib=lib)
+            o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=lin, tau=0.6, lib=lib, form=form)
             want = o.attend(Wf, q, k, v)
             st = o.empty_state(1)
             got = np.stack([o.decode(Wf, st, q[t:t + 1], k[t:t + 1], v[t:t + 1])[0] for t in range(n)])
             if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
-                return f"recurrent != definition at W={W} linear={lin} (max err {np.abs(got - want).max()})"
+                return f"recurrent != definition at W={W} linear={lin} form={form} (max err {np.abs(got - want).max()})"
             S, z = o.state(Wf, k, v)
             if not (np.allclose(st["S"][0], S, rtol=1e-12, atol=1e-12) and np.allclose(st["z"][0], z)):
-                return f"recurrent state != direct sums at W={W} linear={lin}"
+                return f"recurrent state != direct sums at W={W} linear={lin} form={form}"
     return None
 
 
 def pin_state_direct_sums(lib):
     n, Hkv, d, Df = 15, 3, 4, 6
     _, k, v, Wf = _rand_case(6, n, Hkv, Hkv, d, Df)
-    for W in (0, 1, 4, n, n + 2):
-        o = oracle.Oracle(Hkv, Hkv, d, Df, W, linear=True, lib=lib)
+    for W, form in ((0, 0), (1, 0), (4, 0), (n, 0), (n + 2, 0), (4, 1), (0, 2), (4, 2), (n + 2, 2)):
+        o = oracle.Oracle(Hkv, Hkv, d, Df, W, linear=True, lib=lib, form=form)
         for p in (0, 1, 7, n):
             S, z = o.state(Wf, k, v, p)
-            m = max(p - W, 0)
+            m = p if form == 2 else max(p - W, 0)
             pk = np.maximum(k[:m] @ Wf, 0.0)              # [m][Hkv][Df]
             Sw = np.einsum("jgf,jgc->gfc", pk, v[:m])
             zw = pk.sum(0)
             if not (np.allclose(S, Sw, atol=1e-12) and np.allclose(z, zw, atol=1e-12)):
-                return f"state != einsum direct sums at W={W} p={p}"
+                return f"state != einsum direct sums at W={W} p={p} form={form}"
     return None
 
 
@@ -283,22 +288,78 @@ def pin_continue_from_state(lib):
     """Decode continuing from a state built by direct sums == definition."""
     n, Hq, Hkv, d, Df = 20, 4, 2, 5, 6
     q, k, v, Wf = _rand_case(11, n, Hq, Hkv, d, Df)
-    for W in (0, 3, 8):
-        o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib)
+    for W, form in ((0, 0), (3, 0), (8, 0), (3, 1), (8, 2)):
+        o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib, form=form)
         want = o.attend(Wf, q, k, v)
         p0 = 11
         S, z, wk, wv = o.state_from_history(Wf, k, v, p0)
         st = {"S": S[None], "z": z[None], "wk": wk[None], "wv": wv[None], "pos": np.array([p0])}
         got = np.stack([o.decode(Wf, st, q[t:t + 1], k[t:t + 1], v[t:t + 1])[0] for t in range(p0, n)])
         if not np.allclose(got, want[p0:], rtol=1e-10, atol=1e-12):
-            return f"decode continued from a direct-sum state != definition at W={W}"
+            return f"decode continued from a direct-sum state != definition at W={W} form={form}"
+    return None
+
+
+def _masked_linear(q, k, v, Wf, delay):
+    """Causal linear attention over keys j <= t - delay, masked-matrix form
+    (numpy matmuls); 0/0 -> 0."""
+    G = q.shape[1] // k.shape[1]
+    n = q.shape[0]
+    pq = np.maximum(q @ Wf, 0.0)
+    pk = np.maximum(np.repeat(k, G, axis=1) @ Wf, 0.0)
+    vv = np.repeat(v, G, axis=1)
+    mask = np.tril(np.ones((n, n)), -delay)
+    out = np.zeros(q.shape)
+    for h in range(q.shape[1]):
+        M = (pq[:, h] @ pk[:, h].T) * mask
+        den = M.sum(-1)
+        out[:, h] = np.where((den > 0)[:, None], (M @ vv[:, h]) / np.where(den > 0, den, 1.0)[:, None], 0.0)
+    return out
+
+
+def pin_hybrid_forms_are_band_plus_linear(lib):
+    """Forms 1, 2 == SDPA over the band + causal linear attention over the
+    evicted tokens (delay W) or over every token (delay 0)."""
+    n, Hq, Hkv, d, Df = 26, 4, 2, 8, 7
+    q, k, v, Wf = _rand_case(12, n, Hq, Hkv, d, Df)
+    tau = 0.8
+    t = np.arange(n)[:, None]
+    j = np.arange(n)[None, :]
+    for W in (0, 1, 4, 11, n + 3):
+        band = np.zeros(q.shape) if W == 0 else _sdpa(q, k, v, tau, (j <= t) & (j >= t - W + 1))
+        for form, delay in ((1, W), (2, 0)):
+            want = band + _masked_linear(q, k, v, Wf, delay)
+            got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, tau=tau, lib=lib, form=form).attend(Wf, q, k, v)
+            if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
+                return f"form {form} W={W} != band SDPA + linear (max err {np.abs(got - want).max()})"
+    return None
+
+
+def pin_hybrid_v_ones(lib):
+    """V == 1: each non-empty part contributes exactly 1."""
+    n, Hq, Hkv, d, Df = 15, 2, 2, 6, 16
+    q, k, _, Wf = _rand_case(13, n, Hq, Hkv, d, Df, scale=2.0)
+    v = np.ones((n, Hkv, d))
+    pq = np.maximum(q @ Wf, 0.0)
+    pk = np.maximum(k @ Wf, 0.0)
+    for form in (1, 2):
+        for W in (0, 1, 5, n):
+            got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib, form=form).attend(Wf, q, k, v)
+            for tt in range(n):
+                lend = tt + 1 if form == 2 else max(0, tt + 1 - W)
+                for h in range(Hq):
+                    a = sum(pq[tt, h] @ pk[jj, h] for jj in range(lend))
+                    want = (1.0 if W > 0 else 0.0) + (1.0 if a > 0 else 0.0)
+                    if not np.allclose(got[tt, h], want, rtol=1e-12, atol=1e-12):
+                        return f"form {form} V==1 at W={W} t={tt}: {got[tt, h, 0]} != {want}"
     return None
 
 
 ALL_PINS = [pin_worked_example, pin_full_window_is_causal_softmax, pin_band_is_masked_sdpa,
             pin_w0_is_causal_linear, pin_w1_closed_form, pin_recurrent_equals_definition,
             pin_state_direct_sums, pin_v_ones, pin_convex_hull, pin_linearity,
-            pin_gqa_is_repeated_mha, pin_zero_over_zero, pin_continue_from_state]
+            pin_gqa_is_repeated_mha, pin_zero_over_zero, pin_continue_from_state,
+            pin_hybrid_forms_are_band_plus_linear, pin_hybrid_v_ones]
 
 
 def run_all(lib):

@@ -26,7 +26,10 @@ def test_pin(pin):
 #  3 separately normalised "+" merge        4 feature map with Wf transposed
 #  5 decode folds the new token, not the evicted one
 #  6 merge without a common stabiliser      7 softmax scale tau missing
-MUTANTS = [1, 2, 3, 4, 5, 6, 7]
+#  8 hybrid form 2 misses the current token in its linear set
+#  9 hybrid form 2's decode folds the evicted token, not the new one
+# 10 hybrid forms divide the linear term by both denominators
+MUTANTS = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10]
 
 
 @pytest.mark.parametrize("mutant", MUTANTS)
