@@ -63,8 +63,21 @@ enum { GLIDE_PHI_RELU = 0 };
 
 /* flags: GLIDE_NO_LINEAR turns the linear part off (plain sliding-window
  * softmax attention, the "Hybrid" preset with nothing kept beyond the
- * window); W = 0 is then rejected because the attention set is empty. */
-enum { GLIDE_NO_LINEAR = 1 };
+ * window); W = 0 is then rejected because the attention set is empty.
+ *
+ * GLIDE_HYBRID_SUM selects the Appendix's first hybrid-attention equation
+ * (retention-based sliding window) instead of the shared denominator: the
+ * window's softmax output and the linear part's own normalised output
+ * phi(q).S / phi(q).z are added,
+ *   O_t = sum_{j=beta..t} e^{s_j} v_j / sum_{j=beta..t} e^{s_j}  +  A / a,
+ * each term 0 when its set is empty (A / a := 0 when a = 0).  Adding
+ * GLIDE_HYBRID_STATE_ALL selects the Appendix's second equation: the same
+ * sum with the state over every token up to the current one, window tokens
+ * included (linear set [0, t]; S, z then hold tokens [0, p) after p tokens).
+ * The paper states that GLIDE adapts both forms through its merge operator.
+ * GLIDE_HYBRID_STATE_ALL requires GLIDE_HYBRID_SUM; neither combines with
+ * GLIDE_NO_LINEAR. */
+enum { GLIDE_NO_LINEAR = 1, GLIDE_HYBRID_SUM = 2, GLIDE_HYBRID_STATE_ALL = 4 };
 
 typedef struct {
   int32_t n_layers;    /* layers held by one state blob (>= 1) */
@@ -75,7 +88,7 @@ typedef struct {
   int32_t feat_dim;    /* Df: 64 or 128 */
   int32_t dtype;       /* GLIDE_F32 or GLIDE_BF16 */
   int32_t phi;         /* GLIDE_PHI_RELU */
-  int32_t flags;       /* 0 or GLIDE_NO_LINEAR */
+  int32_t flags;       /* 0, GLIDE_NO_LINEAR, GLIDE_HYBRID_SUM, or GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL */
   float sm_scale;      /* tau, the softmax scale (1/sqrt(d) in the Appendix's attention) */
   const int32_t* windows; /* HOST array [n_layers]: W_l = w - delta_l, 0 <= W_l <= 2^20 */
 } glide_config;
@@ -95,9 +108,10 @@ typedef struct {
  * window in batches of up to 8 (staggered over units), so nf lies in
  * [beta - 8, beta] (W = 0: nf = beta); tokens [nf, beta) are "pending": kept
  * in the ring and added to the read-out from there.  glide_prefill and
- * glide_state_flush leave nf = beta.  R = ring_slots = round_up(W + 8, 32)
- * for W > 0, 0 for W = 0.  After p tokens the ring holds tokens [nf, p - 1]
- * (W > 0); other slots are stale.
+ * glide_state_flush leave nf = beta.  With GLIDE_HYBRID_STATE_ALL, beta = p
+ * and every step folds its own token (nf = p).  R = ring_slots =
+ * round_up(W + 8, 32) for W > 0, 0 for W = 0.  After p tokens the ring holds
+ * tokens [min(nf, p - W), p - 1] (W > 0); other slots are stale.
  * Both rings are stored in 32-slot blocks of 32*d elements, in the fragment
  * order of the decode kernel's matrix-core loads; with o = s % 32, block
  * s / 32, element c of the slot is at (within the block)

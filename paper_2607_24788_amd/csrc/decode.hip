@@ -50,7 +50,8 @@ struct WindowTile {
 // Merge of the pieces of a split unit, run by the last of its workgroups to
 // finish (see the end of decode_kernel): the window parts (running max m, sum
 // l, weighted values acc per piece) over one max, plus piece 0's linear part,
-// over the shared denominator; then pos = p + 1.  The records are read with
+// over the shared denominator (hybrid forms: each part normalised on its
+// own, then added); then pos = p + 1.  The records are read with
 // system-coherent loads (they were written through to memory by workgroups
 // that may sit on other XCDs), every load of the workgroup issued before the
 // first wait.
@@ -115,7 +116,11 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
       Ls = fmaf(pl[pc * G + tid], e, Ls);
     }
     const float dn = dnv;
-    if (dn > 0.f) {
+    if (a.form != 0) {  // hybrid forms: each part over its own denominator
+      hs[tid][0] = 1.f / Ls;
+      hs[tid][1] = dn > 0.f ? 1.f / dn : 0.f;
+      hs[tid][2] = 1.f;
+    } else if (dn > 0.f) {
       const float c2 = fmaxf(M, log2f(dn));
       const float ws = exp2f(M - c2), wlin = exp2f(-c2);
       hs[tid][0] = ws;
@@ -181,6 +186,9 @@ void decode_kernel(DecodeArgs a) {
   const bool split = L.npiece > 1;
   const int b = rem / Hkv, g = rem - b * Hkv;
   const int W = L.W, R = L.R;
+  // Wd: the linear part's delay (its set is [0, p + 1 - Wd)): W, or 0 when
+  // the state holds every token (the Appendix's second hybrid form)
+  const int Wd = a.form == 2 ? 0 : W;
   const LayerSections sec = layer_sections(B, Hkv, D, DF, R, sizeof(T));
   char* lay = a.state + L.base;
   const int64_t unit = int64_t(b) * Hkv + g;
@@ -211,13 +219,13 @@ void decode_kernel(DecodeArgs a) {
   float* wl = wm + kWaves * G;             // [waves][G]    window sum e^s
 
   // Linear set after this step: tokens [0, beta).  S, z hold tokens [0, nf);
-  // tokens [nf, beta) are pending (in the ring, or the new token when W = 0)
+  // tokens [nf, beta) are pending (in the ring, or the new token when Wd = 0)
   // and enter the read-out through phi(k_j) v_j.  They are folded for good on
-  // this step when the unit's turn comes (every step when W = 0).
-  const int64_t beta = p + 1 - W > 0 ? p + 1 - W : 0;
+  // this step when the unit's turn comes (every step when Wd = 0).
+  const int64_t beta = p + 1 - Wd > 0 ? p + 1 - Wd : 0;
   const bool lin_unit = a.linear != 0 && beta > 0;
   const bool lin = lin_unit && piece == 0;  // the state pass belongs to piece 0
-  const int fper = W > 0 ? kFoldPeriod : 1;
+  const int fper = Wd > 0 ? kFoldPeriod : 1;
   // nf of a well-formed state lies in [beta - fper, beta]; the clamp keeps
   // every access in bounds whatever the blob holds.
   int64_t nf = *nf_ptr;
@@ -255,8 +263,8 @@ void decode_kernel(DecodeArgs a) {
   const brsrc_t rS = make_rsrc(S, DF * D * 4), rz = make_rsrc(z, DF * 4);
   const brsrc_t rK = make_rsrc(Kr, uint32_t(R) * D * ES), rV = make_rsrc(Vr, uint32_t(R) * D * ES);
   const brsrc_t rW = make_rsrc(Wf, D * DF * ES);
-  const brsrc_t rpk = W > 0 ? rK : rk;  // where pending keys / values live
-  const brsrc_t rpv = W > 0 ? rV : rv;
+  const brsrc_t rpk = Wd > 0 ? rK : rk;  // where pending keys / values live
+  const brsrc_t rpv = Wd > 0 ? rV : rv;
 
   // Tile loads: s0t = (j0 mod R) is a multiple of 32, so the tile is ring
   // block s0t/32 and every fragment load is one contiguous 1 KB read.  Key
@@ -287,16 +295,16 @@ void decode_kernel(DecodeArgs a) {
   {
     const int ia = hq - G, ib = 16 + hq - G;
     const bool pa = hq >= G && ia < npend, pb = ib >= 0 && ib < npend;
-    const int32_t sa = W > 0 ? int32_t((nf + (pa ? ia : 0)) % R) : 0;
-    const int32_t sb = W > 0 ? int32_t((nf + (pb ? ib : 0)) % R) : 0;
+    const int32_t sa = Wd > 0 ? int32_t((nf + (pa ? ia : 0)) % R) : 0;
+    const int32_t sb = Wd > 0 ? int32_t((nf + (pb ? ib : 0)) % R) : 0;
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       Frag<T> fq, fp;
       bload_frag(fq, rq, hq < G ? uint32_t(hq * D + 32 * kk + 8 * lg) * ES : kOOB);
-      const uint32_t oa = W > 0 ? uint32_t(kring_chunk(sa, kk, lg, D)) * ES : uint32_t(32 * kk + 8 * lg) * ES;
+      const uint32_t oa = Wd > 0 ? uint32_t(kring_chunk(sa, kk, lg, D)) * ES : uint32_t(32 * kk + 8 * lg) * ES;
       bload_frag(fp, rpk, pa ? oa : kOOB);
       xa[kk] = frag_or(fq, fp);
-      const uint32_t ob = W > 0 ? uint32_t(kring_chunk(sb, kk, lg, D)) * ES : uint32_t(32 * kk + 8 * lg) * ES;
+      const uint32_t ob = Wd > 0 ? uint32_t(kring_chunk(sb, kk, lg, D)) * ES : uint32_t(32 * kk + 8 * lg) * ES;
       bload_frag(xb[kk], rpk, pb ? ob : kOOB);
     }
   }
@@ -322,7 +330,7 @@ void decode_kernel(DecodeArgs a) {
       const int e = tid + u * kThreads, i = e / D, c = e - i * D;
       const bool ok = i < npend;
       const uint32_t off =
-          W > 0 ? uint32_t(vring_elem(int32_t((nf + (ok ? i : 0)) % R), c, D)) * ES : uint32_t(c) * ES;
+          Wd > 0 ? uint32_t(vring_elem(int32_t((nf + (ok ? i : 0)) % R), c, D)) * ES : uint32_t(c) * ES;
       pvr[u] = bload_elem(rpv, ok ? off : kOOB, T());
     }
     // this wave's S rows and z entries (zeros when S is empty)
@@ -538,9 +546,10 @@ void decode_kernel(DecodeArgs a) {
   }
   __syncthreads();
 
-  // ---- 6. shared-denominator merge over the waves and the new token (and,
-  //         for a split unit, over the pieces: each writes a record, the last
-  //         to finish merges them)
+  // ---- 6. merge over the waves and the new token (and, for a split unit,
+  //         over the pieces: each writes a record, the last to finish merges
+  //         them): one shared denominator, or (hybrid forms) the window's and
+  //         the linear part's normalised outputs added
   const brsrc_t rrec = make_rsrc(a.part + int64_t(blockIdx.x) * part_floats(G, D), uint32_t(part_floats(G, D)) * 4);
   for (int i = tid; i < G * D; i += kThreads) {
     const int hh = i / D, c = i - hh * D;
@@ -585,7 +594,9 @@ void decode_kernel(DecodeArgs a) {
       continue;
     }
     float o;
-    if (W > 0) {
+    if (a.form != 0) {  // the Appendix's hybrid forms: two normalised outputs added
+      o = (W > 0 ? Ac / Ls : 0.f) + (dn > 0.f ? nm / dn : 0.f);
+    } else if (W > 0) {
       if (dn > 0.f) {
         const float c2 = fmaxf(M, log2f(dn));
         const float ws = exp2f(M - c2), wlin = exp2f(-c2);
@@ -639,7 +650,9 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(DecodeArgs a) {
   const int64_t unit = blockIdx.x - int64_t(li) * per_layer;
   const LayerArg L = a.layers[li];
   const int W = L.W, R = L.R;
-  if (W == 0) return;  // W = 0 units fold on every step
+  // units whose linear part is not delayed (W = 0, or the state over every
+  // token) fold on every step
+  if (W == 0 || a.form == 2) return;
   const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, R, sizeof(T));
   char* lay = a.state + L.base;
   const int64_t p = reinterpret_cast<const int64_t*>(lay + sec.pos)[unit];

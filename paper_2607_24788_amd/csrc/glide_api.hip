@@ -25,7 +25,12 @@ glide_status check_cfg(const glide_config* c) {
   if (c->head_dim < 1 || c->feat_dim < 1) return GLIDE_ERR_INVALID;
   if (c->dtype != GLIDE_F32 && c->dtype != GLIDE_BF16) return GLIDE_ERR_INVALID;
   if (c->phi != GLIDE_PHI_RELU) return GLIDE_ERR_INVALID;
-  if (c->flags & ~int32_t(GLIDE_NO_LINEAR)) return GLIDE_ERR_INVALID;
+  if (c->flags & ~int32_t(GLIDE_NO_LINEAR | GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL)) return GLIDE_ERR_INVALID;
+  // the hybrid forms change the linear part: not without one; the state over
+  // every token comes only with the separately normalised sum
+  if ((c->flags & GLIDE_NO_LINEAR) && (c->flags & (GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL)))
+    return GLIDE_ERR_INVALID;
+  if ((c->flags & GLIDE_HYBRID_STATE_ALL) && !(c->flags & GLIDE_HYBRID_SUM)) return GLIDE_ERR_INVALID;
   if (!isfinite(c->sm_scale)) return GLIDE_ERR_INVALID;
   for (int32_t l = 0; l < c->n_layers; ++l) {
     const int32_t W = c->windows[l];
@@ -67,6 +72,12 @@ glide_status check_call(const glide_config* c, void* state, size_t state_bytes, 
 glide_status hip_status(hipError_t e) { return e == hipSuccess ? GLIDE_OK : GLIDE_ERR_HIP; }
 
 bool linear_on(const glide_config* c) { return (c->flags & GLIDE_NO_LINEAR) == 0; }
+
+// 0: GLIDE's shared denominator; 1, 2: the Appendix's hybrid forms
+int32_t merge_form(const glide_config* c) {
+  if (!(c->flags & GLIDE_HYBRID_SUM)) return 0;
+  return (c->flags & GLIDE_HYBRID_STATE_ALL) ? 2 : 1;
+}
 
 int32_t max_window(const glide_config* c) {
   int32_t w = 0;
@@ -146,6 +157,7 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
   a.Hkv = cfg->n_kv_heads;
   a.G = cfg->n_q_heads / cfg->n_kv_heads;
   a.linear = linear_on(cfg) ? 1 : 0;
+  a.form = merge_form(cfg);
   a.tau = cfg->sm_scale;
   for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
@@ -339,6 +351,9 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   a.Hkv = Hkv;
   a.G = Hq / Hkv;
   a.linear = lin ? 1 : 0;
+  a.form = merge_form(cfg);
+  a.band = 1;
+  a.accum = 0;
   a.tau = cfg->sm_scale;
   a.C = chunk;
   a.seg_len = seg_len;

@@ -89,7 +89,8 @@ struct LayerArg {
 // workgroups ("pieces"); piece 0 also does the ring write and the state.
 // Pieces write partial records (running max, sum and weighted values of the
 // window part per head; piece 0 adds the linear part); the piece that
-// finishes last (a per-unit counter in the state) merges them.  The split depends on the configuration only: the pieces are
+// finishes last (a per-unit counter in the state) merges them.  The split
+// depends on the configuration only: the pieces are
 // made as small as possible while every workgroup of the stack still fits in
 // one round of kDecodeSlots resident workgroups (256 CUs x 2), since a
 // second round would be latency-bound; large batches are never split.
@@ -475,7 +476,7 @@ struct DecodeArgs {
   int32_t linear;
   float tau;
   int32_t n_layers;  // layers in this launch (<= kMaxLayersPerLaunch)
-  int32_t pad;
+  int32_t form;      // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
   LayerArg layers[kMaxLayersPerLaunch];  // sorted by decreasing W
   // layer (index into layers) of every piece row: workgroup w of the main
   // pass belongs to layer piece_layer[w / (B*Hkv)].  The rows of every
@@ -531,6 +532,10 @@ struct PrefillArgs {
   int32_t seg0;         // first segment record of the group
   int32_t nseg;         // segments in this group
   int32_t nlayer;       // layers in this launch
+  int32_t form;         // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
+  int32_t band;         // main kernel: 1 runs the window band, 0 skips it (a linear-only pass)
+  int32_t accum;        // main kernel: 1 adds its outputs to what out holds
+  int32_t pad;
   PrefillLayer layers[kMaxLayersPerLaunch];  // the launch's layers, by decreasing window
   int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token
   int32_t seq_len[kMaxSeqPerLaunch];       // new tokens of the sequence

@@ -84,6 +84,7 @@ struct SeqRows {
 struct LayerView {
   char* base;  // the layer's sections in the state blob
   int32_t W, R;
+  int32_t Wd;  // the linear part's delay: W, or 0 when the state holds every token
   const void *q, *k, *v, *wf;
   void* out;
   void *hk, *hv;
@@ -95,6 +96,7 @@ __device__ __forceinline__ LayerView layer_view(const PrefillArgs& a, int ls) {
   v.base = a.state + L.layer_base;
   v.W = L.W;
   v.R = L.R;
+  v.Wd = a.form == 2 ? 0 : L.W;
   v.q = a.q + int64_t(L.li) * a.q_stride;
   v.out = a.out + int64_t(L.li) * a.q_stride;
   v.k = a.k + int64_t(L.li) * a.kv_stride;
@@ -166,6 +168,18 @@ __device__ __forceinline__ void store4(bf16_t* dst, f32x4_t x, float s) {
 }
 __device__ __forceinline__ void store4(float* dst, f32x4_t x, float s) {
   *reinterpret_cast<float4*>(dst) = make_float4(x[0] * s, x[1] * s, x[2] * s, x[3] * s);
+}
+// dst[0..3] += x * s (the second pass of a hybrid-form prefill)
+__device__ __forceinline__ void add4(bf16_t* dst, f32x4_t x, float s) {
+  const uint2 o = *reinterpret_cast<const uint2*>(dst);
+  const float y0 = __uint_as_float(o.x << 16) + x[0] * s, y1 = __uint_as_float(o.x & 0xffff0000u) + x[1] * s;
+  const float y2 = __uint_as_float(o.y << 16) + x[2] * s, y3 = __uint_as_float(o.y & 0xffff0000u) + x[3] * s;
+  *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+}
+__device__ __forceinline__ void add4(float* dst, f32x4_t x, float s) {
+  float4 o = *reinterpret_cast<const float4*>(dst);
+  o.x += x[0] * s; o.y += x[1] * s; o.z += x[2] * s; o.w += x[3] * s;
+  *reinterpret_cast<float4*>(dst) = o;
 }
 __device__ __forceinline__ f32x4_t relu4(f32x4_t x) {
   return f32x4_t{fmaxf(x[0], 0.f), fmaxf(x[1], 0.f), fmaxf(x[2], 0.f), fmaxf(x[3], 0.f)};
@@ -299,8 +313,8 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
   const SeqRows<T, D> sr = seq_rows<T, D, DF>(a, L, bl, g);
   const int sigma = sg - a.seg_base[bl];
   const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
-  int64_t jlo = sr.p0 + s_lo - L.W;
-  const int64_t jhi = sr.p0 + s_hi - L.W;
+  int64_t jlo = sr.p0 + s_lo - L.Wd;
+  const int64_t jhi = sr.p0 + s_hi - L.Wd;
   if (jlo < 0) jlo = 0;
 
   f32x4_t sacc[NT];
@@ -478,8 +492,12 @@ void prefill_main(PrefillArgs a) {
   SeqRows<T, D> sr = seq_rows<T, D, DF>(a, L, bl, g);
   const int sigma = sg - a.seg_base[bl];
   const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
-  const int G = a.G, W = L.W, C = a.C;
+  const int G = a.G, C = a.C;
+  const int W = a.band ? L.W : 0;  // the band's window (0: this pass has no band)
+  const int Wd = L.Wd;             // the linear part's delay
   const bool linear = a.linear != 0;
+  if (!linear && W == 0) return;   // a band-only pass: nothing to add for this layer
+  const bool accum = a.accum != 0;
   // The band works on raw scores q.k scaled by sc2 >= 0 inside the exponent:
   // a negative tau is carried by the queries' sign (negated in registers for
   // the band, undone in the feature map), and a zero tau is raised to 1e-30,
@@ -545,14 +563,14 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) qf[qt][kk].load(Q + sr.qrow(c0 + ti[qt], hh[qt]) * D + 32 * kk + 8 * lg);
   };
-  // delayed keys i' of the chunk (key j = t0 - W + i'), a slab of SL at a time
+  // delayed keys i' of the chunk (key j = t0 - Wd + i'), a slab of SL at a time
   Frag<T> kst[VPT], vst[VPT];
   bool sok[VPT];
   auto load_slab = [&](int s0) {
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
       const int id = tid + u * kMT, r = id / CPR, ch = id - r * CPR;
-      const int64_t j = t0 - W + s0 + r;
+      const int64_t j = t0 - Wd + s0 + r;
       sok[u] = s0 + r < nk && j >= 0;
       kst[u].load((sok[u] ? sr.k(j) : sr.k_safe()) + 8 * ch);
       vst[u].load((sok[u] ? sr.v(j) : sr.v_safe()) + 8 * ch);
@@ -941,8 +959,13 @@ void prefill_main(PrefillArgs a) {
       const float ls = lg_sum(l_run[qt]);
       const float inv = ls > 0.f ? 1.f / ls : 0.f;
       if (ov[qt]) {
+        if (accum) {
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) store4(O + orow[qt] + 16 * ct, acc[qt][ct], inv);
+          for (int ct = 0; ct < CT; ++ct) add4(O + orow[qt] + 16 * ct, acc[qt][ct], inv);
+        } else {
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) store4(O + orow[qt] + 16 * ct, acc[qt][ct], inv);
+        }
       }
     }
     if (!more) break;
@@ -1005,7 +1028,8 @@ __global__ __launch_bounds__(kThreads) void prefill_ringfill(PrefillArgs a) {
 }
 
 // advance: pos += T_b (after every other kernel of the layer read pos); the
-// scan left S, z = the sums over tokens [0, max(0, pos - W)), nothing pending.
+// scan left S, z = the sums over tokens [0, max(0, pos - Wd)), nothing
+// pending.
 template <typename T, int D, int DF>
 __global__ void prefill_advance(PrefillArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1018,7 +1042,7 @@ __global__ void prefill_advance(PrefillArgs a) {
   int64_t* nf = reinterpret_cast<int64_t*>(L.base + sec.nf) + unit;
   const int64_t p = *pos + a.seq_len[bl];
   *pos = p;
-  *nf = p - L.W > 0 ? p - L.W : 0;
+  *nf = p - L.Wd > 0 ? p - L.Wd : 0;
 }
 
 // The kernels of one prefill launch, for the a.nlayer layers of a.layers
@@ -1038,8 +1062,24 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
                          dim3(kThreads), 0, s, a);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kMT), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (a.form == 0) {
+      hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kMT), 0, s, a);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else {
+      // hybrid forms: the linear part normalised on its own, then the band's
+      // normalised output added to it
+      PrefillArgs p = a;
+      p.band = 0;
+      hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kMT), 0, s, p);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      if (window) {
+        p.band = 1;
+        p.linear = 0;
+        p.accum = 1;
+        hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kMT), 0, s, p);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+      }
+    }
   }
   if (window) {
     hipLaunchKernelGGL((prefill_ringfill<T, D, DF>), dim3(32, a.nseq, a.Hkv * nl), dim3(kThreads), 0, s, a);

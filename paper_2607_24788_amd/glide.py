@@ -17,6 +17,8 @@ F32 = 0
 BF16 = 1
 PHI_RELU = 0
 NO_LINEAR = 1
+HYBRID_SUM = 2
+HYBRID_STATE_ALL = 4
 
 STATUS = {0: "GLIDE_OK", -1: "GLIDE_ERR_NULL", -2: "GLIDE_ERR_INVALID", -3: "GLIDE_ERR_UNSUPPORTED",
           -4: "GLIDE_ERR_ALIGN", -5: "GLIDE_ERR_SIZE", -6: "GLIDE_ERR_HIP"}
@@ -136,10 +138,14 @@ def vring_raw(logical, R, d):
 
 
 class Glide:
-    """A configured GLIDE layer stack (mirrors ``glide_config``)."""
+    """A configured GLIDE layer stack (mirrors ``glide_config``).
+
+    ``form`` selects the merge: 0 GLIDE's shared denominator (default), 1 and
+    2 the two hybrid forms (``HYBRID_SUM``, ``HYBRID_SUM | HYBRID_STATE_ALL``).
+    """
 
     def __init__(self, n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, windows,
-                 dtype=torch.bfloat16, sm_scale=None, linear=True, lib=None):
+                 dtype=torch.bfloat16, sm_scale=None, linear=True, lib=None, form=0):
         self.lib = lib if lib is not None else load_library()
         self.windows = [int(w) for w in windows]
         if len(self.windows) != n_layers:
@@ -149,13 +155,15 @@ class Glide:
         code = {torch.float32: F32, torch.bfloat16: BF16}.get(dtype, 99)
         if sm_scale is None:
             sm_scale = head_dim ** -0.5
+        flags = (0 if linear else NO_LINEAR) | {0: 0, 1: HYBRID_SUM, 2: HYBRID_SUM | HYBRID_STATE_ALL}.get(form, 99)
         self.cfg = Config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, code, PHI_RELU,
-                          0 if linear else NO_LINEAR, float(sm_scale), self._win)
+                          flags, float(sm_scale), self._win)
         self.n_layers, self.batch = n_layers, batch
         self.n_q_heads, self.n_kv_heads = n_q_heads, n_kv_heads
         self.head_dim, self.feat_dim = head_dim, feat_dim
         self.sm_scale = float(sm_scale)
         self.linear = linear
+        self.form = form
 
     # -- sizes and layout ----------------------------------------------------
     def state_bytes(self):

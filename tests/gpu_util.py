@@ -41,17 +41,17 @@ class Case:
     """A decode/prefill test case on a small synthetic stack."""
 
     def __init__(self, windows, batch=1, Hq=4, Hkv=4, d=64, Df=64, dtype=torch.float32, linear=True,
-                 tau=None, seed=0, qkv_scale=None, v_scale=None):
+                 tau=None, seed=0, qkv_scale=None, v_scale=None, form=0):
         self.windows = list(windows)
         self.L = len(windows)
         self.B, self.Hq, self.Hkv, self.d, self.Df = batch, Hq, Hkv, d, Df
-        self.dtype, self.linear = dtype, linear
+        self.dtype, self.linear, self.form = dtype, linear, form
         self.tau = d ** -0.5 if tau is None else tau
         self.seed = seed
         self.qkv_scale = d ** -0.5 if qkv_scale is None else qkv_scale
         self.v_scale = self.qkv_scale if v_scale is None else v_scale
         self.g = glide.Glide(self.L, batch, Hq, Hkv, d, Df, self.windows, dtype=dtype, sm_scale=self.tau,
-                             linear=linear)
+                             linear=linear, form=form)
         gen = torch.Generator().manual_seed(seed * 7919 + 17)
         self.phi_w = (torch.randn((self.L, d, Df), generator=gen) * d ** -0.5).to(dtype)
         self._gen = gen
@@ -66,7 +66,11 @@ class Case:
 
     def oracle(self, l):
         return oracle.Oracle(self.Hq, self.Hkv, self.d, self.Df, self.windows[l], linear=self.linear,
-                             tau=self.tau)
+                             tau=self.tau, form=self.form)
+
+    def delay(self, l):
+        """The linear part's delay: the window, or 0 when the state holds every token."""
+        return 0 if self.form == 2 else self.windows[l]
 
     def new_state(self):
         st = self.g.new_state()
@@ -136,7 +140,7 @@ class Case:
                 views["S"][b] = torch.from_numpy(S).float().cuda()
                 views["z"][b] = torch.from_numpy(z).float().cuda()
                 views["pos"][b] = p
-                views["nf"][b] = max(0, p - W)      # nothing pending
+                views["nf"][b] = max(0, p - self.delay(l))      # nothing pending
                 if R:
                     kl = glide.kring_logical(views["kring_raw"][b].cpu(), R, self.d)
                     vl = glide.vring_logical(views["vring_raw"][b].cpu(), R, self.d)
@@ -178,19 +182,20 @@ class Case:
             for b, p in enumerate(positions):
                 assert int(views["pos"][b].min()) == p and int(views["pos"][b].max()) == p, \
                     f"{label} pos layer {l} seq {b}"
-                beta = max(0, p - W)
+                Wd = self.delay(l)
+                beta = max(0, p - Wd)
                 first = beta
                 if self.linear:
                     # the fold step is staggered over units: nf is per KV head
                     nfs = [int(x) for x in views["nf"][b]]
-                    lo = beta if W == 0 else max(0, beta - 8)
+                    lo = beta if Wd == 0 else max(0, beta - 8)
                     assert all(lo <= x <= beta for x in nfs), \
                         f"{label} nf {nfs} outside [{lo}, {beta}] layer {l} seq {b}"
                     first = min(nfs)
                     for nf in sorted(set(nfs)):
                         hs = [h for h, x in enumerate(nfs) if x == nf]
-                        # the oracle's state after n tokens sums tokens [0, n - W)
-                        S, z = o.state(f64(self.phi_w[l]), f64(k[l, b]), f64(v[l, b]), nf + W)
+                        # the oracle's state after n tokens sums tokens [0, n - Wd)
+                        S, z = o.state(f64(self.phi_w[l]), f64(k[l, b]), f64(v[l, b]), nf + Wd)
                         check(f"{label} S layer {l} seq {b} heads {hs} (nf {nf})", f64(views["S"][b, hs]), S[hs],
                               self.dtype, "state")
                         check(f"{label} z layer {l} seq {b} heads {hs} (nf {nf})", f64(views["z"][b, hs]), z[hs],
@@ -203,6 +208,7 @@ class Case:
                         check(f"{label} flushed z layer {l} seq {b}", f64(fv["z"][b]), z, self.dtype, "state")
                 if not R:
                     continue
+                first = min(first, max(0, p - W))   # the window, and the pending tokens
                 kr = glide.kring_logical(views["kring_raw"][b].cpu(), R, self.d)
                 vr = glide.vring_logical(views["vring_raw"][b].cpu(), R, self.d)
                 for j in range(first, p):

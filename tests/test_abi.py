@@ -120,7 +120,23 @@ BAD_CFGS = [
     (dict(n_q_heads=34, n_kv_heads=2), None, -3),                     # G = 17 > 16
     (dict(batch=0), None, -2),
     (dict(dtype=torch.float16), None, -2),                            # unknown element type
+    (dict(form=3), None, -2),                                         # unknown flag bits
+    (dict(windows=[1, 5, 3], linear=False, form=1), None, -2),        # hybrid form without a linear part
 ]
+
+
+def test_hybrid_flag_combinations():
+    """The state over every token only comes with the separately normalised
+    sum; neither hybrid flag combines with the linear part switched off."""
+    ok = mk(windows=[1, 5, 3])
+    for flags, code in ((glide.HYBRID_SUM, 0), (glide.HYBRID_SUM | glide.HYBRID_STATE_ALL, 0),
+                        (glide.HYBRID_STATE_ALL, -2), (glide.NO_LINEAR | glide.HYBRID_SUM, -2),
+                        (8, -2)):
+        ok.cfg.flags = flags
+        assert (ok.state_bytes() > 0) == (code == 0), flags
+        if code:  # rejected before any HIP call (the pointer is never used)
+            s = ok.lib.glide_state_init(ctypes.byref(ok.cfg), ctypes.c_void_p(256), 1 << 30, None)
+            assert s == code, flags
 
 
 @pytest.mark.parametrize("kw,_e,code", BAD_CFGS)
