@@ -28,13 +28,12 @@ def geo_windows(lo, hi, n_layers):
 
 
 def blockwise_windows(w, n_layers, middle_delta):
-    """The paper's three-block allocation (Sec. III-C): early layers keep the
-    whole window (delta = 0), late layers are fully linear (delta = w), the
-    middle block uses ``middle_delta``; 11/10/11 split for 32 layers.
-    Returns the softmax windows W_l = w - delta_l."""
-    e = (n_layers + 2) // 3
-    m = n_layers - 2 * e
-    return [w] * e + [w - middle_delta] * m + [0] * e
+    """The paper's three-block allocation (Sec. III-C, Algorithm 1): early
+    layers keep the whole window (delta = 0), late layers are fully linear
+    (delta = w), the middle block uses ``middle_delta``; 11/10/11 split for 32
+    layers.  Returns the softmax windows W_l = w - delta_l."""
+    from . import allocation
+    return allocation.windows(n_layers, w, middle_delta)
 
 
 @dataclass
@@ -97,6 +96,13 @@ def workload(name):
     if n in ("c4", "c4n", "prefill32k_geo"):
         return Workload("prefill_32L_b4_seq32k_geo16-2048", 32, 4, 32, 8, 128, 128, geo_windows(16, 2048, 32),
                         [32768] * 4, 0, torch.bfloat16, 3)
+    if n in ("c2b", "llama8b_b1_ctx8k_blockwise"):
+        # the paper's (0, w/2, w) allocation at its base window w = 1024
+        return Workload("llama8b_32L_b1_ctx8k_blockwise_w1024_0-w/2-w", 32, 1, 32, 8, 128, 128,
+                        blockwise_windows(1024, 32, 512), [8192], 256, torch.bfloat16, 5)
+    if n in ("c3b", "llama8b_b32_ctx32k_blockwise"):
+        return Workload("llama8b_32L_b32_ctx16k-32k_blockwise_w1024_0-w/2-w", 32, 32, 32, 8, 128, 128,
+                        blockwise_windows(1024, 32, 512), _ragged(2, 32, 16384, 32768), 128, torch.bfloat16, 6)
     if n in ("c5", "llama70b_b8_ctx64k"):
         return Workload("llama70b_80L_b8_ctx64k_geo32-8192", 80, 8, 64, 8, 128, 128, geo_windows(32, 8192, 80),
                         [65536] * 8, 64, torch.bfloat16, 4)
