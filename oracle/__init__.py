@@ -26,7 +26,7 @@ class OracleLayer(ctypes.Structure):
     _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("feat_dim", ctypes.c_int32),
                 ("window", ctypes.c_int32), ("linear", ctypes.c_int32),
-                ("form", ctypes.c_int32), ("tau", ctypes.c_double)]
+                ("form", ctypes.c_int32), ("phi", ctypes.c_int32), ("tau", ctypes.c_double)]
 
 
 _LIBS = {}
@@ -68,14 +68,15 @@ class Oracle:
     """One layer's oracle: Hq, Hkv, d, Df, window W, linear on/off, tau, and
     the merge form (0: GLIDE's shared denominator; 1, 2: the Appendix's two
     hybrid forms, separately normalised outputs added, with the state over
-    the evicted tokens (1) or over every token (2))."""
+    the evicted tokens (1) or over every token (2)), and the feature map
+    (phi 0: ReLU(x Wf); 1: ELU(x Wf) + 1)."""
 
     def __init__(self, n_q_heads, n_kv_heads, head_dim, feat_dim, window, linear=True,
-                 tau=None, lib=None, form=0):
+                 tau=None, lib=None, form=0, phi=0):
         if tau is None:
             tau = 1.0 / np.sqrt(head_dim)
         self.L = OracleLayer(n_q_heads, n_kv_heads, head_dim, feat_dim, window,
-                             1 if linear else 0, int(form), float(tau))
+                             1 if linear else 0, int(form), int(phi), float(tau))
         self.lib = lib if lib is not None else load()
 
     # -- feature map -------------------------------------------------------

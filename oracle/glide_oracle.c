@@ -17,7 +17,10 @@
  *     beta(t)   = max(0, t + 1 - W)
  *     linear set   L = [0, beta)        (empty when the linear part is off)
  *     softmax set  X = [beta, t]        (min(W, t+1) tokens, current included)
- *     phi(x)_f  = max(0, sum_c x_c Wf[c][f])        (ReLU feature map)
+ *     phi(x)_f  = max(0, sum_c x_c Wf[c][f])        (ReLU feature map; or, with
+ *                 oracle_layer.phi = 1, ELU+1: y + 1 for y > 0, e^y otherwise,
+ *                 y = sum_c x_c Wf[c][f]; both from the Appendix's list of
+ *                 feature maps)
  *     a_j       = phi(q_t) . phi(k_j)               for j in L
  *     A = sum_{j in L} a_j v_j ,  a = sum_{j in L} a_j
  *     s_j = tau * q_t . k_j                          for j in X
@@ -69,6 +72,7 @@ typedef struct {
   int32_t window;      /* W >= 0 */
   int32_t linear;      /* 1: linear part on (GLIDE), 0: pure sliding window */
   int32_t form;        /* 0: shared denominator; 1, 2: the Appendix hybrid forms */
+  int32_t phi;         /* 0: ReLU(x Wf); 1: ELU(x Wf) + 1 */
   double  tau;         /* softmax scale */
 } oracle_layer;
 
@@ -85,11 +89,13 @@ static int valid(const oracle_layer* L) {
   if (L->window == 0 && !L->linear) return 0;   /* empty attention set */
   if (L->form < 0 || L->form > 2) return 0;
   if (L->form != 0 && !L->linear) return 0;     /* the forms differ only in the linear part */
+  if (L->phi < 0 || L->phi > 1) return 0;
   return 1;
 }
 
-/* phi(x)_f = max(0, sum_c x_c Wf[c][f]);  Wf is d x Df, row-major. */
-static void phi_row(int d, int Df, const double* Wf, const double* x, double* out) {
+/* phi(x)_f = max(0, y_f) (kind 0) or ELU(y_f) + 1 (kind 1), y_f = sum_c x_c Wf[c][f];
+ * Wf is d x Df, row-major. */
+static void phi_row(int kind, int d, int Df, const double* Wf, const double* x, double* out) {
   for (int f = 0; f < Df; ++f) {
     double acc = 0.0;
     for (int c = 0; c < d; ++c) {
@@ -99,14 +105,18 @@ static void phi_row(int d, int Df, const double* Wf, const double* x, double* ou
       acc += x[c] * Wf[(size_t)c * Df + f];
 #endif
     }
-    out[f] = acc > 0.0 ? acc : 0.0;
+#if ORACLE_MUTANT == 11
+    if (kind == 1) { out[f] = acc > 0.0 ? acc : exp(acc) - 1.0; continue; }   /* mutant: ELU without the +1 */
+#endif
+    if (kind == 1) out[f] = acc > 0.0 ? acc + 1.0 : exp(acc);
+    else out[f] = acc > 0.0 ? acc : 0.0;
   }
 }
 
 void oracle_phi(const oracle_layer* L, const double* Wf, int64_t rows, const double* x, double* out) {
   const int d = L->head_dim, Df = L->feat_dim;
 #pragma omp parallel for schedule(static)
-  for (int64_t r = 0; r < rows; ++r) phi_row(d, Df, Wf, x + r * d, out + r * Df);
+  for (int64_t r = 0; r < rows; ++r) phi_row(L->phi, d, Df, Wf, x + r * d, out + r * Df);
 }
 
 static double dot(int n, const double* a, const double* b) {
@@ -183,7 +193,7 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
     phik = (double*)malloc(sizeof(double) * (size_t)(tmax + 1) * Hkv * Df);
     if (!phik) return -1;
 #pragma omp parallel for schedule(static)
-    for (int64_t r = 0; r < (tmax + 1) * Hkv; ++r) phi_row(d, Df, Wf, k + r * d, phik + r * Df);
+    for (int64_t r = 0; r < (tmax + 1) * Hkv; ++r) phi_row(L->phi, d, Df, Wf, k + r * d, phik + r * Df);
   }
   int err = 0;
 #pragma omp parallel
@@ -217,7 +227,7 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
           for (int c = 0; c < d; ++c) A[c] = 0.0;
 #if ORACLE_MUTANT != 2
           if (L->linear && lend > 0) {
-            phi_row(d, Df, Wf, qt, phq);
+            phi_row(L->phi, d, Df, Wf, qt, phq);
             for (int64_t j = 0; j < lend; ++j) {
               const double aj = dot(Df, phq, phik + ((size_t)j * Hkv + g) * Df);
               const double* vj = v + ((size_t)j * Hkv + g) * d;
@@ -281,7 +291,7 @@ int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
     double* pk = (double*)malloc(sizeof(double) * Df);
     if (!pk) { err = 1; continue; }
     for (int64_t j = 0; j < nfold; ++j) {
-      phi_row(d, Df, Wf, k + ((size_t)j * Hkv + g) * d, pk);
+      phi_row(L->phi, d, Df, Wf, k + ((size_t)j * Hkv + g) * d, pk);
       const double* vj = v + ((size_t)j * Hkv + g) * d;
       for (int f = 0; f < Df; ++f) {
         double* Sr = S + ((size_t)g * Df + f) * d;
@@ -351,7 +361,7 @@ int oracle_decode_batch(const oracle_layer* L, const double* Wf, int32_t B,
       }
 #endif
       if (fk) {
-        phi_row(d, Df, Wf, fk, pk);
+        phi_row(L->phi, d, Df, Wf, fk, pk);
         for (int f = 0; f < Df; ++f) {
           for (int c = 0; c < d; ++c) Sg[(size_t)f * d + c] += pk[f] * fv[c];
           zg[f] += pk[f];
@@ -375,7 +385,7 @@ int oracle_decode_batch(const oracle_layer* L, const double* Wf, int32_t B,
         double a = 0.0;
         for (int c = 0; c < d; ++c) A[c] = 0.0;
         if (L->linear) {
-          phi_row(d, Df, Wf, qt, pq);
+          phi_row(L->phi, d, Df, Wf, qt, pq);
           for (int f = 0; f < Df; ++f) {
             for (int c = 0; c < d; ++c) A[c] += pq[f] * Sg[(size_t)f * d + c];
             a += pq[f] * zg[f];

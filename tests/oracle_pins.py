@@ -63,12 +63,16 @@ def _sdpa(q, k, v, tau, mask):
     return o.permute(1, 0, 2).numpy()
 
 
-def _causal_linear(q, k, v, Wf):
+def _feat(y, phi):
+    return np.maximum(y, 0.0) if phi == 0 else np.where(y > 0, y + 1.0, np.exp(np.minimum(y, 0.0)))
+
+
+def _causal_linear(q, k, v, Wf, phi=0):
     """Causal linear attention, masked-matrix form, with numpy matmuls."""
     G = q.shape[1] // k.shape[1]
     n = q.shape[0]
-    pq = np.maximum(q @ Wf, 0.0)                       # [n][Hq][Df]
-    pk = np.maximum(np.repeat(k, G, axis=1) @ Wf, 0.0)
+    pq = _feat(q @ Wf, phi)                            # [n][Hq][Df]
+    pk = _feat(np.repeat(k, G, axis=1) @ Wf, phi)
     vv = np.repeat(v, G, axis=1)
     num = np.zeros(q.shape)
     den = np.zeros(q.shape[:2])
@@ -89,7 +93,7 @@ def pin_worked_example(lib):
     Wf = np.array(s["Wf"])
     for case in ex["cases"]:
         o = oracle.Oracle(1, 1, 1, 1, case["window"], linear=case["linear"], tau=s["tau"], lib=lib,
-                          form=case.get("form", 0))
+                          form=case.get("form", 0), phi=case.get("phi", 0))
         got = o.attend(Wf, q, k, v).ravel()
         want = np.array([_eval_closed_form(x) for x in case["out"]])
         if not np.allclose(got, want, rtol=1e-12, atol=1e-12):
@@ -147,6 +151,11 @@ def pin_w0_is_causal_linear(lib):
     got = oracle.Oracle(Hq, Hkv, d, Df, 0, linear=True, lib=lib).attend(Wf, q, k, v)
     if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
         return f"W=0 != causal linear attention (max err {np.abs(got - want).max()})"
+    # the ELU+1 feature map (never zero: every denominator is positive)
+    num, den = _causal_linear(q, k, v, Wf, phi=1)
+    got = oracle.Oracle(Hq, Hkv, d, Df, 0, linear=True, lib=lib, phi=1).attend(Wf, q, k, v)
+    if not np.allclose(got, num / den[..., None], rtol=1e-10, atol=1e-12):
+        return f"W=0 ELU+1 != causal linear attention (max err {np.abs(got - num / den[..., None]).max()})"
     return None
 
 
@@ -176,15 +185,15 @@ def pin_recurrent_equals_definition(lib):
     n, Hq, Hkv, d, Df = 21, 4, 2, 6, 5
     q, k, v, Wf = _rand_case(5, n, Hq, Hkv, d, Df, scale=1.5)
     for W in (0, 1, 2, 3, 7, n - 1, n, n + 4):
-        for lin, form in ((True, 0), (False, 0), (True, 1), (True, 2)):
+        for lin, form, phi in ((True, 0, 0), (False, 0, 0), (True, 1, 0), (True, 2, 0), (True, 0, 1), (True, 2, 1)):
             if W == 0 and not lin:
                 continue
-            o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=lin, tau=0.6, lib=lib, form=form)
+            o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=lin, tau=0.6, lib=lib, form=form, phi=phi)
             want = o.attend(Wf, q, k, v)
             st = o.empty_state(1)
             got = np.stack([o.decode(Wf, st, q[t:t + 1], k[t:t + 1], v[t:t + 1])[0] for t in range(n)])
             if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
-                return f"recurrent != definition at W={W} linear={lin} form={form} (max err {np.abs(got - want).max()})"
+                return f"recurrent != definition at W={W} linear={lin} form={form} phi={phi} (max err {np.abs(got - want).max()})"
             S, z = o.state(Wf, k, v)
             if not (np.allclose(st["S"][0], S, rtol=1e-12, atol=1e-12) and np.allclose(st["z"][0], z)):
                 return f"recurrent state != direct sums at W={W} linear={lin} form={form}"
@@ -211,6 +220,10 @@ def pin_v_ones(lib):
     n, Hq, Hkv, d, Df = 16, 4, 2, 6, 6
     q, k, _, Wf = _rand_case(7, n, Hq, Hkv, d, Df, scale=2.0)
     v = np.ones((n, Hkv, d))
+    for W in (0, 3, n):   # ELU+1: phi > 0, so no empty weight mass anywhere
+        got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib, phi=1).attend(Wf, q, k, v)
+        if not np.allclose(got, 1.0, rtol=1e-12, atol=1e-12):
+            return f"V==1 does not give O==1 with ELU+1 at W={W}"
     for W in (0, 1, 3, 9, n):
         got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib).attend(Wf, q, k, v)
         if W == 0:   # 0/0 -> 0 where phi(q_t) . sum_{j<=t} phi(k_j) == 0
