@@ -56,10 +56,12 @@ typedef enum {
 /* Element type of q, k, v, out, the window ring and phi_w.  S and z are fp32. */
 enum { GLIDE_F32 = 0, GLIDE_BF16 = 1 };
 
-/* Feature map: phi(x) = max(0, x . Wf) (the ReLU kernel of the Appendix's
- * feature-map list; Wf is non-learnable, one d x Df matrix per layer shared by
- * every head, applied to queries and keys alike). */
-enum { GLIDE_PHI_RELU = 0 };
+/* Feature map on y = x . Wf (Wf is non-learnable, one d x Df matrix per
+ * layer shared by every head, applied to queries and keys alike), from the
+ * Appendix's feature-map list:
+ *   GLIDE_PHI_RELU  phi = max(0, y)
+ *   GLIDE_PHI_ELU1  phi = ELU(y) + 1 = y + 1 for y > 0, e^y otherwise (never 0) */
+enum { GLIDE_PHI_RELU = 0, GLIDE_PHI_ELU1 = 1 };
 
 /* flags: GLIDE_NO_LINEAR turns the linear part off (plain sliding-window
  * softmax attention, the "Hybrid" preset with nothing kept beyond the
@@ -87,7 +89,7 @@ typedef struct {
   int32_t head_dim;    /* d: 64 or 128 */
   int32_t feat_dim;    /* Df: 64 or 128 */
   int32_t dtype;       /* GLIDE_F32 or GLIDE_BF16 */
-  int32_t phi;         /* GLIDE_PHI_RELU */
+  int32_t phi;         /* GLIDE_PHI_RELU or GLIDE_PHI_ELU1 */
   int32_t flags;       /* 0, GLIDE_NO_LINEAR, GLIDE_HYBRID_SUM, or GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL */
   float sm_scale;      /* tau, the softmax scale (1/sqrt(d) in the Appendix's attention) */
   const int32_t* windows; /* HOST array [n_layers]: W_l = w - delta_l, 0 <= W_l <= 2^20 */
@@ -197,8 +199,8 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
 glide_status glide_state_flush(const glide_config* cfg, void* state, size_t state_bytes,
                                int32_t layer0, int32_t n_layers, const void* phi_w, void* stream);
 
-/* The feature map alone (kernel (d)): out[r][f] = max(0, sum_c x[r][c] Wf[c][f])
- * for r < rows, accumulated in fp32.  x device [rows][d], phi_w device [d][Df]
+/* The feature map alone (kernel (d)): out[r][f] = phi(sum_c x[r][c] Wf[c][f])
+ * (cfg->phi) for r < rows, accumulated in fp32.  x device [rows][d], phi_w device [d][Df]
  * (both cfg->dtype), out device [rows][Df] in cfg->dtype; x and out may be NULL
  * when rows == 0. */
 glide_status glide_feature_map(const glide_config* cfg, const void* phi_w, const void* x,

@@ -362,8 +362,8 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 4 * lg + i;
-        if (row < nrows) ph[row * DF + f0 + 16 * nt + hq] = fmaxf(acc[nt][i], 0.f);
-        if (16 + row < nrows) ph[(16 + row) * DF + f0 + 16 * nt + hq] = fmaxf(acb[nt][i], 0.f);
+        if (row < nrows) ph[row * DF + f0 + 16 * nt + hq] = feat_act(acc[nt][i], a.phi);
+        if (16 + row < nrows) ph[(16 + row) * DF + f0 + 16 * nt + hq] = feat_act(acb[nt][i], a.phi);
       }
     }
   }
@@ -680,7 +680,7 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(DecodeArgs a) {
     const int i = e / DF, f = e - i * DF;
     float acc = 0.f;
     for (int c = 0; c < D; ++c) acc = fmaf(kx[i][c], to_f32(Wf[c * DF + f]), acc);
-    pk[i][f] = fmaxf(acc, 0.f);
+    pk[i][f] = feat_act(acc, a.phi);
   }
   __syncthreads();
   const bool s_nonzero = nf > 0;

@@ -24,7 +24,7 @@ glide_status check_cfg(const glide_config* c) {
   if (c->n_q_heads % c->n_kv_heads) return GLIDE_ERR_INVALID;
   if (c->head_dim < 1 || c->feat_dim < 1) return GLIDE_ERR_INVALID;
   if (c->dtype != GLIDE_F32 && c->dtype != GLIDE_BF16) return GLIDE_ERR_INVALID;
-  if (c->phi != GLIDE_PHI_RELU) return GLIDE_ERR_INVALID;
+  if (c->phi != GLIDE_PHI_RELU && c->phi != GLIDE_PHI_ELU1) return GLIDE_ERR_INVALID;
   if (c->flags & ~int32_t(GLIDE_NO_LINEAR | GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL)) return GLIDE_ERR_INVALID;
   // the hybrid forms change the linear part: not without one; the state over
   // every token comes only with the separately normalised sum
@@ -158,6 +158,7 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
   a.G = cfg->n_q_heads / cfg->n_kv_heads;
   a.linear = linear_on(cfg) ? 1 : 0;
   a.form = merge_form(cfg);
+  a.phi = cfg->phi;
   a.tau = cfg->sm_scale;
   for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
@@ -352,6 +353,7 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   a.G = Hq / Hkv;
   a.linear = lin ? 1 : 0;
   a.form = merge_form(cfg);
+  a.phi = cfg->phi;
   a.band = 1;
   a.accum = 0;
   a.tau = cfg->sm_scale;
@@ -425,7 +427,7 @@ glide_status glide_feature_map(const glide_config* cfg, const void* phi_w, const
   if (!phi_w || (rows > 0 && (!x || !out))) return GLIDE_ERR_NULL;
   if (!aligned(phi_w, 16) || !aligned(x, 16) || !aligned(out, 16)) return GLIDE_ERR_ALIGN;
   return hip_status(launch_phi_rows(phi_w, x, rows, out, cfg->head_dim, cfg->feat_dim, cfg->dtype,
-                                    cfg->dtype == GLIDE_F32, hipStream_t(stream)));
+                                    cfg->dtype == GLIDE_F32, cfg->phi, hipStream_t(stream)));
 }
 
 }  // extern "C"

@@ -244,6 +244,12 @@ __device__ __forceinline__ f32x4_t mma(const Frag<float>& a, const Frag<float>& 
 
 __device__ __forceinline__ f32x4_t zero4() { return f32x4_t{0.f, 0.f, 0.f, 0.f}; }
 
+// The feature map's activation on y = x . Wf: ReLU (phi = 0), or ELU + 1
+// (phi = 1: y + 1 for y > 0, e^y otherwise; never zero).
+__device__ __forceinline__ float feat_act(float y, int phi) {
+  return phi ? (y > 0.f ? y + 1.f : __builtin_amdgcn_exp2f(y * 1.4426950408889634f)) : fmaxf(y, 0.f);
+}
+
 // Fragment of 8 consecutive ROWS of one column from a row-major LDS tile M
 // (row stride rs elements): lane (n = lane%16, g = lane/16) receives
 // M[row0 + e][col0 + n], e = 0..7, where row0 must be equal across each group
@@ -477,6 +483,8 @@ struct DecodeArgs {
   float tau;
   int32_t n_layers;  // layers in this launch (<= kMaxLayersPerLaunch)
   int32_t form;      // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
+  int32_t phi;       // feature map: 0 ReLU, 1 ELU + 1
+  int32_t pad;
   LayerArg layers[kMaxLayersPerLaunch];  // sorted by decreasing W
   // layer (index into layers) of every piece row: workgroup w of the main
   // pass belongs to layer piece_layer[w / (B*Hkv)].  The rows of every
@@ -491,7 +499,7 @@ hipError_t launch_decode(const DecodeArgs& a, int total_wg, int d, int Df, int d
                          hipStream_t stream);
 hipError_t launch_flush(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
 hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* out, int d, int Df, int dtype,
-                           bool out_f32, hipStream_t stream);
+                           bool out_f32, int phi, hipStream_t stream);
 
 // ---------------------------------------------------------------------------
 // Prefill.  Sequences are processed in groups of at most kMaxSeqPerLaunch so
@@ -535,7 +543,7 @@ struct PrefillArgs {
   int32_t form;         // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
   int32_t band;         // main kernel: 1 runs the window band, 0 skips it (a linear-only pass)
   int32_t accum;        // main kernel: 1 adds its outputs to what out holds
-  int32_t pad;
+  int32_t phi;          // feature map: 0 ReLU, 1 ELU + 1
   PrefillLayer layers[kMaxLayersPerLaunch];  // the launch's layers, by decreasing window
   int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token
   int32_t seq_len[kMaxSeqPerLaunch];       // new tokens of the sequence

@@ -19,7 +19,7 @@ constexpr int kThreads = 256;
 // hit the L1.
 template <typename T, int D, int DF, typename OutT>
 __global__ __launch_bounds__(kThreads) void phi_rows_kernel(const T* __restrict__ Wf, const T* __restrict__ x,
-                                                            int64_t rows, OutT* __restrict__ out) {
+                                                            int64_t rows, OutT* __restrict__ out, int phi) {
   constexpr int KS = D / 32, NTW = DF / 16 / 4;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
   const int f0 = wave * NTW * 16;
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kThreads) void phi_rows_kernel(const T* __restrict_
         const int64_t ro = r0 + 4 * lg + i;
         if (ro < rows) {
 #pragma unroll
-          for (int nt = 0; nt < NTW; ++nt) out[ro * DF + f0 + 16 * nt + hq] = from_f32<OutT>(fmaxf(acc[nt][i], 0.f));
+          for (int nt = 0; nt < NTW; ++nt) out[ro * DF + f0 + 16 * nt + hq] = from_f32<OutT>(feat_act(acc[nt][i], phi));
         }
       }
     }
@@ -60,36 +60,36 @@ __global__ __launch_bounds__(kThreads) void phi_rows_kernel(const T* __restrict_
 }
 
 template <typename T, int D, int DF, typename OutT>
-hipError_t launch_rows_t(const void* Wf, const void* x, int64_t rows, void* out, hipStream_t s) {
+hipError_t launch_rows_t(const void* Wf, const void* x, int64_t rows, void* out, int phi, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const int64_t ntile = (rows + 63) / 64;
   const dim3 grid(unsigned(ntile < 1024 ? ntile : 1024));
   hipLaunchKernelGGL((phi_rows_kernel<T, D, DF, OutT>), grid, dim3(kThreads), 0, s, static_cast<const T*>(Wf),
-                     static_cast<const T*>(x), rows, static_cast<OutT*>(out));
+                     static_cast<const T*>(x), rows, static_cast<OutT*>(out), phi);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* out, int d, int Df, int dtype,
-                           bool out_f32, hipStream_t s) {
+                           bool out_f32, int phi, hipStream_t s) {
   if (dtype == GLIDE_BF16) {
     if (out_f32) {
-      if (d == 128 && Df == 128) return launch_rows_t<bf16_t, 128, 128, float>(Wf, x, rows, out, s);
-      if (d == 128 && Df == 64) return launch_rows_t<bf16_t, 128, 64, float>(Wf, x, rows, out, s);
-      if (d == 64 && Df == 128) return launch_rows_t<bf16_t, 64, 128, float>(Wf, x, rows, out, s);
-      if (d == 64 && Df == 64) return launch_rows_t<bf16_t, 64, 64, float>(Wf, x, rows, out, s);
+      if (d == 128 && Df == 128) return launch_rows_t<bf16_t, 128, 128, float>(Wf, x, rows, out, phi, s);
+      if (d == 128 && Df == 64) return launch_rows_t<bf16_t, 128, 64, float>(Wf, x, rows, out, phi, s);
+      if (d == 64 && Df == 128) return launch_rows_t<bf16_t, 64, 128, float>(Wf, x, rows, out, phi, s);
+      if (d == 64 && Df == 64) return launch_rows_t<bf16_t, 64, 64, float>(Wf, x, rows, out, phi, s);
     } else {
-      if (d == 128 && Df == 128) return launch_rows_t<bf16_t, 128, 128, bf16_t>(Wf, x, rows, out, s);
-      if (d == 128 && Df == 64) return launch_rows_t<bf16_t, 128, 64, bf16_t>(Wf, x, rows, out, s);
-      if (d == 64 && Df == 128) return launch_rows_t<bf16_t, 64, 128, bf16_t>(Wf, x, rows, out, s);
-      if (d == 64 && Df == 64) return launch_rows_t<bf16_t, 64, 64, bf16_t>(Wf, x, rows, out, s);
+      if (d == 128 && Df == 128) return launch_rows_t<bf16_t, 128, 128, bf16_t>(Wf, x, rows, out, phi, s);
+      if (d == 128 && Df == 64) return launch_rows_t<bf16_t, 128, 64, bf16_t>(Wf, x, rows, out, phi, s);
+      if (d == 64 && Df == 128) return launch_rows_t<bf16_t, 64, 128, bf16_t>(Wf, x, rows, out, phi, s);
+      if (d == 64 && Df == 64) return launch_rows_t<bf16_t, 64, 64, bf16_t>(Wf, x, rows, out, phi, s);
     }
   } else {
-    if (d == 128 && Df == 128) return launch_rows_t<float, 128, 128, float>(Wf, x, rows, out, s);
-    if (d == 128 && Df == 64) return launch_rows_t<float, 128, 64, float>(Wf, x, rows, out, s);
-    if (d == 64 && Df == 128) return launch_rows_t<float, 64, 128, float>(Wf, x, rows, out, s);
-    if (d == 64 && Df == 64) return launch_rows_t<float, 64, 64, float>(Wf, x, rows, out, s);
+    if (d == 128 && Df == 128) return launch_rows_t<float, 128, 128, float>(Wf, x, rows, out, phi, s);
+    if (d == 128 && Df == 64) return launch_rows_t<float, 128, 64, float>(Wf, x, rows, out, phi, s);
+    if (d == 64 && Df == 128) return launch_rows_t<float, 64, 128, float>(Wf, x, rows, out, phi, s);
+    if (d == 64 && Df == 64) return launch_rows_t<float, 64, 64, float>(Wf, x, rows, out, phi, s);
   }
   return hipErrorInvalidValue;
 }

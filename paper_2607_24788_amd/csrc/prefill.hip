@@ -181,8 +181,8 @@ __device__ __forceinline__ void add4(float* dst, f32x4_t x, float s) {
   o.x += x[0] * s; o.y += x[1] * s; o.z += x[2] * s; o.w += x[3] * s;
   *reinterpret_cast<float4*>(dst) = o;
 }
-__device__ __forceinline__ f32x4_t relu4(f32x4_t x) {
-  return f32x4_t{fmaxf(x[0], 0.f), fmaxf(x[1], 0.f), fmaxf(x[2], 0.f), fmaxf(x[3], 0.f)};
+__device__ __forceinline__ f32x4_t act4(f32x4_t x, int phi) {
+  return f32x4_t{feat_act(x[0], phi), feat_act(x[1], phi), feat_act(x[2], phi), feat_act(x[3], phi)};
 }
 
 // Wf [D][DF] into LDS, natural layout (NTH threads cooperating; every load
@@ -232,9 +232,9 @@ __device__ __forceinline__ void slab_keys(SlabKeys<T, D, DF>& sk, int nw, RowFn 
 #pragma unroll
   for (int kk = 0; kk < D / 32; ++kk) sk.x[kk].load(src + 32 * kk + 8 * lg);
 }
-template <typename T, int D, int DF, int NK, bool kLds>
+template <typename T, int D, int DF, int NK, int PHI, bool kLds>
 __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const Frag<T> (&x)[D / 32], T* pk,
-                                         int nw) {
+                                         int nw, int rlo, int rhi) {
   constexpr int KS = D / 32, FT = DF / 16, PROW = row_t<DF>();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
   const int per = (NK / 16) * FT / nw;
@@ -249,7 +249,14 @@ __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const
       wf.col(wb, kk, 16 * ft);
       acc = mma(wb, x[kk], acc);
     }
-    store4(pk + (16 * kt + hq) * PROW + 16 * ft + 4 * lg, relu4(acc), 1.f);
+    // rows outside [rlo, rhi) are no keys (zero rows): their features must
+    // be 0, which ReLU gives by itself and ELU + 1 (phi(0) = 1) does not
+    const int key = 16 * kt + hq;
+    if constexpr (PHI == 0) {
+      store4(pk + key * PROW + 16 * ft + 4 * lg, act4(acc, 0), 1.f);
+    } else {
+      store4(pk + key * PROW + 16 * ft + 4 * lg, key >= rlo && key < rhi ? act4(acc, PHI) : zero4(), 1.f);
+    }
   }
 }
 
@@ -293,7 +300,7 @@ struct SegLds {
   static constexpr size_t bytes = (size_t(D) * WROW + size_t(kSegSlab) * (PROW + VROW)) * sizeof(T);
 };
 
-template <typename T, int D, int DF>
+template <typename T, int D, int DF, int PHI>
 __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
   using LD = SegLds<T, D, DF>;
   constexpr int CT = D / 16, FT = DF / 16, CPR = D / 8;
@@ -344,8 +351,9 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
       Frag<T> x[D / 32];
 #pragma unroll
       for (int kk = 0; kk < D / 32; ++kk) x[kk] = frag_keep(kx.x[kk], kx.ok);
-      phi_slab<T, D, DF, kSegSlab>(WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))}, x, lds_fresh(pk),
-                                   kSegWaves);
+      const int64_t nrow = jhi - j0;
+      phi_slab<T, D, DF, kSegSlab, PHI>(WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))}, x,
+                                        lds_fresh(pk), kSegWaves, 0, nrow < kSegSlab ? int(nrow) : kSegSlab);
     }
     {
       T* vw = lds_fresh(vs);
@@ -462,7 +470,8 @@ struct MainLds {
   static_assert(bytes <= 160 * 1024, "LDS budget");
 };
 
-template <typename T, int D, int DF>
+// PHI: the feature map (0 ReLU, 1 ELU + 1), one instantiation each
+template <typename T, int D, int DF, int PHI>
 __global__ __launch_bounds__(kMT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void prefill_main(PrefillArgs a) {
   using LD = MainLds<T, D, DF>;
@@ -799,7 +808,12 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
           for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) pv[qt][4 * half + i] = fmaxf(ph[qt][i] * qscale[qt], 0.f);
+            for (int i = 0; i < 4; ++i) {
+              if constexpr (PHI == 0)
+                pv[qt][4 * half + i] = fmaxf(ph[qt][i] * qscale[qt], 0.f);
+              else  // (qscale's sign undoes the band's query negation)
+                pv[qt][4 * half + i] = feat_act(qscale[qt] < 0.f ? -ph[qt][i] : ph[qt][i], PHI) * fabsf(qscale[qt]);
+            }
         }
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) pqf[qt][kf].set8(pv[qt]);
@@ -853,7 +867,10 @@ void prefill_main(PrefillArgs a) {
           Frag<T> x[KS];
 #pragma unroll
           for (int kk = 0; kk < KS; ++kk) x[kk].load(krr + (16 * kt + hq) * KROW + 32 * kk + 8 * lg);
-          phi_slab<T, D, DF, SL>(wf_cols(), x, lds_fresh(pk), kMW);
+          // the slab's keys: i' = s0 + r < nk, and key t0 - Wd + i' >= 0
+          const int64_t rlo = int64_t(Wd) - t0 - s0;
+          phi_slab<T, D, DF, SL, PHI>(wf_cols(), x, lds_fresh(pk), kMW, rlo > 0 ? int(rlo < SL ? rlo : SL) : 0,
+                                      nk - s0);
         }
         __syncthreads();
         const T* pkr = lds_fresh(static_cast<const T*>(pk));
@@ -1053,9 +1070,18 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
   const unsigned nl = unsigned(a.nlayer);
   bool window = false;
   for (int i = 0; i < a.nlayer; ++i) window = window || a.layers[i].W > 0;
+  auto main = [&](const PrefillArgs& m) {
+    if (m.phi)
+      hipLaunchKernelGGL((prefill_main<T, D, DF, 1>), dim3(m.nseg, m.Hkv, nl), dim3(kMT), 0, s, m);
+    else
+      hipLaunchKernelGGL((prefill_main<T, D, DF, 0>), dim3(m.nseg, m.Hkv, nl), dim3(kMT), 0, s, m);
+  };
   if (a.nseg > 0) {
     if (a.linear) {
-      hipLaunchKernelGGL((prefill_segsum<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kSegThreads), 0, s, a);
+      if (a.phi)
+        hipLaunchKernelGGL((prefill_segsum<T, D, DF, 1>), dim3(a.nseg, a.Hkv, nl), dim3(kSegThreads), 0, s, a);
+      else
+        hipLaunchKernelGGL((prefill_segsum<T, D, DF, 0>), dim3(a.nseg, a.Hkv, nl), dim3(kSegThreads), 0, s, a);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       const int E = DF * D + DF;
       hipLaunchKernelGGL((prefill_scan<T, D, DF>), dim3((E / 4 + kThreads - 1) / kThreads, a.nseq, a.Hkv * nl),
@@ -1063,20 +1089,20 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (a.form == 0) {
-      hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kMT), 0, s, a);
+      main(a);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
       // hybrid forms: the linear part normalised on its own, then the band's
       // normalised output added to it
       PrefillArgs p = a;
       p.band = 0;
-      hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kMT), 0, s, p);
+      main(p);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       if (window) {
         p.band = 1;
         p.linear = 0;
         p.accum = 1;
-        hipLaunchKernelGGL((prefill_main<T, D, DF>), dim3(a.nseg, a.Hkv, nl), dim3(kMT), 0, s, p);
+        main(p);
         if ((e = hipGetLastError()) != hipSuccess) return e;
       }
     }

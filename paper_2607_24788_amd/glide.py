@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libglide.so")
 F32 = 0
 BF16 = 1
 PHI_RELU = 0
+PHI_ELU1 = 1
 NO_LINEAR = 1
 HYBRID_SUM = 2
 HYBRID_STATE_ALL = 4
@@ -145,7 +146,7 @@ class Glide:
     """
 
     def __init__(self, n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, windows,
-                 dtype=torch.bfloat16, sm_scale=None, linear=True, lib=None, form=0):
+                 dtype=torch.bfloat16, sm_scale=None, linear=True, lib=None, form=0, phi=PHI_RELU):
         self.lib = lib if lib is not None else load_library()
         self.windows = [int(w) for w in windows]
         if len(self.windows) != n_layers:
@@ -156,7 +157,7 @@ class Glide:
         if sm_scale is None:
             sm_scale = head_dim ** -0.5
         flags = (0 if linear else NO_LINEAR) | {0: 0, 1: HYBRID_SUM, 2: HYBRID_SUM | HYBRID_STATE_ALL}.get(form, 99)
-        self.cfg = Config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, code, PHI_RELU,
+        self.cfg = Config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, code, int(phi),
                           flags, float(sm_scale), self._win)
         self.n_layers, self.batch = n_layers, batch
         self.n_q_heads, self.n_kv_heads = n_q_heads, n_kv_heads
@@ -164,6 +165,7 @@ class Glide:
         self.sm_scale = float(sm_scale)
         self.linear = linear
         self.form = form
+        self.phi = phi
 
     # -- sizes and layout ----------------------------------------------------
     def state_bytes(self):
