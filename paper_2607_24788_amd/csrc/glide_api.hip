@@ -354,8 +354,6 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   a.linear = lin ? 1 : 0;
   a.form = merge_form(cfg);
   a.phi = cfg->phi;
-  a.band = 1;
-  a.accum = 0;
   a.tau = cfg->sm_scale;
   a.C = chunk;
   a.seg_len = seg_len;

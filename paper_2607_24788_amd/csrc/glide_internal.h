@@ -541,8 +541,7 @@ struct PrefillArgs {
   int32_t nseg;         // segments in this group
   int32_t nlayer;       // layers in this launch
   int32_t form;         // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
-  int32_t band;         // main kernel: 1 runs the window band, 0 skips it (a linear-only pass)
-  int32_t accum;        // main kernel: 1 adds its outputs to what out holds
+  int32_t pad0, pad1;
   int32_t phi;          // feature map: 0 ReLU, 1 ELU + 1
   PrefillLayer layers[kMaxLayersPerLaunch];  // the launch's layers, by decreasing window
   int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token

@@ -470,8 +470,11 @@ struct MainLds {
   static_assert(bytes <= 160 * 1024, "LDS budget");
 };
 
-// PHI: the feature map (0 ReLU, 1 ELU + 1), one instantiation each
-template <typename T, int D, int DF, int PHI>
+// PHI: the feature map (0 ReLU, 1 ELU + 1).  PASS: 0 the band and the
+// linear part over one shared denominator; for the hybrid forms, 1 the
+// linear part alone (normalised on its own) and 2 the band alone, its
+// normalised output added to what out holds.  One instantiation each.
+template <typename T, int D, int DF, int PHI, int PASS>
 __global__ __launch_bounds__(kMT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void prefill_main(PrefillArgs a) {
   using LD = MainLds<T, D, DF>;
@@ -502,11 +505,11 @@ void prefill_main(PrefillArgs a) {
   const int sigma = sg - a.seg_base[bl];
   const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
   const int G = a.G, C = a.C;
-  const int W = a.band ? L.W : 0;  // the band's window (0: this pass has no band)
-  const int Wd = L.Wd;             // the linear part's delay
-  const bool linear = a.linear != 0;
-  if (!linear && W == 0) return;   // a band-only pass: nothing to add for this layer
-  const bool accum = a.accum != 0;
+  const int W = PASS == 1 ? 0 : L.W;  // the band's window (0: this pass has no band)
+  const int Wd = L.Wd;                // the linear part's delay
+  const bool linear = PASS != 2 && a.linear != 0;
+  constexpr bool accum = PASS == 2;
+  if (PASS == 2 && W == 0) return;    // a band-only pass: nothing to add for this layer
   // The band works on raw scores q.k scaled by sc2 >= 0 inside the exponent:
   // a negative tau is carried by the queries' sign (negated in registers for
   // the band, undone in the feature map), and a zero tau is raised to 1e-30,
@@ -976,7 +979,7 @@ void prefill_main(PrefillArgs a) {
       const float ls = lg_sum(l_run[qt]);
       const float inv = ls > 0.f ? 1.f / ls : 0.f;
       if (ov[qt]) {
-        if (accum) {
+        if constexpr (accum) {
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct) add4(O + orow[qt] + 16 * ct, acc[qt][ct], inv);
         } else {
@@ -1070,11 +1073,17 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
   const unsigned nl = unsigned(a.nlayer);
   bool window = false;
   for (int i = 0; i < a.nlayer; ++i) window = window || a.layers[i].W > 0;
-  auto main = [&](const PrefillArgs& m) {
-    if (m.phi)
-      hipLaunchKernelGGL((prefill_main<T, D, DF, 1>), dim3(m.nseg, m.Hkv, nl), dim3(kMT), 0, s, m);
-    else
-      hipLaunchKernelGGL((prefill_main<T, D, DF, 0>), dim3(m.nseg, m.Hkv, nl), dim3(kMT), 0, s, m);
+  auto main = [&](int pass) {
+    const dim3 grid(a.nseg, a.Hkv, nl), block(kMT);
+    if (a.phi) {
+      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 0>), grid, block, 0, s, a);
+      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 1>), grid, block, 0, s, a);
+      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 2>), grid, block, 0, s, a);
+    } else {
+      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 0>), grid, block, 0, s, a);
+      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 1>), grid, block, 0, s, a);
+      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 2>), grid, block, 0, s, a);
+    }
   };
   if (a.nseg > 0) {
     if (a.linear) {
@@ -1089,20 +1098,15 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (a.form == 0) {
-      main(a);
+      main(0);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     } else {
       // hybrid forms: the linear part normalised on its own, then the band's
       // normalised output added to it
-      PrefillArgs p = a;
-      p.band = 0;
-      main(p);
+      main(1);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       if (window) {
-        p.band = 1;
-        p.linear = 0;
-        p.accum = 1;
-        main(p);
+        main(2);
         if ((e = hipGetLastError()) != hipSuccess) return e;
       }
     }
