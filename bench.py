@@ -68,6 +68,8 @@ def main():
                          "forms (separately normalised sum; state over the evicted tokens / every token)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-detail", action="store_true",
+                    help="skip the per-step decode distribution and the per-layer (eager and graph) decode runs")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (the known-size kernel that "
                          "calibrates the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -192,9 +194,70 @@ def main():
         "roofline_other": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in
                            (mfma if dominant is hbm else hbm).items()},
     }
+    if not args.no_detail and wl.decode_steps:
+        line["decode_detail"] = decode_detail(g, wl, state, phi, dq, dk, dv, dout, ws, prefill, stream)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, g, state, phi, dq, dk, dv, args.cpu_baseline_seconds, args.form)
     print(json.dumps(line), flush=True)
+
+
+def decode_detail(g, wl, state, phi, dq, dk, dv, dout, ws, prefill, stream, reps=2):
+    """Decode timings outside the timed region (not part of `value`):
+    every step of one pass timed on its own (median, p10, p90 of the
+    whole-stack call), and the same steps as one library call per layer, the
+    way a model that interleaves layers calls it: eagerly, and captured once
+    in a HIP graph and replayed."""
+    import torch
+    L, n = wl.n_layers, wl.decode_steps
+
+    def fresh():
+        g.state_init(state)
+        prefill()
+
+    def per_layer():
+        for s in range(n):
+            for l in range(L):
+                g.decode_step(state, phi[l:l + 1], dq[s, l:l + 1], dk[s, l:l + 1], dv[s, l:l + 1], dout[l:l + 1],
+                              ws, layer0=l, n_layers=1)
+
+    fresh()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    ev[0].record(stream)
+    for s in range(n):
+        g.decode_step(state, phi, dq[s], dk[s], dv[s], dout, ws)
+        ev[s + 1].record(stream)
+    torch.cuda.synchronize()
+    us = sorted(ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(n))
+    pct = lambda f: us[min(n - 1, int(round(f * (n - 1))))]
+
+    def timed(run):
+        best = None
+        for _ in range(reps):
+            fresh()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            run()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) * 1e3 / n
+            best = t if best is None else min(best, t)
+        return best
+
+    eager_us = timed(per_layer)
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.graph(graph, stream=side):
+        per_layer()
+    torch.cuda.synchronize()
+    graph_us = timed(graph.replay)
+    del graph
+    return {"step_us_median": round(pct(0.5), 2), "step_us_p10": round(pct(0.1), 2),
+            "step_us_p90": round(pct(0.9), 2),
+            "tokens_per_s_at_median": round(wl.batch / (pct(0.5) * 1e-6), 2),
+            "per_layer_calls_eager_us_per_step": round(eager_us, 2),
+            "per_layer_calls_graph_us_per_step": round(graph_us, 2),
+            "per_layer_calls_graph_tokens_per_s": round(wl.batch / (graph_us * 1e-6), 2)}
 
 
 def kernel_sources_hash():

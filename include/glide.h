@@ -137,10 +137,11 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
  * at least 256.  Prefill takes one slot per layer of a launch (history rows
  * and per-segment state records) and batches as many layers per launch as
  * the given workspace holds, up to 64; this size holds as many as fit in
- * 1 GiB (at least one).  Decode uses the workspace only when the stack has
- * fewer than 1024 (layer, sequence, KV head) units: long windows are then
- * split over several workgroups, whose partial results it holds.  0 if cfg
- * is invalid. */
+ * 1 GiB (at least one).  Decode uses the workspace only when a layer has
+ * fewer than 512 (sequence, KV head) units: a decode launch with fewer than
+ * 512 units splits long windows over several workgroups, whose partial
+ * results it holds (at most 512 records; the size covers a call over any
+ * subset of the layers).  0 if cfg is invalid. */
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens);
 
 /* Zeroes the whole state: S = 0, z = 0 (S_0, Z_0 of the Sec. II-B
@@ -178,9 +179,11 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
  * group from the window and from S + the pending tokens, pos += 1; on the
  * unit's fold step (one in 8; every step when W = 0) the pending tokens are
  * folded into S and z.  Sequences may sit at different positions (pos lives
- * in the state).  One kernel is enqueued per 64 layers; when windows are
- * split (see glide_workspace_bytes) the workgroup that finishes a unit's last
- * piece merges the pieces' partial results.
+ * in the state).  One kernel is enqueued per 64 layers; each plans its own
+ * window split over the device (see glide_workspace_bytes), so a call over
+ * one layer spreads that layer's windows over many workgroups; the
+ * workgroup that finishes a unit's last piece merges the pieces' partial
+ * results.  Calls over different layer subsets agree up to rounding.
  *   phi_w  device [n_layers][d][Df]
  *   q      device [n_layers][B][Hq][d];  k, v device [n_layers][B][Hkv][d]
  *   out    device [n_layers][B][Hq][d]

@@ -35,6 +35,24 @@ __device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
   return make_float4(__shfl_xor(v.x, m), __shfl_xor(v.y, m), __shfl_xor(v.z, m), __shfl_xor(v.w, m));
 }
 
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_mv(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROW_MASK, 0xf, false));
+}
+// Sum over lanes 0 .. N-1 (N = 16 or 32; other lanes may hold anything)
+// with DPP moves inside 16-lane rows: the result is in lane 0 (N = 16) or in
+// lanes 16 .. 31 (N = 32).
+template <int N>
+__device__ __forceinline__ float dpp_sum_rows(float v) {
+  static_assert(N == 16 || N == 32, "16 or 32 lanes");
+  v += dpp_mv<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
+  v += dpp_mv<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
+  v += dpp_mv<0x141, 0xf>(v);  // row_half_mirror
+  v += dpp_mv<0x140, 0xf>(v);  // row_mirror: every lane holds its row's sum
+  if constexpr (N == 32) v += dpp_mv<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+  return v;
+}
+
 __device__ __forceinline__ int clamp_rel(int64_t x) { return int(x < -1 ? -1 : (x > 32 ? 32 : x)); }
 
 template <typename T, int D>
@@ -51,10 +69,9 @@ struct WindowTile {
 // finish (see the end of decode_kernel): the window parts (running max m, sum
 // l, weighted values acc per piece) over one max, plus piece 0's linear part,
 // over the shared denominator (hybrid forms: each part normalised on its
-// own, then added); then pos = p + 1.  The records are read with
-// system-coherent loads (they were written through to memory by workgroups
-// that may sit on other XCDs), every load of the workgroup issued before the
-// first wait.
+// own, then added); then pos = p + 1.  The pieces of a unit run on one XCD,
+// so the records are read from that XCD's L2 (loads that miss the L1),
+// every load of the workgroup issued before the first wait.
 template <typename T, int D, int DF>
 __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& L, int rem, int64_t p) {
   constexpr int EPT = 4;                   // output elements per thread whose loads go first
@@ -84,11 +101,11 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
   const int mpc = tid / G, mh = tid - mpc * G;
   const bool mok = tid < np * G;
   const uint32_t mo = uint32_t(mh * RH) * 4;
-  const float m0 = bload_f_sys(r0, mok && mpc == 0 ? mo : kOOB);
-  const float m1 = bload_f_sys(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo : kOOB);
-  const float l0 = bload_f_sys(r0, mok && mpc == 0 ? mo + 4 : kOOB);
-  const float l1 = bload_f_sys(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo + 4 : kOOB);
-  const float dnv = bload_f_sys(r0, tid < G ? uint32_t(tid * RH + 2) * 4 : kOOB);  // linear denominator
+  const float m0 = bload_f_l2(r0, mok && mpc == 0 ? mo : kOOB);
+  const float m1 = bload_f_l2(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo : kOOB);
+  const float l0 = bload_f_l2(r0, mok && mpc == 0 ? mo + 4 : kOOB);
+  const float l1 = bload_f_l2(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo + 4 : kOOB);
+  const float dnv = bload_f_l2(r0, tid < G ? uint32_t(tid * RH + 2) * 4 : kOOB);  // linear denominator
   float v[EPT][kMaxPieces], nmv[EPT];
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
@@ -96,10 +113,10 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
     const int hh = i / D, c = i - hh * D;
     const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
     const bool ok = i < n;
-    v[e][0] = bload_f_sys(r0, ok ? o : kOOB);
+    v[e][0] = bload_f_l2(r0, ok ? o : kOOB);
 #pragma unroll
-    for (int pc = 1; pc < kMaxPieces; ++pc) v[e][pc] = bload_f_sys(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
-    nmv[e] = bload_f_sys(r0, ok ? o + D * 4 : kOOB);
+    for (int pc = 1; pc < kMaxPieces; ++pc) v[e][pc] = bload_f_l2(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
+    nmv[e] = bload_f_l2(r0, ok ? o + D * 4 : kOOB);
   }
   // every thread writes its slot (kThreads slots; no branch, so the loads
   // above are not sunk behind the record loads)
@@ -148,9 +165,9 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
   for (int i = tid + EPT * kThreads; i < n; i += kThreads) {  // G * D > EPT * 256 (large G)
     const int hh = i / D, c = i - hh * D;
     const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
-    float Ac = bload_f_sys(r0, o) * pw[hh];
-    for (int pc = 1; pc < np; ++pc) Ac = fmaf(bload_f_sys(r1, (pc - 1) * rs + o), pw[pc * G + hh], Ac);
-    const float nm = hs[hh][1] == 0.f ? 0.f : bload_f_sys(r0, o + D * 4);
+    float Ac = bload_f_l2(r0, o) * pw[hh];
+    for (int pc = 1; pc < np; ++pc) Ac = fmaf(bload_f_l2(r1, (pc - 1) * rs + o), pw[pc * G + hh], Ac);
+    const float nm = hs[hh][1] == 0.f ? 0.f : bload_f_l2(r0, o + D * 4);
     og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
   }
   if (tid == 0) *pos_ptr = p + 1;
@@ -169,6 +186,9 @@ void decode_kernel(DecodeArgs a) {
   constexpr int STEPS = RW / RPS;
   constexpr uint32_t ES = sizeof(T);
   constexpr int PVT = (kFoldPeriod * D + kThreads - 1) / kThreads;  // pending values per thread
+  constexpr int WPR = RW * int(ES) / 16;   // 16-byte pieces per staged Wf row (bf16)
+  constexpr int WCH = D * WPR / 64 > 0 ? D * WPR / 64 : 1;  // staged pieces per lane
+  constexpr int WPITCH = RW + 2;           // staged row pitch in elements (4 bytes of padding)
   static_assert(STEPS * RPS == RW && NTW * 16 == RW, "state rows must tile the wave");
 
   extern __shared__ __align__(16) float smem[];
@@ -177,8 +197,9 @@ void decode_kernel(DecodeArgs a) {
   const int hq = lane & 15, lg = lane >> 4;
   const int G = a.G, B = a.B, Hkv = a.Hkv, Hq = a.Hq;
   const int per_layer = B * Hkv;
-  const int prow = __builtin_amdgcn_readfirstlane(int(blockIdx.x) / per_layer);
-  const int rem = int(blockIdx.x) - prow * per_layer;
+  const int prow = __builtin_amdgcn_readfirstlane(int(blockIdx.x) / a.row_stride);
+  const int rem = int(blockIdx.x) - prow * a.row_stride;
+  if (rem >= per_layer) return;  // padding of a split launch's rows
   // (the table is read a dword at a time: a scalar load, no vector memory wait)
   const uint32_t lw = reinterpret_cast<const uint32_t*>(a.piece_layer)[prow >> 2];
   const LayerArg L = a.layers[(lw >> (8 * (prow & 3))) & 0xffu];
@@ -205,18 +226,69 @@ void decode_kernel(DecodeArgs a) {
   T* og = reinterpret_cast<T*>(a.out) + (tok * Hq + int64_t(g) * G) * D;
   const T* Wf = reinterpret_cast<const T*>(a.phi_w) + int64_t(L.slot) * D * DF;
 
+  // pos and nf: two scalar loads in flight together; the loads that do not
+  // depend on them (the state pass's Wf slice, S rows and z, the queries and
+  // the new key/value) are issued before the first wait for them.
   const int64_t p = *pos_ptr;
+  int64_t nf = *nf_ptr;
 
   float* ph = smem;                        // [G + kFoldPeriod][DF] phi(q_h), then phi(k_j) of pending j
   float* pvl = ph + (G + kFoldPeriod) * DF;  // [kFoldPeriod][D]    values of the pending tokens
   float* kpl = pvl + kFoldPeriod * D;      // [D]           the new key
   float* vpl = kpl + D;                    // [D]           the new value
   float* spl = vpl + D;                    // [kMaxG]       the new token's score (log2 units)
-  float* lnum = spl + kMaxG;               // [waves][G][D] linear numerator partials phi(q).S
-  float* lden = lnum + kWaves * G * D;     // [waves][G]    linear denominator partials phi(q).z
+  float* lnum = spl + kMaxG;               // [waves][RPS][G][D] linear numerator partials phi(q).S
+  float* lden = lnum + kWaves * RPS * G * D;  // [waves][G]    linear denominator partials phi(q).z
   float* wacc = lden + kWaves * G;         // [waves][G][D] window partials sum e^s v
   float* wm = wacc + kWaves * G * D;       // [waves][G]    window running max (log2 units)
   float* wl = wm + kWaves * G;             // [waves][G]    window sum e^s
+  // [waves][D][WPITCH] this wave's Wf columns (bf16), staged for the
+  // column-gather of the feature map's B fragments.  It shares the memory of
+  // lnum .. wl, which are first written after the barrier that follows the
+  // feature map, when every wave has read its staged columns.
+  T* wfs = reinterpret_cast<T*>(lnum) + wave * D * WPITCH;
+
+  const brsrc_t rq = make_rsrc(qg, uint32_t(G * D) * ES);
+  const brsrc_t rk = make_rsrc(kn, D * ES), rv = make_rsrc(vn, D * ES);
+  const brsrc_t rS = make_rsrc(S, DF * D * 4), rz = make_rsrc(z, DF * 4);
+  const brsrc_t rK = make_rsrc(Kr, uint32_t(R) * D * ES), rV = make_rsrc(Vr, uint32_t(R) * D * ES);
+  const brsrc_t rW = make_rsrc(Wf, D * DF * ES);
+
+  // ---- 1. prologue: every load up to the first window tile is issued before
+  //         any of them is waited for.
+  // The state pass belongs to piece 0 of a unit with a linear part; whether
+  // the part is empty yet (beta = 0) or S holds anything (nf > 0) is known
+  // only once pos and nf arrive, so the workgroup that may do it loads its
+  // operands now and drops them then.
+  const bool lin_call = a.linear != 0 && piece == 0;
+  const int f0 = wave * RW;
+  const int lr = lane / LPR, c4 = (lane % LPR) * 4;
+  uint4 wst[WCH];  // bf16: this wave's Wf columns, 16-byte row pieces
+  Frag<T> wb[KS][NTW];
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < WCH; ++i) {
+      const int c = lane + 64 * i, r = c / WPR, x = c - r * WPR;
+      wst[i] = bload16(rW, lin_call ? uint32_t((r * DF + f0 + 8 * x) * ES) : kOOB);
+    }
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+      for (int nt = 0; nt < NTW; ++nt)
+        bload_frag_strided(wb[kk][nt], rW, lin_call ? uint32_t((32 * kk + 8 * lg) * DF + f0 + 16 * nt + hq) * ES : kOOB,
+                           DF * ES);
+  }
+  float4 sr[STEPS];
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s) sr[s] = bload_f4(rS, lin_call ? uint32_t(((f0 + s * RPS + lr) * D + c4) * 4) : kOOB);
+  float zf = bload_f(rz, lin_call && lane < RW ? uint32_t((f0 + lane) * 4) : kOOB);
+  // the new token's element tid % D (its own score, and the ring write at the end)
+  const T kraw = bload_elem(rk, uint32_t(tid % D) * ES, T());
+  const T vraw = bload_elem(rv, uint32_t(tid % D) * ES, T());
+  Frag<T> fq[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) bload_frag(fq[kk], rq, hq < G ? uint32_t(hq * D + 32 * kk + 8 * lg) * ES : kOOB);
 
   // Linear set after this step: tokens [0, beta).  S, z hold tokens [0, nf);
   // tokens [nf, beta) are pending (in the ring, or the new token when Wd = 0)
@@ -228,13 +300,13 @@ void decode_kernel(DecodeArgs a) {
   const int fper = Wd > 0 ? kFoldPeriod : 1;
   // nf of a well-formed state lies in [beta - fper, beta]; the clamp keeps
   // every access in bounds whatever the blob holds.
-  int64_t nf = *nf_ptr;
   nf = nf < beta ? nf : beta;
   nf = nf > beta - fper ? nf : beta - fper;
   nf = nf > 0 ? nf : 0;
   const int npend = lin ? int(beta - nf) : 0;  // 0 .. fper
   const bool fold = npend > 0 && (npend >= fper || (beta + int64_t(unit % fper)) % fper == 0);
   const bool s_nonzero = lin && nf > 0;  // S, z hold something
+  const int32_t nf_slot = R > 0 ? int32_t(nf % R) : 0;  // ring slot of token nf
 
   // Window: tokens [tlo, p] in 32-token tiles.  Ring tiles cover [tlo, p-1];
   // the new token p (not in the ring yet) is a partial of its own.  The
@@ -257,12 +329,6 @@ void decode_kernel(DecodeArgs a) {
   int64_t j0 = (tile0 + it) << 5;
   uint32_t s0 = W > 0 ? uint32_t(j0 % R) : 0u;
   const uint32_t step = W > 0 ? uint32_t((32 * kWaves) % R) : 0u;
-
-  const brsrc_t rq = make_rsrc(qg, uint32_t(G * D) * ES);
-  const brsrc_t rk = make_rsrc(kn, D * ES), rv = make_rsrc(vn, D * ES);
-  const brsrc_t rS = make_rsrc(S, DF * D * 4), rz = make_rsrc(z, DF * 4);
-  const brsrc_t rK = make_rsrc(Kr, uint32_t(R) * D * ES), rV = make_rsrc(Vr, uint32_t(R) * D * ES);
-  const brsrc_t rW = make_rsrc(Wf, D * DF * ES);
   const brsrc_t rpk = Wd > 0 ? rK : rk;  // where pending keys / values live
   const brsrc_t rpv = Wd > 0 ? rV : rv;
 
@@ -282,11 +348,6 @@ void decode_kernel(DecodeArgs a) {
     for (int ct = 0; ct < CT; ++ct) bload_frag(tl.v[ct], rV, base + uint32_t(((ct * 4 + lg) * 16 + hq) * 8) * ES);
   };
 
-  // ---- 1. prologue: every load up to the first window tile is issued before
-  //         any of them is waited for.
-  // the new token's element tid % D (its own score, and the ring write at the end)
-  const T kraw = bload_elem(rk, uint32_t(tid % D) * ES, T());
-  const T vraw = bload_elem(rv, uint32_t(tid % D) * ES, T());
   // rows of the feature-map tile, which are also the queries of the window's
   // QK^T: row hq < G is query head hq, rows G .. G+npend-1 the pending keys
   // (second tile: rows 16 ..), other rows zero.  Columns of QK^T beyond G are
@@ -295,53 +356,56 @@ void decode_kernel(DecodeArgs a) {
   {
     const int ia = hq - G, ib = 16 + hq - G;
     const bool pa = hq >= G && ia < npend, pb = ib >= 0 && ib < npend;
-    const int32_t sa = Wd > 0 ? int32_t((nf + (pa ? ia : 0)) % R) : 0;
-    const int32_t sb = Wd > 0 ? int32_t((nf + (pb ? ib : 0)) % R) : 0;
+    // ring slots of pending tokens nf + i (i < 8 < R: one wrap at most)
+    const int32_t sa = Wd > 0 ? int32_t(wrap_once(uint32_t(nf_slot + (pa ? ia : 0)), uint32_t(R))) : 0;
+    const int32_t sb = Wd > 0 ? int32_t(wrap_once(uint32_t(nf_slot + (pb ? ib : 0)), uint32_t(R))) : 0;
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      Frag<T> fq, fp;
-      bload_frag(fq, rq, hq < G ? uint32_t(hq * D + 32 * kk + 8 * lg) * ES : kOOB);
+      Frag<T> fp;
       const uint32_t oa = Wd > 0 ? uint32_t(kring_chunk(sa, kk, lg, D)) * ES : uint32_t(32 * kk + 8 * lg) * ES;
       bload_frag(fp, rpk, pa ? oa : kOOB);
-      xa[kk] = frag_or(fq, fp);
+      xa[kk] = frag_or(fq[kk], fp);
       const uint32_t ob = Wd > 0 ? uint32_t(kring_chunk(sb, kk, lg, D)) * ES : uint32_t(32 * kk + 8 * lg) * ES;
       bload_frag(xb[kk], rpk, pb ? ob : kOOB);
     }
   }
-  // Wf B fragments of this wave's features (zeros when there is no state pass)
-  // The state pass's loads (Wf, pending values, S rows, z) are issued only by
-  // the workgroup that does it (lin is uniform over the workgroup): other
-  // pieces go straight to their window tiles.
-  const int f0 = wave * RW;
-  Frag<T> wb[KS][NTW];
-  T pvr[PVT];
-  const int lr = lane / LPR, c4 = (lane % LPR) * 4;
-  float4 sr[STEPS];
-  float zf = 0.f;
-  if (lin) {
+  // values of the pending tokens
+  // (raw elements, one per register, issued unconditionally: converted only
+  // where they are used, so no wait holds back the loads that follow)
+  uint32_t pvr[PVT];
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk)
-#pragma unroll
-      for (int nt = 0; nt < NTW; ++nt)
-        bload_frag_strided(wb[kk][nt], rW, uint32_t((32 * kk + 8 * lg) * DF + f0 + 16 * nt + hq) * ES, DF * ES);
-    // values of the pending tokens
-#pragma unroll
-    for (int u = 0; u < PVT; ++u) {
-      const int e = tid + u * kThreads, i = e / D, c = e - i * D;
-      const bool ok = i < npend;
-      const uint32_t off =
-          Wd > 0 ? uint32_t(vring_elem(int32_t((nf + (ok ? i : 0)) % R), c, D)) * ES : uint32_t(c) * ES;
-      pvr[u] = bload_elem(rpv, ok ? off : kOOB, T());
-    }
-    // this wave's S rows and z entries (zeros when S is empty)
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s)
-      sr[s] = bload_f4(rS, s_nonzero ? uint32_t(((f0 + s * RPS + lr) * D + c4) * 4) : kOOB);
-    zf = bload_f(rz, s_nonzero && lane < RW ? uint32_t((f0 + lane) * 4) : kOOB);
+  for (int u = 0; u < PVT; ++u) {
+    const int e = tid + u * kThreads, i = e / D, c = e - i * D;
+    const bool ok = i < npend;
+    const uint32_t off =
+        Wd > 0 ? uint32_t(vring_elem(int32_t(wrap_once(uint32_t(nf_slot + (ok ? i : 0)), uint32_t(R))), c, D)) * ES
+               : uint32_t(c) * ES;
+    pvr[u] = bload_raw(rpv, ok ? off : kOOB, T());
   }
   // first window tile of this wave
   WindowTile<T, D> ta, tb;
   load_tile(ta, s0, W > 0 && it < n_tiles);
+
+  // Wf B fragments of this wave's features: the staged rows are gathered by
+  // column from LDS (the wave reads only what it wrote itself).
+  if constexpr (sizeof(T) == 2) {
+    if (lin) {
+#pragma unroll
+      for (int i = 0; i < WCH; ++i) {
+        const int c = lane + 64 * i, r = c / WPR, x = c - r * WPR;
+        T* d0 = wfs + r * WPITCH + 8 * x;
+        const uint32_t w4[4] = {wst[i].x, wst[i].y, wst[i].z, wst[i].w};
+        // (byte copies: the element reads below must not be ordered before
+        // these writes, which a type-based alias assumption would allow)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) __builtin_memcpy(d0 + 2 * j, &w4[j], 4);
+      }
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+        for (int nt = 0; nt < NTW; ++nt) wb[kk][nt].load_strided(wfs + (32 * kk + 8 * lg) * WPITCH + 16 * nt + hq, WPITCH);
+    }
+  }
 
   // ---- 2. feature map on MFMA: rows x Wf, this wave's RW features, fp32
   if (lin) {
@@ -372,7 +436,7 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int u = 0; u < PVT; ++u) {
       const int e = tid + u * kThreads;
-      if (e < kFoldPeriod * D) pvl[e] = to_f32(pvr[u]);
+      if (e < kFoldPeriod * D) pvl[e] = raw_to_f32(pvr[u], T());
     }
   }
   if (own_p && tid < D) {
@@ -405,6 +469,12 @@ void decode_kernel(DecodeArgs a) {
   //         are unchanged and skipped).  Per-wave partials are summed in the
   //         merge.
   if (lin) {
+    // S, z are zero until the first fold (their memory is not read as such)
+    if (!s_nonzero) {
+#pragma unroll
+      for (int s = 0; s < STEPS; ++s) sr[s] = make_float4(0.f, 0.f, 0.f, 0.f);
+      zf = 0.f;
+    }
     const float* pk = ph + G * DF;
     uint32_t touched = 0;
     float dz = 0.f;
@@ -440,16 +510,12 @@ void decode_kernel(DecodeArgs a) {
         n4.z = fmaf(w, sr[s].z, n4.z);
         n4.w = fmaf(w, sr[s].w, n4.w);
       }
-#pragma unroll
-      for (int off = LPR; off < 64; off <<= 1) {
-        const float4 o = shfl_xor4(n4, off);
-        n4.x += o.x; n4.y += o.y; n4.z += o.z; n4.w += o.w;
-      }
-      if (lr == 0) *reinterpret_cast<float4*>(lnum + (wave * G + hh) * D + c4) = n4;
-      float dp = lane < RW ? pq[f0 + lane] * zf : 0.f;
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) dp += __shfl_xor(dp, off);
-      if (lane == 0) lden[wave * G + hh] = dp;
+      // the RPS row groups of the wave are summed in the merge (no
+      // cross-lane exchange here); the denominator partial over the wave's
+      // RW features is reduced within DPP rows
+      *reinterpret_cast<float4*>(lnum + ((wave * RPS + lr) * G + hh) * D + c4) = n4;
+      const float dp = dpp_sum_rows<RW>(lane < RW ? pq[f0 + lane] * zf : 0.f);
+      if (lane == (RW > 16 ? 16 : 0)) lden[wave * G + hh] = dp;
     }
   }
 
@@ -550,14 +616,16 @@ void decode_kernel(DecodeArgs a) {
   //         over the pieces: each writes a record, the last to finish merges
   //         them): one shared denominator, or (hybrid forms) the window's and
   //         the linear part's normalised outputs added
-  const brsrc_t rrec = make_rsrc(a.part + int64_t(blockIdx.x) * part_floats(G, D), uint32_t(part_floats(G, D)) * 4);
+  const brsrc_t rrec =
+      make_rsrc(a.part + (int64_t(prow) * per_layer + rem) * part_floats(G, D), uint32_t(part_floats(G, D)) * 4);
   for (int i = tid; i < G * D; i += kThreads) {
     const int hh = i / D, c = i - hh * D;
     float nm = 0.f, dn = 0.f;
     if (lin) {
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        nm += lnum[(w * G + hh) * D + c];
+#pragma unroll
+        for (int r = 0; r < RPS; ++r) nm += lnum[((w * RPS + r) * G + hh) * D + c];
         dn += lden[w * G + hh];
       }
     }
@@ -585,12 +653,12 @@ void decode_kernel(DecodeArgs a) {
     if (split) {
       const uint32_t ro = uint32_t(hh * (2 * D + 3)) * 4;
       if (c == 0) {
-        bstore_f_sys(rrec, ro, M);
-        bstore_f_sys(rrec, ro + 4, Ls);
-        bstore_f_sys(rrec, ro + 8, dn);
+        bstore_f_l2(rrec, ro, M);
+        bstore_f_l2(rrec, ro + 4, Ls);
+        bstore_f_l2(rrec, ro + 8, dn);
       }
-      bstore_f_sys(rrec, ro + uint32_t(3 + c) * 4, Ac);
-      if (piece == 0) bstore_f_sys(rrec, ro + uint32_t(3 + D + c) * 4, nm);
+      bstore_f_l2(rrec, ro + uint32_t(3 + c) * 4, Ac);
+      if (piece == 0) bstore_f_l2(rrec, ro + uint32_t(3 + D + c) * 4, nm);
       continue;
     }
     float o;
@@ -610,16 +678,19 @@ void decode_kernel(DecodeArgs a) {
     og[i] = from_f32<T>(o);
   }
   if (split) {
-    // Every record store of the workgroup has reached memory before the
-    // unit's count moves (relaxed device-scope add: no cache write-back);
-    // the workgroup that brings it to npiece merges, then resets it.
+    // The pieces of a unit run on one XCD (same workgroup index modulo 8),
+    // so the records, the count and the merge's loads all meet in that XCD's
+    // L2: every record store of the workgroup has reached the L2 before the
+    // unit's count moves (an add performed in the L2), and the workgroup that
+    // brings it to npiece reads the records from the L2, merges, and resets
+    // the count.
     __shared__ int last;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
-      int* cnt = reinterpret_cast<int*>(lay + sec.cnt) + unit;
-      last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == L.npiece - 1;
-      if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const brsrc_t rc = make_rsrc(lay + sec.cnt + unit * 4, 4);
+      last = __builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(1, rc, 0, 0, 0) == L.npiece - 1;
+      if (last) __builtin_amdgcn_raw_buffer_store_b32(0u, rc, 0, 0, 0);
     }
     __syncthreads();
     if (last) merge_unit<T, D, DF>(a, L, rem, p);
@@ -714,8 +785,13 @@ hipError_t flush_t(const DecodeArgs& a, hipStream_t stream) {
 template <typename T, int D, int DF>
 hipError_t launch_t(const DecodeArgs& a, int total_wg, hipStream_t stream) {
   const int G = a.G;
-  const size_t floats = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D + 2 * D + kMaxG +
-                        2 * (size_t(kWaves) * G * D + kWaves * G) + kWaves * G;
+  // ph, pvl, kpl, vpl, spl; then lnum .. wl, or the staged Wf columns that
+  // share their memory (bf16: kWaves x D rows of RW + 2 elements)
+  const size_t head = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D + 2 * D + kMaxG;
+  constexpr int RPS = 256 / D;  // state rows per wave step (lanes per row: D / 4)
+  const size_t tail = size_t(kWaves) * RPS * G * D + kWaves * G + size_t(kWaves) * G * D + kWaves * G + kWaves * G;
+  const size_t staged = sizeof(T) == 2 ? size_t(kWaves) * D * (DF / kWaves + 2) / 2 : 0;
+  const size_t floats = head + (tail > staged ? tail : staged);
   hipLaunchKernelGGL((decode_kernel<T, D, DF>), dim3(unsigned(total_wg)), dim3(kThreads), floats * sizeof(float),
                      stream, a);
   return hipGetLastError();

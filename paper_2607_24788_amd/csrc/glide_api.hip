@@ -90,31 +90,33 @@ PrefillWorkspace prefill_ws(const glide_config* c, int64_t T, int32_t nl) {
                            linear_on(c), nl);
 }
 
-// Decode window split (pieces per unit of each layer).  The work of a unit
-// is counted in 32-token window tiles plus kStateTiles for the state pass; a
-// layer whose units have work w gets min(kMaxPieces, ceil(w / q)) pieces, with
-// q the smallest piece size (>= 4 tiles) for which the whole stack fits in
-// kDecodeSlots workgroups.  When the units alone fill the slots, nothing is
-// split.
-std::vector<int32_t> decode_pieces(const glide_config* c) {
-  std::vector<int32_t> np(c->n_layers, 1);
+// Decode window split (pieces per unit of each layer of one launch).  The
+// work of a unit is counted in 32-token window tiles plus kStateTiles for the
+// state pass; a layer whose units have work w gets min(kMaxPieces, ceil(w / q))
+// pieces, with q the smallest piece size (>= 4 tiles) for which the launch
+// fits in kDecodeSlots workgroups.  When the launch's units alone fill the
+// slots, nothing is split.  The plan depends only on the launch's layers, so
+// a call over one layer splits that layer's window over the whole device.
+std::vector<int32_t> decode_pieces(const glide_config* c, const int32_t* layers, int32_t n) {
+  std::vector<int32_t> np(n, 1);
   const int64_t per_layer = int64_t(c->batch) * c->n_kv_heads;
-  if (per_layer * c->n_layers >= kDecodeSlots) return np;
+  if (per_layer * n >= kDecodeSlots) return np;
   const int st = linear_on(c) ? kStateTiles : 0;
-  std::vector<int64_t> work(c->n_layers);
+  std::vector<int64_t> work(n);
   int64_t wmax = 4;
-  for (int32_t l = 0; l < c->n_layers; ++l) {
-    work[l] = c->windows[l] > 0 ? decode_tiles_max(c->windows[l]) + st : 0;
-    wmax = std::max(wmax, work[l]);
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t W = c->windows[layers[i]];
+    work[i] = W > 0 ? decode_tiles_max(W) + st : 0;
+    wmax = std::max(wmax, work[i]);
   }
-  auto pieces = [&](int64_t q, int32_t l) {
-    if (work[l] == 0) return int64_t(1);
-    return std::min<int64_t>(kMaxPieces, std::max<int64_t>(1, (work[l] + q - 1) / q));
+  auto pieces = [&](int64_t q, int32_t i) {
+    if (work[i] == 0) return int64_t(1);
+    return std::min<int64_t>(kMaxPieces, std::max<int64_t>(1, (work[i] + q - 1) / q));
   };
   auto wgs = [&](int64_t q) {
-    int64_t n = 0;
-    for (int32_t l = 0; l < c->n_layers; ++l) n += pieces(q, l) * per_layer;
-    return n;
+    int64_t m = 0;
+    for (int32_t i = 0; i < n; ++i) m += pieces(q, i) * per_layer;
+    return m;
   };
   int64_t lo = 4, hi = wmax;  // wgs(wmax) = units <= slots
   while (lo < hi) {
@@ -122,22 +124,29 @@ std::vector<int32_t> decode_pieces(const glide_config* c) {
     if (wgs(mid) <= kDecodeSlots) hi = mid;
     else lo = mid + 1;
   }
-  for (int32_t l = 0; l < c->n_layers; ++l) np[l] = int32_t(pieces(lo, l));
+  for (int32_t i = 0; i < n; ++i) np[i] = int32_t(pieces(lo, i));
   return np;
 }
 
-// Decode workspace: the partial records of every workgroup of a launch when
-// some layer is split (records are indexed by workgroup).
+// Decode workspace bound over every call (what glide_workspace_bytes reports
+// and every decode call requires, whatever its layers): a launch splits only
+// when its units number fewer than kDecodeSlots, and then it has at most
+// kDecodeSlots workgroups, and at most the pieces its layers get at the
+// smallest piece size.
 size_t decode_ws(const glide_config* c) {
-  const std::vector<int32_t> np = decode_pieces(c);
+  const int64_t per_layer = int64_t(c->batch) * c->n_kv_heads;
+  if (per_layer >= kDecodeSlots) return 0;
+  const int st = linear_on(c) ? kStateTiles : 0;
   int64_t wgs = 0;
   bool any = false;
   for (int32_t l = 0; l < c->n_layers; ++l) {
-    wgs += int64_t(np[l]) * c->batch * c->n_kv_heads;
-    any = any || np[l] > 1;
+    const int64_t work = c->windows[l] > 0 ? decode_tiles_max(c->windows[l]) + st : 0;
+    const int64_t p = work ? std::min<int64_t>(kMaxPieces, std::max<int64_t>(1, (work + 3) / 4)) : 1;
+    wgs += p * per_layer;
+    any = any || p > 1;
   }
   if (!any) return 0;
-  return size_t(align256(wgs * part_floats(c->n_q_heads / c->n_kv_heads, c->head_dim) * 4));
+  return size_t(align256(std::min<int64_t>(wgs, kDecodeSlots) * part_floats(c->n_q_heads / c->n_kv_heads, c->head_dim) * 4));
 }
 
 // Decode-style launch descriptor of layers [layer0, layer0 + n): per launch
@@ -145,7 +154,6 @@ size_t decode_ws(const glide_config* c) {
 // (the hardware dispatcher then hands out the longest streams first).
 template <typename Fn>
 glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n_layers, DecodeArgs& a, Fn fn) {
-  const std::vector<int32_t> np = decode_pieces(cfg);
   const int32_t per_layer = cfg->batch * cfg->n_kv_heads;
   std::vector<int32_t> order(n_layers);
   for (int32_t i = 0; i < n_layers; ++i) order[i] = i;
@@ -162,27 +170,29 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
   a.tau = cfg->sm_scale;
   for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
+    int32_t ls[kMaxLayersPerLaunch];
+    for (int32_t i = 0; i < cnt; ++i) ls[i] = layer0 + order[first + i];
+    const std::vector<int32_t> np = decode_pieces(cfg, ls, cnt);
     a.n_layers = cnt;
     int32_t rows = 0;
     bool split = false;
     for (int32_t i = 0; i < cnt; ++i) {  // piece 0 of every layer first
-      const int32_t slot = order[first + i];
-      const int32_t l = layer0 + slot;
+      const int32_t l = ls[i];
       a.layers[i].base = layer_base(cfg, l);
       a.layers[i].W = cfg->windows[l];
       a.layers[i].R = ring_slots(cfg->windows[l]);
-      a.layers[i].slot = slot;
-      a.layers[i].npiece = np[l];
+      a.layers[i].slot = order[first + i];
+      a.layers[i].npiece = np[i];
       a.layers[i].prow0 = rows;
       a.piece_layer[rows++] = uint8_t(i);
-      split = split || np[l] > 1;
+      split = split || np[i] > 1;
     }
     for (int32_t i = 0; i < cnt; ++i) {  // then the other pieces
-      const int32_t l = layer0 + order[first + i];
       a.layers[i].prow1 = rows;
-      for (int32_t r = 1; r < np[l]; ++r) a.piece_layer[rows++] = uint8_t(i);
+      for (int32_t r = 1; r < np[i]; ++r) a.piece_layer[rows++] = uint8_t(i);
     }
-    const glide_status s = hip_status(fn(a, rows * per_layer, split));
+    a.row_stride = split ? (per_layer + 7) / 8 * 8 : per_layer;
+    const glide_status s = hip_status(fn(a, rows * a.row_stride, split));
     if (s != GLIDE_OK) return s;
   }
   return GLIDE_OK;
@@ -273,7 +283,7 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
   a.v = v;
   a.out = out;
   a.part = static_cast<float*>(workspace);
-  return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g, int32_t wgs, bool split) {
+  return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g, int32_t wgs, bool) {
     return launch_decode(g, wgs, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
   });
 }

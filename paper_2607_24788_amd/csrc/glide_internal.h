@@ -90,13 +90,13 @@ struct LayerArg {
 // Pieces write partial records (running max, sum and weighted values of the
 // window part per head; piece 0 adds the linear part); the piece that
 // finishes last (a per-unit counter in the state) merges them.  The split
-// depends on the configuration only: the pieces are
-// made as small as possible while every workgroup of the stack still fits in
-// one round of kDecodeSlots resident workgroups (256 CUs x 2), since a
-// second round would be latency-bound; large batches are never split.
+// depends on the layers of the launch only: the pieces are made as small as
+// possible while every workgroup of the launch still fits in one round of
+// kDecodeSlots resident workgroups (256 CUs x 2), since a second round would
+// be latency-bound; launches with kDecodeSlots units or more are not split.
 constexpr int kDecodeSlots = 512;
 constexpr int kMaxPieces = 16;
-constexpr int kStateTiles = 4;      // state pass cost in 32-token window tiles
+constexpr int kStateTiles = 16;     // state pass cost in 32-token window tiles
 __host__ __device__ inline int decode_tiles_max(int32_t W) { return W > 0 ? (W + 31) / 32 + 1 : 0; }
 // floats of one partial record: per head m, l, dn, acc[d], nm[d]
 __host__ __device__ inline int64_t part_floats(int G, int d) { return int64_t(G) * (2 * d + 3); }
@@ -365,16 +365,36 @@ __device__ __forceinline__ float bload_f(brsrc_t r, uint32_t off) {
 // an older copy.  For data one workgroup writes and another, possibly on
 // another XCD, reads within the same kernel.
 constexpr int kSysCoherent = 1 | 16;
+// XCD-coherent access: loads with sc0 miss the vector L1 and are served by
+// the XCD's L2; plain stores write through the L1 into that L2.  For data
+// one workgroup writes and another on the same XCD reads within a kernel.
+constexpr int kL2Coherent = 1;
 __device__ __forceinline__ float bload_f_sys(brsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSysCoherent));
 }
 __device__ __forceinline__ void bstore_f_sys(brsrc_t r, uint32_t off, float x) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, off, 0, kSysCoherent);
 }
+__device__ __forceinline__ float bload_f_l2(brsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kL2Coherent));
+}
+__device__ __forceinline__ void bstore_f_l2(brsrc_t r, uint32_t off, float x) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, off, 0, 0);
+}
 __device__ __forceinline__ bf16_t bload_elem(brsrc_t r, uint32_t off, bf16_t) {
   return bf16_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
 }
 __device__ __forceinline__ float bload_elem(brsrc_t r, uint32_t off, float) { return bload_f(r, off); }
+// One element, raw, zero-extended into its own 32-bit register (bf16 bits
+// or fp32 bits), converted with raw_to_f32 where it is used.
+__device__ __forceinline__ uint32_t bload_raw(brsrc_t r, uint32_t off, bf16_t) {
+  return uint32_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+}
+__device__ __forceinline__ uint32_t bload_raw(brsrc_t r, uint32_t off, float) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+__device__ __forceinline__ float raw_to_f32(uint32_t x, bf16_t) { return __uint_as_float(x << 16); }
+__device__ __forceinline__ float raw_to_f32(uint32_t x, float) { return __uint_as_float(x); }
 // Fragment loads through a descriptor: 8 consecutive elements at byte offset off.
 __device__ __forceinline__ void bload_frag(Frag<bf16_t>& f, brsrc_t r, uint32_t off) { f.v = bload16(r, off); }
 __device__ __forceinline__ void bload_frag(Frag<float>& f, brsrc_t r, uint32_t off) {
@@ -484,10 +504,13 @@ struct DecodeArgs {
   int32_t n_layers;  // layers in this launch (<= kMaxLayersPerLaunch)
   int32_t form;      // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
   int32_t phi;       // feature map: 0 ReLU, 1 ELU + 1
-  int32_t pad;
+  // workgroups per piece row: B*Hkv, rounded up to a multiple of 8 when a
+  // window is split (the extra workgroups exit at once), so that every piece
+  // of a unit has the same workgroup index modulo 8 and runs on the same XCD
+  int32_t row_stride;
   LayerArg layers[kMaxLayersPerLaunch];  // sorted by decreasing W
   // layer (index into layers) of every piece row: workgroup w of the main
-  // pass belongs to layer piece_layer[w / (B*Hkv)].  The rows of every
+  // pass belongs to layer piece_layer[w / row_stride].  The rows of every
   // layer's piece 0 (the state pass, the longest chain) come first, so their
   // loads are issued, and served, first.
   uint8_t piece_layer[kMaxLayersPerLaunch * kMaxPieces];

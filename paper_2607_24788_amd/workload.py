@@ -96,6 +96,10 @@ def workload(name):
     if n in ("c4", "c4n", "prefill32k_geo"):
         return Workload("prefill_32L_b4_seq32k_geo16-2048", 32, 4, 32, 8, 128, 128, geo_windows(16, 2048, 32),
                         [32768] * 4, 0, torch.bfloat16, 3)
+    if n in ("c2r", "llama8b_b1_ctx8k_reversed"):
+        # the same windows falling with depth, the orientation the paper allocates in
+        return Workload("llama8b_32L_b1_ctx8k_geo2048-16", 32, 1, 32, 8, 128, 128,
+                        geo_windows(16, 2048, 32)[::-1], [8192], 256, torch.bfloat16, 1)
     if n in ("c2b", "llama8b_b1_ctx8k_blockwise"):
         # the paper's (0, w/2, w) allocation at its base window w = 1024
         return Workload("llama8b_32L_b1_ctx8k_blockwise_w1024_0-w/2-w", 32, 1, 32, 8, 128, 128,

@@ -77,20 +77,33 @@ def test_sharp_logits(dtype):
 
 
 def test_layer_subsets_match_full_call():
-    """Per-layer calls and one call over the stack give identical outputs."""
-    case = Case([3, 0, 40, 9], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=6)
-    q, k, v = case.tokens(30)
+    """Per-layer calls and one call over the stack agree: a call plans its own
+    window split, so the two differ only in rounding; both match the oracle,
+    and the rings and positions match bit for bit."""
+    case = Case([3, 0, 40, 9, 300], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=6)
+    n = 40
+    q, k, v = case.tokens(n)
     st_a, st_b = case.new_state(), case.new_state()
     phi = case.phi_w.cuda()
-    for t in range(30):
+    oa_all, ob_all = [], []
+    for t in range(n):
         qs, ks, vs = (x[:, :, t].contiguous().cuda() for x in (q, k, v))
         oa, ob = torch.empty_like(qs), torch.empty_like(qs)
         case.g.decode_step(st_a, phi, qs, ks, vs, oa, case.ws)
         for l in range(case.L):
             case.g.decode_step(st_b, phi[l:l + 1], qs[l:l + 1], ks[l:l + 1], vs[l:l + 1], ob[l:l + 1],
                                case.ws, layer0=l, n_layers=1)
-        assert torch.equal(oa, ob), f"step {t}"
-    assert torch.equal(st_a, st_b)
+        oa_all.append(oa)
+        ob_all.append(ob)
+    torch.cuda.synchronize()
+    oa_all, ob_all = (torch.stack(x, 2).cpu() for x in (oa_all, ob_all))
+    case.check_decode(oa_all, q, k, v, [0] * case.B, n, "stack call")
+    case.check_decode(ob_all, q, k, v, [0] * case.B, n, "per-layer calls")
+    for l in range(case.L):
+        va, vb = case.g.layer_views(st_a, l), case.g.layer_views(st_b, l)
+        for key in ("pos", "nf", "kring_raw", "vring_raw"):
+            assert torch.equal(va[key], vb[key]), f"layer {l} {key}"
+    case.check_state(st_b, k, v, [n] * case.B, "per-layer calls")
 
 
 def test_checkpoint_restore_is_bit_identical():
@@ -134,13 +147,13 @@ def test_deferred_folding_state_every_step():
 
 def test_split_and_unsplit_paths():
     """Few units: long windows are split over several workgroups and merged
-    (the decode workspace holds their partial records); 1024 units and more:
-    one workgroup per unit.  Both follow the definition from a ragged
-    prefilled state."""
+    (the decode workspace holds their partial records); 512 units per layer
+    and more: one workgroup per unit in any call, no decode workspace.  Both
+    follow the definition from a ragged prefilled state."""
     small = Case([0, 5, 40, 300], batch=1, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=9)
-    big = Case([0, 5, 40, 300], batch=32, Hq=16, Hkv=8, d=64, Df=64, dtype=torch.bfloat16, seed=10)
+    big = Case([0, 5, 40, 300], batch=64, Hq=16, Hkv=8, d=64, Df=64, dtype=torch.bfloat16, seed=10)
     assert small.g.workspace_bytes(0) > 256 and big.g.workspace_bytes(0) == 256
-    for case, lens in ((small, [333]), (big, [(37 * i) % 350 for i in range(32)])):
+    for case, lens in ((small, [333]), (big, [(37 * i) % 350 for i in range(64)])):
         n = 6
         q, k, v = case.tokens(max(lens) + n)
         st = case.new_state()
@@ -155,3 +168,37 @@ def test_split_and_unsplit_paths():
             outs.append(o)
         case.check_decode(torch.stack(outs, 2).cpu(), q, k, v, lens, n, f"B={case.B}")
         case.check_state(st, k, v, [x + n for x in lens], f"B={case.B}")
+
+
+@pytest.mark.parametrize("per_layer_call", [False, True])
+@pytest.mark.parametrize("batch,Hkv", [(1, 8), (2, 4), (1, 3)])
+def test_split_pieces_on_one_xcd(batch, Hkv, per_layer_call):
+    """Split windows at 8B-like shapes: a unit's pieces share a workgroup
+    index modulo 8 (rows of B*Hkv workgroups padded to a multiple of 8), and
+    their records meet in one L2.  Long windows, several pieces per unit,
+    whole-stack and per-layer calls, against the oracle."""
+    case = Case([0, 16, 300, 1100, 2100], batch=batch, Hq=4 * Hkv, Hkv=Hkv, d=128, Df=128,
+                dtype=torch.bfloat16, seed=11 + batch + Hkv)
+    pos = [2300 + 37 * b for b in range(batch)]
+    n = 10
+    q, k, v = case.tokens(max(pos) + n)
+    st = case.new_state()
+    case.load_state_from_oracle(st, q, k, v, pos)
+    phi = case.phi_w.cuda()
+    outs = []
+    for step in range(n):
+        sel = lambda x: torch.stack([x[:, b, pos[b] + step] for b in range(batch)], 1).contiguous().cuda()
+        qs, ks, vs = sel(q), sel(k), sel(v)
+        o = torch.empty_like(qs)
+        if per_layer_call:
+            for l in range(case.L):
+                case.g.decode_step(st, phi[l:l + 1], qs[l:l + 1], ks[l:l + 1], vs[l:l + 1], o[l:l + 1], case.ws,
+                                   layer0=l, n_layers=1)
+        else:
+            case.g.decode_step(st, phi, qs, ks, vs, o, case.ws)
+        outs.append(o)
+    out = torch.stack(outs, 2).cpu()
+    case.check_decode(out, q, k, v, pos, n, f"B={batch} Hkv={Hkv}")
+    case.check_state(st, k, v, [p + n for p in pos], f"B={batch} Hkv={Hkv}")
+    for l in range(case.L):
+        assert int(case.g.layer_views(st, l)["cnt"].abs().max()) == 0, f"layer {l}: split counts not reset"
