@@ -76,9 +76,11 @@ template <typename T, int D, int DF>
 __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& L, int rem, int64_t p) {
   constexpr int EPT = 4;                   // output elements per thread whose loads go first
   static_assert(kMaxPieces * kMaxG <= kThreads, "one (piece, head) scalar pair per thread");
-  __shared__ float pw[kThreads];  // [piece][G]: m, then its weight e^(m - M)
-  __shared__ float pl[kThreads];  // [piece][G]: l
-  __shared__ float hs[kMaxG][3];            // per head: window weight, linear weight, 1 / denominator
+  __shared__ float pw[kThreads];  // [piece][G]: m
+  __shared__ float pe[kThreads];  // [piece][G]: the piece's weight e^(m - M)
+  __shared__ float pl[kThreads];  // [piece][G]: l e^(m - M)
+  __shared__ float pd[kMaxG];     // per head: the linear denominator
+  __shared__ float pm[kMaxG];     // per head: M, the max over the pieces
   const int G = a.G, B = a.B, Hkv = a.Hkv, Hq = a.Hq;
   const int per_layer = B * Hkv;
   const int np = L.npiece;
@@ -120,55 +122,59 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
   }
   // every thread writes its slot (kThreads slots; no branch, so the loads
   // above are not sunk behind the record loads)
-  pw[tid] = m0 + m1;  // at most one of the two is not an OOB zero
-  pl[tid] = l0 + l1;
+  const float mm = m0 + m1, ll = l0 + l1;  // at most one of each pair is not an OOB zero
+  pw[tid] = mm;
+  if (tid < kMaxG) pd[tid] = dnv;
   __syncthreads();
-  if (tid < G) {
+  // the weight of each (piece, head), one thread each
+  if (mok) {
     float M = -INFINITY;
-    for (int pc = 0; pc < np; ++pc) M = fmaxf(M, pw[pc * G + tid]);
-    float Ls = 0.f;
-    for (int pc = 0; pc < np; ++pc) {
-      const float e = pw[pc * G + tid] == -INFINITY ? 0.f : exp2f(pw[pc * G + tid] - M);
-      pw[pc * G + tid] = e;
-      Ls = fmaf(pl[pc * G + tid], e, Ls);
+#pragma unroll
+    for (int pc = 0; pc < kMaxPieces; ++pc)
+      if (pc < np) M = fmaxf(M, pw[pc * G + mh]);
+    const float w = mm == -INFINITY ? 0.f : exp2f(mm - M);
+    pe[tid] = w;
+    pl[tid] = ll * w;
+    if (mpc == 0) pm[mh] = M;
+  }
+  __syncthreads();
+  auto out_elem = [&](int i, const float (&vp)[kMaxPieces], float nm) {
+    const int hh = i / D;
+    const float M = pm[hh];
+    float Ls = 0.f, Ac = 0.f;
+#pragma unroll
+    for (int pc = 0; pc < kMaxPieces; ++pc) {
+      if (pc < np) {
+        Ls += pl[pc * G + hh];
+        Ac = fmaf(vp[pc], pe[pc * G + hh], Ac);
+      }
     }
-    const float dn = dnv;
+    const float dn = pd[hh];
+    float o;
     if (a.form != 0) {  // hybrid forms: each part over its own denominator
-      hs[tid][0] = 1.f / Ls;
-      hs[tid][1] = dn > 0.f ? 1.f / dn : 0.f;
-      hs[tid][2] = 1.f;
+      o = Ac / Ls + (dn > 0.f ? nm / dn : 0.f);
     } else if (dn > 0.f) {
       const float c2 = fmaxf(M, log2f(dn));
       const float ws = exp2f(M - c2), wlin = exp2f(-c2);
-      hs[tid][0] = ws;
-      hs[tid][1] = wlin;
-      hs[tid][2] = 1.f / (Ls * ws + dn * wlin);
+      o = (Ac * ws + nm * wlin) / (Ls * ws + dn * wlin);
     } else {
-      hs[tid][0] = 1.f;
-      hs[tid][1] = 0.f;
-      hs[tid][2] = 1.f / Ls;
+      o = Ac / Ls;
     }
-  }
-  __syncthreads();
+    og[i] = from_f32<T>(o);
+  };
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     const int i = tid + e * kThreads;
-    if (i < n) {
-      const int hh = i / D;
-      float Ac = 0.f;
-#pragma unroll
-      for (int pc = 0; pc < kMaxPieces; ++pc) Ac = pc < np ? fmaf(v[e][pc], pw[pc * G + hh], Ac) : Ac;
-      const float nm = hs[hh][1] == 0.f ? 0.f : nmv[e];
-      og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
-    }
+    if (i < n) out_elem(i, v[e], nmv[e]);
   }
   for (int i = tid + EPT * kThreads; i < n; i += kThreads) {  // G * D > EPT * 256 (large G)
     const int hh = i / D, c = i - hh * D;
     const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
-    float Ac = bload_f_l2(r0, o) * pw[hh];
-    for (int pc = 1; pc < np; ++pc) Ac = fmaf(bload_f_l2(r1, (pc - 1) * rs + o), pw[pc * G + hh], Ac);
-    const float nm = hs[hh][1] == 0.f ? 0.f : bload_f_l2(r0, o + D * 4);
-    og[i] = from_f32<T>((Ac * hs[hh][0] + nm * hs[hh][1]) * hs[hh][2]);
+    float vp[kMaxPieces];
+    vp[0] = bload_f_l2(r0, o);
+#pragma unroll
+    for (int pc = 1; pc < kMaxPieces; ++pc) vp[pc] = bload_f_l2(r1, pc < np ? (pc - 1) * rs + o : kOOB);
+    out_elem(i, vp, bload_f_l2(r0, o + D * 4));
   }
   if (tid == 0) *pos_ptr = p + 1;
 }
@@ -237,7 +243,8 @@ void decode_kernel(DecodeArgs a) {
   float* kpl = pvl + kFoldPeriod * D;      // [D]           the new key
   float* vpl = kpl + D;                    // [D]           the new value
   float* spl = vpl + D;                    // [kMaxG]       the new token's score (log2 units)
-  float* lnum = spl + kMaxG;               // [waves][RPS][G][D] linear numerator partials phi(q).S
+  float* pa = spl + kMaxG;                 // [kMaxG][kFoldPeriod] phi(q_h).phi(k_j) of pending j
+  float* lnum = pa + kMaxG * kFoldPeriod;               // [waves][RPS][G][D] linear numerator partials phi(q).S
   float* lden = lnum + kWaves * RPS * G * D;  // [waves][G]    linear denominator partials phi(q).z
   float* wacc = lden + kWaves * G;         // [waves][G][D] window partials sum e^s v
   float* wm = wacc + kWaves * G * D;       // [waves][G]    window running max (log2 units)
@@ -462,20 +469,20 @@ void decode_kernel(DecodeArgs a) {
     if (lane < G) spl[lane] = d * sc2;
   }
 
-  // ---- 4. state: the pending tokens are added to this wave's S rows in
-  //         registers (S' = S + sum_j phi(k_j)^T v_j, z' likewise), the
-  //         read-out phi(q_h).S', phi(q_h).z' is taken from them, and on a
-  //         fold step S', z' are written back (rows no pending token touches
-  //         are unchanged and skipped).  Per-wave partials are summed in the
-  //         merge.
-  if (lin) {
-    // S, z are zero until the first fold (their memory is not read as such)
-    if (!s_nonzero) {
-#pragma unroll
-      for (int s = 0; s < STEPS; ++s) sr[s] = make_float4(0.f, 0.f, 0.f, 0.f);
-      zf = 0.f;
-    }
-    const float* pk = ph + G * DF;
+  // ---- 4. state.  The read-out of the pending tokens [nf, beta) needs no
+  //         update of S: phi(q_h).S' = phi(q_h).S + sum_j a_hj v_j with
+  //         a_hj = phi(q_h).phi(k_j) (z' likewise), so each wave reads out
+  //         its S rows as loaded and the a_hj enter in the merge.  On a fold
+  //         step the pending tokens are first added to the S rows, in
+  //         registers, S', z' are written back (rows no pending token touches
+  //         are unchanged and skipped), and the read-out is taken from S'.
+  //         (Folding after this step's results are out, with the rows read
+  //         again, made the B=1 step slower: the extra reads land at the end
+  //         of the launch.)
+  const bool early = fold;  // fold before the read-out
+  const float* pk = ph + G * DF;
+  // S' = S + sum_j phi(k_j)^T v_j on the wave's rows (and z'), written back
+  auto fold_rows = [&](float4 (&rows)[STEPS], float& zrow) {
     uint32_t touched = 0;
     float dz = 0.f;
     for (int i = 0; i < npend; ++i) {
@@ -484,21 +491,28 @@ void decode_kernel(DecodeArgs a) {
       for (int s = 0; s < STEPS; ++s) {
         const float w = pk[i * DF + f0 + s * RPS + lr];
         touched |= uint32_t(w != 0.f) << s;
-        sr[s].x = fmaf(w, vv.x, sr[s].x);
-        sr[s].y = fmaf(w, vv.y, sr[s].y);
-        sr[s].z = fmaf(w, vv.z, sr[s].z);
-        sr[s].w = fmaf(w, vv.w, sr[s].w);
+        rows[s].x = fmaf(w, vv.x, rows[s].x);
+        rows[s].y = fmaf(w, vv.y, rows[s].y);
+        rows[s].z = fmaf(w, vv.z, rows[s].z);
+        rows[s].w = fmaf(w, vv.w, rows[s].w);
       }
       if (lane < RW) dz += pk[i * DF + f0 + lane];
     }
-    zf += dz;
-    if (fold) {
-      // On the first fold every row is written, whatever the memory held.
+    zrow += dz;
+    // On the first fold every row is written, whatever the memory held.
 #pragma unroll
-      for (int s = 0; s < STEPS; ++s)
-        if (!s_nonzero || ((touched >> s) & 1u)) store_nt(S + (f0 + s * RPS + lr) * D + c4, sr[s]);
-      if (lane < RW && (dz != 0.f || !s_nonzero)) z[f0 + lane] = zf;
+    for (int s = 0; s < STEPS; ++s)
+      if (!s_nonzero || ((touched >> s) & 1u)) store_nt(S + (f0 + s * RPS + lr) * D + c4, rows[s]);
+    if (lane < RW && (dz != 0.f || !s_nonzero)) z[f0 + lane] = zrow;
+  };
+  if (lin) {
+    // S, z are zero until the first fold (their memory is not read as such)
+    if (!s_nonzero) {
+#pragma unroll
+      for (int s = 0; s < STEPS; ++s) sr[s] = make_float4(0.f, 0.f, 0.f, 0.f);
+      zf = 0.f;
     }
+    if (early) fold_rows(sr, zf);
     for (int hh = 0; hh < G; ++hh) {
       const float* pq = ph + hh * DF;
       float4 n4 = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -516,6 +530,23 @@ void decode_kernel(DecodeArgs a) {
       *reinterpret_cast<float4*>(lnum + ((wave * RPS + lr) * G + hh) * D + c4) = n4;
       const float dp = dpp_sum_rows<RW>(lane < RW ? pq[f0 + lane] * zf : 0.f);
       if (lane == (RW > 16 ? 16 : 0)) lden[wave * G + hh] = dp;
+    }
+    if (!early && npend > 0) {
+      // a_hj = phi(q_h).phi(k_j): 16 lanes (one DPP row) per head, DF / 16
+      // features each
+      constexpr int FPL = DF / 16;
+      const int hh = tid >> 4, sub = tid & 15;
+      const bool hv = hh < G;
+      float qf[FPL];
+#pragma unroll
+      for (int j = 0; j < FPL; ++j) qf[j] = hv ? ph[hh * DF + sub * FPL + j] : 0.f;
+      for (int i = 0; i < npend; ++i) {
+        float d = 0.f;
+#pragma unroll
+        for (int j = 0; j < FPL; ++j) d = fmaf(qf[j], pk[i * DF + sub * FPL + j], d);
+        d = dpp_sum_rows<16>(d);
+        if (hv && sub == 0) pa[hh * kFoldPeriod + i] = d;
+      }
     }
   }
 
@@ -627,6 +658,13 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
         for (int r = 0; r < RPS; ++r) nm += lnum[((w * RPS + r) * G + hh) * D + c];
         dn += lden[w * G + hh];
+      }
+      if (!early) {  // the pending tokens: sum_j a_hj v_j, sum_j a_hj
+        for (int j = 0; j < npend; ++j) {
+          const float aj = pa[hh * kFoldPeriod + j];
+          nm = fmaf(aj, pvl[j * D + c], nm);
+          dn += aj;
+        }
       }
     }
     float M = -INFINITY, Ls = 0.f, Ac = 0.f;
@@ -785,9 +823,9 @@ hipError_t flush_t(const DecodeArgs& a, hipStream_t stream) {
 template <typename T, int D, int DF>
 hipError_t launch_t(const DecodeArgs& a, int total_wg, hipStream_t stream) {
   const int G = a.G;
-  // ph, pvl, kpl, vpl, spl; then lnum .. wl, or the staged Wf columns that
+  // ph, pvl, kpl, vpl, spl, pa; then lnum .. wl, or the staged Wf columns that
   // share their memory (bf16: kWaves x D rows of RW + 2 elements)
-  const size_t head = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D + 2 * D + kMaxG;
+  const size_t head = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D + 2 * D + kMaxG + kMaxG * kFoldPeriod;
   constexpr int RPS = 256 / D;  // state rows per wave step (lanes per row: D / 4)
   const size_t tail = size_t(kWaves) * RPS * G * D + kWaves * G + size_t(kWaves) * G * D + kWaves * G + kWaves * G;
   const size_t staged = sizeof(T) == 2 ? size_t(kWaves) * D * (DF / kWaves + 2) / 2 : 0;

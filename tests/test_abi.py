@@ -186,10 +186,13 @@ def test_decode_argument_errors():
     assert _decode(g, ptrs=(4096, None, 4096, 4096, 4096)) == -1
     assert _decode(g, ptrs=(4096, 4096, 4096 + 2, 4096, 4096)) == -4   # q misaligned
     assert _decode(g, ptrs=(4096, 4096, 4096, 4096, 4104)) == -4       # out misaligned
-    # few units: the window split needs the workspace for its partial records
-    assert _decode(g, ws=None) == -1
-    assert _decode(g, ws=(1 << 20) + 16) == -4
-    assert _decode(g, ws_bytes=g.workspace_bytes(0) - 1) == -5
+    # few units and a long window: the window split needs the workspace for
+    # its partial records (checked before anything is launched)
+    gs = mk(windows=[0, 5, 300])
+    assert gs.workspace_bytes(0) > 256
+    assert _decode(gs, ws=None) == -1
+    assert _decode(gs, ws=(1 << 20) + 16) == -4
+    assert _decode(gs, ws_bytes=gs.workspace_bytes(0) - 1) == -5
 
 
 
@@ -211,8 +214,9 @@ def test_flush_argument_errors():
 
 
 def test_workspace_sizes():
-    # 12 units: split windows, one partial record (G x (2d + 3) floats) per workgroup
-    g = mk(n_layers=3, batch=2, n_q_heads=8, n_kv_heads=2, feat_dim=64)
+    # 12 units, one long window: split windows, one partial record
+    # (G x (2d + 3) floats) per workgroup
+    g = mk(n_layers=3, batch=2, n_q_heads=8, n_kv_heads=2, feat_dim=64, windows=[0, 5, 300])
     rec = 4 * (2 * 128 + 3) * 4
     assert g.workspace_bytes(0) >= 3 * 2 * 2 * rec
     assert g.workspace_bytes(0) <= 3 * 2 * 2 * 16 * rec + 256
