@@ -69,7 +69,7 @@ class Oracle:
     the merge form (0: GLIDE's shared denominator; 1, 2: the Appendix's two
     hybrid forms, separately normalised outputs added, with the state over
     the evicted tokens (1) or over every token (2)), and the feature map
-    (phi 0: ReLU(x Wf); 1: ELU(x Wf) + 1)."""
+    (phi 0: ReLU(x Wf); 1: ELU(x Wf) + 1; 2: softmax(x Wf) over the features)."""
 
     def __init__(self, n_q_heads, n_kv_heads, head_dim, feat_dim, window, linear=True,
                  tau=None, lib=None, form=0, phi=0):

@@ -20,7 +20,9 @@
  *     phi(x)_f  = max(0, sum_c x_c Wf[c][f])        (ReLU feature map; or, with
  *                 oracle_layer.phi = 1, ELU+1: y + 1 for y > 0, e^y otherwise,
  *                 y = sum_c x_c Wf[c][f]; both from the Appendix's list of
- *                 feature maps)
+ *                 feature maps; or, with oracle_layer.phi = 2, the softmax
+ *                 feature map Sec. III-B names as its default choice:
+ *                 e^{y_f} / sum_f' e^{y_f'}, over the Df projected features)
  *     a_j       = phi(q_t) . phi(k_j)               for j in L
  *     A = sum_{j in L} a_j v_j ,  a = sum_{j in L} a_j
  *     s_j = tau * q_t . k_j                          for j in X
@@ -72,7 +74,7 @@ typedef struct {
   int32_t window;      /* W >= 0 */
   int32_t linear;      /* 1: linear part on (GLIDE), 0: pure sliding window */
   int32_t form;        /* 0: shared denominator; 1, 2: the Appendix hybrid forms */
-  int32_t phi;         /* 0: ReLU(x Wf); 1: ELU(x Wf) + 1 */
+  int32_t phi;         /* 0: ReLU(x Wf); 1: ELU(x Wf) + 1; 2: softmax(x Wf) */
   double  tau;         /* softmax scale */
 } oracle_layer;
 
@@ -89,13 +91,34 @@ static int valid(const oracle_layer* L) {
   if (L->window == 0 && !L->linear) return 0;   /* empty attention set */
   if (L->form < 0 || L->form > 2) return 0;
   if (L->form != 0 && !L->linear) return 0;     /* the forms differ only in the linear part */
-  if (L->phi < 0 || L->phi > 1) return 0;
+  if (L->phi < 0 || L->phi > 2) return 0;
   return 1;
 }
 
-/* phi(x)_f = max(0, y_f) (kind 0) or ELU(y_f) + 1 (kind 1), y_f = sum_c x_c Wf[c][f];
- * Wf is d x Df, row-major. */
+/* phi(x)_f = max(0, y_f) (kind 0), ELU(y_f) + 1 (kind 1), or e^{y_f} / sum_f' e^{y_f'}
+ * (kind 2), y_f = sum_c x_c Wf[c][f]; Wf is d x Df, row-major. */
 static void phi_row(int kind, int d, int Df, const double* Wf, const double* x, double* out) {
+  if (kind == 2) {
+    /* softmax over the projected features, with the row maximum subtracted
+       (which leaves the value unchanged) */
+    double ymax = -INFINITY;
+    for (int f = 0; f < Df; ++f) {
+      double acc = 0.0;
+      for (int c = 0; c < d; ++c) acc += x[c] * Wf[(size_t)c * Df + f];
+      out[f] = acc;
+      if (acc > ymax) ymax = acc;
+    }
+    double sum = 0.0;
+    for (int f = 0; f < Df; ++f) {
+      out[f] = exp(out[f] - ymax);
+      sum += out[f];
+    }
+#if ORACLE_MUTANT == 12
+    sum = 1.0;                                    /* mutant: exponentials not normalised */
+#endif
+    for (int f = 0; f < Df; ++f) out[f] /= sum;
+    return;
+  }
   for (int f = 0; f < Df; ++f) {
     double acc = 0.0;
     for (int c = 0; c < d; ++c) {

@@ -64,6 +64,9 @@ def _sdpa(q, k, v, tau, mask):
 
 
 def _feat(y, phi):
+    if phi == 2:  # softmax over the features (numpy's own exp and sum)
+        e = np.exp(y - y.max(axis=-1, keepdims=True))
+        return e / e.sum(axis=-1, keepdims=True)
     return np.maximum(y, 0.0) if phi == 0 else np.where(y > 0, y + 1.0, np.exp(np.minimum(y, 0.0)))
 
 
@@ -156,6 +159,11 @@ def pin_w0_is_causal_linear(lib):
     got = oracle.Oracle(Hq, Hkv, d, Df, 0, linear=True, lib=lib, phi=1).attend(Wf, q, k, v)
     if not np.allclose(got, num / den[..., None], rtol=1e-10, atol=1e-12):
         return f"W=0 ELU+1 != causal linear attention (max err {np.abs(got - num / den[..., None]).max()})"
+    # the softmax feature map (positive features: every denominator is positive)
+    num, den = _causal_linear(q, k, v, Wf, phi=2)
+    got = oracle.Oracle(Hq, Hkv, d, Df, 0, linear=True, lib=lib, phi=2).attend(Wf, q, k, v)
+    if not np.allclose(got, num / den[..., None], rtol=1e-10, atol=1e-12):
+        return f"W=0 softmax phi != causal linear attention (max err {np.abs(got - num / den[..., None]).max()})"
     return None
 
 
@@ -368,11 +376,63 @@ def pin_hybrid_v_ones(lib):
     return None
 
 
+def pin_softmax_worked_example(lib):
+    """The softmax feature map on a hand-derived example (golden fixture)."""
+    ex = json.load(open(GOLDEN))["softmax"]
+    s = ex["setup"]
+    q = np.array(s["q"]).reshape(3, 1, 1)
+    k = np.array(s["k"]).reshape(3, 1, 1)
+    v = np.array(s["v"]).reshape(3, 1, 1)
+    Wf = np.array(s["Wf"])
+    for case in ex["cases"]:
+        o = oracle.Oracle(1, 1, 1, 2, case["window"], linear=True, tau=s["tau"], lib=lib, phi=2)
+        got = o.attend(Wf, q, k, v).ravel()
+        want = np.array([_eval_closed_form(x) for x in case["out"]])
+        if not np.allclose(got, want, rtol=1e-12, atol=1e-12):
+            return f"softmax worked example W={case['window']}: {got} != {want}"
+        S, z = o.state(Wf, k, v)
+        wS = np.array([_eval_closed_form(x) for x in case["S"]])
+        wz = np.array([_eval_closed_form(x) for x in case["z"]])
+        if not (np.allclose(S.ravel(), wS, rtol=1e-12, atol=1e-12) and np.allclose(z.ravel(), wz, rtol=1e-12, atol=1e-12)):
+            return f"softmax worked example state W={case['window']}: S={S.ravel()} z={z.ravel()}"
+    return None
+
+
+def pin_softmax_features(lib):
+    """Softmax features: positive, summing to one per row, unchanged when the
+    same amount is added to every projected feature; with Wf = 0 they are
+    uniform (1/Df), so at tau = 0 every token weighs e^0 = 1 in the window and
+    1/Df in the linear part: O_t = (sum_win v + sum_lin v / Df) / (n_win + n_lin / Df)."""
+    n, Hq, Hkv, d, Df = 23, 4, 2, 6, 9
+    q, k, v, Wf = _rand_case(11, n, Hq, Hkv, d, Df, scale=2.0)
+    o = oracle.Oracle(Hq, Hkv, d, Df, 5, linear=True, lib=lib, phi=2)
+    f = o.phi(Wf, q)
+    if not (np.all(f > 0) and np.allclose(f.sum(-1), 1.0, rtol=0, atol=1e-13)):
+        return "softmax features are not a distribution over the features"
+    u = np.random.default_rng(12).standard_normal(d)
+    f2 = o.phi(Wf + u[:, None], q)   # adds q.u to every projected feature
+    if not np.allclose(f, f2, rtol=1e-11, atol=1e-14):
+        return "softmax features change under a common shift of the projection"
+    Z = np.zeros((d, Df))
+    for W in (0, 1, 4, 30):
+        got = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, tau=0.0, lib=lib, phi=2).attend(Z, q, k, v)
+        G = Hq // Hkv
+        want = np.zeros_like(got)
+        for t in range(n):
+            b = max(0, t + 1 - W)
+            vs = np.repeat(v, G, axis=1)
+            want[t] = (vs[b:t + 1].sum(0) + vs[:b].sum(0) / Df) / ((t + 1 - b) + b / Df)
+        if not np.allclose(got, want, rtol=1e-11, atol=1e-13):
+            return f"uniform softmax features, W={W}: max err {np.abs(got - want).max()}"
+    return None
+
+
 ALL_PINS = [pin_worked_example, pin_full_window_is_causal_softmax, pin_band_is_masked_sdpa,
             pin_w0_is_causal_linear, pin_w1_closed_form, pin_recurrent_equals_definition,
             pin_state_direct_sums, pin_v_ones, pin_convex_hull, pin_linearity,
             pin_gqa_is_repeated_mha, pin_zero_over_zero, pin_continue_from_state,
-            pin_hybrid_forms_are_band_plus_linear, pin_hybrid_v_ones]
+            pin_hybrid_forms_are_band_plus_linear, pin_hybrid_v_ones, pin_softmax_worked_example,
+            pin_softmax_features]
 
 
 def run_all(lib):

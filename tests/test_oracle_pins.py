@@ -30,7 +30,8 @@ def test_pin(pin):
 #  9 hybrid form 2's decode folds the evicted token, not the new one
 # 10 hybrid forms divide the linear term by both denominators
 # 11 the ELU+1 feature map without the + 1
-MUTANTS = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11]
+# 12 the softmax feature map without its normalisation
+MUTANTS = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12]
 
 
 @pytest.mark.parametrize("mutant", MUTANTS)
