@@ -66,6 +66,8 @@ def main():
     ap.add_argument("--form", type=int, default=0, choices=(0, 1, 2),
                     help="merge: 0 GLIDE's shared denominator (default); 1, 2 the Appendix's two hybrid "
                          "forms (separately normalised sum; state over the evicted tokens / every token)")
+    ap.add_argument("--phi", type=int, default=0, choices=(0, 1, 2),
+                    help="feature map: 0 ReLU (default), 1 ELU + 1, 2 softmax over the features")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-detail", action="store_true",
@@ -92,7 +94,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     g = glide.Glide(wl.n_layers, wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.feat_dim, wl.windows,
-                    dtype=wl.dtype, sm_scale=wl.tau, form=args.form)
+                    dtype=wl.dtype, sm_scale=wl.tau, form=args.form, phi=args.phi)
     lens = list(wl.context)
     cu = [0]
     for n in lens:
@@ -155,7 +157,7 @@ def main():
     dec_step_s = dec_ms * 1e-3 / max(wl.decode_steps, 1)
     pre_flops = prefill_flops(wl, lens)
     mfma_peak = MFMA_BF16_PEAK if wl.dtype == torch.bfloat16 else MFMA_FP32_PEAK
-    traffic = measured_traffic(wl.name) if args.form == 0 else None
+    traffic = measured_traffic(wl.name) if args.form == 0 and args.phi == 0 else None
     hbm = {"bound": "hbm", "kernel": "decode step (decode_kernel; split windows merged by their last piece)",
            "achieved": dec_bytes / dec_step_s / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
            "frac": dec_bytes / dec_step_s / HBM_PEAK,
@@ -183,7 +185,7 @@ def main():
         "dtype": {torch.bfloat16: "bf16", torch.float32: "fp32"}[wl.dtype],
         "data": "synthetic (seeded N(0,1)/sqrt(d) q,k,v; Wf ~ N(0,1/d))"
                 + ("; prefill inputs of one layer reused by every layer" if share_prefill else ""),
-        "config": dict(wl.describe(), chunk=wl.chunk, **({"form": args.form} if args.form else {})),
+        "config": dict(wl.describe(), chunk=wl.chunk, **({"form": args.form} if args.form else {}), **({"phi": args.phi} if args.phi else {})),
         "decode_tokens_per_s": round(dec_tok_s, 2),
         "decode_us_per_step": round(dec_step_s * 1e6, 2),
         "decode_hbm_frac": round(hbm["frac"], 4),
@@ -197,7 +199,7 @@ def main():
     if not args.no_detail and wl.decode_steps:
         line["decode_detail"] = decode_detail(g, wl, state, phi, dq, dk, dv, dout, ws, prefill, stream)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, g, state, phi, dq, dk, dv, args.cpu_baseline_seconds, args.form)
+        line["cpu_baseline"] = cpu_baseline(wl, g, state, phi, dq, dk, dv, args.cpu_baseline_seconds, args.form, args.phi)
     print(json.dumps(line), flush=True)
 
 
@@ -307,7 +309,7 @@ def copy_probe(mib):
     print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "copies": 5}), flush=True)
 
 
-def cpu_baseline(wl, g, state, phi, dq, dk, dv, budget_s, form=0):
+def cpu_baseline(wl, g, state, phi, dq, dk, dv, budget_s, form=0, fmap=0):
     """The CPU oracle (plain C, float64, OpenMP over (sequence, KV head)) on a
     bounded sample: full-stack decode steps starting from the GPU's state after
     the last timed step, repeated until `budget_s` of CPU time."""
@@ -339,7 +341,7 @@ def cpu_baseline(wl, g, state, phi, dq, dk, dv, budget_s, form=0):
                 wv[b, :, :n] = vl[b][:, idx]
         st["wk"], st["wv"] = wk, wv
         states.append(st)
-    oras = [oracle.Oracle(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.feat_dim, W, tau=wl.tau, form=form)
+    oras = [oracle.Oracle(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.feat_dim, W, tau=wl.tau, form=form, phi=fmap)
             for W in wl.windows]
     wf = [phi[l].double().cpu().numpy() for l in range(wl.n_layers)]
     q = dq[0].double().cpu().numpy()

@@ -59,9 +59,11 @@ enum { GLIDE_F32 = 0, GLIDE_BF16 = 1 };
 /* Feature map on y = x . Wf (Wf is non-learnable, one d x Df matrix per
  * layer shared by every head, applied to queries and keys alike), from the
  * Appendix's feature-map list:
- *   GLIDE_PHI_RELU  phi = max(0, y)
- *   GLIDE_PHI_ELU1  phi = ELU(y) + 1 = y + 1 for y > 0, e^y otherwise (never 0) */
-enum { GLIDE_PHI_RELU = 0, GLIDE_PHI_ELU1 = 1 };
+ *   GLIDE_PHI_RELU     phi = max(0, y)
+ *   GLIDE_PHI_ELU1     phi = ELU(y) + 1 = y + 1 for y > 0, e^y otherwise (never 0)
+ *   GLIDE_PHI_SOFTMAX  phi = softmax(y) over the Df features, e^{y_f} / sum e^{y_f'}
+ *                      (the default kernel choice of Sec. III-B; positive, sums to 1) */
+enum { GLIDE_PHI_RELU = 0, GLIDE_PHI_ELU1 = 1, GLIDE_PHI_SOFTMAX = 2 };
 
 /* flags: GLIDE_NO_LINEAR turns the linear part off (plain sliding-window
  * softmax attention, the "Hybrid" preset with nothing kept beyond the
@@ -89,7 +91,7 @@ typedef struct {
   int32_t head_dim;    /* d: 64 or 128 */
   int32_t feat_dim;    /* Df: 64 or 128 */
   int32_t dtype;       /* GLIDE_F32 or GLIDE_BF16 */
-  int32_t phi;         /* GLIDE_PHI_RELU or GLIDE_PHI_ELU1 */
+  int32_t phi;         /* GLIDE_PHI_RELU, GLIDE_PHI_ELU1 or GLIDE_PHI_SOFTMAX */
   int32_t flags;       /* 0, GLIDE_NO_LINEAR, GLIDE_HYBRID_SUM, or GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL */
   float sm_scale;      /* tau, the softmax scale (1/sqrt(d) in the Appendix's attention) */
   const int32_t* windows; /* HOST array [n_layers]: W_l = w - delta_l, 0 <= W_l <= 2^20 */

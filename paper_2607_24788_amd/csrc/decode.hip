@@ -35,24 +35,6 @@ __device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
   return make_float4(__shfl_xor(v.x, m), __shfl_xor(v.y, m), __shfl_xor(v.z, m), __shfl_xor(v.w, m));
 }
 
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ float dpp_mv(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROW_MASK, 0xf, false));
-}
-// Sum over lanes 0 .. N-1 (N = 16 or 32; other lanes may hold anything)
-// with DPP moves inside 16-lane rows: the result is in lane 0 (N = 16) or in
-// lanes 16 .. 31 (N = 32).
-template <int N>
-__device__ __forceinline__ float dpp_sum_rows(float v) {
-  static_assert(N == 16 || N == 32, "16 or 32 lanes");
-  v += dpp_mv<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
-  v += dpp_mv<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
-  v += dpp_mv<0x141, 0xf>(v);  // row_half_mirror
-  v += dpp_mv<0x140, 0xf>(v);  // row_mirror: every lane holds its row's sum
-  if constexpr (N == 32) v += dpp_mv<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
-  return v;
-}
-
 __device__ __forceinline__ int clamp_rel(int64_t x) { return int(x < -1 ? -1 : (x > 32 ? 32 : x)); }
 
 template <typename T, int D>
@@ -450,6 +432,10 @@ void decode_kernel(DecodeArgs a) {
     kpl[tid] = to_f32(kraw);
     vpl[tid] = to_f32(vraw);
   }
+  if (lin && a.phi == GLIDE_PHI_SOFTMAX) {  // the softmax map: normalise every row of ph
+    __syncthreads();
+    softmax_rows_lds<DF, kThreads>(ph, DF, G + npend);
+  }
   if (tid < kMaxG) spl[tid] = -INFINITY;
   __syncthreads();
 
@@ -792,6 +778,10 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(DecodeArgs a) {
     pk[i][f] = feat_act(acc, a.phi);
   }
   __syncthreads();
+  if (a.phi == GLIDE_PHI_SOFTMAX) {
+    softmax_rows_lds<DF, kThreads>(&pk[0][0], DF, n);
+    __syncthreads();
+  }
   const bool s_nonzero = nf > 0;
   for (int e = tid; e < DF * D / 4; e += kThreads) {
     const int f = e / (D / 4), c4 = (e - f * (D / 4)) * 4;

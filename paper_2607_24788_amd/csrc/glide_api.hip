@@ -24,7 +24,7 @@ glide_status check_cfg(const glide_config* c) {
   if (c->n_q_heads % c->n_kv_heads) return GLIDE_ERR_INVALID;
   if (c->head_dim < 1 || c->feat_dim < 1) return GLIDE_ERR_INVALID;
   if (c->dtype != GLIDE_F32 && c->dtype != GLIDE_BF16) return GLIDE_ERR_INVALID;
-  if (c->phi != GLIDE_PHI_RELU && c->phi != GLIDE_PHI_ELU1) return GLIDE_ERR_INVALID;
+  if (c->phi != GLIDE_PHI_RELU && c->phi != GLIDE_PHI_ELU1 && c->phi != GLIDE_PHI_SOFTMAX) return GLIDE_ERR_INVALID;
   if (c->flags & ~int32_t(GLIDE_NO_LINEAR | GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL)) return GLIDE_ERR_INVALID;
   // the hybrid forms change the linear part: not without one; the state over
   // every token comes only with the separately normalised sum

@@ -244,10 +244,76 @@ __device__ __forceinline__ f32x4_t mma(const Frag<float>& a, const Frag<float>& 
 
 __device__ __forceinline__ f32x4_t zero4() { return f32x4_t{0.f, 0.f, 0.f, 0.f}; }
 
-// The feature map's activation on y = x . Wf: ReLU (phi = 0), or ELU + 1
-// (phi = 1: y + 1 for y > 0, e^y otherwise; never zero).
+// The feature map's activation on y = x . Wf: ReLU (phi = 0), ELU + 1
+// (phi = 1: y + 1 for y > 0, e^y otherwise; never zero), or, for the softmax
+// map (phi = 2), y itself: the row is normalised afterwards by a pass over all
+// its features (softmax_rows_lds, or in registers where one wave holds them).
 __device__ __forceinline__ float feat_act(float y, int phi) {
-  return phi ? (y > 0.f ? y + 1.f : __builtin_amdgcn_exp2f(y * 1.4426950408889634f)) : fmaxf(y, 0.f);
+  return phi == GLIDE_PHI_ELU1   ? (y > 0.f ? y + 1.f : __builtin_amdgcn_exp2f(y * 1.4426950408889634f))
+         : phi == GLIDE_PHI_RELU ? fmaxf(y, 0.f)
+                                 : y;
+}
+
+// Cross-lane reductions with DPP moves inside 16-lane rows.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_mv(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROW_MASK, 0xf, false));
+}
+// Sum over lanes 0 .. N-1 of each 32-lane half (N = 16 or 32; other lanes may
+// hold anything): every lane of a row holds its row's sum (N = 16), or lanes
+// 16 .. 31 hold the 32-lane sum (N = 32).
+template <int N>
+__device__ __forceinline__ float dpp_sum_rows(float v) {
+  static_assert(N == 16 || N == 32, "16 or 32 lanes");
+  v += dpp_mv<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
+  v += dpp_mv<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
+  v += dpp_mv<0x141, 0xf>(v);  // row_half_mirror
+  v += dpp_mv<0x140, 0xf>(v);  // row_mirror: every lane holds its row's sum
+  if constexpr (N == 32) v += dpp_mv<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+  return v;
+}
+// Maximum over the 16 lanes of each row, in every lane of the row.
+__device__ __forceinline__ float dpp_max_row16(float v) {
+  v = fmaxf(v, dpp_mv<0xb1, 0xf>(v));
+  v = fmaxf(v, dpp_mv<0x4e, 0xf>(v));
+  v = fmaxf(v, dpp_mv<0x141, 0xf>(v));
+  v = fmaxf(v, dpp_mv<0x140, 0xf>(v));
+  return v;
+}
+
+// The softmax feature map's normalisation, in place, on rows [0, nrows) of an
+// fp32 LDS matrix (row r at base + r * stride, DF features): x <- e^(x - max)
+// / sum e^(x - max).  16 lanes (one DPP row) per row, DF / 16 features each;
+// every thread of the workgroup (NTH threads) calls it, between barriers.
+template <int DF, int NTH>
+__device__ __forceinline__ void softmax_rows_lds(float* base, int stride, int nrows) {
+  constexpr int FPL = DF / 16;
+  const int sub = int(threadIdx.x) & 15;
+  for (int r0 = 0; r0 < nrows; r0 += NTH / 16) {
+    const int r = r0 + int(threadIdx.x >> 4);
+    const bool ok = r < nrows;
+    float* row = base + (ok ? r : 0) * stride + sub * FPL;
+    float x[FPL];
+    float m = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < FPL; ++j) {
+      x[j] = ok ? row[j] : 0.f;
+      m = fmaxf(m, x[j]);
+    }
+    m = dpp_max_row16(m);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < FPL; ++j) {
+      x[j] = __builtin_amdgcn_exp2f((x[j] - m) * 1.4426950408889634f);
+      s += x[j];
+    }
+    s = dpp_sum_rows<16>(s);
+    const float inv = 1.f / s;
+    if (ok) {
+#pragma unroll
+      for (int j = 0; j < FPL; ++j) row[j] = x[j] * inv;
+    }
+  }
 }
 
 // Fragment of 8 consecutive ROWS of one column from a row-major LDS tile M

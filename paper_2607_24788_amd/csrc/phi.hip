@@ -1,12 +1,14 @@
-// Feature map phi(x) = max(0, x . Wf) (the ReLU kernel of the GLIDE
-// Appendix's feature-map list; Wf non-learnable, d x Df, one per layer), for
-// dense rows x[rows][d] (glide_feature_map and the prefill's q, k and history
-// rows).  The decode step computes its few rows inside its own kernel.
+// Feature map phi(x) = act(x . Wf) (ReLU, ELU + 1 or the softmax over the
+// features; Wf non-learnable, d x Df, one per layer), for dense rows
+// x[rows][d] (glide_feature_map).  The decode step and the prefill compute
+// their rows inside their own kernels.
 //
 // Persistent workgroups of 4 waves; wave w owns features [w*Df/4, (w+1)*Df/4)
 // and keeps their Wf B fragments in registers for the whole launch; the
 // workgroup walks 64-row tiles: A = 16 rows (k = head dim), B = Wf (k = head
-// dim, n = features), fp32 accumulation, ReLU on store.
+// dim, n = features), fp32 accumulation, the activation on store.  The
+// softmax map's rows are spread over the four waves: their raw values go to
+// LDS (dynamic, only for that map), each row is normalised there, then stored.
 #include "glide_internal.h"
 
 namespace glide {
@@ -47,12 +49,28 @@ __global__ __launch_bounds__(kThreads) void phi_rows_kernel(const T* __restrict_
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) acc[nt] = mma(fa[kk], wb[kk][nt], acc[nt]);
       }
+      if (phi == GLIDE_PHI_SOFTMAX) {  // uniform over the launch
+        extern __shared__ float yt[];   // [16][DF]
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t ro = r0 + 4 * lg + i;
-        if (ro < rows) {
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int nt = 0; nt < NTW; ++nt) out[ro * DF + f0 + 16 * nt + hq] = from_f32<OutT>(feat_act(acc[nt][i], phi));
+          for (int nt = 0; nt < NTW; ++nt) yt[(4 * lg + i) * DF + f0 + 16 * nt + hq] = acc[nt][i];
+        __syncthreads();
+        softmax_rows_lds<DF, kThreads>(yt, DF, 16);
+        __syncthreads();
+        for (int e = threadIdx.x; e < 16 * DF; e += kThreads) {
+          const int64_t ro = r0 + e / DF;
+          if (ro < rows) out[ro * DF + e % DF] = from_f32<OutT>(yt[e]);
+        }
+        __syncthreads();
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t ro = r0 + 4 * lg + i;
+          if (ro < rows) {
+#pragma unroll
+            for (int nt = 0; nt < NTW; ++nt) out[ro * DF + f0 + 16 * nt + hq] = from_f32<OutT>(feat_act(acc[nt][i], phi));
+          }
         }
       }
     }
@@ -64,7 +82,8 @@ hipError_t launch_rows_t(const void* Wf, const void* x, int64_t rows, void* out,
   if (rows == 0) return hipSuccess;
   const int64_t ntile = (rows + 63) / 64;
   const dim3 grid(unsigned(ntile < 1024 ? ntile : 1024));
-  hipLaunchKernelGGL((phi_rows_kernel<T, D, DF, OutT>), grid, dim3(kThreads), 0, s, static_cast<const T*>(Wf),
+  const size_t lds = phi == GLIDE_PHI_SOFTMAX ? size_t(16) * DF * sizeof(float) : 0;
+  hipLaunchKernelGGL((phi_rows_kernel<T, D, DF, OutT>), grid, dim3(kThreads), lds, s, static_cast<const T*>(Wf),
                      static_cast<const T*>(x), rows, static_cast<OutT*>(out), phi);
   return hipGetLastError();
 }

@@ -238,6 +238,66 @@ __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const
   constexpr int KS = D / 32, FT = DF / 16, PROW = row_t<DF>();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
   const int per = (NK / 16) * FT / nw;
+  if constexpr (PHI == GLIDE_PHI_SOFTMAX) {
+    // The softmax map needs each key row's max and sum over all DF features;
+    // the row's feature tiles are spread over WPK = FT / per waves (per <= 4
+    // tiles each, one key tile per wave).  Each wave reduces its part (its
+    // lanes, then the row's 4 lane groups), the parts meet in the 16 spare
+    // elements at the end of the row, two barriers apart.
+    constexpr int kPerMax = 4;
+    const int kt = (wave * per) / FT, ft0 = (wave * per) % FT, wk = ft0 / per, WPK = FT / per;
+    const int key = 16 * kt + hq;
+    f32x4_t acc[kPerMax];
+    float m = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kPerMax; ++u) {
+      acc[u] = zero4();
+      if (u < per) {
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          Frag<T> wb;
+          wf.col(wb, kk, 16 * (ft0 + u));
+          acc[u] = mma(wb, x[kk], acc[u]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m = fmaxf(m, acc[u][i]);
+      }
+    }
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    char* pad = reinterpret_cast<char*>(pk + key * PROW + DF);  // [0, 4): maxima, [4, 8): sums (floats)
+    if (lg == 0) __builtin_memcpy(pad + 4 * wk, &m, 4);
+    __syncthreads();
+    float M = -INFINITY;
+    for (int w = 0; w < WPK; ++w) {
+      float t;
+      __builtin_memcpy(&t, pad + 4 * w, 4);
+      M = fmaxf(M, t);
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < kPerMax; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[u][i] = u < per ? __builtin_amdgcn_exp2f((acc[u][i] - M) * 1.4426950408889634f) : 0.f;
+        sum += acc[u][i];
+      }
+    sum += __shfl_xor(sum, 16);
+    sum += __shfl_xor(sum, 32);
+    if (lg == 0) __builtin_memcpy(pad + 16 + 4 * wk, &sum, 4);
+    __syncthreads();
+    float tot = 0.f;
+    for (int w = 0; w < WPK; ++w) {
+      float t;
+      __builtin_memcpy(&t, pad + 16 + 4 * w, 4);
+      tot += t;
+    }
+    const bool is_key = key >= rlo && key < rhi;
+#pragma unroll
+    for (int u = 0; u < kPerMax; ++u)
+      if (u < per) store4(pk + key * PROW + 16 * (ft0 + u) + 4 * lg, is_key ? acc[u] : zero4(), 1.f / tot);
+    return;
+  }
   for (int u = 0; u < per; ++u) {
     const int tile = wave * per + u, kt = tile / FT, ft = tile - kt * FT;
     // transposed (Wf^T K^T): lane (hq, lg) gets features 16ft+4lg .. +3 of
@@ -795,6 +855,55 @@ void prefill_main(PrefillArgs a) {
       // 32kf+4lg+i and 32kf+16+4lg+i of its query row in fragment kf
       Frag<T> pqf[2][KSF];
       const auto wf = wf_cols();
+      // the softmax map: each query row's max and 1 / sum over its DF
+      // features, from a first pass (running max and rescaled sum per lane,
+      // then over the row's 4 lane groups)
+      float qmax[2] = {0.f, 0.f}, qinv[2] = {1.f, 1.f};
+      if constexpr (PHI == GLIDE_PHI_SOFTMAX) {
+        float m[2] = {-INFINITY, -INFINITY}, sm[2] = {0.f, 0.f};
+#pragma unroll
+        for (int kf = 0; kf < KSF; ++kf) {
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            f32x4_t ph[2] = {zero4(), zero4()};
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk) {
+              Frag<T> wa;
+              wf.col(wa, kk, 32 * kf + 16 * half);
+#pragma unroll
+              for (int qt = 0; qt < 2; ++qt) ph[qt] = mma(wa, qf[qt][kk], ph[qt]);
+            }
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) {
+              float y[4], mg = -INFINITY;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                y[i] = qscale[qt] < 0.f ? -ph[qt][i] : ph[qt][i];
+                mg = fmaxf(mg, y[i]);
+              }
+              const float mn = fmaxf(m[qt], mg);
+              float add = 0.f;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) add += __builtin_amdgcn_exp2f((y[i] - mn) * kLog2e);
+              sm[qt] = sm[qt] * __builtin_amdgcn_exp2f((m[qt] - mn) * kLog2e) + add;
+              m[qt] = mn;
+            }
+          }
+        }
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+#pragma unroll
+          for (int off = 16; off < 64; off <<= 1) {
+            const float mo = __shfl_xor(m[qt], off), so = __shfl_xor(sm[qt], off);
+            const float mn = fmaxf(m[qt], mo);
+            sm[qt] = sm[qt] * __builtin_amdgcn_exp2f((m[qt] - mn) * kLog2e) +
+                     so * __builtin_amdgcn_exp2f((mo - mn) * kLog2e);
+            m[qt] = mn;
+          }
+          qmax[qt] = m[qt];
+          qinv[qt] = 1.f / sm[qt];
+        }
+      }
 #pragma unroll
       for (int kf = 0; kf < KSF; ++kf) {
         float pv[2][8];
@@ -814,6 +923,10 @@ void prefill_main(PrefillArgs a) {
             for (int i = 0; i < 4; ++i) {
               if constexpr (PHI == 0)
                 pv[qt][4 * half + i] = fmaxf(ph[qt][i] * qscale[qt], 0.f);
+              else if constexpr (PHI == GLIDE_PHI_SOFTMAX)
+                pv[qt][4 * half + i] =
+                    __builtin_amdgcn_exp2f(((qscale[qt] < 0.f ? -ph[qt][i] : ph[qt][i]) - qmax[qt]) * kLog2e) *
+                    qinv[qt] * fabsf(qscale[qt]);
               else  // (qscale's sign undoes the band's query negation)
                 pv[qt][4 * half + i] = feat_act(qscale[qt] < 0.f ? -ph[qt][i] : ph[qt][i], PHI) * fabsf(qscale[qt]);
             }
@@ -1075,7 +1188,11 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
   for (int i = 0; i < a.nlayer; ++i) window = window || a.layers[i].W > 0;
   auto main = [&](int pass) {
     const dim3 grid(a.nseg, a.Hkv, nl), block(kMT);
-    if (a.phi) {
+    if (a.phi == GLIDE_PHI_SOFTMAX) {
+      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 0>), grid, block, 0, s, a);
+      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 1>), grid, block, 0, s, a);
+      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 2>), grid, block, 0, s, a);
+    } else if (a.phi) {
       if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 0>), grid, block, 0, s, a);
       if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 1>), grid, block, 0, s, a);
       if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 2>), grid, block, 0, s, a);
@@ -1087,7 +1204,9 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
   };
   if (a.nseg > 0) {
     if (a.linear) {
-      if (a.phi)
+      if (a.phi == GLIDE_PHI_SOFTMAX)
+        hipLaunchKernelGGL((prefill_segsum<T, D, DF, 2>), dim3(a.nseg, a.Hkv, nl), dim3(kSegThreads), 0, s, a);
+      else if (a.phi)
         hipLaunchKernelGGL((prefill_segsum<T, D, DF, 1>), dim3(a.nseg, a.Hkv, nl), dim3(kSegThreads), 0, s, a);
       else
         hipLaunchKernelGGL((prefill_segsum<T, D, DF, 0>), dim3(a.nseg, a.Hkv, nl), dim3(kSegThreads), 0, s, a);

@@ -17,6 +17,7 @@ F32 = 0
 BF16 = 1
 PHI_RELU = 0
 PHI_ELU1 = 1
+PHI_SOFTMAX = 2
 NO_LINEAR = 1
 HYBRID_SUM = 2
 HYBRID_STATE_ALL = 4

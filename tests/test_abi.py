@@ -121,7 +121,7 @@ BAD_CFGS = [
     (dict(batch=0), None, -2),
     (dict(dtype=torch.float16), None, -2),                            # unknown element type
     (dict(form=3), None, -2),                                         # unknown flag bits
-    (dict(phi=2), None, -2),                                          # unknown feature map
+    (dict(phi=3), None, -2),                                          # unknown feature map
     (dict(windows=[1, 5, 3], linear=False, form=1), None, -2),        # hybrid form without a linear part
 ]
 
