@@ -26,7 +26,8 @@ class OracleLayer(ctypes.Structure):
     _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("feat_dim", ctypes.c_int32),
                 ("window", ctypes.c_int32), ("linear", ctypes.c_int32),
-                ("form", ctypes.c_int32), ("phi", ctypes.c_int32), ("tau", ctypes.c_double)]
+                ("form", ctypes.c_int32), ("phi", ctypes.c_int32), ("wf_per_head", ctypes.c_int32),
+                ("tau", ctypes.c_double)]
 
 
 _LIBS = {}
@@ -72,16 +73,16 @@ class Oracle:
     (phi 0: ReLU(x Wf); 1: ELU(x Wf) + 1; 2: softmax(x Wf) over the features)."""
 
     def __init__(self, n_q_heads, n_kv_heads, head_dim, feat_dim, window, linear=True,
-                 tau=None, lib=None, form=0, phi=0):
+                 tau=None, lib=None, form=0, phi=0, wf_per_head=False):
         if tau is None:
             tau = 1.0 / np.sqrt(head_dim)
         self.L = OracleLayer(n_q_heads, n_kv_heads, head_dim, feat_dim, window,
-                             1 if linear else 0, int(form), int(phi), float(tau))
+                             1 if linear else 0, int(form), int(phi), 1 if wf_per_head else 0, float(tau))
         self.lib = lib if lib is not None else load()
 
     # -- feature map -------------------------------------------------------
     def phi(self, Wf, x):
-        """phi(x) = max(0, x @ Wf) over the last axis; x [..., d] -> [..., Df]."""
+        """phi(x @ Wf) over the last axis with one Wf [d][Df]; x [..., d] -> [..., Df]."""
         L = self.L
         x, xp = _d(x)
         Wf, wp = _d(Wf)

@@ -23,6 +23,8 @@
  *                 feature maps; or, with oracle_layer.phi = 2, the softmax
  *                 feature map Sec. III-B names as its default choice:
  *                 e^{y_f} / sum_f' e^{y_f'}, over the Df projected features)
+ *                 (Wf: one per layer, or, with oracle_layer.wf_per_head, one per
+ *                 KV head, used for that group's queries and keys)
  *     a_j       = phi(q_t) . phi(k_j)               for j in L
  *     A = sum_{j in L} a_j v_j ,  a = sum_{j in L} a_j
  *     s_j = tau * q_t . k_j                          for j in X
@@ -75,6 +77,7 @@ typedef struct {
   int32_t linear;      /* 1: linear part on (GLIDE), 0: pure sliding window */
   int32_t form;        /* 0: shared denominator; 1, 2: the Appendix hybrid forms */
   int32_t phi;         /* 0: ReLU(x Wf); 1: ELU(x Wf) + 1; 2: softmax(x Wf) */
+  int32_t wf_per_head; /* 0: one Wf [d][Df] per layer; 1: one per KV head, [Hkv][d][Df] */
   double  tau;         /* softmax scale */
 } oracle_layer;
 
@@ -83,6 +86,18 @@ typedef struct {
 #ifndef ORACLE_MUTANT
 #define ORACLE_MUTANT 0
 #endif
+
+/* The feature map's Wf for KV head g: the layer's one matrix, or, per head,
+ * the g-th (shared by the G query heads of the group and applied to the
+ * group's keys, so that phi(q_h) and phi(k_j) meet in one feature space). */
+static const double* wf_of(const oracle_layer* L, const double* Wf, int g) {
+#if ORACLE_MUTANT == 13
+  (void)g;
+  return Wf;                                     /* mutant: every head takes head 0's Wf */
+#else
+  return L->wf_per_head ? Wf + (size_t)g * L->head_dim * L->feat_dim : Wf;
+#endif
+}
 
 static int valid(const oracle_layer* L) {
   if (!L) return 0;
@@ -136,6 +151,7 @@ static void phi_row(int kind, int d, int Df, const double* Wf, const double* x, 
   }
 }
 
+/* phi of dense rows with one Wf [d][Df] (per head: the caller passes that head's matrix). */
 void oracle_phi(const oracle_layer* L, const double* Wf, int64_t rows, const double* x, double* out) {
   const int d = L->head_dim, Df = L->feat_dim;
 #pragma omp parallel for schedule(static)
@@ -216,7 +232,8 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
     phik = (double*)malloc(sizeof(double) * (size_t)(tmax + 1) * Hkv * Df);
     if (!phik) return -1;
 #pragma omp parallel for schedule(static)
-    for (int64_t r = 0; r < (tmax + 1) * Hkv; ++r) phi_row(L->phi, d, Df, Wf, k + r * d, phik + r * Df);
+    for (int64_t r = 0; r < (tmax + 1) * Hkv; ++r)
+      phi_row(L->phi, d, Df, wf_of(L, Wf, (int)(r % Hkv)), k + r * d, phik + r * Df);
   }
   int err = 0;
 #pragma omp parallel
@@ -250,7 +267,7 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
           for (int c = 0; c < d; ++c) A[c] = 0.0;
 #if ORACLE_MUTANT != 2
           if (L->linear && lend > 0) {
-            phi_row(L->phi, d, Df, Wf, qt, phq);
+            phi_row(L->phi, d, Df, wf_of(L, Wf, g), qt, phq);
             for (int64_t j = 0; j < lend; ++j) {
               const double aj = dot(Df, phq, phik + ((size_t)j * Hkv + g) * Df);
               const double* vj = v + ((size_t)j * Hkv + g) * d;
@@ -314,7 +331,7 @@ int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
     double* pk = (double*)malloc(sizeof(double) * Df);
     if (!pk) { err = 1; continue; }
     for (int64_t j = 0; j < nfold; ++j) {
-      phi_row(L->phi, d, Df, Wf, k + ((size_t)j * Hkv + g) * d, pk);
+      phi_row(L->phi, d, Df, wf_of(L, Wf, g), k + ((size_t)j * Hkv + g) * d, pk);
       const double* vj = v + ((size_t)j * Hkv + g) * d;
       for (int f = 0; f < Df; ++f) {
         double* Sr = S + ((size_t)g * Df + f) * d;
@@ -384,7 +401,7 @@ int oracle_decode_batch(const oracle_layer* L, const double* Wf, int32_t B,
       }
 #endif
       if (fk) {
-        phi_row(L->phi, d, Df, Wf, fk, pk);
+        phi_row(L->phi, d, Df, wf_of(L, Wf, g), fk, pk);
         for (int f = 0; f < Df; ++f) {
           for (int c = 0; c < d; ++c) Sg[(size_t)f * d + c] += pk[f] * fv[c];
           zg[f] += pk[f];
@@ -408,7 +425,7 @@ int oracle_decode_batch(const oracle_layer* L, const double* Wf, int32_t B,
         double a = 0.0;
         for (int c = 0; c < d; ++c) A[c] = 0.0;
         if (L->linear) {
-          phi_row(L->phi, d, Df, Wf, qt, pq);
+          phi_row(L->phi, d, Df, wf_of(L, Wf, g), qt, pq);
           for (int f = 0; f < Df; ++f) {
             for (int c = 0; c < d; ++c) A[c] += pq[f] * Sg[(size_t)f * d + c];
             a += pq[f] * zg[f];

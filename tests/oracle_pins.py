@@ -427,12 +427,47 @@ def pin_softmax_features(lib):
     return None
 
 
+def pin_per_head_feature_map(lib):
+    """One Wf per KV head: every group is the one-Wf layer of its own heads
+    run alone (G query heads, one KV head, that head's Wf), in the definition
+    form, the state and the recurrent form; equal matrices give the shared
+    case back."""
+    n, Hq, Hkv, d, Df = 17, 6, 3, 5, 7
+    q, k, v, _ = _rand_case(14, n, Hq, Hkv, d, Df)
+    Wh = np.random.default_rng(15).standard_normal((Hkv, d, Df)) / np.sqrt(d)
+    G = Hq // Hkv
+    for phi in (0, 2):
+        for W in (0, 4):
+            o = oracle.Oracle(Hq, Hkv, d, Df, W, linear=True, lib=lib, phi=phi, wf_per_head=True)
+            got = o.attend(Wh, q, k, v)
+            S, z = o.state(Wh, k, v)
+            st = o.empty_state(1)
+            dec = np.stack([o.decode(Wh, st, q[t][None], k[t][None], v[t][None])[0] for t in range(n)])
+            for g in range(Hkv):
+                og = oracle.Oracle(G, 1, d, Df, W, linear=True, lib=lib, phi=phi)
+                sl = slice(g * G, (g + 1) * G)
+                want = og.attend(Wh[g], q[:, sl], k[:, g:g + 1], v[:, g:g + 1])
+                if not np.allclose(got[:, sl], want, rtol=1e-12, atol=1e-12):
+                    return f"per-head Wf, phi {phi} W={W}: group {g} != its own layer"
+                if not np.allclose(dec[:, sl], want, rtol=1e-10, atol=1e-12):
+                    return f"per-head Wf, phi {phi} W={W}: recurrent form of group {g} != definition"
+                Sg, zg = og.state(Wh[g], k[:, g:g + 1], v[:, g:g + 1])
+                if not (np.allclose(S[g], Sg[0], rtol=1e-12, atol=1e-12) and np.allclose(z[g], zg[0], rtol=1e-12, atol=1e-12)):
+                    return f"per-head Wf, phi {phi} W={W}: state of group {g}"
+    same = np.repeat(Wh[:1], Hkv, 0)
+    a = oracle.Oracle(Hq, Hkv, d, Df, 3, lib=lib, wf_per_head=True).attend(same, q, k, v)
+    b = oracle.Oracle(Hq, Hkv, d, Df, 3, lib=lib).attend(Wh[0], q, k, v)
+    if not np.allclose(a, b, rtol=1e-13, atol=1e-13):
+        return "per-head Wf with equal matrices != one shared Wf"
+    return None
+
+
 ALL_PINS = [pin_worked_example, pin_full_window_is_causal_softmax, pin_band_is_masked_sdpa,
             pin_w0_is_causal_linear, pin_w1_closed_form, pin_recurrent_equals_definition,
             pin_state_direct_sums, pin_v_ones, pin_convex_hull, pin_linearity,
             pin_gqa_is_repeated_mha, pin_zero_over_zero, pin_continue_from_state,
             pin_hybrid_forms_are_band_plus_linear, pin_hybrid_v_ones, pin_softmax_worked_example,
-            pin_softmax_features]
+            pin_softmax_features, pin_per_head_feature_map]
 
 
 def run_all(lib):

@@ -31,7 +31,8 @@ def test_pin(pin):
 # 10 hybrid forms divide the linear term by both denominators
 # 11 the ELU+1 feature map without the + 1
 # 12 the softmax feature map without its normalisation
-MUTANTS = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12]
+# 13 per-head feature maps: every head takes head 0's Wf
+MUTANTS = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13]
 
 
 @pytest.mark.parametrize("mutant", MUTANTS)
