@@ -80,8 +80,14 @@ enum { GLIDE_PHI_RELU = 0, GLIDE_PHI_ELU1 = 1, GLIDE_PHI_SOFTMAX = 2 };
  * included (linear set [0, t]; S, z then hold tokens [0, p) after p tokens).
  * The paper states that GLIDE adapts both forms through its merge operator.
  * GLIDE_HYBRID_STATE_ALL requires GLIDE_HYBRID_SUM; neither combines with
- * GLIDE_NO_LINEAR. */
-enum { GLIDE_NO_LINEAR = 1, GLIDE_HYBRID_SUM = 2, GLIDE_HYBRID_STATE_ALL = 4 };
+ * GLIDE_NO_LINEAR.
+ *
+ * GLIDE_PER_HEAD_PHI gives every KV head its own feature-map matrix: phi_w is
+ * then [n_layers][Hkv][d][Df], and head g's matrix maps the queries of its
+ * group and its own keys (so that phi(q_h) . phi(k_j) pairs one feature
+ * space; S and z are per KV head already).  It combines with every other
+ * flag.  glide_feature_map takes one [d][Df] matrix either way. */
+enum { GLIDE_NO_LINEAR = 1, GLIDE_HYBRID_SUM = 2, GLIDE_HYBRID_STATE_ALL = 4, GLIDE_PER_HEAD_PHI = 8 };
 
 typedef struct {
   int32_t n_layers;    /* layers held by one state blob (>= 1) */
@@ -92,7 +98,8 @@ typedef struct {
   int32_t feat_dim;    /* Df: 64 or 128 */
   int32_t dtype;       /* GLIDE_F32 or GLIDE_BF16 */
   int32_t phi;         /* GLIDE_PHI_RELU, GLIDE_PHI_ELU1 or GLIDE_PHI_SOFTMAX */
-  int32_t flags;       /* 0, GLIDE_NO_LINEAR, GLIDE_HYBRID_SUM, or GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL */
+  int32_t flags;       /* 0, GLIDE_NO_LINEAR, GLIDE_HYBRID_SUM, or GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL,
+                          each optionally | GLIDE_PER_HEAD_PHI */
   float sm_scale;      /* tau, the softmax scale (1/sqrt(d) in the Appendix's attention) */
   const int32_t* windows; /* HOST array [n_layers]: W_l = w - delta_l, 0 <= W_l <= 2^20 */
 } glide_config;

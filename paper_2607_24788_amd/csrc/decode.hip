@@ -212,7 +212,8 @@ void decode_kernel(DecodeArgs a) {
   const T* kn = reinterpret_cast<const T*>(a.k) + (tok * Hkv + g) * D;
   const T* vn = reinterpret_cast<const T*>(a.v) + (tok * Hkv + g) * D;
   T* og = reinterpret_cast<T*>(a.out) + (tok * Hq + int64_t(g) * G) * D;
-  const T* Wf = reinterpret_cast<const T*>(a.phi_w) + int64_t(L.slot) * D * DF;
+  const T* Wf = reinterpret_cast<const T*>(a.phi_w) +
+                (a.wf_heads ? int64_t(L.slot) * Hkv + g : int64_t(L.slot)) * D * DF;
 
   // pos and nf: two scalar loads in flight together; the loads that do not
   // depend on them (the state pass's Wf slice, S rows and z, the queries and
@@ -763,7 +764,8 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(DecodeArgs a) {
   float* z = reinterpret_cast<float*>(lay + sec.z) + unit * DF;
   const T* Kr = reinterpret_cast<const T*>(lay + sec.K) + unit * int64_t(R) * D;
   const T* Vr = reinterpret_cast<const T*>(lay + sec.V) + unit * int64_t(R) * D;
-  const T* Wf = reinterpret_cast<const T*>(a.phi_w) + int64_t(L.slot) * D * DF;
+  const T* Wf = reinterpret_cast<const T*>(a.phi_w) +
+                (a.wf_heads ? int64_t(L.slot) * a.Hkv + int64_t(unit % a.Hkv) : int64_t(L.slot)) * D * DF;
   for (int e = tid; e < n * D; e += kThreads) {
     const int i = e / D, c = e - i * D;
     const int32_t slot = int32_t((nf + i) % R);

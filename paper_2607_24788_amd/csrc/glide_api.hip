@@ -25,7 +25,8 @@ glide_status check_cfg(const glide_config* c) {
   if (c->head_dim < 1 || c->feat_dim < 1) return GLIDE_ERR_INVALID;
   if (c->dtype != GLIDE_F32 && c->dtype != GLIDE_BF16) return GLIDE_ERR_INVALID;
   if (c->phi != GLIDE_PHI_RELU && c->phi != GLIDE_PHI_ELU1 && c->phi != GLIDE_PHI_SOFTMAX) return GLIDE_ERR_INVALID;
-  if (c->flags & ~int32_t(GLIDE_NO_LINEAR | GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL)) return GLIDE_ERR_INVALID;
+  if (c->flags & ~int32_t(GLIDE_NO_LINEAR | GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL | GLIDE_PER_HEAD_PHI))
+    return GLIDE_ERR_INVALID;
   // the hybrid forms change the linear part: not without one; the state over
   // every token comes only with the separately normalised sum
   if ((c->flags & GLIDE_NO_LINEAR) && (c->flags & (GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL)))
@@ -167,6 +168,7 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
   a.linear = linear_on(cfg) ? 1 : 0;
   a.form = merge_form(cfg);
   a.phi = cfg->phi;
+  a.wf_heads = (cfg->flags & GLIDE_PER_HEAD_PHI) ? 1 : 0;
   a.tau = cfg->sm_scale;
   for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
@@ -352,7 +354,9 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   a.wf = static_cast<const char*>(phi_w);
   a.q_stride = T * Hq * d * es;
   a.kv_stride = T * Hkv * d * es;
-  a.wf_stride = int64_t(d) * Df * es;
+  const bool wf_heads = (cfg->flags & GLIDE_PER_HEAD_PHI) != 0;
+  a.wf_stride = int64_t(wf_heads ? Hkv : 1) * d * Df * es;
+  a.wf_hs = wf_heads ? int32_t(int64_t(d) * Df * es) : 0;
   a.ws = static_cast<char*>(workspace);
   a.ws_slot = int64_t(w.slot);
   a.ws_hv = int64_t(w.hv);

@@ -574,6 +574,8 @@ struct DecodeArgs {
   // window is split (the extra workgroups exit at once), so that every piece
   // of a unit has the same workgroup index modulo 8 and runs on the same XCD
   int32_t row_stride;
+  int32_t wf_heads;  // 1: phi_w holds one Wf per KV head ([layer][Hkv][d][Df])
+  int32_t pad;
   LayerArg layers[kMaxLayersPerLaunch];  // sorted by decreasing W
   // layer (index into layers) of every piece row: workgroup w of the main
   // pass belongs to layer piece_layer[w / row_stride].  The rows of every
@@ -613,7 +615,7 @@ struct PrefillArgs {
   const char* k;        // [n][T][Hkv][d]  (kv_stride)
   const char* v;        // [n][T][Hkv][d]  (kv_stride)
   char* out;            // [n][T][Hq][d]   (q_stride)
-  const char* wf;       // [n][d][Df]      (wf_stride)
+  const char* wf;       // [n][d][Df], or [n][Hkv][d][Df] (wf_stride; head stride wf_hs)
   int64_t q_stride, kv_stride, wf_stride;
   char* ws;             // workspace: slot ls at ls * ws_slot bytes; per slot
   int64_t ws_slot;      //   history keys [B][Hkv][Wcap][d] at 0, history values at ws_hv,
@@ -630,7 +632,8 @@ struct PrefillArgs {
   int32_t nseg;         // segments in this group
   int32_t nlayer;       // layers in this launch
   int32_t form;         // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
-  int32_t pad0, pad1;
+  int32_t wf_hs;        // bytes between the KV heads' Wf (0: one Wf per layer)
+  int32_t pad1;
   int32_t phi;          // feature map: 0 ReLU, 1 ELU + 1
   PrefillLayer layers[kMaxLayersPerLaunch];  // the launch's layers, by decreasing window
   int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token

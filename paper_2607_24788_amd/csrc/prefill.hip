@@ -404,7 +404,7 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
     }
   };
   if (jlo < jhi) load_slab(jlo);
-  stage_wf<T, D, DF, kSegThreads>(static_cast<const T*>(L.wf), Wn);
+  stage_wf<T, D, DF, kSegThreads>(reinterpret_cast<const T*>(static_cast<const char*>(L.wf) + int64_t(g) * a.wf_hs), Wn);
   for (int64_t j0 = jlo; j0 < jhi; j0 += kSegSlab) {
     __syncthreads();  // Wf staged; the previous slab's readers are done
     {
@@ -592,7 +592,7 @@ void prefill_main(PrefillArgs a) {
   // Wf columns, with a fresh LDS base per phase
   auto wf_cols = [&]() {
     if constexpr (LD::kWfLds) return WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))};
-    else return WfCols<T, D, DF, false>{static_cast<const T*>(L.wf)};
+    else return WfCols<T, D, DF, false>{reinterpret_cast<const T*>(static_cast<const char*>(L.wf) + int64_t(g) * a.wf_hs)};
   };
 
   // ---- pass geometry: chunk c0 (nk tokens from absolute position t0), rows
@@ -692,7 +692,7 @@ void prefill_main(PrefillArgs a) {
   //         segment start (the scan's record), fp32, into LDS (S transposed);
   //         they stay there for the whole walk
   if (linear) {
-    if constexpr (LD::kWfLds) stage_wf<T, D, DF, kMT>(static_cast<const T*>(L.wf), Wn);
+    if constexpr (LD::kWfLds) stage_wf<T, D, DF, kMT>(reinterpret_cast<const T*>(static_cast<const char*>(L.wf) + int64_t(g) * a.wf_hs), Wn);
     const float* S0 = L.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
     constexpr int NS = DF * D / 4 / kMT;
     static_assert(NS * kMT * 4 == DF * D, "even split");

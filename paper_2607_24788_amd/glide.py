@@ -21,6 +21,7 @@ PHI_SOFTMAX = 2
 NO_LINEAR = 1
 HYBRID_SUM = 2
 HYBRID_STATE_ALL = 4
+PER_HEAD_PHI = 8
 
 STATUS = {0: "GLIDE_OK", -1: "GLIDE_ERR_NULL", -2: "GLIDE_ERR_INVALID", -3: "GLIDE_ERR_UNSUPPORTED",
           -4: "GLIDE_ERR_ALIGN", -5: "GLIDE_ERR_SIZE", -6: "GLIDE_ERR_HIP"}
@@ -147,7 +148,8 @@ class Glide:
     """
 
     def __init__(self, n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, windows,
-                 dtype=torch.bfloat16, sm_scale=None, linear=True, lib=None, form=0, phi=PHI_RELU):
+                 dtype=torch.bfloat16, sm_scale=None, linear=True, lib=None, form=0, phi=PHI_RELU,
+                 per_head_phi=False):
         self.lib = lib if lib is not None else load_library()
         self.windows = [int(w) for w in windows]
         if len(self.windows) != n_layers:
@@ -158,6 +160,8 @@ class Glide:
         if sm_scale is None:
             sm_scale = head_dim ** -0.5
         flags = (0 if linear else NO_LINEAR) | {0: 0, 1: HYBRID_SUM, 2: HYBRID_SUM | HYBRID_STATE_ALL}.get(form, 99)
+        if per_head_phi:
+            flags |= PER_HEAD_PHI
         self.cfg = Config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, code, int(phi),
                           flags, float(sm_scale), self._win)
         self.n_layers, self.batch = n_layers, batch
@@ -167,6 +171,7 @@ class Glide:
         self.linear = linear
         self.form = form
         self.phi = phi
+        self.per_head_phi = per_head_phi
 
     # -- sizes and layout ----------------------------------------------------
     def state_bytes(self):

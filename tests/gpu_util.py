@@ -41,19 +41,21 @@ class Case:
     """A decode/prefill test case on a small synthetic stack."""
 
     def __init__(self, windows, batch=1, Hq=4, Hkv=4, d=64, Df=64, dtype=torch.float32, linear=True,
-                 tau=None, seed=0, qkv_scale=None, v_scale=None, form=0, phi=0):
+                 tau=None, seed=0, qkv_scale=None, v_scale=None, form=0, phi=0, per_head_phi=False):
         self.windows = list(windows)
         self.L = len(windows)
         self.B, self.Hq, self.Hkv, self.d, self.Df = batch, Hq, Hkv, d, Df
         self.dtype, self.linear, self.form, self.phi = dtype, linear, form, phi
+        self.per_head_phi = per_head_phi
         self.tau = d ** -0.5 if tau is None else tau
         self.seed = seed
         self.qkv_scale = d ** -0.5 if qkv_scale is None else qkv_scale
         self.v_scale = self.qkv_scale if v_scale is None else v_scale
         self.g = glide.Glide(self.L, batch, Hq, Hkv, d, Df, self.windows, dtype=dtype, sm_scale=self.tau,
-                             linear=linear, form=form, phi=phi)
+                             linear=linear, form=form, phi=phi, per_head_phi=per_head_phi)
         gen = torch.Generator().manual_seed(seed * 7919 + 17)
-        self.phi_w = (torch.randn((self.L, d, Df), generator=gen) * d ** -0.5).to(dtype)
+        wshape = (self.L, Hkv, d, Df) if per_head_phi else (self.L, d, Df)
+        self.phi_w = (torch.randn(wshape, generator=gen) * d ** -0.5).to(dtype)
         self._gen = gen
 
     def tokens(self, n):
@@ -66,7 +68,7 @@ class Case:
 
     def oracle(self, l):
         return oracle.Oracle(self.Hq, self.Hkv, self.d, self.Df, self.windows[l], linear=self.linear,
-                             tau=self.tau, form=self.form, phi=self.phi)
+                             tau=self.tau, form=self.form, phi=self.phi, wf_per_head=self.per_head_phi)
 
     def delay(self, l):
         """The linear part's delay: the window, or 0 when the state holds every token."""

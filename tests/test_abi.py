@@ -132,7 +132,8 @@ def test_hybrid_flag_combinations():
     ok = mk(windows=[1, 5, 3])
     for flags, code in ((glide.HYBRID_SUM, 0), (glide.HYBRID_SUM | glide.HYBRID_STATE_ALL, 0),
                         (glide.HYBRID_STATE_ALL, -2), (glide.NO_LINEAR | glide.HYBRID_SUM, -2),
-                        (8, -2)):
+                        (glide.PER_HEAD_PHI, 0), (glide.PER_HEAD_PHI | glide.HYBRID_SUM, 0),
+                        (16, -2)):
         ok.cfg.flags = flags
         assert (ok.state_bytes() > 0) == (code == 0), flags
         if code:  # rejected before any HIP call (the pointer is never used)
