@@ -170,10 +170,14 @@ def main():
             "traffic": traffic and traffic["prefill_call_bytes"],
             "algorithmic_flops_per_launch": pre_flops, "avg_launch_us": pre_ms * 1e3}
     dominant = hbm if dec_ms >= pre_ms else mfma
+    has_decode = wl.decode_steps > 0
+    if not has_decode:  # a prefill-only workload: no decode figures
+        dominant = mfma
 
     line = {
         "metric": "decode tokens/s per layer-stack + % HBM peak; prefill tokens/s + % MFMA",
-        "value": round(dec_tok_s, 2),
+        # prefill-only workloads report their prefill throughput instead
+        "value": round(dec_tok_s if has_decode else pre_tok_s, 2),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": steps,
@@ -186,15 +190,15 @@ def main():
         "data": "synthetic (seeded N(0,1)/sqrt(d) q,k,v; Wf ~ N(0,1/d))"
                 + ("; prefill inputs of one layer reused by every layer" if share_prefill else ""),
         "config": dict(wl.describe(), chunk=wl.chunk, **({"form": args.form} if args.form else {}), **({"phi": args.phi} if args.phi else {})),
-        "decode_tokens_per_s": round(dec_tok_s, 2),
-        "decode_us_per_step": round(dec_step_s * 1e6, 2),
-        "decode_hbm_frac": round(hbm["frac"], 4),
+        "decode_tokens_per_s": round(dec_tok_s, 2) if has_decode else None,
+        "decode_us_per_step": round(dec_step_s * 1e6, 2) if has_decode else None,
+        "decode_hbm_frac": round(hbm["frac"], 4) if has_decode else None,
         "prefill_tokens_per_s": round(pre_tok_s, 1),
         "prefill_ms": round(pre_ms, 3),
         "prefill_mfma_frac": round(mfma["frac"], 4),
         "roofline": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in dominant.items()},
-        "roofline_other": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in
-                           (mfma if dominant is hbm else hbm).items()},
+        "roofline_other": ({k: (round(v, 4) if isinstance(v, float) else v) for k, v in
+                            (mfma if dominant is hbm else hbm).items()} if has_decode else None),
     }
     if not args.no_detail and wl.decode_steps:
         line["decode_detail"] = decode_detail(g, wl, state, phi, dq, dk, dv, dout, ws, prefill, stream)
