@@ -6,10 +6,12 @@
 //   2. phi of the G query heads and of the pending keys (tokens that have
 //      left the window but are not yet folded into S, z) on MFMA against Wf,
 //      each wave producing the features of the state rows it owns;
-//   3. state: S' = S + sum_pending phi(k_j)^T v_j (and z') in registers, the
-//      read-out phi(q_h).S', phi(q_h).z' from the same pass over S; on the
-//      unit's fold step S', z' are written back (deferred folding: at most
-//      one write of the state per kFoldPeriod steps);
+//   3. state: the read-out phi(q_h).S, phi(q_h).z from one pass over the S
+//      rows, plus the pending tokens through a_hj = phi(q_h).phi(k_j)
+//      (sum_j a_hj v_j, sum_j a_hj); on the unit's fold step the pending
+//      tokens are first added to the rows in registers, S', z' written back
+//      and read out (deferred folding: at most one write of the state per
+//      kFoldPeriod steps);
 //   4. window: the W most recent tokens (ring tokens p-W+1 .. p-1 plus the new
 //      token taken straight from the input) are streamed in 32-token tiles,
 //      the next tile's loads in flight while the current one is computed;
@@ -17,8 +19,10 @@
 //      16-wide tile dimension; online softmax in the log2 domain;
 //   5. merge of the two parts over one shared denominator, output, pos += 1.
 //
-// One workgroup of 4 waves handles one unit; units of the call are ordered by
-// decreasing window so the longest streams start first.
+// One workgroup of 4 waves handles one unit, or one piece of a unit's window
+// when a launch has few units (the pieces of a unit run on one XCD and meet
+// in its L2; the last to finish merges them); units of the call are ordered
+// by decreasing window so the longest streams start first.
 #include <math.h>
 
 #include "glide_internal.h"
