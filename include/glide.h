@@ -167,7 +167,8 @@ glide_status glide_state_init(const glide_config* cfg, void* state, size_t state
  * C in [32, 256] that is a multiple of 32 gives the same result up to
  * rounding).  Pending tokens are folded first (as glide_state_flush); on
  * return nf = max(0, p - W).
- *   phi_w  device [n_layers][d][Df]        (layer layer0 first)
+ *   phi_w  device [n_layers][d][Df]        (layer layer0 first; [n_layers][Hkv][d][Df]
+ *          with GLIDE_PER_HEAD_PHI)
  *   q      device [n_layers][T][Hq][d]     T = total_tokens, packed by sequence
  *   k, v   device [n_layers][T][Hkv][d]
  *   cu_seqlens_host  HOST [B+1], cu[0] = 0, non-decreasing, cu[B] = T
@@ -193,7 +194,7 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
  * one layer spreads that layer's windows over many workgroups; the
  * workgroup that finishes a unit's last piece merges the pieces' partial
  * results.  Calls over different layer subsets agree up to rounding.
- *   phi_w  device [n_layers][d][Df]
+ *   phi_w  device [n_layers][d][Df]  ([n_layers][Hkv][d][Df] with GLIDE_PER_HEAD_PHI)
  *   q      device [n_layers][B][Hq][d];  k, v device [n_layers][B][Hkv][d]
  *   out    device [n_layers][B][Hq][d]
  *   workspace  device, 256-byte aligned, >= glide_workspace_bytes(cfg, 0);
@@ -206,15 +207,18 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
 /* Folds every pending token of layers [layer0, layer0 + n_layers) into S and
  * z (nf := max(0, p - W)), so that S and z hold exactly the Sec. II-B sums
  * over the linear part of the next token.  Outputs of later steps are
- * unchanged up to rounding.  phi_w device [n_layers][d][Df] (layer layer0
- * first).  Nothing to do without the linear part. */
+ * unchanged up to rounding.  phi_w device [n_layers][d][Df], layer layer0 first
+ * ([n_layers][Hkv][d][Df] with GLIDE_PER_HEAD_PHI).  Nothing to do without the
+ * linear part. */
 glide_status glide_state_flush(const glide_config* cfg, void* state, size_t state_bytes,
                                int32_t layer0, int32_t n_layers, const void* phi_w, void* stream);
 
 /* The feature map alone (kernel (d)): out[r][f] = phi(sum_c x[r][c] Wf[c][f])
- * (cfg->phi) for r < rows, accumulated in fp32.  x device [rows][d], phi_w device [d][Df]
- * (both cfg->dtype), out device [rows][Df] in cfg->dtype; x and out may be NULL
- * when rows == 0. */
+ * (cfg->phi; the softmax map normalises each row over its Df features) for
+ * r < rows, accumulated in fp32.  x device [rows][d], phi_w device [d][Df] (one
+ * matrix, also with GLIDE_PER_HEAD_PHI: the caller passes the head's), both
+ * cfg->dtype; out device [rows][Df] in cfg->dtype; x and out may be NULL when
+ * rows == 0. */
 glide_status glide_feature_map(const glide_config* cfg, const void* phi_w, const void* x,
                                int64_t rows, void* out, void* stream);
 
