@@ -52,6 +52,12 @@ def load(path=None):
     lib.oracle_state.argtypes = [P, _c_double_p, ctypes.c_int64, _c_double_p, _c_double_p,
                                  _c_double_p, _c_double_p]
     lib.oracle_state.restype = ctypes.c_int
+    lib.oracle_attend_gated.argtypes = [P, _c_double_p, ctypes.c_int64, _c_double_p, _c_double_p,
+                                        _c_double_p, _c_double_p, ctypes.c_int64, _c_int64_p, _c_double_p]
+    lib.oracle_attend_gated.restype = ctypes.c_int
+    lib.oracle_state_gated.argtypes = [P, _c_double_p, ctypes.c_int64, _c_double_p, _c_double_p, _c_double_p,
+                                       _c_double_p, _c_double_p]
+    lib.oracle_state_gated.restype = ctypes.c_int
     lib.oracle_decode_batch.argtypes = [P, _c_double_p, ctypes.c_int32, _c_double_p, _c_double_p,
                                         _c_double_p, _c_double_p, _c_int64_p, _c_double_p,
                                         _c_double_p, _c_double_p, _c_double_p]
@@ -128,6 +134,43 @@ class Oracle:
                                    S.ctypes.data_as(_c_double_p), z.ctypes.data_as(_c_double_p))
         if rc != 0:
             raise ValueError("oracle_state rejected its arguments")
+        return S, z
+
+    # -- gated linear state (GLA-style decay) ---------------------------------
+    def attend_gated(self, Wf, q, k, v, log_gates, positions=None):
+        """The definition form with a gated linear state: log_gates [n][Hkv]
+        (<= 0); a linear-set token j read at time t weighs
+        e^{sum_{i=j+1..t} log_gates[i]}."""
+        L = self.L
+        q, qp = _d(q)
+        k, kp = _d(k)
+        v, vp = _d(v)
+        lg, lgp = _d(log_gates)
+        Wf, wp = _d(Wf)
+        n = q.shape[0]
+        pos = np.arange(n, dtype=np.int64) if positions is None else np.ascontiguousarray(positions, np.int64)
+        out = np.empty((len(pos), L.n_q_heads, L.head_dim), np.float64)
+        rc = self.lib.oracle_attend_gated(ctypes.byref(L), wp, n, qp, kp, vp, lgp, len(pos),
+                                          pos.ctypes.data_as(_c_int64_p), out.ctypes.data_as(_c_double_p))
+        if rc != 0:
+            raise ValueError("oracle_attend_gated rejected its arguments")
+        return out
+
+    def state_gated(self, Wf, k, v, log_gates, p=None):
+        """(S, z) of the gated state after the first p tokens (decayed through token p - 1)."""
+        L = self.L
+        k, kp = _d(k)
+        v, vp = _d(v)
+        lg, lgp = _d(log_gates)
+        Wf, wp = _d(Wf)
+        if p is None:
+            p = k.shape[0]
+        S = np.empty((L.n_kv_heads, L.feat_dim, L.head_dim), np.float64)
+        z = np.empty((L.n_kv_heads, L.feat_dim), np.float64)
+        rc = self.lib.oracle_state_gated(ctypes.byref(L), wp, int(p), kp, vp, lgp,
+                                         S.ctypes.data_as(_c_double_p), z.ctypes.data_as(_c_double_p))
+        if rc != 0:
+            raise ValueError("oracle_state_gated rejected its arguments")
         return S, z
 
     # -- recurrent form ------------------------------------------------------

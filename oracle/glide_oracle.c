@@ -30,6 +30,11 @@
  *     s_j = tau * q_t . k_j                          for j in X
  *     O_t = (sum_{j in X} e^{s_j} v_j + A) / (sum_{j in X} e^{s_j} + a)
  *
+ *   With a gated (GLA-style) linear state (oracle_attend_gated / oracle_state_gated,
+ *   one log-gate lg[t][g] <= 0 per token and KV head; the paper names GLA-style
+ *   gating among the linear forms it supports without fixing the gate), each
+ *   a_j is weighted by e^{sum_{i=j+1..t} lg[i][g]}: the decay since j arrived.
+ *
  *   i.e. the softmax window and the linear state share one denominator (the
  *   "merge weighted by the normalising denominators" of Sec. II-A / III-B).
  *   The expression is evaluated with a stabiliser c = max(m, ln a)
@@ -216,9 +221,34 @@ static void merge(int form, int d, int has_sm, const double* sm_num, double sm_d
  * out [n_out][Hq][d].  phi(k_j) is evaluated once per key and reused.
  * Returns 0, or -1 on invalid arguments.
  */
-int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
-                  const double* q, const double* k, const double* v,
-                  int64_t n_out, const int64_t* pos, double* out) {
+/* Cumulative log-gates of the gated linear state: Gc[t][g] = sum_{i <= t} lg[i][g]
+ * (NULL when ungated).  A linear-set token j read at time t weighs
+ * e^{Gc[t] - Gc[j]}: it has decayed by the gates of the tokens after it. */
+static double* cum_gates(const double* lg, int64_t n, int Hkv) {
+  if (!lg || n <= 0) return NULL;
+  double* Gc = (double*)malloc(sizeof(double) * (size_t)n * Hkv);
+  if (!Gc) return NULL;
+  for (int g = 0; g < Hkv; ++g) {
+    double acc = 0.0;
+    for (int64_t t = 0; t < n; ++t) {
+      acc += lg[(size_t)t * Hkv + g];
+      Gc[(size_t)t * Hkv + g] = acc;
+    }
+  }
+  return Gc;
+}
+static double decay(const double* Gc, int Hkv, int g, int64_t t, int64_t j) {
+  if (!Gc) return 1.0;
+#if ORACLE_MUTANT == 14
+  return exp(Gc[(size_t)t * Hkv + g] - (j > 0 ? Gc[(size_t)(j - 1) * Hkv + g] : 0.0));  /* mutant: j's own gate too */
+#else
+  return exp(Gc[(size_t)t * Hkv + g] - Gc[(size_t)j * Hkv + g]);
+#endif
+}
+
+static int attend_impl(const oracle_layer* L, const double* Wf, int64_t n,
+                       const double* q, const double* k, const double* v, const double* lg,
+                       int64_t n_out, const int64_t* pos, double* out) {
   if (!valid(L) || n < 0 || n_out < 0) return -1;
   for (int64_t i = 0; i < n_out; ++i)
     if (pos[i] < 0 || pos[i] >= n) return -1;
@@ -235,6 +265,8 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
     for (int64_t r = 0; r < (tmax + 1) * Hkv; ++r)
       phi_row(L->phi, d, Df, wf_of(L, Wf, (int)(r % Hkv)), k + r * d, phik + r * Df);
   }
+  double* Gc = cum_gates(lg, tmax + 1, Hkv);
+  if (lg && tmax >= 0 && !Gc) { free(phik); return -1; }
   int err = 0;
 #pragma omp parallel
   {
@@ -269,7 +301,7 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
           if (L->linear && lend > 0) {
             phi_row(L->phi, d, Df, wf_of(L, Wf, g), qt, phq);
             for (int64_t j = 0; j < lend; ++j) {
-              const double aj = dot(Df, phq, phik + ((size_t)j * Hkv + g) * Df);
+              const double aj = dot(Df, phq, phik + ((size_t)j * Hkv + g) * Df) * decay(Gc, Hkv, g, t, j);
               const double* vj = v + ((size_t)j * Hkv + g) * d;
               for (int c = 0; c < d; ++c) A[c] += aj * vj[c];
               a += aj;
@@ -309,7 +341,24 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
     free(phq); free(A); free(num);
   }
   free(phik);
+  free(Gc);
   return err ? -1 : 0;
+}
+
+int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
+                  const double* q, const double* k, const double* v,
+                  int64_t n_out, const int64_t* pos, double* out) {
+  return attend_impl(L, Wf, n, q, k, v, NULL, n_out, pos, out);
+}
+
+/* The gated linear state (GLA-style decay, one log-gate lg[t][g] <= 0 per
+ * token and KV head): the definition form with every linear-set token
+ * weighted by the decay since it arrived. */
+int oracle_attend_gated(const oracle_layer* L, const double* Wf, int64_t n,
+                        const double* q, const double* k, const double* v, const double* lg,
+                        int64_t n_out, const int64_t* pos, double* out) {
+  if (!lg) return -1;
+  return attend_impl(L, Wf, n, q, k, v, lg, n_out, pos, out);
 }
 
 /*
@@ -318,13 +367,15 @@ int oracle_attend(const oracle_layer* L, const double* Wf, int64_t n,
  * (j < p in form 2).  Both zero when p <= W (forms 0, 1) or when the linear
  * part is off.
  */
-int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
-                 const double* k, const double* v, double* S, double* z) {
+static int state_impl(const oracle_layer* L, const double* Wf, int64_t p,
+                      const double* k, const double* v, const double* lg, double* S, double* z) {
   if (!valid(L) || p < 0) return -1;
   const int Hkv = L->n_kv_heads, d = L->head_dim, Df = L->feat_dim, W = L->window;
   memset(S, 0, sizeof(double) * (size_t)Hkv * Df * d);
   memset(z, 0, sizeof(double) * (size_t)Hkv * Df);
   const int64_t nfold = !L->linear ? 0 : L->form == 2 ? p : (p - W > 0 ? p - W : 0);
+  double* Gc = cum_gates(lg, p, Hkv);
+  if (lg && p > 0 && !Gc) return -1;
   int err = 0;
 #pragma omp parallel for schedule(static)
   for (int g = 0; g < Hkv; ++g) {
@@ -332,16 +383,31 @@ int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
     if (!pk) { err = 1; continue; }
     for (int64_t j = 0; j < nfold; ++j) {
       phi_row(L->phi, d, Df, wf_of(L, Wf, g), k + ((size_t)j * Hkv + g) * d, pk);
+      const double w = decay(Gc, Hkv, g, p - 1, j);   /* decayed through token p - 1 */
       const double* vj = v + ((size_t)j * Hkv + g) * d;
       for (int f = 0; f < Df; ++f) {
         double* Sr = S + ((size_t)g * Df + f) * d;
-        for (int c = 0; c < d; ++c) Sr[c] += pk[f] * vj[c];
-        z[(size_t)g * Df + f] += pk[f];
+        for (int c = 0; c < d; ++c) Sr[c] += w * pk[f] * vj[c];
+        z[(size_t)g * Df + f] += w * pk[f];
       }
     }
     free(pk);
   }
+  free(Gc);
   return err ? -1 : 0;
+}
+
+int oracle_state(const oracle_layer* L, const double* Wf, int64_t p,
+                 const double* k, const double* v, double* S, double* z) {
+  return state_impl(L, Wf, p, k, v, NULL, S, z);
+}
+
+/* The gated state after p tokens: the same sums, each token decayed by the
+ * gates of the tokens after it up to token p - 1. */
+int oracle_state_gated(const oracle_layer* L, const double* Wf, int64_t p,
+                       const double* k, const double* v, const double* lg, double* S, double* z) {
+  if (!lg) return -1;
+  return state_impl(L, Wf, p, k, v, lg, S, z);
 }
 
 /*

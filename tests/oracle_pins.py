@@ -462,12 +462,67 @@ def pin_per_head_feature_map(lib):
     return None
 
 
+def pin_gated_linear_state(lib):
+    """The gated (GLA-style) linear state: zero gates give the ungated layer;
+    at W = 0 it is the decay-masked linear-attention product
+    (phi(Q) phi(K)^T * D) V with D[t, j] = e^{G_t - G_j} (numpy cumulative
+    sums); and the state equals the recurrence S <- e^{g_p} S plus the token
+    leaving the window, decayed by the gates since it arrived."""
+    n, Hq, Hkv, d, Df = 21, 4, 2, 5, 6
+    q, k, v, Wf = _rand_case(16, n, Hq, Hkv, d, Df)
+    lg = -np.random.default_rng(17).uniform(0.0, 0.4, (n, Hkv))
+    G = Hq // Hkv
+    for W in (0, 1, 5):
+        for form in (0, 2):
+            o = oracle.Oracle(Hq, Hkv, d, Df, W, lib=lib, form=form)
+            if not np.allclose(o.attend_gated(Wf, q, k, v, np.zeros((n, Hkv))), o.attend(Wf, q, k, v),
+                               rtol=1e-13, atol=1e-13):
+                return f"gated with zero gates != ungated, W={W} form {form}"
+            Sa, za = o.state_gated(Wf, k, v, np.zeros((n, Hkv)))
+            Sb, zb = o.state(Wf, k, v)
+            if not (np.allclose(Sa, Sb, rtol=1e-13, atol=1e-13) and np.allclose(za, zb, rtol=1e-13, atol=1e-13)):
+                return f"gated state with zero gates != ungated, W={W} form {form}"
+    # W = 0: the decay-masked product
+    Gc = np.cumsum(lg, axis=0)                                      # [n][Hkv]
+    pq = _feat(q @ Wf, 0)
+    pk = _feat(np.repeat(k, G, axis=1) @ Wf, 0)
+    vv = np.repeat(v, G, axis=1)
+    Gh = np.repeat(Gc, G, axis=1)                                   # [n][Hq]
+    want = np.zeros(q.shape)
+    for h in range(Hq):
+        Dm = np.tril(np.exp(Gh[:, h][:, None] - Gh[:, h][None, :]))
+        A = (pq[:, h] @ pk[:, h].T) * Dm
+        den = A.sum(1)
+        want[:, h] = np.where((den > 0)[:, None], (A @ vv[:, h]) / np.where(den > 0, den, 1.0)[:, None], 0.0)
+    got = oracle.Oracle(Hq, Hkv, d, Df, 0, lib=lib).attend_gated(Wf, q, k, v, lg)
+    if not np.allclose(got, want, rtol=1e-10, atol=1e-12):
+        return f"gated W=0 != decay-masked linear attention (max err {np.abs(got - want).max()})"
+    # the recurrence
+    for W in (0, 3):
+        o = oracle.Oracle(Hq, Hkv, d, Df, W, lib=lib)
+        S = np.zeros((Hkv, Df, d))
+        z = np.zeros((Hkv, Df))
+        for p in range(n):
+            S *= np.exp(lg[p])[:, None, None]
+            z *= np.exp(lg[p])[:, None]
+            e = p - W
+            if e >= 0:
+                w = np.exp(lg[e + 1:p + 1].sum(0))                   # gates of tokens e+1 .. p
+                fk = _feat(np.einsum("gc,cf->gf", k[e], Wf), 0)
+                S += w[:, None, None] * fk[:, :, None] * v[e][:, None, :]
+                z += w[:, None] * fk
+            Sg, zg = o.state_gated(Wf, k, v, lg, p + 1)
+            if not (np.allclose(S, Sg, rtol=1e-11, atol=1e-13) and np.allclose(z, zg, rtol=1e-11, atol=1e-13)):
+                return f"gated state != recurrence at p={p + 1}, W={W}"
+    return None
+
+
 ALL_PINS = [pin_worked_example, pin_full_window_is_causal_softmax, pin_band_is_masked_sdpa,
             pin_w0_is_causal_linear, pin_w1_closed_form, pin_recurrent_equals_definition,
             pin_state_direct_sums, pin_v_ones, pin_convex_hull, pin_linearity,
             pin_gqa_is_repeated_mha, pin_zero_over_zero, pin_continue_from_state,
             pin_hybrid_forms_are_band_plus_linear, pin_hybrid_v_ones, pin_softmax_worked_example,
-            pin_softmax_features, pin_per_head_feature_map]
+            pin_softmax_features, pin_per_head_feature_map, pin_gated_linear_state]
 
 
 def run_all(lib):

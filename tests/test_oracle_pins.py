@@ -32,7 +32,8 @@ def test_pin(pin):
 # 11 the ELU+1 feature map without the + 1
 # 12 the softmax feature map without its normalisation
 # 13 per-head feature maps: every head takes head 0's Wf
-MUTANTS = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13]
+# 14 the gated state decays a token by its own gate as well
+MUTANTS = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14]
 
 
 @pytest.mark.parametrize("mutant", MUTANTS)
