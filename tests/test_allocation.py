@@ -96,13 +96,17 @@ def test_blockwise_search_picks_the_best_candidate():
 
 def test_bench_decode_bytes_contain_the_kv_io_model():
     """bench.py's algorithmic decode bytes = the KV I/O model (window K/V of
-    every softmax layer) + the per-unit state, token and output terms."""
+    every softmax layer) + the per-unit state, token and output terms; the
+    state is written once per fold period by default, every step on request."""
     import bench
     from paper_2607_24788_amd import workload as Wm
-    for name in ("c2", "c2b", "c3b"):
+    for name in ("c2", "c2b", "c3b", "c3", "c5"):
         wl = Wm.workload(name)
         d, Df, G, e = wl.head_dim, wl.feat_dim, wl.G, 2
-        other = (2 * d * e + 2 * d * e + 2 * G * d * e + 2 * Df * d * 4 + 2 * Df * 4) * wl.batch * wl.n_kv_heads
-        other = other * wl.n_layers + wl.n_layers * d * Df * e
+        units = wl.batch * wl.n_kv_heads
+        tok = (2 * d * e + 2 * d * e + 2 * G * d * e + Df * d * 4 + Df * 4) * units * wl.n_layers
+        wf = wl.n_layers * d * Df * e
         kv = wl.batch * A.kv_io_bytes(wl.windows, 10 ** 9, wl.n_kv_heads, d, e)
-        assert bench.decode_bytes(wl) == kv + other, name
+        write = sum((1 if W == 0 else 1 / bench.FOLD_PERIOD) * (Df * d * 4 + Df * 4) * units for W in wl.windows)
+        assert bench.decode_bytes(wl, state_write=1) == kv + tok + wf + (Df * d * 4 + Df * 4) * units * wl.n_layers
+        assert bench.decode_bytes(wl) == round(kv + tok + wf + write), name

@@ -38,7 +38,7 @@ def _positions(n, chunk):
     return sorted(p for p in pos if 0 <= p < n)
 
 
-@pytest.mark.parametrize("name", ["c2", "c3", "c3b", "c5", "c4u"])
+@pytest.mark.parametrize("name", ["c2", "c3", "c3b", "c5", "c4u", "c4"])
 def test_full_size_sampled(name):
     wl = W.workload(name)
     dev = torch.device("cuda:0")
