@@ -146,11 +146,12 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
  * at least 256.  Prefill takes one slot per layer of a launch (history rows
  * and per-segment state records) and batches as many layers per launch as
  * the given workspace holds, up to 64; this size holds as many as fit in
- * 1 GiB (at least one).  Decode uses the workspace only when a layer has
- * fewer than 512 (sequence, KV head) units: a decode launch with fewer than
- * 512 units splits long windows over several workgroups, whose partial
- * results it holds (at most 512 records; the size covers a call over any
- * subset of the layers).  0 if cfg is invalid. */
+ * 1 GiB (at least one).  Decode uses the workspace only when a launch has
+ * fewer (sequence, KV head) units than the device holds resident decode
+ * workgroups in one round (two per compute unit: 512 on MI355X): it then
+ * splits long windows over several workgroups, whose partial results it
+ * holds.  The size bounds that for every call on any device (at most 1024
+ * records; a call over any subset of the layers).  0 if cfg is invalid. */
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens);
 
 /* Zeroes the whole state: S = 0, z = 0 (S_0, Z_0 of the Sec. II-B

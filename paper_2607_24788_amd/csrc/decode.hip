@@ -20,9 +20,9 @@
 //   5. merge of the two parts over one shared denominator, output, pos += 1.
 //
 // One workgroup of 4 waves handles one unit, or one piece of a unit's window
-// when a launch has few units (the pieces of a unit run on one XCD and meet
-// in its L2; the last to finish merges them); units of the call are ordered
-// by decreasing window so the longest streams start first.
+// when a launch has few units (each piece writes a partial record to memory;
+// the last to finish merges them); units of the call are ordered by
+// decreasing window so the longest streams start first.
 #include <math.h>
 
 #include "glide_internal.h"
@@ -55,9 +55,10 @@ struct WindowTile {
 // finish (see the end of decode_kernel): the window parts (running max m, sum
 // l, weighted values acc per piece) over one max, plus piece 0's linear part,
 // over the shared denominator (hybrid forms: each part normalised on its
-// own, then added); then pos = p + 1.  The pieces of a unit run on one XCD,
-// so the records are read from that XCD's L2 (loads that miss the L1),
-// every load of the workgroup issued before the first wait.
+// own, then added); then pos = p + 1.  The pieces may run on different XCDs,
+// whose L2s are not coherent with each other: the records were written
+// through to memory and are read from there, every load of the workgroup
+// issued before the first wait.
 template <typename T, int D, int DF>
 __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& L, int rem, int64_t p) {
   constexpr int EPT = 4;                   // output elements per thread whose loads go first
@@ -89,11 +90,11 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
   const int mpc = tid / G, mh = tid - mpc * G;
   const bool mok = tid < np * G;
   const uint32_t mo = uint32_t(mh * RH) * 4;
-  const float m0 = bload_f_l2(r0, mok && mpc == 0 ? mo : kOOB);
-  const float m1 = bload_f_l2(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo : kOOB);
-  const float l0 = bload_f_l2(r0, mok && mpc == 0 ? mo + 4 : kOOB);
-  const float l1 = bload_f_l2(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo + 4 : kOOB);
-  const float dnv = bload_f_l2(r0, tid < G ? uint32_t(tid * RH + 2) * 4 : kOOB);  // linear denominator
+  const float m0 = bload_f_sys(r0, mok && mpc == 0 ? mo : kOOB);
+  const float m1 = bload_f_sys(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo : kOOB);
+  const float l0 = bload_f_sys(r0, mok && mpc == 0 ? mo + 4 : kOOB);
+  const float l1 = bload_f_sys(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo + 4 : kOOB);
+  const float dnv = bload_f_sys(r0, tid < G ? uint32_t(tid * RH + 2) * 4 : kOOB);  // linear denominator
   float v[EPT][kMaxPieces], nmv[EPT];
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
@@ -101,10 +102,10 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
     const int hh = i / D, c = i - hh * D;
     const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
     const bool ok = i < n;
-    v[e][0] = bload_f_l2(r0, ok ? o : kOOB);
+    v[e][0] = bload_f_sys(r0, ok ? o : kOOB);
 #pragma unroll
-    for (int pc = 1; pc < kMaxPieces; ++pc) v[e][pc] = bload_f_l2(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
-    nmv[e] = bload_f_l2(r0, ok ? o + D * 4 : kOOB);
+    for (int pc = 1; pc < kMaxPieces; ++pc) v[e][pc] = bload_f_sys(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
+    nmv[e] = bload_f_sys(r0, ok ? o + D * 4 : kOOB);
   }
   // every thread writes its slot (kThreads slots; no branch, so the loads
   // above are not sunk behind the record loads)
@@ -157,10 +158,10 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
     const int hh = i / D, c = i - hh * D;
     const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
     float vp[kMaxPieces];
-    vp[0] = bload_f_l2(r0, o);
+    vp[0] = bload_f_sys(r0, o);
 #pragma unroll
-    for (int pc = 1; pc < kMaxPieces; ++pc) vp[pc] = bload_f_l2(r1, pc < np ? (pc - 1) * rs + o : kOOB);
-    out_elem(i, vp, bload_f_l2(r0, o + D * 4));
+    for (int pc = 1; pc < kMaxPieces; ++pc) vp[pc] = bload_f_sys(r1, pc < np ? (pc - 1) * rs + o : kOOB);
+    out_elem(i, vp, bload_f_sys(r0, o + D * 4));
   }
   if (tid == 0) *pos_ptr = p + 1;
 }
@@ -191,7 +192,6 @@ void decode_kernel(DecodeArgs a) {
   const int per_layer = B * Hkv;
   const int prow = __builtin_amdgcn_readfirstlane(int(blockIdx.x) / a.row_stride);
   const int rem = int(blockIdx.x) - prow * a.row_stride;
-  if (rem >= per_layer) return;  // padding of a split launch's rows
   // (the table is read a dword at a time: a scalar load, no vector memory wait)
   const uint32_t lw = reinterpret_cast<const uint32_t*>(a.piece_layer)[prow >> 2];
   const LayerArg L = a.layers[(lw >> (8 * (prow & 3))) & 0xffu];
@@ -682,12 +682,12 @@ void decode_kernel(DecodeArgs a) {
     if (split) {
       const uint32_t ro = uint32_t(hh * (2 * D + 3)) * 4;
       if (c == 0) {
-        bstore_f_l2(rrec, ro, M);
-        bstore_f_l2(rrec, ro + 4, Ls);
-        bstore_f_l2(rrec, ro + 8, dn);
+        bstore_f_sys(rrec, ro, M);
+        bstore_f_sys(rrec, ro + 4, Ls);
+        bstore_f_sys(rrec, ro + 8, dn);
       }
-      bstore_f_l2(rrec, ro + uint32_t(3 + c) * 4, Ac);
-      if (piece == 0) bstore_f_l2(rrec, ro + uint32_t(3 + D + c) * 4, nm);
+      bstore_f_sys(rrec, ro + uint32_t(3 + c) * 4, Ac);
+      if (piece == 0) bstore_f_sys(rrec, ro + uint32_t(3 + D + c) * 4, nm);
       continue;
     }
     float o;
@@ -707,19 +707,18 @@ void decode_kernel(DecodeArgs a) {
     og[i] = from_f32<T>(o);
   }
   if (split) {
-    // The pieces of a unit run on one XCD (same workgroup index modulo 8),
-    // so the records, the count and the merge's loads all meet in that XCD's
-    // L2: every record store of the workgroup has reached the L2 before the
-    // unit's count moves (an add performed in the L2), and the workgroup that
-    // brings it to npiece reads the records from the L2, merges, and resets
-    // the count.
+    // Every record store of the workgroup has reached memory (written
+    // through, and waited for) before the unit's count moves; the count is
+    // a device-scope add, performed where every XCD sees it.  The workgroup
+    // that brings it to npiece reads the records from memory, merges, and
+    // resets the count.
     __shared__ int last;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
-      const brsrc_t rc = make_rsrc(lay + sec.cnt + unit * 4, 4);
-      last = __builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(1, rc, 0, 0, 0) == L.npiece - 1;
-      if (last) __builtin_amdgcn_raw_buffer_store_b32(0u, rc, 0, 0, 0);
+      int* cnt = reinterpret_cast<int*>(lay + sec.cnt) + unit;
+      last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == L.npiece - 1;
+      if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
     if (last) merge_unit<T, D, DF>(a, L, rem, p);

@@ -4,6 +4,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "glide_internal.h"
@@ -91,17 +92,38 @@ PrefillWorkspace prefill_ws(const glide_config* c, int64_t T, int32_t nl) {
                            linear_on(c), nl);
 }
 
+// Resident decode workgroups of one round on the current device:
+// kDecodeWgPerCu per compute unit, at most kMaxDecodeSlots.  Queried once per
+// device (the CU count does not change while the process runs).
+glide_status decode_slots(int32_t* out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static int32_t slots[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return GLIDE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(mu);
+  if (slots[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+      return GLIDE_ERR_HIP;
+    slots[dev] = int32_t(std::min<int64_t>(kMaxDecodeSlots, int64_t(cus) * kDecodeWgPerCu));
+  }
+  *out = slots[dev];
+  return GLIDE_OK;
+}
+
 // Decode window split (pieces per unit of each layer of one launch).  The
 // work of a unit is counted in 32-token window tiles plus kStateTiles for the
 // state pass; a layer whose units have work w gets min(kMaxPieces, ceil(w / q))
 // pieces, with q the smallest piece size (>= 4 tiles) for which the launch
-// fits in kDecodeSlots workgroups.  When the launch's units alone fill the
-// slots, nothing is split.  The plan depends only on the launch's layers, so
-// a call over one layer splits that layer's window over the whole device.
-std::vector<int32_t> decode_pieces(const glide_config* c, const int32_t* layers, int32_t n) {
+// fits in `slots` workgroups.  When the launch's units alone fill the slots,
+// nothing is split.  The plan depends only on the launch's layers and the
+// device, so a call over one layer splits that layer's window over the whole
+// device.
+std::vector<int32_t> decode_pieces(const glide_config* c, const int32_t* layers, int32_t n, int32_t slots) {
   std::vector<int32_t> np(n, 1);
   const int64_t per_layer = int64_t(c->batch) * c->n_kv_heads;
-  if (per_layer * n >= kDecodeSlots) return np;
+  if (per_layer * n >= slots) return np;
   const int st = linear_on(c) ? kStateTiles : 0;
   std::vector<int64_t> work(n);
   int64_t wmax = 4;
@@ -122,21 +144,22 @@ std::vector<int32_t> decode_pieces(const glide_config* c, const int32_t* layers,
   int64_t lo = 4, hi = wmax;  // wgs(wmax) = units <= slots
   while (lo < hi) {
     const int64_t mid = (lo + hi) / 2;
-    if (wgs(mid) <= kDecodeSlots) hi = mid;
+    if (wgs(mid) <= slots) hi = mid;
     else lo = mid + 1;
   }
   for (int32_t i = 0; i < n; ++i) np[i] = int32_t(pieces(lo, i));
   return np;
 }
 
-// Decode workspace bound over every call (what glide_workspace_bytes reports
-// and every decode call requires, whatever its layers): a launch splits only
-// when its units number fewer than kDecodeSlots, and then it has at most
-// kDecodeSlots workgroups, and at most the pieces its layers get at the
-// smallest piece size.
+// Decode workspace bound over every call on any device (what
+// glide_workspace_bytes reports and every decode call requires, whatever its
+// layers): a launch splits only when its units number fewer than its device's
+// slots (at most kMaxDecodeSlots), and then it has at most that many
+// workgroups, and at most the pieces its layers get at the smallest piece
+// size.
 size_t decode_ws(const glide_config* c) {
   const int64_t per_layer = int64_t(c->batch) * c->n_kv_heads;
-  if (per_layer >= kDecodeSlots) return 0;
+  if (per_layer >= kMaxDecodeSlots) return 0;
   const int st = linear_on(c) ? kStateTiles : 0;
   int64_t wgs = 0;
   bool any = false;
@@ -147,7 +170,8 @@ size_t decode_ws(const glide_config* c) {
     any = any || p > 1;
   }
   if (!any) return 0;
-  return size_t(align256(std::min<int64_t>(wgs, kDecodeSlots) * part_floats(c->n_q_heads / c->n_kv_heads, c->head_dim) * 4));
+  return size_t(align256(std::min<int64_t>(wgs, kMaxDecodeSlots) *
+                         part_floats(c->n_q_heads / c->n_kv_heads, c->head_dim) * 4));
 }
 
 // Decode-style launch descriptor of layers [layer0, layer0 + n): per launch
@@ -156,6 +180,9 @@ size_t decode_ws(const glide_config* c) {
 template <typename Fn>
 glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n_layers, DecodeArgs& a, Fn fn) {
   const int32_t per_layer = cfg->batch * cfg->n_kv_heads;
+  int32_t slots = 0;
+  const glide_status ss = decode_slots(&slots);
+  if (ss != GLIDE_OK) return ss;
   std::vector<int32_t> order(n_layers);
   for (int32_t i = 0; i < n_layers; ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
@@ -174,7 +201,7 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
     int32_t ls[kMaxLayersPerLaunch];
     for (int32_t i = 0; i < cnt; ++i) ls[i] = layer0 + order[first + i];
-    const std::vector<int32_t> np = decode_pieces(cfg, ls, cnt);
+    const std::vector<int32_t> np = decode_pieces(cfg, ls, cnt, slots);
     a.n_layers = cnt;
     int32_t rows = 0;
     bool split = false;
@@ -193,7 +220,7 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
       a.layers[i].prow1 = rows;
       for (int32_t r = 1; r < np[i]; ++r) a.piece_layer[rows++] = uint8_t(i);
     }
-    a.row_stride = split ? (per_layer + 7) / 8 * 8 : per_layer;
+    a.row_stride = per_layer;
     const glide_status s = hip_status(fn(a, rows * a.row_stride, split));
     if (s != GLIDE_OK) return s;
   }

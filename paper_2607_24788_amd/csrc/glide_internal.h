@@ -90,11 +90,14 @@ struct LayerArg {
 // Pieces write partial records (running max, sum and weighted values of the
 // window part per head; piece 0 adds the linear part); the piece that
 // finishes last (a per-unit counter in the state) merges them.  The split
-// depends on the layers of the launch only: the pieces are made as small as
-// possible while every workgroup of the launch still fits in one round of
-// kDecodeSlots resident workgroups (256 CUs x 2), since a second round would
-// be latency-bound; launches with kDecodeSlots units or more are not split.
-constexpr int kDecodeSlots = 512;
+// depends on the layers of the launch and on the device: the pieces are made
+// as small as possible while every workgroup of the launch still fits in one
+// round of resident workgroups (kDecodeWgPerCu per CU, from the device's CU
+// count), since a second round would be latency-bound; launches with that
+// many units or more are not split.  kMaxDecodeSlots bounds the round on any
+// device (and with it the partial records the workspace must hold).
+constexpr int kDecodeWgPerCu = 2;
+constexpr int kMaxDecodeSlots = 1024;
 constexpr int kMaxPieces = 16;
 constexpr int kStateTiles = 16;     // state pass cost in 32-token window tiles
 __host__ __device__ inline int decode_tiles_max(int32_t W) { return W > 0 ? (W + 31) / 32 + 1 : 0; }
@@ -429,23 +432,13 @@ __device__ __forceinline__ float bload_f(brsrc_t r, uint32_t off) {
 // System-coherent access (cache policy sc0 sc1): stores are written through
 // to memory and loads are served from memory, not from a cache that may hold
 // an older copy.  For data one workgroup writes and another, possibly on
-// another XCD, reads within the same kernel.
+// another XCD (each XCD has its own L2), reads within the same kernel.
 constexpr int kSysCoherent = 1 | 16;
-// XCD-coherent access: loads with sc0 miss the vector L1 and are served by
-// the XCD's L2; plain stores write through the L1 into that L2.  For data
-// one workgroup writes and another on the same XCD reads within a kernel.
-constexpr int kL2Coherent = 1;
 __device__ __forceinline__ float bload_f_sys(brsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSysCoherent));
 }
 __device__ __forceinline__ void bstore_f_sys(brsrc_t r, uint32_t off, float x) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, off, 0, kSysCoherent);
-}
-__device__ __forceinline__ float bload_f_l2(brsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kL2Coherent));
-}
-__device__ __forceinline__ void bstore_f_l2(brsrc_t r, uint32_t off, float x) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, off, 0, 0);
 }
 __device__ __forceinline__ bf16_t bload_elem(brsrc_t r, uint32_t off, bf16_t) {
   return bf16_t(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
@@ -570,10 +563,7 @@ struct DecodeArgs {
   int32_t n_layers;  // layers in this launch (<= kMaxLayersPerLaunch)
   int32_t form;      // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
   int32_t phi;       // feature map: 0 ReLU, 1 ELU + 1
-  // workgroups per piece row: B*Hkv, rounded up to a multiple of 8 when a
-  // window is split (the extra workgroups exit at once), so that every piece
-  // of a unit has the same workgroup index modulo 8 and runs on the same XCD
-  int32_t row_stride;
+  int32_t row_stride;  // workgroups per piece row: B * Hkv
   int32_t wf_heads;  // 1: phi_w holds one Wf per KV head ([layer][Hkv][d][Df])
   int32_t pad;
   LayerArg layers[kMaxLayersPerLaunch];  // sorted by decreasing W

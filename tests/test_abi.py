@@ -221,8 +221,9 @@ def test_workspace_sizes():
     rec = 4 * (2 * 128 + 3) * 4
     assert g.workspace_bytes(0) >= 3 * 2 * 2 * rec
     assert g.workspace_bytes(0) <= 3 * 2 * 2 * 16 * rec + 256
-    # many units of similar windows: no unit is worth splitting, no decode workspace
-    big = mk(n_layers=4, batch=64, n_q_heads=16, n_kv_heads=8, windows=[0, 5, 64, 100])
+    # a layer with as many units as any device holds resident decode
+    # workgroups (1024): nothing is ever split, no decode workspace
+    big = mk(n_layers=4, batch=128, n_q_heads=16, n_kv_heads=8, windows=[0, 5, 64, 100])
     assert big.workspace_bytes(0) == 256
     assert g.workspace_bytes(100000) > g.workspace_bytes(10)
 

@@ -147,13 +147,14 @@ def test_deferred_folding_state_every_step():
 
 def test_split_and_unsplit_paths():
     """Few units: long windows are split over several workgroups and merged
-    (the decode workspace holds their partial records); 512 units per layer
-    and more: one workgroup per unit in any call, no decode workspace.  Both
-    follow the definition from a ragged prefilled state."""
+    (the decode workspace holds their partial records); 1024 units per layer
+    and more (at least the resident decode workgroups of any device): one
+    workgroup per unit in any call, no decode workspace.  Both follow the
+    definition from a ragged prefilled state."""
     small = Case([0, 5, 40, 300], batch=1, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=9)
-    big = Case([0, 5, 40, 300], batch=64, Hq=16, Hkv=8, d=64, Df=64, dtype=torch.bfloat16, seed=10)
+    big = Case([0, 5, 40, 300], batch=128, Hq=16, Hkv=8, d=64, Df=64, dtype=torch.bfloat16, seed=10)
     assert small.g.workspace_bytes(0) > 256 and big.g.workspace_bytes(0) == 256
-    for case, lens in ((small, [333]), (big, [(37 * i) % 350 for i in range(64)])):
+    for case, lens in ((small, [333]), (big, [(37 * i) % 350 for i in range(128)])):
         n = 6
         q, k, v = case.tokens(max(lens) + n)
         st = case.new_state()
