@@ -50,7 +50,9 @@ typedef enum {
   GLIDE_ERR_UNSUPPORTED = -3, /* valid per the definition, not built here (d, Df, G, dtype) */
   GLIDE_ERR_ALIGN = -4,       /* a device pointer is not 16-byte aligned (state: 256) */
   GLIDE_ERR_SIZE = -5,        /* state or workspace smaller than required */
-  GLIDE_ERR_HIP = -6          /* a HIP launch failed */
+  GLIDE_ERR_HIP = -6,         /* a HIP launch failed */
+  GLIDE_ERR_SCRATCH = -7      /* glide_decode_step_noalloc: the call needs more than the library's
+                                 fixed decode scratch (GLIDE_DECODE_SCRATCH_BYTES) */
 } glide_status;
 
 /* Element type of q, k, v, out, the window ring and phi_w.  S and z are fp32. */
@@ -204,6 +206,29 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
                                int32_t layer0, int32_t n_layers, const void* phi_w,
                                const void* q, const void* k, const void* v, void* out,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Size of the fixed decode scratch of glide_decode_step_noalloc, per GPU. */
+#define GLIDE_DECODE_SCRATCH_BYTES (16u << 20)
+
+/* glide_decode_step without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  The same kernels and the same result as
+ * glide_decode_step; the partial records of split windows go to a fixed
+ * array of GLIDE_DECODE_SCRATCH_BYTES that the library holds on every GPU it
+ * runs on, until the process ends (its address is looked up once per device,
+ * on the first call with that device current).  Nothing is allocated or
+ * freed.  A config whose decode workspace (glide_workspace_bytes(cfg, 0))
+ * exceeds the scratch is rejected with GLIDE_ERR_SCRATCH before any HIP call
+ * (G <= 15 at d = 128 always fits).  Every call on one GPU shares that GPU's
+ * scratch: calls that overlap in time on one GPU (other streams, other
+ * threads) race and may return wrong results; serialise them.  The records
+ * are written before they are read within each call, so no call needs the
+ * scratch cleared.  Arguments, layouts and errors otherwise as for
+ * glide_decode_step. */
+glide_status glide_decode_step_noalloc(const glide_config* cfg, void* state, size_t state_bytes,
+                                       int32_t layer0, int32_t n_layers, const void* phi_w,
+                                       const void* q, const void* k, const void* v, void* out,
+                                       void* stream);
 
 /* Folds every pending token of layers [layer0, layer0 + n_layers) into S and
  * z (nf := max(0, p - W)), so that S and z hold exactly the Sec. II-B sums

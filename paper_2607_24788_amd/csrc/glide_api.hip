@@ -227,6 +227,30 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
   return GLIDE_OK;
 }
 
+// The allocation-free decode entry point's scratch: partial records of split
+// windows, GLIDE_DECODE_SCRATCH_BYTES per GPU, held until the process ends.
+// Host code never passes `scratch` itself to a kernel (in host code the name
+// stands for a host-side shadow); it passes the device address that
+// hipGetSymbolAddress returns for the current device, looked up once per
+// device.
+static __device__ __align__(256) float scratch[GLIDE_DECODE_SCRATCH_BYTES / sizeof(float)];
+
+glide_status scratch_address(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return GLIDE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return GLIDE_ERR_HIP;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return GLIDE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -240,6 +264,7 @@ const char* glide_status_string(glide_status s) {
     case GLIDE_ERR_ALIGN: return "misaligned device pointer (16 bytes; state 256 bytes)";
     case GLIDE_ERR_SIZE: return "state or workspace too small";
     case GLIDE_ERR_HIP: return "HIP launch failed";
+    case GLIDE_ERR_SCRATCH: return "the call needs more than the fixed decode scratch (GLIDE_DECODE_SCRATCH_BYTES)";
   }
   return "unknown status";
 }
@@ -315,6 +340,23 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
   return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g, int32_t wgs, bool) {
     return launch_decode(g, wgs, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
   });
+}
+
+glide_status glide_decode_step_noalloc(const glide_config* cfg, void* state, size_t state_bytes,
+                                       int32_t layer0, int32_t n_layers, const void* phi_w, const void* q,
+                                       const void* k, const void* v, void* out, void* stream) {
+  glide_status s = check_call(cfg, state, state_bytes, layer0, n_layers);
+  if (s != GLIDE_OK) return s;
+  const size_t need = decode_ws(cfg);
+  if (need > GLIDE_DECODE_SCRATCH_BYTES) return GLIDE_ERR_SCRATCH;
+  if (!phi_w || !q || !k || !v || !out) return GLIDE_ERR_NULL;
+  void* ws = nullptr;
+  if (need) {
+    s = scratch_address(&ws);
+    if (s != GLIDE_OK) return s;
+  }
+  return glide_decode_step(cfg, state, state_bytes, layer0, n_layers, phi_w, q, k, v, out, ws,
+                           need ? size_t(GLIDE_DECODE_SCRATCH_BYTES) : 0, stream);
 }
 
 glide_status glide_state_flush(const glide_config* cfg, void* state, size_t state_bytes, int32_t layer0,

@@ -24,10 +24,11 @@ HYBRID_STATE_ALL = 4
 PER_HEAD_PHI = 8
 
 STATUS = {0: "GLIDE_OK", -1: "GLIDE_ERR_NULL", -2: "GLIDE_ERR_INVALID", -3: "GLIDE_ERR_UNSUPPORTED",
-          -4: "GLIDE_ERR_ALIGN", -5: "GLIDE_ERR_SIZE", -6: "GLIDE_ERR_HIP"}
+          -4: "GLIDE_ERR_ALIGN", -5: "GLIDE_ERR_SIZE", -6: "GLIDE_ERR_HIP", -7: "GLIDE_ERR_SCRATCH"}
+DECODE_SCRATCH_BYTES = 16 << 20
 
 EXPORTS = ["glide_state_bytes", "glide_state_layout", "glide_workspace_bytes", "glide_state_init",
-           "glide_prefill", "glide_decode_step", "glide_state_flush", "glide_feature_map",
+           "glide_prefill", "glide_decode_step", "glide_decode_step_noalloc", "glide_state_flush", "glide_feature_map",
            "glide_status_string"]
 
 
@@ -87,6 +88,9 @@ def load_library(path=None):
     lib.glide_decode_step.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp, vp,
                                       vp, vp, vp, ctypes.c_size_t, vp]
     lib.glide_decode_step.restype = ctypes.c_int
+    lib.glide_decode_step_noalloc.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp,
+                                              vp, vp, vp, vp]
+    lib.glide_decode_step_noalloc.restype = ctypes.c_int
     lib.glide_state_flush.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp]
     lib.glide_state_flush.restype = ctypes.c_int
     lib.glide_feature_map.argtypes = [cfgp, vp, vp, ctypes.c_int64, vp, vp]
@@ -243,6 +247,17 @@ class Glide:
                                        _ptr(out), _ptr(workspace), ws_bytes, _stream(stream))
         if s:
             raise GlideError(s, "glide_decode_step", self.lib)
+
+    def decode_step_noalloc(self, state, phi_w, q, k, v, out, layer0=0, n_layers=None, stream=None):
+        """decode_step with no workspace: split-window records go to the
+        library's fixed per-GPU scratch (calls on one GPU must not overlap)."""
+        if n_layers is None:
+            n_layers = self.n_layers - layer0
+        s = self.lib.glide_decode_step_noalloc(ctypes.byref(self.cfg), _ptr(state),
+                                               state.numel() * state.element_size(), int(layer0), int(n_layers),
+                                               _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(stream))
+        if s:
+            raise GlideError(s, "glide_decode_step_noalloc", self.lib)
 
     def prefill(self, state, phi_w, q, k, v, cu_seqlens, out, workspace, layer0=0, n_layers=None, chunk=0,
                 stream=None):

@@ -266,3 +266,26 @@ def test_feature_map_argument_errors():
 def test_status_strings(lib):
     for code in glide.STATUS:
         assert lib.glide_status_string(code)
+
+
+def test_noalloc_decode_rejects_before_any_hip_call():
+    """glide_decode_step_noalloc validates on the host: a config whose decode
+    workspace exceeds the fixed scratch gets GLIDE_ERR_SCRATCH, other errors
+    the codes glide_decode_step gives (no HIP call is made)."""
+    P = [ctypes.c_void_p(4096)] * 5
+
+    def call(g, state=256, n=1):
+        return g.lib.glide_decode_step_noalloc(ctypes.byref(g.cfg), ctypes.c_void_p(state) if state else None,
+                                               g.state_bytes(), 0, n, *P, None)
+    # G = 16 at d = 128, few units and huge windows: 1024 records of 16 x 259 floats > 16 MiB
+    big = mk(n_layers=3, batch=32, n_q_heads=16, n_kv_heads=1, windows=[1 << 20] * 3)
+    assert big.workspace_bytes(0) > glide.DECODE_SCRATCH_BYTES
+    assert call(big) == -7
+    assert "scratch" in big.lib.glide_status_string(-7).decode()
+    g = mk()
+    assert g.workspace_bytes(0) <= glide.DECODE_SCRATCH_BYTES
+    assert call(g, state=None) == -1
+    assert call(g, state=260) == -4
+    assert call(g, n=4) == -2
+    assert g.lib.glide_decode_step_noalloc(ctypes.byref(g.cfg), ctypes.c_void_p(256), g.state_bytes(), 0, 1,
+                                           None, *P[1:], None) == -1
