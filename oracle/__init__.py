@@ -71,6 +71,12 @@ def _d(a):
     return a, a.ctypes.data_as(_c_double_p)
 
 
+def _shape(name, a, want):
+    """Raise unless array a has shape `want` (the C code reads exactly that)."""
+    if tuple(a.shape) != tuple(want):
+        raise ValueError(f"{name} has shape {tuple(a.shape)}, expected {tuple(want)}")
+
+
 class Oracle:
     """One layer's oracle: Hq, Hkv, d, Df, window W, linear on/off, tau, and
     the merge form (0: GLIDE's shared denominator; 1, 2: the Appendix's two
@@ -92,12 +98,27 @@ class Oracle:
         L = self.L
         x, xp = _d(x)
         Wf, wp = _d(Wf)
+        _shape("Wf", Wf, (L.head_dim, L.feat_dim))
+        if x.shape[-1] != L.head_dim:
+            raise ValueError(f"x rows have {x.shape[-1]} elements, expected {L.head_dim}")
         rows = x.size // L.head_dim
         out = np.empty(x.shape[:-1] + (L.feat_dim,), np.float64)
         self.lib.oracle_phi(ctypes.byref(L), wp, rows, xp, out.ctypes.data_as(_c_double_p))
         return out
 
     # -- definition (quadratic) form ----------------------------------------
+    def _wf_shape(self):
+        L = self.L
+        return ((L.n_kv_heads,) if L.wf_per_head else ()) + (L.head_dim, L.feat_dim)
+
+    def _check_history(self, Wf, q, k, v, n):
+        L = self.L
+        _shape("Wf", Wf, self._wf_shape())
+        if q is not None:
+            _shape("q", q, (n, L.n_q_heads, L.head_dim))
+        _shape("k", k, (n, L.n_kv_heads, L.head_dim))
+        _shape("v", v, (n, L.n_kv_heads, L.head_dim))
+
     def attend(self, Wf, q, k, v, positions=None):
         """O_t for one sequence.  q [n][Hq][d], k/v [n][Hkv][d].
 
@@ -109,6 +130,7 @@ class Oracle:
         v, vp = _d(v)
         Wf, wp = _d(Wf)
         n = q.shape[0]
+        self._check_history(Wf, q, k, v, n)
         if positions is None:
             positions = np.arange(n, dtype=np.int64)
         pos = np.ascontiguousarray(np.asarray(positions, dtype=np.int64))
@@ -128,6 +150,9 @@ class Oracle:
         Wf, wp = _d(Wf)
         if p is None:
             p = k.shape[0]
+        self._check_history(Wf, None, k, v, k.shape[0])
+        if not 0 <= p <= k.shape[0]:
+            raise ValueError(f"p = {p} outside [0, {k.shape[0]}]")
         S = np.empty((L.n_kv_heads, L.feat_dim, L.head_dim), np.float64)
         z = np.empty((L.n_kv_heads, L.feat_dim), np.float64)
         rc = self.lib.oracle_state(ctypes.byref(L), wp, int(p), kp, vp,
@@ -148,6 +173,8 @@ class Oracle:
         lg, lgp = _d(log_gates)
         Wf, wp = _d(Wf)
         n = q.shape[0]
+        self._check_history(Wf, q, k, v, n)
+        _shape("log_gates", lg, (n, L.n_kv_heads))
         pos = np.arange(n, dtype=np.int64) if positions is None else np.ascontiguousarray(positions, np.int64)
         out = np.empty((len(pos), L.n_q_heads, L.head_dim), np.float64)
         rc = self.lib.oracle_attend_gated(ctypes.byref(L), wp, n, qp, kp, vp, lgp, len(pos),
@@ -165,6 +192,10 @@ class Oracle:
         Wf, wp = _d(Wf)
         if p is None:
             p = k.shape[0]
+        self._check_history(Wf, None, k, v, k.shape[0])
+        _shape("log_gates", lg, (k.shape[0], L.n_kv_heads))
+        if not 0 <= p <= k.shape[0]:
+            raise ValueError(f"p = {p} outside [0, {k.shape[0]}]")
         S = np.empty((L.n_kv_heads, L.feat_dim, L.head_dim), np.float64)
         z = np.empty((L.n_kv_heads, L.feat_dim), np.float64)
         rc = self.lib.oracle_state_gated(ctypes.byref(L), wp, int(p), kp, vp, lgp,
@@ -200,6 +231,14 @@ class Oracle:
         k, kp = _d(k)
         v, vp = _d(v)
         Wf, wp = _d(Wf)
+        _shape("Wf", Wf, self._wf_shape())
+        _shape("q", q, (B, L.n_q_heads, L.head_dim))
+        _shape("k", k, (B, L.n_kv_heads, L.head_dim))
+        _shape("v", v, (B, L.n_kv_heads, L.head_dim))
+        _shape("S", st["S"], (B, L.n_kv_heads, L.feat_dim, L.head_dim))
+        _shape("z", st["z"], (B, L.n_kv_heads, L.feat_dim))
+        _shape("wk", st["wk"], (B, L.n_kv_heads, L.window, L.head_dim))
+        _shape("wv", st["wv"], (B, L.n_kv_heads, L.window, L.head_dim))
         out = np.empty((B, L.n_q_heads, L.head_dim), np.float64)
         P = lambda a: a.ctypes.data_as(_c_double_p)
         rc = self.lib.oracle_decode_batch(ctypes.byref(L), wp, B, P(st["S"]), P(st["z"]),

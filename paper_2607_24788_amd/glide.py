@@ -106,6 +106,24 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _check(name, t, numel=None, dtype=None):
+    """The library reads and writes through raw pointers and cannot see sizes
+    or layouts: refuse a tensor that is not a contiguous device tensor of the
+    expected element type holding at least `numel` elements."""
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, at least {numel} needed")
+
+
 def _stream(stream):
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -219,6 +237,20 @@ class Glide:
             "window": lay.window, "ring_slots": R,
         }
 
+    def _wf_numel(self, n_layers):
+        return n_layers * (self.n_kv_heads if self.per_head_phi else 1) * self.head_dim * self.feat_dim
+
+    def _check_decode(self, state, phi_w, q, k, v, out, n_layers):
+        dt = self.torch_dtype
+        _check("state", state)
+        _check("phi_w", phi_w, self._wf_numel(n_layers), dt)
+        nq = n_layers * self.batch * self.n_q_heads * self.head_dim
+        nkv = n_layers * self.batch * self.n_kv_heads * self.head_dim
+        _check("q", q, nq, dt)
+        _check("k", k, nkv, dt)
+        _check("v", v, nkv, dt)
+        _check("out", out, nq, dt)
+
     # -- calls ---------------------------------------------------------------
     def state_init(self, state, stream=None):
         s = self.lib.glide_state_init(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
@@ -233,6 +265,8 @@ class Glide:
         """Fold every pending token into S, z (nf := max(0, pos - W))."""
         if n_layers is None:
             n_layers = self.n_layers - layer0
+        _check("state", state)
+        _check("phi_w", phi_w, self._wf_numel(n_layers), self.torch_dtype)
         s = self.lib.glide_state_flush(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
                                        int(layer0), int(n_layers), _ptr(phi_w), _stream(stream))
         if s:
@@ -241,6 +275,8 @@ class Glide:
     def decode_step(self, state, phi_w, q, k, v, out, workspace=None, layer0=0, n_layers=None, stream=None):
         if n_layers is None:
             n_layers = self.n_layers - layer0
+        self._check_decode(state, phi_w, q, k, v, out, n_layers)
+        _check("workspace", workspace)
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         s = self.lib.glide_decode_step(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
                                        int(layer0), int(n_layers), _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v),
@@ -253,6 +289,7 @@ class Glide:
         library's fixed per-GPU scratch (calls on one GPU must not overlap)."""
         if n_layers is None:
             n_layers = self.n_layers - layer0
+        self._check_decode(state, phi_w, q, k, v, out, n_layers)
         s = self.lib.glide_decode_step_noalloc(ctypes.byref(self.cfg), _ptr(state),
                                                state.numel() * state.element_size(), int(layer0), int(n_layers),
                                                _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(stream))
@@ -267,6 +304,14 @@ class Glide:
         if len(cu) != self.batch + 1:
             raise ValueError("cu_seqlens needs batch + 1 entries")
         cu_arr = (ctypes.c_int32 * len(cu))(*cu)
+        T, dt = cu[-1], self.torch_dtype
+        _check("state", state)
+        _check("phi_w", phi_w, self._wf_numel(n_layers), dt)
+        _check("q", q, n_layers * T * self.n_q_heads * self.head_dim, dt)
+        _check("k", k, n_layers * T * self.n_kv_heads * self.head_dim, dt)
+        _check("v", v, n_layers * T * self.n_kv_heads * self.head_dim, dt)
+        _check("out", out, n_layers * T * self.n_q_heads * self.head_dim, dt)
+        _check("workspace", workspace)
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         s = self.lib.glide_prefill(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
                                    int(layer0), int(n_layers), _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v), cu_arr,
@@ -277,6 +322,9 @@ class Glide:
 
     def feature_map(self, phi_w, x, out, stream=None):
         rows = out.numel() // self.feat_dim
+        _check("phi_w", phi_w, self.head_dim * self.feat_dim, self.torch_dtype)
+        _check("x", x, rows * self.head_dim, self.torch_dtype)
+        _check("out", out, rows * self.feat_dim, self.torch_dtype)
         s = self.lib.glide_feature_map(ctypes.byref(self.cfg), _ptr(phi_w), _ptr(x), int(rows), _ptr(out),
                                        _stream(stream))
         if s:

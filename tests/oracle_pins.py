@@ -40,7 +40,7 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "wor
 
 
 def _eval_closed_form(expr):
-    return float(eval(expr, {"__builtins__": {}}, {"e": math.e, "exp": math.exp}))
+    return float(eval(expr, {"__builtins__": {}}, {"e": math.e, "exp": math.exp, "log": math.log}))
 
 
 def _rand_case(seed, n, Hq, Hkv, d, Df, scale=1.0):
@@ -517,12 +517,63 @@ def pin_gated_linear_state(lib):
     return None
 
 
+def pin_per_head_mirrored_worked_example(lib):
+    """Per-head feature maps on the worked example: KV head 0 takes Wf = 1 and
+    the example's inputs; KV head 1 takes Wf = -1 and the example's q and k
+    negated (v unchanged).  phi_1(-x) = max(0, -(-x)) = phi_0(x) and
+    (-q).(-k) = q.k, so both heads must give the worked example's closed
+    forms (W in {0, 1, 2}).  A map that ignored the head would give head 1
+    phi(q) = 0: no linear part at all."""
+    ex = json.load(open(GOLDEN))
+    s = ex["setup"]
+    q0, k0, v0 = (np.array(s[x]) for x in ("q", "k", "v"))
+    q = np.stack([q0, -q0], 1)[:, :, None]          # [3][2 heads][d = 1]
+    k = np.stack([k0, -k0], 1)[:, :, None]
+    v = np.stack([v0, v0], 1)[:, :, None]
+    Wf = np.array([[[1.0]], [[-1.0]]])              # [Hkv][d][Df]
+    for case in ex["cases"]:
+        if case.get("form", 0) != 0 or case.get("phi", 0) != 0 or not case["linear"] or case["window"] > 2:
+            continue
+        o = oracle.Oracle(2, 2, 1, 1, case["window"], tau=s["tau"], lib=lib, wf_per_head=True)
+        got = o.attend(Wf, q, k, v)[:, :, 0]
+        want = np.array([_eval_closed_form(x) for x in case["out"]])
+        for h in range(2):
+            if not np.allclose(got[:, h], want, rtol=1e-12, atol=1e-12):
+                return f"per-head mirrored worked example W={case['window']} head {h}: {got[:, h]} != {want}"
+    return None
+
+
+def pin_gated_worked_example(lib):
+    """The gated state on the hand-derived worked example (tests/golden,
+    "gated"): a constant log-gate -ln 2, W in {0, 1, 2}, outputs and the
+    state after the three tokens in closed form."""
+    ex = json.load(open(GOLDEN))
+    s, gx = ex["setup"], ex["gated"]
+    q = np.array(s["q"]).reshape(3, 1, 1)
+    k = np.array(s["k"]).reshape(3, 1, 1)
+    v = np.array(s["v"]).reshape(3, 1, 1)
+    Wf = np.array(s["Wf"])
+    lg = np.full((3, 1), _eval_closed_form(gx["log_gate"]))
+    for case in gx["cases"]:
+        o = oracle.Oracle(1, 1, 1, 1, case["window"], tau=s["tau"], lib=lib)
+        got = o.attend_gated(Wf, q, k, v, lg).ravel()
+        want = np.array([_eval_closed_form(x) for x in case["out"]])
+        if not np.allclose(got, want, rtol=1e-12, atol=1e-12):
+            return f"gated worked example W={case['window']}: {got} != {want}"
+        S, z = o.state_gated(Wf, k, v, lg)
+        if not (abs(S.item() - _eval_closed_form(case["S"])) < 1e-12
+                and abs(z.item() - _eval_closed_form(case["z"])) < 1e-12):
+            return f"gated worked example state W={case['window']}: S={S.item()} z={z.item()}"
+    return None
+
+
 ALL_PINS = [pin_worked_example, pin_full_window_is_causal_softmax, pin_band_is_masked_sdpa,
             pin_w0_is_causal_linear, pin_w1_closed_form, pin_recurrent_equals_definition,
             pin_state_direct_sums, pin_v_ones, pin_convex_hull, pin_linearity,
             pin_gqa_is_repeated_mha, pin_zero_over_zero, pin_continue_from_state,
             pin_hybrid_forms_are_band_plus_linear, pin_hybrid_v_ones, pin_softmax_worked_example,
-            pin_softmax_features, pin_per_head_feature_map, pin_gated_linear_state]
+            pin_softmax_features, pin_per_head_feature_map, pin_gated_linear_state, pin_gated_worked_example,
+            pin_per_head_mirrored_worked_example]
 
 
 def run_all(lib):

@@ -289,3 +289,19 @@ def test_noalloc_decode_rejects_before_any_hip_call():
     assert call(g, n=4) == -2
     assert g.lib.glide_decode_step_noalloc(ctypes.byref(g.cfg), ctypes.c_void_p(256), g.state_bytes(), 0, 1,
                                            None, *P[1:], None) == -1
+
+
+def test_binding_refuses_tensors_the_kernels_would_overrun():
+    """The binding checks every tensor before the ctypes call (device,
+    contiguous, element type, size): the library sees raw pointers only."""
+    g = mk()
+    t = lambda *shape, dt=torch.bfloat16: torch.zeros(shape, dtype=dt)
+    args = (t(16, dt=torch.uint8), t(3, 128, 64), t(3, 2, 8, 128), t(3, 2, 2, 128), t(3, 2, 2, 128),
+            t(3, 2, 8, 128))
+    with pytest.raises(ValueError, match="device tensor"):
+        g.decode_step(*args)
+    with pytest.raises(ValueError, match="device tensor"):
+        g.prefill(args[0], args[1], t(3, 5, 8, 128), t(3, 5, 2, 128), t(3, 5, 2, 128), [0, 2, 5],
+                  t(3, 5, 8, 128), t(256, dt=torch.uint8))
+    with pytest.raises(ValueError, match="device tensor"):
+        g.feature_map(t(128, 64), t(4, 128), t(4, 64))

@@ -42,4 +42,4 @@ def test_pins_reject_planted_mistake(mutant):
         path = obuild.build(os.path.join(td, f"liboracle_m{mutant}.so"), mutant=mutant)
         lib = oracle.load(path)
         fails = oracle_pins.run_all(lib)
-    assert fails, f"mutant {mutant} passed every pin"
+    assert len(fails) >= 2, f"mutant {mutant} failed fewer than two pins: {fails}"
