@@ -151,8 +151,10 @@ class Oracle:
         if p is None:
             p = k.shape[0]
         self._check_history(Wf, None, k, v, k.shape[0])
-        if not 0 <= p <= k.shape[0]:
-            raise ValueError(f"p = {p} outside [0, {k.shape[0]}]")
+        # the sums read tokens [0, p - W) (every token before p in form 2)
+        nfold = 0 if not L.linear else (p if L.form == 2 else max(0, p - L.window))
+        if p < 0 or nfold > k.shape[0]:
+            raise ValueError(f"the state after p = {p} tokens needs {nfold} of the {k.shape[0]} given")
         S = np.empty((L.n_kv_heads, L.feat_dim, L.head_dim), np.float64)
         z = np.empty((L.n_kv_heads, L.feat_dim), np.float64)
         rc = self.lib.oracle_state(ctypes.byref(L), wp, int(p), kp, vp,
