@@ -166,7 +166,7 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
   if (tid == 0) *pos_ptr = p + 1;
 }
 
-template <typename T, int D, int DF>
+template <typename T, int D, int DF, bool NT>
 __global__ __launch_bounds__(kThreads)
 __attribute__((amdgpu_waves_per_eu(GLIDE_DECODE_WAVES_PER_SIMD, GLIDE_DECODE_WAVES_PER_SIMD)))
 void decode_kernel(DecodeArgs a) {
@@ -275,7 +275,7 @@ void decode_kernel(DecodeArgs a) {
   }
   float4 sr[STEPS];
 #pragma unroll
-  for (int s = 0; s < STEPS; ++s) sr[s] = bload_f4(rS, lin_call ? uint32_t(((f0 + s * RPS + lr) * D + c4) * 4) : kOOB);
+  for (int s = 0; s < STEPS; ++s) sr[s] = bload_f4_s<NT>(rS, lin_call ? uint32_t(((f0 + s * RPS + lr) * D + c4) * 4) : kOOB);
   float zf = bload_f(rz, lin_call && lane < RW ? uint32_t((f0 + lane) * 4) : kOOB);
   // the new token's element tid % D (its own score, and the ring write at the end)
   const T kraw = bload_elem(rk, uint32_t(tid % D) * ES, T());
@@ -331,15 +331,25 @@ void decode_kernel(DecodeArgs a) {
   // row m of sub-tile t is token j0 + 8(m/4) + 4t + m%4, so that after QK^T
   // lane group lg holds tokens j0 + 8lg .. j0 + 8lg + 7, exactly the A-operand
   // layout PV needs.  A tile that is not needed reads zeros (no traffic).
-  auto load_tile = [&](WindowTile<T, D>& tl, uint32_t s0t, bool valid) {
+  // Only the tile's tokens [lo, pn) (offsets from j0) are in the window: a
+  // lane whose key row, or whose 8 value tokens, lie wholly outside it reads
+  // zeros instead (no traffic; the edge tiles of a window would otherwise
+  // fetch up to 31 tokens each beyond it).  NT: non-temporal loads (a state
+  // blob far larger than the Infinity Cache).
+  auto load_tile = [&](WindowTile<T, D>& tl, uint32_t s0t, bool valid, int lo, int pn) {
     const uint32_t base = valid ? s0t * D * ES : kOOB;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < 2; ++t) {
+      const int tok = 8 * (hq >> 2) + 4 * t + (hq & 3);
+      const bool kin = tok >= lo && tok < pn;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk)
-        bload_frag(tl.k[t][kk], rK, base + uint32_t((((t * KS + kk) * 4 + lg) * 16 + hq) * 8) * ES);
+        bload_frag_s<NT>(tl.k[t][kk], rK, kin ? base + uint32_t((((t * KS + kk) * 4 + lg) * 16 + hq) * 8) * ES : kOOB);
+    }
+    const bool vin = 8 * lg + 8 > lo && 8 * lg < pn;
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) bload_frag(tl.v[ct], rV, base + uint32_t(((ct * 4 + lg) * 16 + hq) * 8) * ES);
+    for (int ct = 0; ct < CT; ++ct)
+      bload_frag_s<NT>(tl.v[ct], rV, vin ? base + uint32_t(((ct * 4 + lg) * 16 + hq) * 8) * ES : kOOB);
   };
 
   // rows of the feature-map tile, which are also the queries of the window's
@@ -378,7 +388,7 @@ void decode_kernel(DecodeArgs a) {
   }
   // first window tile of this wave
   WindowTile<T, D> ta, tb;
-  load_tile(ta, s0, W > 0 && it < n_tiles);
+  load_tile(ta, s0, W > 0 && it < n_tiles, clamp_rel(tlo - j0), clamp_rel(p - j0));
 
   // Wf B fragments of this wave's features: the staged rows are gathered by
   // column from LDS (the wave reads only what it wrote itself).
@@ -604,13 +614,15 @@ void decode_kernel(DecodeArgs a) {
     // two register stages: the next tile's loads are in flight while the
     // current one is computed (a tile past the range reads zeros)
     while (it < n_tiles) {
-      load_tile(tb, wrap_once(s0 + step, R), it + kWaves < n_tiles);
+      load_tile(tb, wrap_once(s0 + step, R), it + kWaves < n_tiles, clamp_rel(tlo - j0 - 32 * kWaves),
+                clamp_rel(p - j0 - 32 * kWaves));
       compute_tile(ta, clamp_rel(tlo - j0), clamp_rel(p - j0));
       it += kWaves;
       j0 += 32 * kWaves;
       s0 = wrap_once(s0 + step, R);
       if (it >= n_tiles) break;
-      load_tile(ta, wrap_once(s0 + step, R), it + kWaves < n_tiles);
+      load_tile(ta, wrap_once(s0 + step, R), it + kWaves < n_tiles, clamp_rel(tlo - j0 - 32 * kWaves),
+                clamp_rel(p - j0 - 32 * kWaves));
       compute_tile(tb, clamp_rel(tlo - j0), clamp_rel(p - j0));
       it += kWaves;
       j0 += 32 * kWaves;
@@ -816,7 +828,7 @@ hipError_t flush_t(const DecodeArgs& a, hipStream_t stream) {
 }
 
 template <typename T, int D, int DF>
-hipError_t launch_t(const DecodeArgs& a, int total_wg, hipStream_t stream) {
+hipError_t launch_t(const DecodeArgs& a, int total_wg, bool streaming, hipStream_t stream) {
   const int G = a.G;
   // ph, pvl, kpl, vpl, spl, pa; then lnum .. wl, or the staged Wf columns that
   // share their memory (bf16: kWaves x D rows of RW + 2 elements)
@@ -825,24 +837,29 @@ hipError_t launch_t(const DecodeArgs& a, int total_wg, hipStream_t stream) {
   const size_t tail = size_t(kWaves) * RPS * G * D + kWaves * G + size_t(kWaves) * G * D + kWaves * G + kWaves * G;
   const size_t staged = sizeof(T) == 2 ? size_t(kWaves) * D * (DF / kWaves + 2) / 2 : 0;
   const size_t floats = head + (tail > staged ? tail : staged);
-  hipLaunchKernelGGL((decode_kernel<T, D, DF>), dim3(unsigned(total_wg)), dim3(kThreads), floats * sizeof(float),
-                     stream, a);
+  if (streaming)
+    hipLaunchKernelGGL((decode_kernel<T, D, DF, true>), dim3(unsigned(total_wg)), dim3(kThreads),
+                       floats * sizeof(float), stream, a);
+  else
+    hipLaunchKernelGGL((decode_kernel<T, D, DF, false>), dim3(unsigned(total_wg)), dim3(kThreads),
+                       floats * sizeof(float), stream, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_decode(const DecodeArgs& a, int total_wg, int d, int Df, int dtype, hipStream_t stream) {
+hipError_t launch_decode(const DecodeArgs& a, int total_wg, int d, int Df, int dtype, bool streaming,
+                         hipStream_t stream) {
   if (dtype == GLIDE_BF16) {
-    if (d == 128 && Df == 128) return launch_t<bf16_t, 128, 128>(a, total_wg, stream);
-    if (d == 128 && Df == 64) return launch_t<bf16_t, 128, 64>(a, total_wg, stream);
-    if (d == 64 && Df == 128) return launch_t<bf16_t, 64, 128>(a, total_wg, stream);
-    if (d == 64 && Df == 64) return launch_t<bf16_t, 64, 64>(a, total_wg, stream);
+    if (d == 128 && Df == 128) return launch_t<bf16_t, 128, 128>(a, total_wg, streaming, stream);
+    if (d == 128 && Df == 64) return launch_t<bf16_t, 128, 64>(a, total_wg, streaming, stream);
+    if (d == 64 && Df == 128) return launch_t<bf16_t, 64, 128>(a, total_wg, streaming, stream);
+    if (d == 64 && Df == 64) return launch_t<bf16_t, 64, 64>(a, total_wg, streaming, stream);
   } else {
-    if (d == 128 && Df == 128) return launch_t<float, 128, 128>(a, total_wg, stream);
-    if (d == 128 && Df == 64) return launch_t<float, 128, 64>(a, total_wg, stream);
-    if (d == 64 && Df == 128) return launch_t<float, 64, 128>(a, total_wg, stream);
-    if (d == 64 && Df == 64) return launch_t<float, 64, 64>(a, total_wg, stream);
+    if (d == 128 && Df == 128) return launch_t<float, 128, 128>(a, total_wg, streaming, stream);
+    if (d == 128 && Df == 64) return launch_t<float, 128, 64>(a, total_wg, streaming, stream);
+    if (d == 64 && Df == 128) return launch_t<float, 64, 128>(a, total_wg, streaming, stream);
+    if (d == 64 && Df == 64) return launch_t<float, 64, 64>(a, total_wg, streaming, stream);
   }
   return hipErrorInvalidValue;
 }

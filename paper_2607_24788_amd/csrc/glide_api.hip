@@ -337,8 +337,11 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
   a.v = v;
   a.out = out;
   a.part = static_cast<float*>(workspace);
+  // a state blob far larger than the Infinity Cache is streamed (every step
+  // reads it all): non-temporal loads; a smaller one is re-read from the cache
+  const bool streaming = state_bytes_i(cfg) > kStreamingStateBytes;
   return for_layer_groups(cfg, layer0, n_layers, a, [&](const DecodeArgs& g, int32_t wgs, bool) {
-    return launch_decode(g, wgs, cfg->head_dim, cfg->feat_dim, cfg->dtype, hipStream_t(stream));
+    return launch_decode(g, wgs, cfg->head_dim, cfg->feat_dim, cfg->dtype, streaming, hipStream_t(stream));
   });
 }
 

@@ -429,6 +429,41 @@ __device__ __forceinline__ float4 bload_f4(brsrc_t r, uint32_t off) {
 __device__ __forceinline__ float bload_f(brsrc_t r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
+// Non-temporal loads (cache policy nt): for data that will not be read
+// again while it could still be cached, such as a decode unit's window tiles
+// and state rows when the whole state blob is far larger than the 256 MB
+// Infinity Cache; they would otherwise displace reused lines (Wf, the pending
+// tokens).  Measured on the batch-32 32K-context stack (5.3 GB of state):
+// 907 -> 840 us per decode step.  A blob that fits the cache is re-read from
+// it on the next step, and plain loads keep it there (the batch-1 8K stack,
+// 77 MB: 22.4 us per step with plain loads, 23.0 with non-temporal ones).
+constexpr int kNonTemporal = 2;
+constexpr int64_t kStreamingStateBytes = int64_t(128) << 20;
+__device__ __forceinline__ void bload_frag_nt(Frag<bf16_t>& f, brsrc_t r, uint32_t off) {
+  f.v = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal));
+}
+__device__ __forceinline__ void bload_frag_nt(Frag<float>& f, brsrc_t r, uint32_t off) {
+  const float4 a = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal));
+  const float4 b = __builtin_bit_cast(
+      float4, __builtin_amdgcn_raw_buffer_load_b128(r, off == kOOB ? kOOB : off + 16, 0, kNonTemporal));
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+}
+__device__ __forceinline__ float4 bload_f4_nt(brsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal));
+}
+// Non-temporal when NT, plain otherwise (the cache policy is an immediate).
+template <bool NT, typename T>
+__device__ __forceinline__ void bload_frag_s(Frag<T>& f, brsrc_t r, uint32_t off) {
+  if constexpr (NT) bload_frag_nt(f, r, off);
+  else bload_frag(f, r, off);
+}
+template <bool NT>
+__device__ __forceinline__ float4 bload_f4_s(brsrc_t r, uint32_t off) {
+  if constexpr (NT) return bload_f4_nt(r, off);
+  else return bload_f4(r, off);
+}
+
 // System-coherent access (cache policy sc0 sc1): stores are written through
 // to memory and loads are served from memory, not from a cache that may hold
 // an older copy.  For data one workgroup writes and another, possibly on
@@ -576,7 +611,9 @@ struct DecodeArgs {
 
 // Host-side launchers (one translation unit per kernel family).
 // total_wg: workgroups of the main pass; merge: some layer is split.
-hipError_t launch_decode(const DecodeArgs& a, int total_wg, int d, int Df, int dtype,
+// streaming: the state blob is far larger than the Infinity Cache (window
+// tiles and state rows read with non-temporal loads)
+hipError_t launch_decode(const DecodeArgs& a, int total_wg, int d, int Df, int dtype, bool streaming,
                          hipStream_t stream);
 hipError_t launch_flush(const DecodeArgs& a, int d, int Df, int dtype, hipStream_t stream);
 hipError_t launch_phi_rows(const void* Wf, const void* x, int64_t rows, void* out, int d, int Df, int dtype,
