@@ -88,8 +88,22 @@ enum { GLIDE_PHI_RELU = 0, GLIDE_PHI_ELU1 = 1, GLIDE_PHI_SOFTMAX = 2 };
  * then [n_layers][Hkv][d][Df], and head g's matrix maps the queries of its
  * group and its own keys (so that phi(q_h) . phi(k_j) pairs one feature
  * space; S and z are per KV head already).  It combines with every other
- * flag.  glide_feature_map takes one [d][Df] matrix either way. */
-enum { GLIDE_NO_LINEAR = 1, GLIDE_HYBRID_SUM = 2, GLIDE_HYBRID_STATE_ALL = 4, GLIDE_PER_HEAD_PHI = 8 };
+ * flag.  glide_feature_map takes one [d][Df] matrix either way.
+ *
+ * GLIDE_GATED gives the linear state a data-dependent decay, the GLA-style
+ * gating Sec. III-B names among the linear forms GLIDE supports (the paper
+ * does not fix the gate; here one scalar log-gate g_j <= 0 per token and KV
+ * head, passed in by the caller): a linear-set token j read at position t
+ * weighs e^{G_t - G_j}, G_t = g_0 + ... + g_t, i.e. it has decayed by the
+ * gates of every token after it (window tokens included):
+ *   A = sum_{j < beta} e^{G_t - G_j} (phi(q_t).phi(k_j)) v_j,  a likewise,
+ * and after p tokens S = sum_{j < p - W} e^{G_{p-1} - G_j} phi(k_j)^T v_j,
+ * z likewise (decayed through token p - 1).  The softmax window is not
+ * gated.  Prefill and decode then take log_gates (fp32, every value <= 0 and
+ * finite; the library does not check device data).  Only with the shared
+ * denominator (no hybrid flag) and the linear part on. */
+enum { GLIDE_NO_LINEAR = 1, GLIDE_HYBRID_SUM = 2, GLIDE_HYBRID_STATE_ALL = 4, GLIDE_PER_HEAD_PHI = 8,
+       GLIDE_GATED = 16 };
 
 typedef struct {
   int32_t n_layers;    /* layers held by one state blob (>= 1) */
@@ -100,8 +114,8 @@ typedef struct {
   int32_t feat_dim;    /* Df: 64 or 128 */
   int32_t dtype;       /* GLIDE_F32 or GLIDE_BF16 */
   int32_t phi;         /* GLIDE_PHI_RELU, GLIDE_PHI_ELU1 or GLIDE_PHI_SOFTMAX */
-  int32_t flags;       /* 0, GLIDE_NO_LINEAR, GLIDE_HYBRID_SUM, or GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL,
-                          each optionally | GLIDE_PER_HEAD_PHI */
+  int32_t flags;       /* 0, GLIDE_NO_LINEAR, GLIDE_HYBRID_SUM, GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL
+                          or GLIDE_GATED, each optionally | GLIDE_PER_HEAD_PHI */
   float sm_scale;      /* tau, the softmax scale (1/sqrt(d) in the Appendix's attention) */
   const int32_t* windows; /* HOST array [n_layers]: W_l = w - delta_l, 0 <= W_l <= 2^20 */
 } glide_config;
@@ -116,6 +130,12 @@ typedef struct {
  *   z     fp32  [B][Hkv][Df]      sum of phi(k_j) over the same tokens
  *   kring dtype [B][Hkv][R*d]     keys, token j in slot s = j mod R
  *   vring dtype [B][Hkv][R*d]     values, token j in slot s = j mod R
+ *   gate  fp64  [B][Hkv][2]       GLIDE_GATED only: G_{p-1} (the cumulative
+ *                                 log-gate through the last token consumed)
+ *                                 and G_f, the position S and z are decayed to
+ *                                 (S = sum_{j < nf} e^{G_f - G_j} ...)
+ *   gring fp64  [B][Hkv][R]       GLIDE_GATED only: G_j of ring token j, slot
+ *                                 j mod R (empty sections have size 0)
  * Deferred folding: the linear part of the next read-out covers tokens
  * [0, beta), beta = max(0, p - W).  Decode steps fold the tokens leaving the
  * window in batches of up to 8 (staggered over units), so nf lies in
@@ -132,6 +152,7 @@ typedef struct {
  *   vring: [c/16][o/8][c%16][o%8]                                          */
 typedef struct {
   int64_t pos_offset, nf_offset, cnt_offset, s_offset, z_offset, kring_offset, vring_offset;
+  int64_t gate_offset, gring_offset;
   int64_t layer_offset, layer_bytes;
   int32_t window;      /* W_l */
   int32_t ring_slots;  /* R_l */
@@ -174,13 +195,15 @@ glide_status glide_state_init(const glide_config* cfg, void* state, size_t state
  *          with GLIDE_PER_HEAD_PHI)
  *   q      device [n_layers][T][Hq][d]     T = total_tokens, packed by sequence
  *   k, v   device [n_layers][T][Hkv][d]
+ *   log_gates  device fp32 [n_layers][T][Hkv] with GLIDE_GATED (the log-gate
+ *          of every new token), else NULL
  *   cu_seqlens_host  HOST [B+1], cu[0] = 0, non-decreasing, cu[B] = T
  *   out    device [n_layers][T][Hq][d]
  *   workspace device, >= glide_workspace_bytes(cfg, T)
  * Element types follow cfg->dtype; device pointers 16-byte aligned. */
 glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_bytes,
                            int32_t layer0, int32_t n_layers, const void* phi_w,
-                           const void* q, const void* k, const void* v,
+                           const void* q, const void* k, const void* v, const float* log_gates,
                            const int32_t* cu_seqlens_host, int64_t total_tokens, int32_t chunk,
                            void* out, void* workspace, size_t workspace_bytes, void* stream);
 
@@ -199,13 +222,15 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
  * results.  Calls over different layer subsets agree up to rounding.
  *   phi_w  device [n_layers][d][Df]  ([n_layers][Hkv][d][Df] with GLIDE_PER_HEAD_PHI)
  *   q      device [n_layers][B][Hq][d];  k, v device [n_layers][B][Hkv][d]
+ *   log_gates  device fp32 [n_layers][B][Hkv] with GLIDE_GATED (the new
+ *          token's log-gate), else NULL
  *   out    device [n_layers][B][Hq][d]
  *   workspace  device, 256-byte aligned, >= glide_workspace_bytes(cfg, 0);
  *              may be NULL when that is 256 (nothing is split) */
 glide_status glide_decode_step(const glide_config* cfg, void* state, size_t state_bytes,
                                int32_t layer0, int32_t n_layers, const void* phi_w,
-                               const void* q, const void* k, const void* v, void* out,
-                               void* workspace, size_t workspace_bytes, void* stream);
+                               const void* q, const void* k, const void* v, const float* log_gates,
+                               void* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Size of the fixed decode scratch of glide_decode_step_noalloc, per GPU. */
 #define GLIDE_DECODE_SCRATCH_BYTES (16u << 20)
@@ -227,15 +252,16 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
  * glide_decode_step. */
 glide_status glide_decode_step_noalloc(const glide_config* cfg, void* state, size_t state_bytes,
                                        int32_t layer0, int32_t n_layers, const void* phi_w,
-                                       const void* q, const void* k, const void* v, void* out,
-                                       void* stream);
+                                       const void* q, const void* k, const void* v,
+                                       const float* log_gates, void* out, void* stream);
 
 /* Folds every pending token of layers [layer0, layer0 + n_layers) into S and
  * z (nf := max(0, p - W)), so that S and z hold exactly the Sec. II-B sums
  * over the linear part of the next token.  Outputs of later steps are
  * unchanged up to rounding.  phi_w device [n_layers][d][Df], layer layer0 first
  * ([n_layers][Hkv][d][Df] with GLIDE_PER_HEAD_PHI).  Nothing to do without the
- * linear part. */
+ * linear part.  With GLIDE_GATED, S and z are decayed to the last token
+ * consumed (G_f := G_{p-1}). */
 glide_status glide_state_flush(const glide_config* cfg, void* state, size_t state_bytes,
                                int32_t layer0, int32_t n_layers, const void* phi_w, void* stream);
 

@@ -224,6 +224,15 @@ void decode_kernel(DecodeArgs a) {
   // the new key/value) are issued before the first wait for them.
   const int64_t p = *pos_ptr;
   int64_t nf = *nf_ptr;
+  // gated state (GLIDE_GATED): the new token's log-gate, G_{p-1} and G_f of
+  // the unit (scalar loads beside pos and nf); the unit's piece 0 keeps them
+  const bool gated = a.gated != 0 && piece == 0;
+  const LayerSections secg = layer_sections(B, Hkv, D, DF, R, sizeof(T), gated);
+  double* gst = reinterpret_cast<double*>(lay + secg.G) + 2 * unit;  // [G_{p-1}, G_f]
+  double* grg = reinterpret_cast<double*>(lay + secg.GR) + unit * int64_t(R);
+  const float gnew = gated ? a.gates[tok * Hkv + g] : 0.f;
+  const double gcur0 = gated ? gst[0] : 0.0, gfold = gated ? gst[1] : 0.0;
+  const double gcur = gcur0 + double(gnew);  // G_p
 
   float* ph = smem;                        // [G + kFoldPeriod][DF] phi(q_h), then phi(k_j) of pending j
   float* pvl = ph + (G + kFoldPeriod) * DF;  // [kFoldPeriod][D]    values of the pending tokens
@@ -301,6 +310,14 @@ void decode_kernel(DecodeArgs a) {
   const bool fold = npend > 0 && (npend >= fper || (beta + int64_t(unit % fper)) % fper == 0);
   const bool s_nonzero = lin && nf > 0;  // S, z hold something
   const int32_t nf_slot = R > 0 ? int32_t(nf % R) : 0;  // ring slot of token nf
+  // gated: S, z are decayed to G_f; read at p they weigh e^{G_p - G_f}, and
+  // pending token j weighs e^{G_p - G_j} (its G_j from the gate ring; the new
+  // token itself, pending when Wd = 0, weighs 1)
+  __shared__ float pend_decay[kFoldPeriod];
+  const bool gate_pend = gated && lin && Wd > 0 && npend > 0;
+  if (gate_pend && tid < npend)
+    pend_decay[tid] = decay_exp(float(gcur - grg[wrap_once(uint32_t(nf_slot + tid), uint32_t(R))]));
+  const float sdecay = gated && s_nonzero ? decay_exp(float(gcur - gfold)) : 1.f;
 
   // Window: tokens [tlo, p] in 32-token tiles.  Ring tiles cover [tlo, p-1];
   // the new token p (not in the ring yet) is a partial of its own.  The
@@ -453,6 +470,10 @@ void decode_kernel(DecodeArgs a) {
   }
   if (tid < kMaxG) spl[tid] = -INFINITY;
   __syncthreads();
+  if (gate_pend) {  // the pending keys' features carry their decay
+    for (int e = tid; e < npend * DF; e += kThreads) ph[G * DF + e] *= pend_decay[e / DF];
+    __syncthreads();
+  }
 
   const float sc2 = a.tau * kLog2e;
   // ---- 3. the new token's score, one per query head (wave 0)
@@ -503,8 +524,8 @@ void decode_kernel(DecodeArgs a) {
     // On the first fold every row is written, whatever the memory held.
 #pragma unroll
     for (int s = 0; s < STEPS; ++s)
-      if (!s_nonzero || ((touched >> s) & 1u)) store_nt(S + (f0 + s * RPS + lr) * D + c4, rows[s]);
-    if (lane < RW && (dz != 0.f || !s_nonzero)) z[f0 + lane] = zrow;
+      if (!s_nonzero || gated || ((touched >> s) & 1u)) store_nt(S + (f0 + s * RPS + lr) * D + c4, rows[s]);
+    if (lane < RW && (dz != 0.f || !s_nonzero || gated)) z[f0 + lane] = zrow;
   };
   if (lin) {
     // S, z are zero until the first fold (their memory is not read as such)
@@ -512,6 +533,11 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
       for (int s = 0; s < STEPS; ++s) sr[s] = make_float4(0.f, 0.f, 0.f, 0.f);
       zf = 0.f;
+    } else if (gated) {  // S, z decayed from G_f to G_p
+#pragma unroll
+      for (int s = 0; s < STEPS; ++s)
+        sr[s] = make_float4(sr[s].x * sdecay, sr[s].y * sdecay, sr[s].z * sdecay, sr[s].w * sdecay);
+      zf *= sdecay;
     }
     if (early) fold_rows(sr, zf);
     for (int hh = 0; hh < G; ++hh) {
@@ -746,6 +772,11 @@ void decode_kernel(DecodeArgs a) {
   if (tid == 0 && piece == 0) {
     if (!split) *pos_ptr = p + 1;  // a split unit's position moves in merge_unit
     if (fold) *nf_ptr = beta;
+    if (gated) {
+      gst[0] = gcur;
+      if (fold) gst[1] = gcur;
+      if (W > 0) grg[p % R] = gcur;
+    }
   }
 }
 
@@ -774,7 +805,15 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(DecodeArgs a) {
   nf = nf > beta - kFoldPeriod ? nf : beta - kFoldPeriod;
   nf = nf > 0 ? nf : 0;
   const int n = int(beta - nf);
-  if (n == 0) return;
+  // gated: S, z (decayed to G_f) and the pending tokens are brought to
+  // G_{p-1}, the last token consumed
+  const bool gated = a.gated != 0;
+  const LayerSections secg = layer_sections(a.B, a.Hkv, D, DF, R, sizeof(T), gated);
+  double* gst = reinterpret_cast<double*>(lay + secg.G) + 2 * unit;
+  const double* grg = reinterpret_cast<const double*>(lay + secg.GR) + unit * int64_t(R);
+  const double gcur = gated ? gst[0] : 0.0;
+  const bool regate = gated && nf > 0 && gst[1] != gcur;
+  if (n == 0 && !regate) return;
   float* S = reinterpret_cast<float*>(lay + sec.S) + unit * DF * D;
   float* z = reinterpret_cast<float*>(lay + sec.z) + unit * DF;
   const T* Kr = reinterpret_cast<const T*>(lay + sec.K) + unit * int64_t(R) * D;
@@ -799,10 +838,19 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(DecodeArgs a) {
     softmax_rows_lds<DF, kThreads>(&pk[0][0], DF, n);
     __syncthreads();
   }
+  if (gated && n > 0) {
+    for (int e = tid; e < n * DF; e += kThreads) {
+      const int i = e / DF, f = e - i * DF;
+      pk[i][f] *= decay_exp(float(gcur - grg[(nf + i) % R]));
+    }
+    __syncthreads();
+  }
   const bool s_nonzero = nf > 0;
+  const float sd = gated && s_nonzero ? decay_exp(float(gcur - gst[1])) : 1.f;
   for (int e = tid; e < DF * D / 4; e += kThreads) {
     const int f = e / (D / 4), c4 = (e - f * (D / 4)) * 4;
     float4 sv = s_nonzero ? *reinterpret_cast<const float4*>(S + f * D + c4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    sv.x *= sd; sv.y *= sd; sv.z *= sd; sv.w *= sd;
     for (int i = 0; i < n; ++i) {
       const float w = pk[i][f];
       sv.x = fmaf(w, vx[i][c4], sv.x);
@@ -813,11 +861,15 @@ __global__ __launch_bounds__(kThreads) void flush_kernel(DecodeArgs a) {
     *reinterpret_cast<float4*>(S + f * D + c4) = sv;
   }
   for (int f = tid; f < DF; f += kThreads) {
-    float zf = s_nonzero ? z[f] : 0.f;
+    float zf = s_nonzero ? z[f] * sd : 0.f;
     for (int i = 0; i < n; ++i) zf += pk[i][f];
     z[f] = zf;
   }
-  if (tid == 0) *nf_ptr = beta;
+  __syncthreads();  // every thread has read G_f
+  if (tid == 0) {
+    *nf_ptr = beta;
+    if (gated) gst[1] = gcur;
+  }
 }
 
 template <typename T, int D, int DF>

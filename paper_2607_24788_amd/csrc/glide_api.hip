@@ -26,8 +26,11 @@ glide_status check_cfg(const glide_config* c) {
   if (c->head_dim < 1 || c->feat_dim < 1) return GLIDE_ERR_INVALID;
   if (c->dtype != GLIDE_F32 && c->dtype != GLIDE_BF16) return GLIDE_ERR_INVALID;
   if (c->phi != GLIDE_PHI_RELU && c->phi != GLIDE_PHI_ELU1 && c->phi != GLIDE_PHI_SOFTMAX) return GLIDE_ERR_INVALID;
-  if (c->flags & ~int32_t(GLIDE_NO_LINEAR | GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL | GLIDE_PER_HEAD_PHI))
+  if (c->flags &
+      ~int32_t(GLIDE_NO_LINEAR | GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL | GLIDE_PER_HEAD_PHI | GLIDE_GATED))
     return GLIDE_ERR_INVALID;
+  // a gate decays the linear part: not without one
+  if ((c->flags & GLIDE_GATED) && (c->flags & GLIDE_NO_LINEAR)) return GLIDE_ERR_INVALID;
   // the hybrid forms change the linear part: not without one; the state over
   // every token comes only with the separately normalised sum
   if ((c->flags & GLIDE_NO_LINEAR) && (c->flags & (GLIDE_HYBRID_SUM | GLIDE_HYBRID_STATE_ALL)))
@@ -42,14 +45,18 @@ glide_status check_cfg(const glide_config* c) {
   if (c->n_q_heads / c->n_kv_heads > kMaxG) return GLIDE_ERR_UNSUPPORTED;
   if (c->head_dim != 64 && c->head_dim != 128) return GLIDE_ERR_UNSUPPORTED;
   if (c->feat_dim != 64 && c->feat_dim != 128) return GLIDE_ERR_UNSUPPORTED;
+  // the gated state is built for the shared denominator only
+  if ((c->flags & GLIDE_GATED) && (c->flags & GLIDE_HYBRID_SUM)) return GLIDE_ERR_UNSUPPORTED;
   return GLIDE_OK;
 }
+
+bool gated_on(const glide_config* c) { return (c->flags & GLIDE_GATED) != 0; }
 
 int esize(const glide_config* c) { return c->dtype == GLIDE_BF16 ? 2 : 4; }
 
 LayerSections sections(const glide_config* c, int32_t l) {
   return layer_sections(c->batch, c->n_kv_heads, c->head_dim, c->feat_dim, ring_slots(c->windows[l]),
-                        esize(c));
+                        esize(c), gated_on(c));
 }
 
 int64_t layer_base(const glide_config* c, int32_t l) {
@@ -89,7 +96,7 @@ int32_t max_window(const glide_config* c) {
 
 PrefillWorkspace prefill_ws(const glide_config* c, int64_t T, int32_t nl) {
   return prefill_workspace(T, c->batch, c->n_kv_heads, c->head_dim, c->feat_dim, esize(c), max_window(c),
-                           linear_on(c), nl);
+                           linear_on(c), nl, gated_on(c));
 }
 
 // Resident decode workgroups of one round on the current device:
@@ -196,6 +203,7 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
   a.form = merge_form(cfg);
   a.phi = cfg->phi;
   a.wf_heads = (cfg->flags & GLIDE_PER_HEAD_PHI) ? 1 : 0;
+  a.gated = gated_on(cfg) ? 1 : 0;
   a.tau = cfg->sm_scale;
   for (int32_t first = 0; first < n_layers; first += kMaxLayersPerLaunch) {
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
@@ -290,6 +298,8 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
   out->z_offset = base + sec.z;
   out->kring_offset = base + sec.K;
   out->vring_offset = base + sec.V;
+  out->gate_offset = base + sec.G;
+  out->gring_offset = base + sec.GR;
   out->window = cfg->windows[layer];
   out->ring_slots = ring_slots(cfg->windows[layer]);
   return GLIDE_OK;
@@ -315,12 +325,15 @@ glide_status glide_state_init(const glide_config* cfg, void* state, size_t state
 
 glide_status glide_decode_step(const glide_config* cfg, void* state, size_t state_bytes, int32_t layer0,
                                int32_t n_layers, const void* phi_w, const void* q, const void* k,
-                               const void* v, void* out, void* workspace, size_t workspace_bytes,
-                               void* stream) {
+                               const void* v, const float* log_gates, void* out, void* workspace,
+                               size_t workspace_bytes, void* stream) {
   glide_status s = check_call(cfg, state, state_bytes, layer0, n_layers);
   if (s != GLIDE_OK) return s;
   if (!phi_w || !q || !k || !v || !out) return GLIDE_ERR_NULL;
-  if (!aligned(phi_w, 16) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
+  if (gated_on(cfg) && !log_gates) return GLIDE_ERR_NULL;
+  if (!gated_on(cfg) && log_gates) return GLIDE_ERR_INVALID;
+  if (!aligned(phi_w, 16) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(log_gates, 4))
     return GLIDE_ERR_ALIGN;
   const size_t need = decode_ws(cfg);
   if (need) {
@@ -336,6 +349,7 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
   a.k = k;
   a.v = v;
   a.out = out;
+  a.gates = log_gates;
   a.part = static_cast<float*>(workspace);
   // a state blob far larger than the Infinity Cache is streamed (every step
   // reads it all): non-temporal loads; a smaller one is re-read from the cache
@@ -347,7 +361,8 @@ glide_status glide_decode_step(const glide_config* cfg, void* state, size_t stat
 
 glide_status glide_decode_step_noalloc(const glide_config* cfg, void* state, size_t state_bytes,
                                        int32_t layer0, int32_t n_layers, const void* phi_w, const void* q,
-                                       const void* k, const void* v, void* out, void* stream) {
+                                       const void* k, const void* v, const float* log_gates, void* out,
+                                       void* stream) {
   glide_status s = check_call(cfg, state, state_bytes, layer0, n_layers);
   if (s != GLIDE_OK) return s;
   const size_t need = decode_ws(cfg);
@@ -358,7 +373,7 @@ glide_status glide_decode_step_noalloc(const glide_config* cfg, void* state, siz
     s = scratch_address(&ws);
     if (s != GLIDE_OK) return s;
   }
-  return glide_decode_step(cfg, state, state_bytes, layer0, n_layers, phi_w, q, k, v, out, ws,
+  return glide_decode_step(cfg, state, state_bytes, layer0, n_layers, phi_w, q, k, v, log_gates, out, ws,
                            need ? size_t(GLIDE_DECODE_SCRATCH_BYTES) : 0, stream);
 }
 
@@ -380,12 +395,15 @@ glide_status glide_state_flush(const glide_config* cfg, void* state, size_t stat
 
 glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_bytes, int32_t layer0,
                            int32_t n_layers, const void* phi_w, const void* q, const void* k, const void* v,
-                           const int32_t* cu_seqlens_host, int64_t total_tokens, int32_t chunk, void* out,
-                           void* workspace, size_t workspace_bytes, void* stream) {
+                           const float* log_gates, const int32_t* cu_seqlens_host, int64_t total_tokens,
+                           int32_t chunk, void* out, void* workspace, size_t workspace_bytes, void* stream) {
   glide_status s = check_call(cfg, state, state_bytes, layer0, n_layers);
   if (s != GLIDE_OK) return s;
   if (!phi_w || !q || !k || !v || !out || !cu_seqlens_host) return GLIDE_ERR_NULL;
-  if (!aligned(phi_w, 16) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
+  if (gated_on(cfg) && !log_gates) return GLIDE_ERR_NULL;
+  if (!gated_on(cfg) && log_gates) return GLIDE_ERR_INVALID;
+  if (!aligned(phi_w, 16) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(log_gates, 4))
     return GLIDE_ERR_ALIGN;
   if (total_tokens < 0) return GLIDE_ERR_INVALID;
   if (cu_seqlens_host[0] != 0 || cu_seqlens_host[cfg->batch] != total_tokens) return GLIDE_ERR_INVALID;
@@ -433,6 +451,11 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   a.ws_slot = int64_t(w.slot);
   a.ws_hv = int64_t(w.hv);
   a.ws_seg = int64_t(w.seg);
+  a.ws_hg = int64_t(w.hg);
+  a.ws_gc = int64_t(w.gc);
+  a.gated = gated_on(cfg) ? 1 : 0;
+  a.gates = log_gates;
+  a.g_stride = T * Hkv;
   a.B = B;
   a.Hq = Hq;
   a.Hkv = Hkv;

@@ -55,11 +55,15 @@ __host__ __device__ inline int64_t kring_chunk(int32_t slot, int kk, int g, int 
 }
 
 // Byte offsets of the sections of one layer, relative to the layer's start.
+// A gated layer (GLIDE_GATED) appends, per unit, G_cur and G_fold (fp64) and
+// a ring of the cumulative log-gates G_j of its ring tokens (fp64, slot j mod
+// R); the other offsets do not depend on it.
 struct LayerSections {
-  int64_t pos, nf, cnt, S, z, K, V, bytes;
+  int64_t pos, nf, cnt, S, z, K, V, G, GR, bytes;
 };
 
-__host__ __device__ inline LayerSections layer_sections(int B, int Hkv, int d, int Df, int R, int esize) {
+__host__ __device__ inline LayerSections layer_sections(int B, int Hkv, int d, int Df, int R, int esize,
+                                                        bool gated = false) {
   LayerSections s;
   const int64_t units = int64_t(B) * Hkv;
   s.pos = 0;
@@ -69,9 +73,14 @@ __host__ __device__ inline LayerSections layer_sections(int B, int Hkv, int d, i
   s.z = s.S + align256(units * Df * d * 4);
   s.K = s.z + align256(units * Df * 4);
   s.V = s.K + align256(units * int64_t(R) * d * esize);
-  s.bytes = s.V + align256(units * int64_t(R) * d * esize);
+  s.G = s.V + align256(units * int64_t(R) * d * esize);
+  s.GR = s.G + (gated ? align256(units * 16) : 0);
+  s.bytes = s.GR + (gated ? align256(units * int64_t(R) * 8) : 0);
   return s;
 }
+
+// exp(x) of a log-decay x <= 0 (fp32, base-2 hardware exponential).
+__device__ __forceinline__ float decay_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
 
 // Per-layer description handed to kernels by value.
 struct LayerArg {
@@ -599,6 +608,8 @@ struct DecodeArgs {
   int32_t form;      // 0: shared denominator; 1, 2: the Appendix's hybrid forms (2: state over every token)
   int32_t phi;       // feature map: 0 ReLU, 1 ELU + 1
   int32_t row_stride;  // workgroups per piece row: B * Hkv
+  int32_t gated;       // GLIDE_GATED: log_gates [layer][B][Hkv] fp32, gate sections in the state
+  const float* gates;
   int32_t wf_heads;  // 1: phi_w holds one Wf per KV head ([layer][Hkv][d][Df])
   int32_t pad;
   LayerArg layers[kMaxLayersPerLaunch];  // sorted by decreasing W
@@ -662,6 +673,11 @@ struct PrefillArgs {
   int32_t wf_hs;        // bytes between the KV heads' Wf (0: one Wf per layer)
   int32_t pad1;
   int32_t phi;          // feature map: 0 ReLU, 1 ELU + 1
+  int32_t gated;        // GLIDE_GATED: log_gates [n][T][Hkv] fp32 (layer li at li * g_stride floats)
+  int32_t pad2;
+  const float* gates;
+  int64_t g_stride;
+  int64_t ws_hg, ws_gc;  // per slot: history G [B][Hkv][Wcap] fp64, new tokens' G [T][Hkv] fp64
   PrefillLayer layers[kMaxLayersPerLaunch];  // the launch's layers, by decreasing window
   int32_t seq_start[kMaxSeqPerLaunch];     // packed row of the sequence's first new token
   int32_t seq_len[kMaxSeqPerLaunch];       // new tokens of the sequence
@@ -688,13 +704,14 @@ inline int32_t segment_chunks(int64_t T, int Hkv, int32_t chunk, int32_t nl) {
 }
 
 struct PrefillWorkspace {
-  size_t hk, hv, seg, slot;  // offsets within a slot, and the slot's bytes
+  size_t hk, hv, seg, hg, gc, slot;  // offsets within a slot, and the slot's bytes
 };
 
 // One layer's slot for calls of T tokens in launches of nl layers: the
 // records bound takes the shortest segment any legal chunk gives for T.
+// Gated: the history tokens' and the new tokens' cumulative log-gates (fp64).
 inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hkv, int d, int Df, int esize, int Wcap,
-                                          bool linear, int32_t nl) {
+                                          bool linear, int32_t nl, bool gated = false) {
   PrefillWorkspace w;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -710,6 +727,8 @@ inline PrefillWorkspace prefill_workspace(int64_t T, int B, int Hkv, int d, int 
   w.hk = take(size_t(B) * Hkv * Wcap * d * esize);
   w.hv = take(size_t(B) * Hkv * Wcap * d * esize);
   w.seg = take(linear ? (size_t(T / seg_min) + B) * Hkv * (size_t(Df) * d + Df) * 4 : 0);
+  w.hg = take(gated ? size_t(B) * Hkv * Wcap * 8 : 0);
+  w.gc = take(gated ? size_t(T) * Hkv * 8 : 0);
   w.slot = off;
   return w;
 }

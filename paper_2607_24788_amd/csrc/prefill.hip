@@ -89,6 +89,8 @@ struct LayerView {
   void* out;
   void *hk, *hv;
   float* seg;
+  int ls;      // slot of the layer within the launch
+  int li;      // position of the layer in the call
 };
 __device__ __forceinline__ LayerView layer_view(const PrefillArgs& a, int ls) {
   const PrefillLayer& L = a.layers[ls];
@@ -106,6 +108,8 @@ __device__ __forceinline__ LayerView layer_view(const PrefillArgs& a, int ls) {
   v.hk = slot;
   v.hv = slot + a.ws_hv;
   v.seg = reinterpret_cast<float*>(slot + a.ws_seg);
+  v.ls = ls;
+  v.li = L.li;
   return v;
 }
 
@@ -127,6 +131,38 @@ __device__ __forceinline__ SeqRows<T, D> seq_rows(const PrefillArgs& a, const La
   r.p0 = reinterpret_cast<const int64_t*>(L.base + sec.pos)[unit];
   r.h0 = r.p0 - L.W > 0 ? r.p0 - L.W : 0;
   return r;
+}
+
+// Cumulative log-gates G_j of a gated prefill (GLIDE_GATED): those of the new
+// tokens from this call's scan (gc [T][Hkv], workspace), those of the history
+// tokens from their copy of the gate ring (hg), and G_{p0-1}, the state's G at
+// the call's start (the reference its incoming S, z are decayed to).
+struct SeqGates {
+  const double *gc, *hg;
+  double g0;
+  int64_t p0, h0;
+  int start, Hkv, g;
+  __device__ double at(int64_t j) const {
+    if (j >= p0) return gc[(int64_t(start) + (j - p0)) * Hkv + g];
+    if (j == p0 - 1 || j < h0) return g0;
+    return hg[j - h0];
+  }
+};
+template <typename T, int D, int DF>
+__device__ __forceinline__ SeqGates seq_gates(const PrefillArgs& a, const LayerView& L, const SeqRows<T, D>& sr) {
+  SeqGates q;
+  char* slot = a.ws + int64_t(L.ls) * a.ws_slot;
+  const int64_t unit = int64_t(sr.b) * a.Hkv + sr.g;
+  q.gc = reinterpret_cast<const double*>(slot + a.ws_gc);
+  q.hg = reinterpret_cast<const double*>(slot + a.ws_hg) + unit * a.Wcap;
+  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T), true);
+  q.g0 = reinterpret_cast<const double*>(L.base + sec.G)[2 * unit];
+  q.p0 = sr.p0;
+  q.h0 = sr.h0;
+  q.start = sr.start;
+  q.Hkv = a.Hkv;
+  q.g = sr.g;
+  return q;
 }
 
 // Sequence (within the group) owning segment sg.
@@ -232,9 +268,11 @@ __device__ __forceinline__ void slab_keys(SlabKeys<T, D, DF>& sk, int nw, RowFn 
 #pragma unroll
   for (int kk = 0; kk < D / 32; ++kk) sk.x[kk].load(src + 32 * kk + 8 * lg);
 }
+// kw: the weight of the lane's key row (16 kt + hq) multiplied into its
+// features (a gated segment's decay; 1 otherwise).
 template <typename T, int D, int DF, int NK, int PHI, bool kLds>
 __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const Frag<T> (&x)[D / 32], T* pk,
-                                         int nw, int rlo, int rhi) {
+                                         int nw, int rlo, int rhi, float kw = 1.f) {
   constexpr int KS = D / 32, FT = DF / 16, PROW = row_t<DF>();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
   const int per = (NK / 16) * FT / nw;
@@ -295,7 +333,7 @@ __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const
     const bool is_key = key >= rlo && key < rhi;
 #pragma unroll
     for (int u = 0; u < kPerMax; ++u)
-      if (u < per) store4(pk + key * PROW + 16 * (ft0 + u) + 4 * lg, is_key ? acc[u] : zero4(), 1.f / tot);
+      if (u < per) store4(pk + key * PROW + 16 * (ft0 + u) + 4 * lg, is_key ? acc[u] : zero4(), kw / tot);
     return;
   }
   for (int u = 0; u < per; ++u) {
@@ -313,9 +351,9 @@ __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const
     // be 0, which ReLU gives by itself and ELU + 1 (phi(0) = 1) does not
     const int key = 16 * kt + hq;
     if constexpr (PHI == 0) {
-      store4(pk + key * PROW + 16 * ft + 4 * lg, act4(acc, 0), 1.f);
+      store4(pk + key * PROW + 16 * ft + 4 * lg, act4(acc, 0), kw);
     } else {
-      store4(pk + key * PROW + 16 * ft + 4 * lg, key >= rlo && key < rhi ? act4(acc, PHI) : zero4(), 1.f);
+      store4(pk + key * PROW + 16 * ft + 4 * lg, key >= rlo && key < rhi ? act4(acc, PHI) : zero4(), kw);
     }
   }
 }
@@ -341,6 +379,49 @@ __global__ __launch_bounds__(kThreads) void prefill_gather(PrefillArgs a) {
     const int32_t s = int32_t((sr.h0 + i) % L.R);
     hk[int64_t(i) * D + c] = Kr[kring_elem(s, c, D)];
     hv[int64_t(i) * D + c] = Vr[vring_elem(s, c, D)];
+  }
+  if (a.gated) {  // the history tokens' G_j, from the gate ring
+    const LayerSections sg = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T), true);
+    const double* grg = reinterpret_cast<const double*>(L.base + sg.GR) + unit * L.R;
+    double* hg = reinterpret_cast<double*>(a.ws + int64_t(L.ls) * a.ws_slot + a.ws_hg) + unit * a.Wcap;
+    for (int i = blockIdx.x * kThreads + threadIdx.x; i < n; i += gridDim.x * kThreads) hg[i] = grg[(sr.h0 + i) % L.R];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// gates (GLIDE_GATED): the cumulative log-gates of the new tokens of one
+// (sequence, KV head), G_t = G_{p0-1} + g_{p0} + ... + g_t, in fp64 (an
+// inclusive scan over blocks of consecutive tokens, one block per thread).
+template <typename T, int D, int DF>
+__global__ __launch_bounds__(kThreads) void prefill_gates(PrefillArgs a) {
+  __shared__ double part[kThreads];
+  const int bl = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
+  const LayerView L = layer_view(a, blockIdx.z);
+  const int Tb = a.seq_len[bl], start = a.seq_start[bl];
+  const int64_t unit = int64_t(a.seq0 + bl) * a.Hkv + g;
+  const LayerSections sec = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T), true);
+  const double g0 = reinterpret_cast<const double*>(L.base + sec.G)[2 * unit];
+  const float* gin = a.gates + int64_t(L.li) * a.g_stride;
+  double* gc = reinterpret_cast<double*>(a.ws + int64_t(L.ls) * a.ws_slot + a.ws_gc);
+  const int per = (Tb + kThreads - 1) / kThreads;
+  const int i0 = tid * per, i1 = min(Tb, i0 + per);
+  double sum = 0.0;
+  for (int i = i0; i < i1; ++i) sum += double(gin[(int64_t(start) + i) * a.Hkv + g]);
+  part[tid] = sum;
+  __syncthreads();
+  if (tid == 0) {
+    double run = g0;
+    for (int t = 0; t < kThreads; ++t) {
+      const double x = part[t];
+      part[t] = run;
+      run += x;
+    }
+  }
+  __syncthreads();
+  double run = part[tid];
+  for (int i = i0; i < i1; ++i) {
+    run += double(gin[(int64_t(start) + i) * a.Hkv + g]);
+    gc[(int64_t(start) + i) * a.Hkv + g] = run;
   }
 }
 
@@ -383,6 +464,14 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
   int64_t jlo = sr.p0 + s_lo - L.Wd;
   const int64_t jhi = sr.p0 + s_hi - L.Wd;
   if (jlo < 0) jlo = 0;
+  // gated: each delayed key decayed to the segment's last query (the scan
+  // carries the records from one segment's end to the next)
+  SeqGates gt{};
+  double gend = 0.0;
+  if (a.gated) {
+    gt = seq_gates<T, D, DF>(a, L, sr);
+    gend = gt.at(sr.p0 + s_hi - 1);
+  }
 
   f32x4_t sacc[NT];
 #pragma unroll
@@ -412,8 +501,13 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
 #pragma unroll
       for (int kk = 0; kk < D / 32; ++kk) x[kk] = frag_keep(kx.x[kk], kx.ok);
       const int64_t nrow = jhi - j0;
+      float kw = 1.f;
+      if (a.gated) {
+        const int64_t j = j0 + 16 * slab_key_tile<D, DF, kSegSlab>(kSegWaves) + hq;
+        kw = j < jhi ? decay_exp(float(gend - gt.at(j))) : 0.f;
+      }
       phi_slab<T, D, DF, kSegSlab, PHI>(WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))}, x,
-                                        lds_fresh(pk), kSegWaves, 0, nrow < kSegSlab ? int(nrow) : kSegSlab);
+                                        lds_fresh(pk), kSegWaves, 0, nrow < kSegSlab ? int(nrow) : kSegSlab, kw);
     }
     {
       T* vw = lds_fresh(vs);
@@ -472,7 +566,19 @@ __global__ __launch_bounds__(kThreads) void prefill_scan(PrefillArgs a) {
   float4 run = *reinterpret_cast<const float4*>(st);
   auto rec = [&](int sg) { return reinterpret_cast<float4*>(L.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * E + e); };
   const int s1 = a.seg_base[bl + 1];
-  int sg = a.seg_base[bl];
+  const int sb = a.seg_base[bl];
+  int sg = sb;
+  // gated: the running state is decayed across each segment, from G at the
+  // token before it to G at its last token, before the segment's increment
+  // (decayed to that last token) is added
+  SeqGates gt{};
+  if (a.gated) gt = seq_gates<T, D, DF>(a, L, seq_rows<T, D, DF>(a, L, bl, g));
+  const int Tb = a.seq_len[bl];
+  auto seg_decay = [&](int sgi) {
+    if (!a.gated) return 1.f;
+    const int lo = (sgi - sb) * a.seg_len, hi = min(Tb, lo + a.seg_len);
+    return decay_exp(float(gt.at(gt.p0 + hi - 1) - gt.at(gt.p0 + lo - 1)));
+  };
   // eight records' loads in flight at a time (the sum itself is serial)
   for (; sg + 8 <= s1; sg += 8) {
     float4 d[8];
@@ -481,13 +587,15 @@ __global__ __launch_bounds__(kThreads) void prefill_scan(PrefillArgs a) {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       *rec(sg + u) = run;
-      run.x += d[u].x; run.y += d[u].y; run.z += d[u].z; run.w += d[u].w;
+      const float f = seg_decay(sg + u);
+      run.x = run.x * f + d[u].x; run.y = run.y * f + d[u].y; run.z = run.z * f + d[u].z; run.w = run.w * f + d[u].w;
     }
   }
   for (; sg < s1; ++sg) {
     const float4 d = *rec(sg);
     *rec(sg) = run;
-    run.x += d.x; run.y += d.y; run.z += d.z; run.w += d.w;
+    const float f = seg_decay(sg);
+    run.x = run.x * f + d.x; run.y = run.y * f + d.y; run.z = run.z * f + d.z; run.w = run.w * f + d.w;
   }
   *reinterpret_cast<float4*>(st) = run;
 }
@@ -534,7 +642,13 @@ struct MainLds {
 // linear part over one shared denominator; for the hybrid forms, 1 the
 // linear part alone (normalised on its own) and 2 the band alone, its
 // normalised output added to what out holds.  One instantiation each.
-template <typename T, int D, int DF, int PHI, int PASS>
+// GATED (PASS 0 only): the gated linear state.  S_c is decayed to G_{t0-1}
+// (the token before the chunk); row t reads it scaled by e^{G_t - G_{t0-1}},
+// the masked block weighs pair (t, j) by e^{G_t - G_j} element by element
+// (every factor <= 1, whatever the gates), and on the chunk's last pass
+// S_{c+1} = e^{G_e - G_{t0-1}} S_c + sum_j e^{G_e - G_j} phi(k_j)^T v_j,
+// G_e the chunk's last token, after the masked block has read phi(k).
+template <typename T, int D, int DF, int PHI, int PASS, bool GATED = false>
 __global__ __launch_bounds__(kMT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void prefill_main(PrefillArgs a) {
   using LD = MainLds<T, D, DF>;
@@ -565,6 +679,9 @@ void prefill_main(PrefillArgs a) {
   const int sigma = sg - a.seg_base[bl];
   const int s_lo = sigma * a.seg_len, s_hi = min(a.seq_len[bl], s_lo + a.seg_len);
   const int G = a.G, C = a.C;
+  SeqGates gt{};
+  if constexpr (GATED) gt = seq_gates<T, D, DF>(a, L, sr);
+  __shared__ float gk_lds[LD::SLAB];  // gated: G_j - G_{t0-1} of the slab's delayed keys
   const int W = PASS == 1 ? 0 : L.W;  // the band's window (0: this pass has no band)
   const int Wd = L.Wd;                // the linear part's delay
   const bool linear = PASS != 2 && a.linear != 0;
@@ -851,6 +968,17 @@ void prefill_main(PrefillArgs a) {
         // (with the band's queries negated, phi takes them back: -(-q) Wf)
         qscale[qt] = (W > 0 && qneg) ? -__builtin_amdgcn_exp2f(-m0) : __builtin_amdgcn_exp2f(-m0);
       }
+      // gated: G_t - G_{t0-1} of each row and its read-out factor
+      float gqr[2] = {0.f, 0.f}, fq[2] = {1.f, 1.f};
+      double gref = 0.0;
+      if constexpr (GATED) {
+        gref = gt.at(t0 - 1);
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          gqr[qt] = float(gt.at(t0 + ti[qt]) - gref);
+          fq[qt] = decay_exp(gqr[qt]);
+        }
+      }
       // phi(q) 2^-m, transposed: lane (row hq, group lg) gets features
       // 32kf+4lg+i and 32kf+16+4lg+i of its query row in fragment kf
       Frag<T> pqf[2][KSF];
@@ -938,12 +1066,25 @@ void prefill_main(PrefillArgs a) {
       const float* Sr = lds_fresh(static_cast<const float*>(St)) + hq * SROW;
 #pragma unroll
       for (int kf = 0; kf < KSF; ++kf) {
+        Frag<T> rq[2];  // the read-out's phi(q): decayed when gated
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          if constexpr (GATED) {
+            float x[8];
+            pqf[qt][kf].to_floats(x);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) x[i] *= fq[qt];
+            rq[qt].set8(x);
+          } else {
+            rq[qt] = pqf[qt][kf];
+          }
+        }
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
           Frag<T> fs;
           load_row2_f32(fs, Sr + 16 * ct * SROW, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fs, pqf[qt][kf], acc[qt][ct]);
+          for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fs, rq[qt], acc[qt][ct]);
         }
       }
       float den[2];
@@ -962,7 +1103,7 @@ void prefill_main(PrefillArgs a) {
           dz = fmaf(qv[4], zb.x, dz); dz = fmaf(qv[5], zb.y, dz);
           dz = fmaf(qv[6], zb.z, dz); dz = fmaf(qv[7], zb.w, dz);
         }
-        den[qt] = dz;
+        den[qt] = dz * fq[qt];
       }
       // the chunk's delayed keys, SL at a time: phi(k) into LDS, the masked
       // block i' <= ti of every query row, and (last pass: every read-out of
@@ -975,6 +1116,12 @@ void prefill_main(PrefillArgs a) {
           __syncthreads();  // the previous slab's readers are done
           load_slab(s0);
           put_slab();
+        }
+        if constexpr (GATED) {
+          if (tid < SL) {
+            const int64_t j = t0 - Wd + s0 + tid;
+            gk_lds[tid] = (s0 + tid < nk && j >= 0) ? float(gt.at(j) - gref) : 0.f;
+          }
         }
         __syncthreads();  // keys and values staged; the read-outs of S_c, z_c are done
         {
@@ -991,10 +1138,11 @@ void prefill_main(PrefillArgs a) {
         __syncthreads();
         const T* pkr = lds_fresh(static_cast<const T*>(pk));
         const T* vsr = lds_fresh(static_cast<const T*>(vs));
-        if (last_pass) {
-          // every S tile (and z slice) has one owner wave: plain updates.
-          // Lane (hq, lg) gets features 16ft+4lg.. of value column 16ct+hq,
-          // 4 consecutive floats of S^T
+        // S_{c+1} = dch S_c + phi(k)^T v (dch: the chunk's decay, applied with
+        // the first slab; 1 ungated).  Every S tile (and z slice) has one
+        // owner wave: plain updates.  Lane (hq, lg) gets features 16ft+4lg..
+        // of value column 16ct+hq, 4 consecutive floats of S^T
+        auto state_update = [&](float dch) {
           float* Sw = lds_fresh(St);
           float* zw = lds_fresh(zs);
 #pragma unroll
@@ -1012,14 +1160,20 @@ void prefill_main(PrefillArgs a) {
             }
             float4* sp = reinterpret_cast<float4*>(Sw + (16 * ct + hq) * SROW + 16 * ft + 4 * lg);
             float4 s4 = *sp;
-            s4.x += d[0]; s4.y += d[1]; s4.z += d[2]; s4.w += d[3];
+            if constexpr (GATED) {
+              s4.x = fmaf(s4.x, dch, d[0]); s4.y = fmaf(s4.y, dch, d[1]);
+              s4.z = fmaf(s4.z, dch, d[2]); s4.w = fmaf(s4.w, dch, d[3]);
+            } else {
+              s4.x += d[0]; s4.y += d[1]; s4.z += d[2]; s4.w += d[3];
+            }
             *sp = s4;
             if (ct == 0) {
               zp = lg_sum(zp);
-              if (lg == 0) zw[16 * ft + hq] += zp;
+              if (lg == 0) zw[16 * ft + hq] = fmaf(zw[16 * ft + hq], GATED ? dch : 1.f, zp);
             }
           }
-        }
+        };
+        if (!GATED && last_pass) state_update(1.f);
         // scores: key row m of sub-tile t of 32-key block kb is
         // i' = s0 + 32kb + 8(m/4) + 4t + m%4
 #pragma unroll
@@ -1046,8 +1200,11 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
-              for (int i = 0; i < 4; ++i)
-                pv[4 * t + i] = (s0 + 32 * kb + 8 * lg + 4 * t + i <= ti[qt]) ? sc[qt][t][i] : 0.f;
+              for (int i = 0; i < 4; ++i) {
+                const int kr_ = 32 * kb + 8 * lg + 4 * t + i;  // the key within the slab
+                const float w = GATED ? decay_exp(gqr[qt] - gk_lds[kr_]) : 1.f;
+                pv[4 * t + i] = (s0 + kr_ <= ti[qt]) ? sc[qt][t][i] * w : 0.f;
+              }
             pf[qt].set8(pv);
             den[qt] += pf[qt].sum();
           }
@@ -1057,6 +1214,21 @@ void prefill_main(PrefillArgs a) {
             load_colfrag(fv, vsr, VROW, 32 * kb + 8 * lg, 16 * ct);
 #pragma unroll
             for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
+          }
+        }
+        if constexpr (GATED) {
+          if (last_pass) {
+            // the masked block has read phi(k): each key row is now decayed
+            // to the chunk's last token, then S_{c+1}
+            __syncthreads();
+            const float gend_rel = float(gt.at(t0 + nk - 1) - gref);
+            T* pkw = lds_fresh(pk);
+            for (int e = tid; e < SL * DF; e += kMT) {
+              const int r = e / DF, f = e - r * DF;
+              pkw[r * PROW + f] = from_f32<T>(to_f32(pkw[r * PROW + f]) * decay_exp(gend_rel - gk_lds[r]));
+            }
+            __syncthreads();
+            state_update(s0 == 0 ? decay_exp(gend_rel) : 1.f);
           }
         }
       }
@@ -1140,6 +1312,13 @@ __global__ __launch_bounds__(kThreads) void prefill_ringfill(PrefillArgs a) {
     f.load(sr.k(j) + 8 * ch);
     store8(Kr + kring_elem(int32_t(j % L.R), 8 * ch, D), f);
   }
+  if (a.gated) {  // the ring tokens' G_j
+    const LayerSections sg = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T), true);
+    double* grg = reinterpret_cast<double*>(L.base + sg.GR) + unit * L.R;
+    const SeqGates gt = seq_gates<T, D, DF>(a, L, sr);
+    for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < n; idx += stride)
+      grg[(jlo + idx) % L.R] = gt.at(jlo + idx);
+  }
   const int64_t m0 = jlo >> 3;
   const int ng = int(((pend - 1) >> 3) - m0 + 1);
   for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < ng * D; idx += stride) {
@@ -1176,6 +1355,14 @@ __global__ void prefill_advance(PrefillArgs a) {
   const int64_t p = *pos + a.seq_len[bl];
   *pos = p;
   *nf = p - L.Wd > 0 ? p - L.Wd : 0;
+  if (a.gated && a.seq_len[bl] > 0) {  // G_{p-1}; the scan left S, z decayed to it
+    const LayerSections sg = layer_sections(a.B, a.Hkv, D, DF, L.R, sizeof(T), true);
+    double* gst = reinterpret_cast<double*>(L.base + sg.G) + 2 * unit;
+    const double* gc = reinterpret_cast<const double*>(a.ws + int64_t(L.ls) * a.ws_slot + a.ws_gc);
+    const double ge = gc[(int64_t(a.seq_start[bl]) + a.seq_len[bl] - 1) * a.Hkv + g];
+    gst[0] = ge;
+    gst[1] = ge;
+  }
 }
 
 // The kernels of one prefill launch, for the a.nlayer layers of a.layers
@@ -1188,6 +1375,12 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
   for (int i = 0; i < a.nlayer; ++i) window = window || a.layers[i].W > 0;
   auto main = [&](int pass) {
     const dim3 grid(a.nseg, a.Hkv, nl), block(kMT);
+    if (a.gated) {  // the shared denominator only
+      if (a.phi == GLIDE_PHI_SOFTMAX) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 0, true>), grid, block, 0, s, a);
+      else if (a.phi) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 0, true>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 0, true>), grid, block, 0, s, a);
+      return;
+    }
     if (a.phi == GLIDE_PHI_SOFTMAX) {
       if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 0>), grid, block, 0, s, a);
       if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 1>), grid, block, 0, s, a);
@@ -1202,6 +1395,10 @@ hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
       if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 2>), grid, block, 0, s, a);
     }
   };
+  if (a.gated) {  // the new tokens' cumulative log-gates, before any kernel reads them
+    hipLaunchKernelGGL((prefill_gates<T, D, DF>), dim3(a.nseq, a.Hkv, nl), dim3(kThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   if (a.nseg > 0) {
     if (a.linear) {
       if (a.phi == GLIDE_PHI_SOFTMAX)

@@ -22,6 +22,7 @@ NO_LINEAR = 1
 HYBRID_SUM = 2
 HYBRID_STATE_ALL = 4
 PER_HEAD_PHI = 8
+GATED = 16
 
 STATUS = {0: "GLIDE_OK", -1: "GLIDE_ERR_NULL", -2: "GLIDE_ERR_INVALID", -3: "GLIDE_ERR_UNSUPPORTED",
           -4: "GLIDE_ERR_ALIGN", -5: "GLIDE_ERR_SIZE", -6: "GLIDE_ERR_HIP", -7: "GLIDE_ERR_SCRATCH"}
@@ -53,7 +54,8 @@ class LayerLayout(ctypes.Structure):
     _fields_ = [("pos_offset", ctypes.c_int64), ("nf_offset", ctypes.c_int64), ("cnt_offset", ctypes.c_int64),
                 ("s_offset", ctypes.c_int64),
                 ("z_offset", ctypes.c_int64), ("kring_offset", ctypes.c_int64),
-                ("vring_offset", ctypes.c_int64), ("layer_offset", ctypes.c_int64),
+                ("vring_offset", ctypes.c_int64), ("gate_offset", ctypes.c_int64),
+                ("gring_offset", ctypes.c_int64), ("layer_offset", ctypes.c_int64),
                 ("layer_bytes", ctypes.c_int64), ("window", ctypes.c_int32),
                 ("ring_slots", ctypes.c_int32)]
 
@@ -81,15 +83,15 @@ def load_library(path=None):
     lib.glide_workspace_bytes.restype = ctypes.c_size_t
     lib.glide_state_init.argtypes = [cfgp, vp, ctypes.c_size_t, vp]
     lib.glide_state_init.restype = ctypes.c_int
-    lib.glide_prefill.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp,
+    lib.glide_prefill.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp, vp,
                                   ctypes.POINTER(ctypes.c_int32), ctypes.c_int64, ctypes.c_int32, vp, vp,
                                   ctypes.c_size_t, vp]
     lib.glide_prefill.restype = ctypes.c_int
     lib.glide_decode_step.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp, vp,
-                                      vp, vp, vp, ctypes.c_size_t, vp]
+                                      vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.glide_decode_step.restype = ctypes.c_int
     lib.glide_decode_step_noalloc.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp,
-                                              vp, vp, vp, vp]
+                                              vp, vp, vp, vp, vp]
     lib.glide_decode_step_noalloc.restype = ctypes.c_int
     lib.glide_state_flush.argtypes = [cfgp, vp, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32, vp, vp]
     lib.glide_state_flush.restype = ctypes.c_int
@@ -171,7 +173,7 @@ class Glide:
 
     def __init__(self, n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, windows,
                  dtype=torch.bfloat16, sm_scale=None, linear=True, lib=None, form=0, phi=PHI_RELU,
-                 per_head_phi=False):
+                 per_head_phi=False, gated=False):
         self.lib = lib if lib is not None else load_library()
         self.windows = [int(w) for w in windows]
         if len(self.windows) != n_layers:
@@ -184,6 +186,8 @@ class Glide:
         flags = (0 if linear else NO_LINEAR) | {0: 0, 1: HYBRID_SUM, 2: HYBRID_SUM | HYBRID_STATE_ALL}.get(form, 99)
         if per_head_phi:
             flags |= PER_HEAD_PHI
+        if gated:
+            flags |= GATED
         self.cfg = Config(n_layers, batch, n_q_heads, n_kv_heads, head_dim, feat_dim, code, int(phi),
                           flags, float(sm_scale), self._win)
         self.n_layers, self.batch = n_layers, batch
@@ -194,6 +198,7 @@ class Glide:
         self.form = form
         self.phi = phi
         self.per_head_phi = per_head_phi
+        self.gated = gated
 
     # -- sizes and layout ----------------------------------------------------
     def state_bytes(self):
@@ -234,11 +239,24 @@ class Glide:
             "z": view(lay.z_offset, B * H * Df, torch.float32, (B, H, Df), 4),
             "kring_raw": view(lay.kring_offset, B * H * R * d, self.torch_dtype, (B, H, R * d), es),
             "vring_raw": view(lay.vring_offset, B * H * R * d, self.torch_dtype, (B, H, R * d), es),
+            # gated state only (empty otherwise): [G_{p-1}, G_f] and the gate ring, fp64
+            "gate": view(lay.gate_offset, B * H * 2 if self.gated else 0, torch.float64, (B, H, 2) if self.gated
+                         else (0,), 8),
+            "gring": view(lay.gring_offset, B * H * R if self.gated else 0, torch.float64, (B, H, R) if self.gated
+                          else (0,), 8),
             "window": lay.window, "ring_slots": R,
         }
 
     def _wf_numel(self, n_layers):
         return n_layers * (self.n_kv_heads if self.per_head_phi else 1) * self.head_dim * self.feat_dim
+
+    def _check_gates(self, log_gates, numel):
+        if self.gated:
+            if log_gates is None:
+                raise ValueError("a gated stack needs log_gates")
+            _check("log_gates", log_gates, numel, torch.float32)
+        elif log_gates is not None:
+            raise ValueError("log_gates given to a stack that is not gated")
 
     def _check_decode(self, state, phi_w, q, k, v, out, n_layers):
         dt = self.torch_dtype
@@ -272,32 +290,37 @@ class Glide:
         if s:
             raise GlideError(s, "glide_state_flush", self.lib)
 
-    def decode_step(self, state, phi_w, q, k, v, out, workspace=None, layer0=0, n_layers=None, stream=None):
+    def decode_step(self, state, phi_w, q, k, v, out, workspace=None, layer0=0, n_layers=None, stream=None,
+                    log_gates=None):
         if n_layers is None:
             n_layers = self.n_layers - layer0
         self._check_decode(state, phi_w, q, k, v, out, n_layers)
+        self._check_gates(log_gates, n_layers * self.batch * self.n_kv_heads)
         _check("workspace", workspace)
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         s = self.lib.glide_decode_step(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
                                        int(layer0), int(n_layers), _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v),
-                                       _ptr(out), _ptr(workspace), ws_bytes, _stream(stream))
+                                       _ptr(log_gates), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream))
         if s:
             raise GlideError(s, "glide_decode_step", self.lib)
 
-    def decode_step_noalloc(self, state, phi_w, q, k, v, out, layer0=0, n_layers=None, stream=None):
+    def decode_step_noalloc(self, state, phi_w, q, k, v, out, layer0=0, n_layers=None, stream=None,
+                            log_gates=None):
         """decode_step with no workspace: split-window records go to the
         library's fixed per-GPU scratch (calls on one GPU must not overlap)."""
         if n_layers is None:
             n_layers = self.n_layers - layer0
         self._check_decode(state, phi_w, q, k, v, out, n_layers)
+        self._check_gates(log_gates, n_layers * self.batch * self.n_kv_heads)
         s = self.lib.glide_decode_step_noalloc(ctypes.byref(self.cfg), _ptr(state),
                                                state.numel() * state.element_size(), int(layer0), int(n_layers),
-                                               _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(stream))
+                                               _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v), _ptr(log_gates), _ptr(out),
+                                               _stream(stream))
         if s:
             raise GlideError(s, "glide_decode_step_noalloc", self.lib)
 
     def prefill(self, state, phi_w, q, k, v, cu_seqlens, out, workspace, layer0=0, n_layers=None, chunk=0,
-                stream=None):
+                stream=None, log_gates=None):
         if n_layers is None:
             n_layers = self.n_layers - layer0
         cu = [int(x) for x in cu_seqlens]
@@ -312,9 +335,11 @@ class Glide:
         _check("v", v, n_layers * T * self.n_kv_heads * self.head_dim, dt)
         _check("out", out, n_layers * T * self.n_q_heads * self.head_dim, dt)
         _check("workspace", workspace)
+        self._check_gates(log_gates, n_layers * T * self.n_kv_heads)
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
         s = self.lib.glide_prefill(ctypes.byref(self.cfg), _ptr(state), state.numel() * state.element_size(),
-                                   int(layer0), int(n_layers), _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v), cu_arr,
+                                   int(layer0), int(n_layers), _ptr(phi_w), _ptr(q), _ptr(k), _ptr(v),
+                                   _ptr(log_gates), cu_arr,
                                    int(cu[-1]), int(chunk), _ptr(out), _ptr(workspace), ws_bytes,
                                    _stream(stream))
         if s:

@@ -50,7 +50,7 @@ def align(x):
     return (x + 255) // 256 * 256
 
 
-def expected_layout(B, Hkv, d, Df, windows, es):
+def expected_layout(B, Hkv, d, Df, windows, es, gated=False):
     """The documented layout (include/glide.h), computed independently."""
     off = 0
     out = []
@@ -64,21 +64,25 @@ def expected_layout(B, Hkv, d, Df, windows, es):
         z = S + align(units * Df * d * 4)
         K = z + align(units * Df * 4)
         V = K + align(units * R * d * es)
-        end = V + align(units * R * d * es)
-        out.append(dict(pos=pos, nf=nf, cnt=cnt, S=S, z=z, K=K, V=V, R=R, bytes=end - off))
+        Gs = V + align(units * R * d * es)
+        GR = Gs + (align(units * 16) if gated else 0)
+        end = GR + (align(units * R * 8) if gated else 0)
+        out.append(dict(pos=pos, nf=nf, cnt=cnt, S=S, z=z, K=K, V=V, G=Gs, GR=GR, R=R, bytes=end - off))
         off = end
     return out, off
 
 
+@pytest.mark.parametrize("gated", [False, True])
 @pytest.mark.parametrize("dtype,es", [(torch.bfloat16, 2), (torch.float32, 4)])
-def test_layout_matches_documentation(dtype, es):
-    g = mk(dtype=dtype, n_layers=6, windows=[0, 1, 7, 8, 64, 4096])
-    exp, total = expected_layout(2, 2, 128, 64, g.windows, es)
+def test_layout_matches_documentation(dtype, es, gated):
+    g = mk(dtype=dtype, n_layers=6, windows=[0, 1, 7, 8, 64, 4096], gated=gated)
+    exp, total = expected_layout(2, 2, 128, 64, g.windows, es, gated)
     assert g.state_bytes() == total
     for l, e in enumerate(exp):
         lay = g.layout(l)
         assert (lay.pos_offset, lay.nf_offset, lay.cnt_offset, lay.s_offset, lay.z_offset, lay.kring_offset,
-                lay.vring_offset) == (e["pos"], e["nf"], e["cnt"], e["S"], e["z"], e["K"], e["V"])
+                lay.vring_offset, lay.gate_offset, lay.gring_offset) == (
+                    e["pos"], e["nf"], e["cnt"], e["S"], e["z"], e["K"], e["V"], e["G"], e["GR"])
         assert lay.ring_slots == e["R"] and lay.window == g.windows[l]
         assert lay.layer_bytes == e["bytes"]
         assert lay.ring_slots == 0 or (lay.ring_slots % 32 == 0 and lay.ring_slots >= lay.window + 8)
@@ -133,7 +137,9 @@ def test_hybrid_flag_combinations():
     for flags, code in ((glide.HYBRID_SUM, 0), (glide.HYBRID_SUM | glide.HYBRID_STATE_ALL, 0),
                         (glide.HYBRID_STATE_ALL, -2), (glide.NO_LINEAR | glide.HYBRID_SUM, -2),
                         (glide.PER_HEAD_PHI, 0), (glide.PER_HEAD_PHI | glide.HYBRID_SUM, 0),
-                        (16, -2)):
+                        (glide.GATED, 0), (glide.GATED | glide.PER_HEAD_PHI, 0),
+                        (glide.GATED | glide.NO_LINEAR, -2), (glide.GATED | glide.HYBRID_SUM, -3),
+                        (32, -2)):
         ok.cfg.flags = flags
         assert (ok.state_bytes() > 0) == (code == 0), flags
         if code:  # rejected before any HIP call (the pointer is never used)
@@ -165,13 +171,13 @@ def test_null_arguments(lib):
     assert lib.glide_state_layout(ctypes.byref(g.cfg), -1, ctypes.byref(out)) == -2
 
 
-def _decode(g, state=256, size=None, layer0=0, n=1, ptrs=(4096,) * 5, ws=1 << 20, ws_bytes=None):
+def _decode(g, state=256, size=None, layer0=0, n=1, ptrs=(4096,) * 5, ws=1 << 20, ws_bytes=None, gates=None):
     size = g.state_bytes() if size is None else size
     ws_bytes = g.workspace_bytes(0) if ws_bytes is None else ws_bytes
     P = [ctypes.c_void_p(x) if x is not None else None for x in ptrs]
     return g.lib.glide_decode_step(ctypes.byref(g.cfg), ctypes.c_void_p(state) if state else None, size,
-                                   layer0, n, P[0], P[1], P[2], P[3], P[4],
-                                   ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
+                                   layer0, n, P[0], P[1], P[2], P[3], ctypes.c_void_p(gates) if gates else None,
+                                   P[4], ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
 
 
 def test_decode_argument_errors():
@@ -228,12 +234,13 @@ def test_workspace_sizes():
     assert g.workspace_bytes(100000) > g.workspace_bytes(10)
 
 
-def _prefill(g, cu, total, chunk=0, ws_bytes=None, state=256, ptrs=(4096,) * 6):
+def _prefill(g, cu, total, chunk=0, ws_bytes=None, state=256, ptrs=(4096,) * 6, gates=None):
     arr = (ctypes.c_int32 * len(cu))(*cu)
     ws_bytes = g.workspace_bytes(total) if ws_bytes is None else ws_bytes
     P = [ctypes.c_void_p(x) if x is not None else None for x in ptrs]
     return g.lib.glide_prefill(ctypes.byref(g.cfg), ctypes.c_void_p(state), g.state_bytes(), 0, 1, P[0], P[1],
-                               P[2], P[3], arr, total, chunk, P[4], P[5], ws_bytes, None)
+                               P[2], P[3], ctypes.c_void_p(gates) if gates else None, arr, total, chunk, P[4],
+                               P[5], ws_bytes, None)
 
 
 def test_prefill_argument_errors():
@@ -276,7 +283,7 @@ def test_noalloc_decode_rejects_before_any_hip_call():
 
     def call(g, state=256, n=1):
         return g.lib.glide_decode_step_noalloc(ctypes.byref(g.cfg), ctypes.c_void_p(state) if state else None,
-                                               g.state_bytes(), 0, n, *P, None)
+                                               g.state_bytes(), 0, n, *P[:4], None, P[4], None)
     # G = 16 at d = 128, few units and huge windows: 1024 records of 16 x 259 floats > 16 MiB
     big = mk(n_layers=3, batch=32, n_q_heads=16, n_kv_heads=1, windows=[1 << 20] * 3)
     assert big.workspace_bytes(0) > glide.DECODE_SCRATCH_BYTES
@@ -288,7 +295,7 @@ def test_noalloc_decode_rejects_before_any_hip_call():
     assert call(g, state=260) == -4
     assert call(g, n=4) == -2
     assert g.lib.glide_decode_step_noalloc(ctypes.byref(g.cfg), ctypes.c_void_p(256), g.state_bytes(), 0, 1,
-                                           None, *P[1:], None) == -1
+                                           None, *P[1:4], None, P[4], None) == -1
 
 
 def test_binding_refuses_tensors_the_kernels_would_overrun():
@@ -305,3 +312,15 @@ def test_binding_refuses_tensors_the_kernels_would_overrun():
                   t(3, 5, 8, 128), t(256, dt=torch.uint8))
     with pytest.raises(ValueError, match="device tensor"):
         g.feature_map(t(128, 64), t(4, 128), t(4, 64))
+
+
+def test_gate_arguments():
+    """log_gates: required (and 4-byte aligned) exactly when the stack is
+    gated; rejected before any HIP call otherwise."""
+    ug, gg = mk(), mk(gated=True)
+    assert _decode(ug, gates=8192) == -2          # gates for an ungated stack
+    assert _decode(gg) == -1                      # gated without gates
+    assert _decode(gg, gates=8194) == -4          # misaligned
+    assert _prefill(ug, [0, 2, 3], 3, gates=8192) == -2
+    assert _prefill(gg, [0, 2, 3], 3) == -1
+    assert _prefill(gg, [0, 2, 3], 3, gates=8194) == -4
