@@ -88,14 +88,14 @@ class Run:
     """One workload resident on the GPU: library handle, state, workspace and
     every input of the prefill and of each decode step."""
 
-    def __init__(self, wl, form=0, phi_kind=0):
+    def __init__(self, wl, form=0, phi_kind=0, gated=False):
         import torch
         from paper_2607_24788_amd import glide, workload as W
         self.wl = wl
-        self.form, self.phi_kind = form, phi_kind
+        self.form, self.phi_kind, self.gated = form, phi_kind, gated
         dev = torch.device("cuda:0")
         self.g = glide.Glide(wl.n_layers, wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.feat_dim,
-                             wl.windows, dtype=wl.dtype, sm_scale=wl.tau, form=form, phi=phi_kind)
+                             wl.windows, dtype=wl.dtype, sm_scale=wl.tau, form=form, phi=phi_kind, gated=gated)
         self.lens = list(wl.context)
         self.cu = [0]
         for n in self.lens:
@@ -116,6 +116,10 @@ class Run:
         self.dv = torch.empty_like(self.dk)
         for s in range(S):
             self.dq[s], self.dk[s], self.dv[s] = W.decode_inputs(wl, s, device=dev)
+        self.pg = self.dg = None
+        if gated:
+            self.pg = torch.stack([W.prefill_log_gates(wl, l, self.lens, device=dev) for l in range(n_pre)])
+            self.dg = torch.stack([W.decode_log_gates(wl, s, device=dev) for s in range(S)])
         self.pout = torch.empty((n_pre, T, wl.n_q_heads, wl.head_dim), dtype=wl.dtype, device=dev)
         self.dout = torch.empty((L, wl.batch, wl.n_q_heads, wl.head_dim), dtype=wl.dtype, device=dev)
         self.state = self.g.new_state(dev)
@@ -127,20 +131,23 @@ class Run:
         if self.share_prefill:
             for l in range(wl.n_layers):
                 g.prefill(self.state, self.phi[l:l + 1], self.qp, self.kp, self.vp, self.cu, self.pout, self.ws,
-                          layer0=l, n_layers=1, chunk=wl.chunk)
+                          layer0=l, n_layers=1, chunk=wl.chunk, log_gates=self.pg)
         else:
-            g.prefill(self.state, self.phi, self.qp, self.kp, self.vp, self.cu, self.pout, self.ws, chunk=wl.chunk)
+            g.prefill(self.state, self.phi, self.qp, self.kp, self.vp, self.cu, self.pout, self.ws, chunk=wl.chunk,
+                      log_gates=self.pg)
 
     def fresh(self):
         self.g.state_init(self.state)
         self.prefill()
 
     def decode(self, s):
-        self.g.decode_step(self.state, self.phi, self.dq[s], self.dk[s], self.dv[s], self.dout, self.ws)
+        self.g.decode_step(self.state, self.phi, self.dq[s], self.dk[s], self.dv[s], self.dout, self.ws,
+                           log_gates=None if self.dg is None else self.dg[s])
 
     def decode_layer(self, s, l):
         self.g.decode_step(self.state, self.phi[l:l + 1], self.dq[s, l:l + 1], self.dk[s, l:l + 1],
-                           self.dv[s, l:l + 1], self.dout[l:l + 1], self.ws, layer0=l, n_layers=1)
+                           self.dv[s, l:l + 1], self.dout[l:l + 1], self.ws, layer0=l, n_layers=1,
+                           log_gates=None if self.dg is None else self.dg[s, l:l + 1])
 
     def timed_steps(self, steps, warmup):
         """The timed region: `warmup` untimed, then `steps` whole passes (init,
@@ -179,7 +186,7 @@ class Run:
         dec_bytes = decode_bytes(wl)
         pre_flops = prefill_flops(wl, self.lens)
         mfma_peak = MFMA_BF16_PEAK if wl.dtype == torch.bfloat16 else MFMA_FP32_PEAK
-        traffic = measured_traffic(wl.name) if self.form == 0 and self.phi_kind == 0 else None
+        traffic = measured_traffic(wl.name) if self.form == 0 and self.phi_kind == 0 and not self.gated else None
         hbm = {"bound": "hbm", "kernel": "decode step (decode_kernel over the whole stack; split windows "
                                          "merged by their last piece)",
                "achieved": dec_bytes / dec_step_s / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
@@ -294,6 +301,8 @@ def main():
                          "forms (separately normalised sum; state over the evicted tokens / every token)")
     ap.add_argument("--phi", type=int, default=0, choices=(0, 1, 2),
                     help="feature map: 0 ReLU (default), 1 ELU + 1, 2 softmax over the features")
+    ap.add_argument("--gated", action="store_true",
+                    help="the gated (GLA-style) linear state: log-gates uniform in [-0.4, 0] per token and KV head")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-detail", action="store_true",
@@ -319,7 +328,10 @@ def main():
     big = sum(wl.context) > 1_000_000 or wl.batch * max(wl.context) > 400_000
     steps = args.steps if args.steps is not None else (3 if big else 10)
     warmup = args.warmup if args.warmup is not None else (1 if big else 2)
-    run = Run(wl, args.form, args.phi)
+    if args.gated and args.form:
+        print("the gated state combines with the shared denominator only (--form 0)", file=sys.stderr)
+        sys.exit(2)
+    run = Run(wl, args.form, args.phi, args.gated)
     wall, pre_ms, dec_ms = run.timed_steps(steps, warmup)
     f = run.figures(pre_ms, dec_ms)
     has_decode = wl.decode_steps > 0
@@ -340,7 +352,7 @@ def main():
         "data": "synthetic (seeded N(0,1)/sqrt(d) q,k,v; Wf ~ N(0,1/d))"
                 + ("; prefill inputs of one layer reused by every layer" if run.share_prefill else ""),
         "config": dict(wl.describe(), chunk=wl.chunk, **({"form": args.form} if args.form else {}),
-                       **({"phi": args.phi} if args.phi else {})),
+                       **({"phi": args.phi} if args.phi else {}), **({"gated": True} if args.gated else {})),
         "decode_tokens_per_s": f["decode_tokens_per_s"] and round(f["decode_tokens_per_s"], 2),
         "decode_us_per_step": f["decode_us_per_step"] and round(f["decode_us_per_step"], 2),
         "decode_hbm_frac": f["decode_hbm_frac"] and round(f["decode_hbm_frac"], 4),
@@ -355,10 +367,10 @@ def main():
     if not args.no_detail and has_decode:
         line["decode_detail"] = run.detail()
         print("decode detail done", file=sys.stderr, flush=True)
-    if not args.no_cpu_baseline and has_decode:
+    if not args.no_cpu_baseline and has_decode and not args.gated:
         line["cpu_baseline"] = cpu_baseline(run, args.cpu_baseline_seconds)
         print("cpu baseline done", file=sys.stderr, flush=True)
-    if args.workload == "c3" and not args.no_extra and args.form == 0 and args.phi == 0:
+    if args.workload == "c3" and not args.no_extra and args.form == 0 and args.phi == 0 and not args.gated:
         del run
         torch.cuda.empty_cache()
         line["b1_ctx8k"] = batch1_block(W.workload("c2"), args.no_detail)

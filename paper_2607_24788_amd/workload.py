@@ -10,6 +10,7 @@ Input recipe (every tensor, every workload):
   q, k, v ~ N(0, 1) / sqrt(d), rounded to the element type (round to nearest even)
   Wf[l]   ~ N(0, 1/d)  (variance 1/d), one d x Df matrix per layer
   tau     = 1/sqrt(d)
+  log-gates of the gated state (when used) ~ U[-0.4, 0], fp32, per token and KV head
 Random streams are torch Philox generators seeded from (workload seed,
 layer, tensor, part) so any slice can be regenerated on its own.
 """
@@ -119,7 +120,7 @@ ALL = ["c1", "c2", "c3", "c4u", "c4", "c5"]
 # ---------------------------------------------------------------------------
 # Seeded tensors.
 
-_TENSOR_ID = {"q": 1, "k": 2, "v": 3, "phi_w": 4, "dq": 5, "dk": 6, "dv": 7}
+_TENSOR_ID = {"q": 1, "k": 2, "v": 3, "phi_w": 4, "dq": 5, "dk": 6, "dv": 7, "gate": 8, "dgate": 9}
 
 
 def _gen(seed, layer, tensor, part, device):
@@ -168,3 +169,20 @@ def decode_inputs(wl, step, layers=None, device="cpu", qkv_scale=None):
         k[i] = randn(k.shape[1:], wl.seed, l, "dk", step, s, wl.dtype, device)
         v[i] = randn(v.shape[1:], wl.seed, l, "dv", step, s, wl.dtype, device)
     return q, k, v
+
+
+GATE_LO = -0.4  # log-gates of the gated state: uniform in [GATE_LO, 0]
+
+
+def prefill_log_gates(wl, layer, seqlens, part=0, device="cpu"):
+    """Packed log-gates of one layer's prefill, [T][Hkv] fp32, uniform in
+    [GATE_LO, 0] (the paper fixes no gate; a per-token decay of e^-0.4 .. 1)."""
+    T = int(sum(seqlens))
+    g = _gen(wl.seed, layer, "gate", part, device)
+    return torch.rand((T, wl.n_kv_heads), generator=g, device=device) * GATE_LO
+
+
+def decode_log_gates(wl, step, device="cpu"):
+    """Log-gates of one decode step, [L][B][Hkv] fp32, uniform in [GATE_LO, 0]."""
+    g = _gen(wl.seed, 0, "dgate", step, device)
+    return torch.rand((wl.n_layers, wl.batch, wl.n_kv_heads), generator=g, device=device) * GATE_LO
