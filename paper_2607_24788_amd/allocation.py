@@ -15,6 +15,10 @@ layer itself):
   KV I/O column of the fine-tuned accuracy table): every softmax layer reads
   its window's keys and values, min(W_l, context) tokens of
   2 * n_kv_heads * head_dim elements; linear-only layers read none.
+* The accumulated KV I/O of decoding a sequence token by token (Sec. IV,
+  "KV I/O Efficient Reasoning Scalability", and the figure of accumulated KV
+  I/O against sequence length): the per-token I/O above summed over the
+  tokens, each reading min(W_l, t) tokens while the window fills.
 * The theoretical decode speedup of three equal blocks over the (0, 0, 0)
   hybrid baseline (Sec. III-C, "Speedup").
 """
@@ -89,6 +93,20 @@ def kv_io_bytes(windows_, context, n_kv_heads, head_dim, elem_bytes=2):
     for W in windows_:
         n = context if W is None else min(W, context)
         total += n * per_token
+    return total
+
+
+def accumulated_kv_io_bytes(windows_, n_tokens, n_kv_heads, head_dim, elem_bytes=2):
+    """KV-cache bytes read over a whole decode of n_tokens: token t (1-based)
+    reads min(W_l, t) cached tokens of every softmax layer (W_l = None: the
+    whole context, t tokens).  Per layer that is sum_{t=1..n} min(W, t) =
+    n(n+1)/2 for n <= W, else W(W+1)/2 + (n - W) W."""
+    per_token = 2 * n_kv_heads * head_dim * elem_bytes
+    n = int(n_tokens)
+    total = 0
+    for W in windows_:
+        m = n if W is None else min(W, n)
+        total += (m * (m + 1) // 2 + (n - m) * m) * per_token
     return total
 
 

@@ -110,3 +110,30 @@ def test_bench_decode_bytes_contain_the_kv_io_model():
         write = sum((1 if W == 0 else 1 / bench.FOLD_PERIOD) * (Df * d * 4 + Df * 4) * units for W in wl.windows)
         assert bench.decode_bytes(wl, state_write=1) == kv + tok + wf + (Df * d * 4 + Df * 4) * units * wl.n_layers
         assert bench.decode_bytes(wl) == round(kv + tok + wf + write), name
+
+
+def test_accumulated_kv_io_reproduces_the_figure():
+    """Accumulated KV I/O over a 128K-token decode (Sec. IV and its figure of
+    KV I/O against sequence length), Llama-3-8B shape, w = 1024, the 10/12/10
+    split that reproduces the table's MB/token.  The paper's figures come out
+    of this one model under two unit conventions (its "GB" values are 10^12-
+    scale):
+      caption, (0,0,0):        16.3  = MiB summed over 128,000 tokens / 10^6
+      text, (0,15w/16,w):      5.5   = the same convention (the text's 5.5-11.0)
+      text, baseline:          "over 17.5" = bytes over 131,072 tokens / 10^12
+    The caption's 5.2 for (0,15w/16,w) and the text's 11.0 for (0,0,w) are
+    not reproduced (5.48 and 11.22 under the first convention)."""
+    sizes = (10, 12, 10)
+    acc = lambda wins, n: A.accumulated_kv_io_bytes(wins, n, 8, 128, 2)
+    base = [1024] * 32                           # (0, 0, 0): every layer keeps the whole window
+    glide = A.windows(32, 1024, 960, sizes)      # (0, 15w/16, w)
+    late = A.windows(32, 1024, 0, sizes)         # (0, 0, w): the last block linear
+    mib6 = lambda b: b / A.MIB / 1e6
+    assert round(mib6(acc(base, 128_000)), 1) == 16.3
+    assert round(mib6(acc(glide, 128_000)), 1) == 5.5
+    assert 17.5 < acc(base, 131_072) / 1e12 < 17.6
+    assert abs(mib6(acc(late, 128_000)) - 11.22) < 0.01
+    # closed form against the plain sum of the per-token model, and the warm-up
+    for n in (1, 63, 64, 65, 1023, 1024, 1025, 5000):
+        assert acc(glide, n) == sum(A.kv_io_bytes(glide, t, 8, 128, 2) for t in range(1, n + 1))
+    assert A.accumulated_kv_io_bytes([None], 10, 1, 1, 1) == 2 * sum(range(1, 11))   # full attention: t tokens
