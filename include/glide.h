@@ -197,7 +197,9 @@ glide_status glide_state_init(const glide_config* cfg, void* state, size_t state
  *   k, v   device [n_layers][T][Hkv][d]
  *   log_gates  device fp32 [n_layers][T][Hkv] with GLIDE_GATED (the log-gate
  *          of every new token), else NULL
- *   cu_seqlens_host  HOST [B+1], cu[0] = 0, non-decreasing, cu[B] = T
+ *   cu_seqlens_host  HOST [B+1], cu[0] = 0, non-decreasing, cu[B] = T; one
+ *          sequence's new q rows must span less than 2 GiB (T_b * Hq * d *
+ *          element bytes < 2^31, else GLIDE_ERR_UNSUPPORTED)
  *   out    device [n_layers][T][Hq][d]
  *   workspace device, >= glide_workspace_bytes(cfg, T)
  * Element types follow cfg->dtype; device pointers 16-byte aligned. */

@@ -409,6 +409,11 @@ glide_status glide_prefill(const glide_config* cfg, void* state, size_t state_by
   if (cu_seqlens_host[0] != 0 || cu_seqlens_host[cfg->batch] != total_tokens) return GLIDE_ERR_INVALID;
   for (int32_t b = 0; b < cfg->batch; ++b)
     if (cu_seqlens_host[b + 1] < cu_seqlens_host[b]) return GLIDE_ERR_INVALID;
+  // the kernels address one sequence's new rows with 32-bit byte offsets
+  for (int32_t b = 0; b < cfg->batch; ++b)
+    if (int64_t(cu_seqlens_host[b + 1] - cu_seqlens_host[b]) * cfg->n_q_heads * cfg->head_dim * esize(cfg) >=
+        (int64_t(1) << 31))
+      return GLIDE_ERR_UNSUPPORTED;
   if (chunk == 0) chunk = 64;
   if (chunk < 32 || chunk > 256 || chunk % 32) return GLIDE_ERR_INVALID;
   const size_t need = glide_workspace_bytes(cfg, total_tokens);

@@ -776,23 +776,44 @@ void prefill_main(PrefillArgs a) {
     }
   };
   // band tiles: this thread's chunk of tile n (K and V), for buffer n % 2
+  // Band rows are read through buffer descriptors with 32-bit byte offsets
+  // per lane (the host guarantees a sequence's rows span less than 2 GiB): a
+  // row outside the band, or a history row of a tile that has none, reads
+  // zeros with no memory access.  New tokens' rows are Hkv * D elements
+  // apart; history rows (a continuing prefill) are consecutive.
   Frag<T> sk, sv;
-  bool fok = false;
   const bool stager = tid < 32 * CPR;  // wave-uniform
   const int srr = tid / CPR, sch = tid - srr * CPR;
+  const uint32_t rowb = uint32_t(a.Hkv) * D * sizeof(T);
   auto fetch = [&](int n) {
     if (stager) {
-      const int64_t j = kb0 + 32 * int64_t(n) + srr;
-      fok = j >= klo && j <= khi;
-      sk.load((fok ? sr.k(j) : sr.k_safe()) + 8 * sch);
-      sv.load((fok ? sr.v(j) : sr.v_safe()) + 8 * sch);
+      const int64_t jt = kb0 + 32 * int64_t(n);   // the tile's first key (uniform)
+      const int lo = int(klo - jt), hi = int(khi - jt);
+      const bool ok = srr >= lo && srr <= hi;
+      const int jr = int(jt - sr.p0) + srr;        // key relative to the first new token
+      const T* kn = sr.kin + (int64_t(sr.start) * a.Hkv + g) * D;
+      const T* vn = sr.vin + (int64_t(sr.start) * a.Hkv + g) * D;
+      const uint32_t nb = uint32_t(a.seq_len[bl]) * rowb;
+      const uint32_t cb = uint32_t(8 * sizeof(T)) * sch;  // the thread's 8-element chunk of the row
+      const uint32_t on = ok && jr >= 0 ? uint32_t(jr) * rowb + cb : kOOB;
+      bload_frag(sk, make_rsrc(kn, nb), on);
+      bload_frag(sv, make_rsrc(vn, nb), on);
+      if (jt < sr.p0) {  // the tile reaches into the history rows
+        const uint32_t hb = uint32_t(sr.p0 - sr.h0) * D * sizeof(T);
+        const uint32_t oh = ok && jr < 0 ? uint32_t(jr + int(sr.p0 - sr.h0)) * uint32_t(D * sizeof(T)) + cb : kOOB;
+        Frag<T> hk, hv;
+        bload_frag(hk, make_rsrc(sr.kh, hb), oh);
+        bload_frag(hv, make_rsrc(sr.vh, hb), oh);
+        sk = frag_or(sk, hk);
+        sv = frag_or(sv, hv);
+      }
     }
   };
   auto store = [&](int n) {
     if (stager) {
       T* kt = lds_fresh(bnd + (n & 1) * BAND);
-      store8(kt + srr * KROW + 8 * sch, frag_keep(sk, fok));
-      store8(kt + 32 * KROW + srr * VROW + 8 * sch, frag_keep(sv, fok));
+      store8(kt + srr * KROW + 8 * sch, sk);
+      store8(kt + 32 * KROW + srr * VROW + 8 * sch, sv);
     }
   };
   // (with a band, the first slab of delayed keys is loaded only after it:
