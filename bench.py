@@ -532,11 +532,75 @@ def cpu_baseline(run, budget_s):
             omp.omp_set_num_threads(threads)
         one = {"value": round(len(seqs) * s1 / e1, 3), "unit": "tokens/s", "cores": 1,
                "sample": f"{s1} steps, {e1:.1f} s"}
+    li = [0] * wl.n_layers if run.share_prefill else list(range(wl.n_layers))
+    n0 = run.lens[0]
+    pre = prefill_sample(wl, run.lens, oras, wf,
+                         lambda l: tuple(x[li[l], :n0].double().cpu().numpy() for x in (run.qp, run.kp, run.vp)),
+                         run.form)
+    pre["cores"] = threads
     return {"value": round(len(seqs) * steps / el, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{steps} full-stack decode steps ({wl.n_layers} layers) of sequences {seqs} of the batch "
                       f"of {wl.batch}, from the GPU state after the benchmark, {el:.1f} s; sequences are "
                       f"independent, so tokens/s = sequences x steps / time",
-            "one_thread": one, "cpu_model": _cpu_model()}
+            "one_thread": one, "prefill": pre, "cpu_model": _cpu_model()}
+
+
+def _sum_linear_and_band(n, W, form):
+    """Over the positions t < n of one sequence: the summed size of the
+    linear set (tokens before the window, every token up to t in form 2) and
+    of the window."""
+    band = n * (n + 1) // 2 if W >= n else W * (W + 1) // 2 + (n - W) * W
+    lin = n * (n + 1) // 2 if form == 2 else ((n - W) * (n - W + 1) // 2 if n > W else 0)
+    return lin, band
+
+
+def prefill_sample(wl, lens, oras, wf, inputs, form, positions=24):
+    """The oracle's prefill (its quadratic definition form, every output
+    position evaluated from the whole history) on a bounded sample: sequence
+    0 through the smallest-, middle- and largest-window layers at
+    `positions` evenly spaced positions, then scaled to the whole prefill of
+    the workload.  Per query head a position t costs the oracle
+    (Df + d) x |linear set| + 3d x |window| multiply-adds, plus phi of every
+    key row up to the last sampled position once per call; the phi time is
+    measured on its own and the rest gives one rate per unit of that cost.
+    The result is labelled extrapolated."""
+    import numpy as np
+    d, Df, Hq, Hkv = wl.head_dim, wl.feat_dim, wl.n_q_heads, wl.n_kv_heads
+    order = sorted(range(wl.n_layers), key=lambda l: wl.windows[l])
+    layers = sorted({order[0], order[len(order) // 2], order[-1]})
+    n0 = lens[0]
+    pos = np.array(sorted({int((i + 0.5) * n0 / positions) for i in range(positions)}), dtype=np.int64)
+    rows = (int(pos[-1]) + 1) * Hkv
+    t_att = units = 0.0
+    t_phi = None
+    for l in layers:
+        q, k, v = inputs(l)
+        if t_phi is None:
+            t0 = time.perf_counter()
+            oras[l].phi(wf[l], k[:int(pos[-1]) + 1])
+            t_phi = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        oras[l].attend(wf[l], q, k, v, positions=pos)
+        t_att += time.perf_counter() - t0 - t_phi
+        W = wl.windows[l]
+        for t in pos:
+            beta = max(0, int(t) + 1 - W)
+            lin = int(t) + 1 if form == 2 else beta
+            units += Hq * ((Df + d) * lin + 3 * d * (int(t) + 1 - beta))
+    rate = max(t_att, 1e-9) / units
+    est = 0.0
+    for W in wl.windows:
+        for n in lens:
+            lin, band = _sum_linear_and_band(n, W, form)
+            est += t_phi / rows * n * Hkv + rate * Hq * ((Df + d) * lin + 3 * d * band)
+    tokens = sum(lens)
+    return {"value": round(tokens / est, 4), "unit": "tokens/s", "kind": "oracle", "extrapolated": True,
+            "estimated_seconds": round(est, 1),
+            "sample": f"sequence 0 ({n0} tokens) through layers {layers} (windows "
+                      f"{[wl.windows[l] for l in layers]}) at {len(pos)} evenly spaced positions each: "
+                      f"{t_att + len(layers) * t_phi:.1f} s, scaled to {tokens} tokens x {wl.n_layers} layers by "
+                      f"the oracle's per-position cost ((Df + d) per linear-set token and 3d per window token, "
+                      f"per query head) and its phi time per key row"}
 
 
 def _cpu_model():
