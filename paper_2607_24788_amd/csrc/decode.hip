@@ -39,6 +39,27 @@ __device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
   return make_float4(__shfl_xor(v.x, m), __shfl_xor(v.y, m), __shfl_xor(v.z, m), __shfl_xor(v.w, m));
 }
 
+__device__ __forceinline__ uint2 bload8(brsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+
+// A wave-uniform 64-bit value from vector registers, in scalar registers.
+__device__ __forceinline__ uint64_t uniform64(uint32_t lo, uint32_t hi) {
+  return uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(int(lo)))) |
+         (uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(int(hi)))) << 32);
+}
+
+// x mod R for a position x >= 0 (a 64-bit remainder only past 2^32).
+__device__ __forceinline__ int32_t ring_slot(int64_t x, int32_t R) {
+  return (uint64_t(x) >> 32) == 0 ? int32_t(uint32_t(x) % uint32_t(R)) : int32_t(x % R);
+}
+
+// (slot + off) mod R, for an offset of a few rings at most.
+__device__ __forceinline__ int32_t ring_add(int32_t slot, int64_t off, int32_t R) {
+  const int32_t m = (slot + int32_t(off)) % R;
+  return m < 0 ? m + R : m;
+}
+
 __device__ __forceinline__ int clamp_rel(int64_t x) { return int(x < -1 ? -1 : (x > 32 ? 32 : x)); }
 
 template <typename T, int D>
@@ -181,7 +202,8 @@ void decode_kernel(DecodeArgs a) {
   constexpr int PVT = (kFoldPeriod * D + kThreads - 1) / kThreads;  // pending values per thread
   constexpr int WPR = RW * int(ES) / 16;   // 16-byte pieces per staged Wf row (bf16)
   constexpr int WCH = D * WPR / 64 > 0 ? D * WPR / 64 : 1;  // staged pieces per lane
-  constexpr int WPITCH = RW + 2;           // staged row pitch in elements (4 bytes of padding)
+  constexpr int WPITCH = RW + 4;           // staged row pitch in elements (8 bytes of padding: the
+                                           // column reads are 8-byte transposing LDS reads)
   static_assert(STEPS * RPS == RW && NTW * 16 == RW, "state rows must tile the wave");
 
   extern __shared__ __align__(16) float smem[];
@@ -219,20 +241,23 @@ void decode_kernel(DecodeArgs a) {
   const T* Wf = reinterpret_cast<const T*>(a.phi_w) +
                 (a.wf_heads ? int64_t(L.slot) * Hkv + g : int64_t(L.slot)) * D * DF;
 
-  // pos and nf: two scalar loads in flight together; the loads that do not
-  // depend on them (the state pass's Wf slice, S rows and z, the queries and
-  // the new key/value) are issued before the first wait for them.
-  const int64_t p = *pos_ptr;
-  int64_t nf = *nf_ptr;
-  // gated state (GLIDE_GATED): the new token's log-gate, G_{p-1} and G_f of
-  // the unit (scalar loads beside pos and nf); the unit's piece 0 keeps them
+  // pos and nf (gated: also G_{p-1}, G_f and the new token's log-gate) are
+  // the workgroup's first loads; every load that does not depend on them
+  // (the state pass's Wf slice, S rows and z, the queries, the new
+  // key/value) follows before the first wait.  They are vector loads read
+  // back into scalar registers: scalar loads share one counter with the
+  // kernel arguments, so a wait for an argument fetched after them would
+  // also wait for them, and hold back the loads behind it.  The compiler
+  // barrier keeps this issue order.
   const bool gated = a.gated != 0 && piece == 0;
   const LayerSections secg = layer_sections(B, Hkv, D, DF, R, sizeof(T), gated);
   double* gst = reinterpret_cast<double*>(lay + secg.G) + 2 * unit;  // [G_{p-1}, G_f]
   double* grg = reinterpret_cast<double*>(lay + secg.GR) + unit * int64_t(R);
-  const float gnew = gated ? a.gates[tok * Hkv + g] : 0.f;
-  const double gcur0 = gated ? gst[0] : 0.0, gfold = gated ? gst[1] : 0.0;
-  const double gcur = gcur0 + double(gnew);  // G_p
+  const uint2 pw = bload8(make_rsrc(pos_ptr, 8), 0);
+  const uint2 nw = bload8(make_rsrc(nf_ptr, 8), 0);
+  const uint4 gw = bload16(make_rsrc(gst, gated ? 16 : 0), 0);
+  const float gnw = bload_f(make_rsrc(gated ? a.gates + (tok * Hkv + g) : a.gates, gated ? 4 : 0), 0);
+  __asm__ volatile("" ::: "memory");
 
   float* ph = smem;                        // [G + kFoldPeriod][DF] phi(q_h), then phi(k_j) of pending j
   float* pvl = ph + (G + kFoldPeriod) * DF;  // [kFoldPeriod][D]    values of the pending tokens
@@ -293,6 +318,14 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) bload_frag(fq[kk], rq, hq < G ? uint32_t(hq * D + 32 * kk + 8 * lg) * ES : kOOB);
 
+  // (pos, nf and the gate values are read back into scalar registers here)
+  const int64_t p = int64_t(uniform64(pw.x, pw.y));
+  int64_t nf = int64_t(uniform64(nw.x, nw.y));
+  const float gnew = gated ? __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, gnw))) : 0.f;
+  const double gcur0 = gated ? __builtin_bit_cast(double, uniform64(gw.x, gw.y)) : 0.0;
+  const double gfold = gated ? __builtin_bit_cast(double, uniform64(gw.z, gw.w)) : 0.0;
+  const double gcur = gcur0 + double(gnew);  // G_p
+
   // Linear set after this step: tokens [0, beta).  S, z hold tokens [0, nf);
   // tokens [nf, beta) are pending (in the ring, or the new token when Wd = 0)
   // and enter the read-out through phi(k_j) v_j.  They are folded for good on
@@ -307,9 +340,13 @@ void decode_kernel(DecodeArgs a) {
   nf = nf > beta - fper ? nf : beta - fper;
   nf = nf > 0 ? nf : 0;
   const int npend = lin ? int(beta - nf) : 0;  // 0 .. fper
-  const bool fold = npend > 0 && (npend >= fper || (beta + int64_t(unit % fper)) % fper == 0);
+  // (fper is a power of two: the unit's turn is (beta + unit) mod fper = 0)
+  const bool fold = npend > 0 && (npend >= fper || ((beta + unit) & (fper - 1)) == 0);
   const bool s_nonzero = lin && nf > 0;  // S, z hold something
-  const int32_t nf_slot = R > 0 ? int32_t(nf % R) : 0;  // ring slot of token nf
+  // Ring slots in 32-bit arithmetic: the slot of p once, every other slot
+  // from it by an offset of less than a few rings.
+  const int32_t pr = R > 0 ? ring_slot(p, R) : 0;  // ring slot of token p
+  const int32_t nf_slot = R > 0 ? ring_add(pr, nf - p, R) : 0;  // ring slot of token nf
   // gated: S, z are decayed to G_f; read at p they weigh e^{G_p - G_f}, and
   // pending token j weighs e^{G_p - G_j} (its G_j from the gate ring; the new
   // token itself, pending when Wd = 0, weighs 1)
@@ -328,7 +365,7 @@ void decode_kernel(DecodeArgs a) {
   const int n_all = W > 0 ? int((p >> 5) - tile0 + 1) : 0;
   int t_first = 0, n_tiles = n_all;
   if (split) {
-    const int off = lin_unit ? kStateTiles : 0;
+    const int off = lin_unit ? a.state_tiles : 0;
     const int share = (n_all + off + L.npiece - 1) / L.npiece;
     t_first = piece * share - off;
     t_first = t_first > 0 ? t_first : 0;
@@ -338,7 +375,7 @@ void decode_kernel(DecodeArgs a) {
   const bool own_p = W > 0 && t_first <= n_all - 1 && n_all - 1 < n_tiles;  // the new token's partial
   int it = t_first + wave;
   int64_t j0 = (tile0 + it) << 5;
-  uint32_t s0 = W > 0 ? uint32_t(j0 % R) : 0u;
+  uint32_t s0 = W > 0 ? uint32_t(ring_add(pr, j0 - p, R)) : 0u;
   const uint32_t step = W > 0 ? uint32_t((32 * kWaves) % R) : 0u;
   const brsrc_t rpk = Wd > 0 ? rK : rk;  // where pending keys / values live
   const brsrc_t rpv = Wd > 0 ? rV : rv;
@@ -424,7 +461,7 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
-        for (int nt = 0; nt < NTW; ++nt) wb[kk][nt].load_strided(wfs + (32 * kk + 8 * lg) * WPITCH + 16 * nt + hq, WPITCH);
+        for (int nt = 0; nt < NTW; ++nt) load_colfrag(wb[kk][nt], wfs, WPITCH, 32 * kk + 8 * lg, 16 * nt);
     }
   }
 
@@ -765,7 +802,7 @@ void decode_kernel(DecodeArgs a) {
   // ---- 7. the new token into its ring slot (no token of this step reads
   //         that slot), position and fold count
   if (W > 0 && piece == 0 && tid < D) {
-    const int32_t sn = int32_t(p % R);
+    const int32_t sn = pr;
     Kr[kring_elem(sn, tid, D)] = kraw;
     Vr[vring_elem(sn, tid, D)] = vraw;
   }
@@ -775,7 +812,7 @@ void decode_kernel(DecodeArgs a) {
     if (gated) {
       gst[0] = gcur;
       if (fold) gst[1] = gcur;
-      if (W > 0) grg[p % R] = gcur;
+      if (W > 0) grg[pr] = gcur;
     }
   }
 }
@@ -887,7 +924,7 @@ hipError_t launch_t(const DecodeArgs& a, int total_wg, bool streaming, hipStream
   const size_t head = size_t(G + kFoldPeriod) * DF + size_t(kFoldPeriod) * D + 2 * D + kMaxG + kMaxG * kFoldPeriod;
   constexpr int RPS = 256 / D;  // state rows per wave step (lanes per row: D / 4)
   const size_t tail = size_t(kWaves) * RPS * G * D + kWaves * G + size_t(kWaves) * G * D + kWaves * G + kWaves * G;
-  const size_t staged = sizeof(T) == 2 ? size_t(kWaves) * D * (DF / kWaves + 2) / 2 : 0;
+  const size_t staged = sizeof(T) == 2 ? size_t(kWaves) * D * (DF / kWaves + 4) / 2 : 0;
   const size_t floats = head + (tail > staged ? tail : staged);
   if (streaming)
     hipLaunchKernelGGL((decode_kernel<T, D, DF, true>), dim3(unsigned(total_wg)), dim3(kThreads),

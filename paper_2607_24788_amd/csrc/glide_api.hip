@@ -120,28 +120,43 @@ glide_status decode_slots(int32_t* out) {
 }
 
 // Decode window split (pieces per unit of each layer of one launch).  The
-// work of a unit is counted in 32-token window tiles plus kStateTiles for the
-// state pass; a layer whose units have work w gets min(kMaxPieces, ceil(w / q))
-// pieces, with q the smallest piece size (>= 4 tiles) for which the launch
-// fits in `slots` workgroups.  When the launch's units alone fill the slots,
-// nothing is split.  The plan depends only on the launch's layers and the
-// device, so a call over one layer splits that layer's window over the whole
-// device.
-std::vector<int32_t> decode_pieces(const glide_config* c, const int32_t* layers, int32_t n, int32_t slots) {
-  std::vector<int32_t> np(n, 1);
+// work of a unit is counted in 32-token window tiles plus kStateTilesLatency
+// for the state pass; a layer whose units have work w gets
+// min(cap, ceil(w / q)) pieces, with q the smallest piece size (>= 4 tiles)
+// for which the launch fits in `slots` workgroups, and cap the most pieces
+// that still give every piece four tiles or more (one per wave), one when
+// the window has fewer than kSplitMinTiles tiles.  When the launch's units
+// alone fill the slots, nothing is split.  The plan depends only on the
+// launch's layers and the device, so a call over one layer splits that
+// layer's window over the whole device.  state_tiles: the state pass's weight
+// in the shares of the pieces (the kernel gives piece 0 that many tiles
+// fewer), kStateTilesStream once pieces are long enough for the launch to be
+// bandwidth-bound.
+struct DecodePlan {
+  std::vector<int32_t> np;  // pieces per unit, per layer of the launch
+  int32_t state_tiles;
+};
+
+DecodePlan decode_pieces(const glide_config* c, const int32_t* layers, int32_t n, int32_t slots) {
+  DecodePlan plan{std::vector<int32_t>(n, 1), kStateTilesLatency};
   const int64_t per_layer = int64_t(c->batch) * c->n_kv_heads;
-  if (per_layer * n >= slots) return np;
-  const int st = linear_on(c) ? kStateTiles : 0;
-  std::vector<int64_t> work(n);
+  if (per_layer * n >= slots) return plan;
+  const int st = linear_on(c) ? kStateTilesLatency : 0;
+  std::vector<int64_t> work(n), cap(n);
   int64_t wmax = 4;
+  bool any = false;
   for (int32_t i = 0; i < n; ++i) {
     const int32_t W = c->windows[layers[i]];
-    work[i] = W > 0 ? decode_tiles_max(W) + st : 0;
+    const int64_t tiles = decode_tiles_max(W);
+    work[i] = W > 0 ? tiles + st : 0;
+    cap[i] = tiles >= kSplitMinTiles ? std::min<int64_t>(kMaxPieces, tiles / 4) : 1;
     wmax = std::max(wmax, work[i]);
+    any = any || cap[i] > 1;
   }
+  if (!any) return plan;
   auto pieces = [&](int64_t q, int32_t i) {
     if (work[i] == 0) return int64_t(1);
-    return std::min<int64_t>(kMaxPieces, std::max<int64_t>(1, (work[i] + q - 1) / q));
+    return std::min<int64_t>(cap[i], std::max<int64_t>(1, (work[i] + q - 1) / q));
   };
   auto wgs = [&](int64_t q) {
     int64_t m = 0;
@@ -154,8 +169,9 @@ std::vector<int32_t> decode_pieces(const glide_config* c, const int32_t* layers,
     if (wgs(mid) <= slots) hi = mid;
     else lo = mid + 1;
   }
-  for (int32_t i = 0; i < n; ++i) np[i] = int32_t(pieces(lo, i));
-  return np;
+  for (int32_t i = 0; i < n; ++i) plan.np[i] = int32_t(pieces(lo, i));
+  if (lo >= kStreamPieceTiles) plan.state_tiles = kStateTilesStream;
+  return plan;
 }
 
 // Decode workspace bound over every call on any device (what
@@ -163,16 +179,18 @@ std::vector<int32_t> decode_pieces(const glide_config* c, const int32_t* layers,
 // layers): a launch splits only when its units number fewer than its device's
 // slots (at most kMaxDecodeSlots), and then it has at most that many
 // workgroups, and at most the pieces its layers get at the smallest piece
-// size.
+// size (none for a window of fewer than kSplitMinTiles tiles).
 size_t decode_ws(const glide_config* c) {
   const int64_t per_layer = int64_t(c->batch) * c->n_kv_heads;
   if (per_layer >= kMaxDecodeSlots) return 0;
-  const int st = linear_on(c) ? kStateTiles : 0;
+  const int st = linear_on(c) ? kStateTilesLatency : 0;
   int64_t wgs = 0;
   bool any = false;
   for (int32_t l = 0; l < c->n_layers; ++l) {
-    const int64_t work = c->windows[l] > 0 ? decode_tiles_max(c->windows[l]) + st : 0;
-    const int64_t p = work ? std::min<int64_t>(kMaxPieces, std::max<int64_t>(1, (work + 3) / 4)) : 1;
+    const int64_t tiles = decode_tiles_max(c->windows[l]);
+    const int64_t work = c->windows[l] > 0 ? tiles + st : 0;
+    const int64_t cap = tiles >= kSplitMinTiles ? std::min<int64_t>(kMaxPieces, tiles / 4) : 1;
+    const int64_t p = work ? std::min<int64_t>(cap, std::max<int64_t>(1, (work + 3) / 4)) : 1;
     wgs += p * per_layer;
     any = any || p > 1;
   }
@@ -209,7 +227,9 @@ glide_status for_layer_groups(const glide_config* cfg, int32_t layer0, int32_t n
     const int32_t cnt = std::min(kMaxLayersPerLaunch, n_layers - first);
     int32_t ls[kMaxLayersPerLaunch];
     for (int32_t i = 0; i < cnt; ++i) ls[i] = layer0 + order[first + i];
-    const std::vector<int32_t> np = decode_pieces(cfg, ls, cnt, slots);
+    const DecodePlan plan = decode_pieces(cfg, ls, cnt, slots);
+    const std::vector<int32_t>& np = plan.np;
+    a.state_tiles = plan.state_tiles;
     a.n_layers = cnt;
     int32_t rows = 0;
     bool split = false;

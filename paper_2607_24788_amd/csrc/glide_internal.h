@@ -21,6 +21,7 @@ __host__ __device__ inline int64_t align256(int64_t x) { return (x + 255) & ~int
 // units, so on every step about 1/kFoldPeriod of the state is written back
 // instead of all of it.  W = 0 layers (no ring) fold every step.
 constexpr int kFoldPeriod = 8;
+static_assert((kFoldPeriod & (kFoldPeriod - 1)) == 0, "the fold turn is a bit mask");
 
 // Ring slots of a layer with softmax window W: R >= W + kFoldPeriod holds the
 // window, the pending tokens and keeps the new token's slot distinct from
@@ -108,7 +109,18 @@ struct LayerArg {
 constexpr int kDecodeWgPerCu = 2;
 constexpr int kMaxDecodeSlots = 1024;
 constexpr int kMaxPieces = 16;
-constexpr int kStateTiles = 16;     // state pass cost in 32-token window tiles
+// The state pass of piece 0 counted in 32-token window tiles, for the shares
+// of a split window: in a latency-bound launch (small pieces) it is a chain
+// of dependent loads and LDS steps that lasts as long as about 16 tiles; in
+// a bandwidth-bound one (pieces of kStreamPieceTiles tiles or more) it costs
+// its bytes, about 4 tiles.
+constexpr int kStateTilesLatency = 16;
+constexpr int kStateTilesStream = 4;
+constexpr int kStreamPieceTiles = 32;
+// A unit whose window has fewer tiles than this is not split: the merge of
+// the pieces (records written through to memory, a counter, the records read
+// back) lasts longer than a whole workgroup's pass over such a window.
+constexpr int kSplitMinTiles = 10;
 __host__ __device__ inline int decode_tiles_max(int32_t W) { return W > 0 ? (W + 31) / 32 + 1 : 0; }
 // floats of one partial record: per head m, l, dn, acc[d], nm[d]
 __host__ __device__ inline int64_t part_floats(int G, int d) { return int64_t(G) * (2 * d + 3); }
@@ -611,7 +623,7 @@ struct DecodeArgs {
   int32_t gated;       // GLIDE_GATED: log_gates [layer][B][Hkv] fp32, gate sections in the state
   const float* gates;
   int32_t wf_heads;  // 1: phi_w holds one Wf per KV head ([layer][Hkv][d][Df])
-  int32_t pad;
+  int32_t state_tiles;  // the state pass's weight in window tiles for the shares of split windows
   LayerArg layers[kMaxLayersPerLaunch];  // sorted by decreasing W
   // layer (index into layers) of every piece row: workgroup w of the main
   // pass belongs to layer piece_layer[w / row_stride].  The rows of every

@@ -31,7 +31,7 @@ def _eager(case, st, phi, qs, ks, vs):
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 def test_graph_per_layer_decode_matches_eager(dtype):
     d = 128 if dtype == torch.bfloat16 else 64
-    case = Case([3, 0, 40, 9, 130], batch=3, Hq=8, Hkv=2, d=d, Df=d, dtype=dtype, seed=8)
+    case = Case([3, 0, 40, 9, 330], batch=3, Hq=8, Hkv=2, d=d, Df=d, dtype=dtype, seed=8)
     n0, n = 20, 24
     q, k, v = case.tokens(n0 + n)
     phi = case.phi_w.cuda()

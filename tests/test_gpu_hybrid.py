@@ -17,8 +17,8 @@ FORMS = [1, 2]
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_decode_from_empty(form, dtype):
     """70 decode steps from an empty state, every output and the final state
-    checked; few units, so long windows are split over workgroups."""
-    case = Case([0, 1, 5, 33, 64], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=dtype, seed=40 + form, form=form)
+    checked; few units, so the long window (330) is split over workgroups."""
+    case = Case([0, 1, 5, 33, 64, 330], batch=2, Hq=8, Hkv=2, d=128, Df=128, dtype=dtype, seed=40 + form, form=form)
     q, k, v = case.tokens(70)
     st = case.new_state()
     out = case.decode_steps(st, q, k, v, 0, 70)
@@ -57,10 +57,11 @@ def test_prefill_chunks(form, chunk):
 @pytest.mark.parametrize("form", FORMS)
 def test_continuing_prefill_then_decode(form):
     """prefill(n1), prefill(n2) from the reached state, then decode steps at
-    ragged positions: every output and the state against the definition."""
-    case = Case([0, 3, 40, 129], batch=3, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=60 + form,
+    ragged positions (the 330 window split over workgroups, with a linear
+    part): every output and the state against the definition."""
+    case = Case([0, 3, 40, 129, 330], batch=3, Hq=8, Hkv=2, d=128, Df=128, dtype=torch.bfloat16, seed=60 + form,
                 form=form)
-    n1 = [20, 0, 150]
+    n1 = [20, 0, 350]
     n2 = [70, 45, 9]
     tot = [a + b for a, b in zip(n1, n2)]
     q, k, v = case.tokens(max(tot) + 12)

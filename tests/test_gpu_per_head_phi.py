@@ -38,9 +38,9 @@ def test_prefill_ragged(phi, d, Df):
 
 @pytest.mark.parametrize("form", [0, 1])
 def test_prefill_then_decode(form):
-    case = Case([0, 3, 40, 129], batch=2, Hq=16, Hkv=4, d=128, Df=128, dtype=torch.bfloat16, seed=120 + form,
+    case = Case([0, 3, 40, 129, 330], batch=2, Hq=16, Hkv=4, d=128, Df=128, dtype=torch.bfloat16, seed=120 + form,
                 form=form, per_head_phi=True)
-    lens = [150, 37]
+    lens = [400, 37]
     q, k, v = case.tokens(max(lens) + 10)
     st = case.new_state()
     case.prefill(st, q, k, v, [0] * 2, lens, chunk=32)

@@ -15,7 +15,7 @@ pytestmark = pytest.mark.gpu
 CASES = [
     # windows, batch, Hq, Hkv, d, Df, dtype, prefill lengths, decode steps
     ([0, 300, 2000], 2, 16, 2, 128, 128, torch.bfloat16, [700, 1500], 3),
-    ([5, 100], 1, 4, 1, 64, 64, torch.float32, [150], 2),
+    ([5, 400], 1, 4, 1, 64, 64, torch.float32, [450], 2),
 ]
 
 
