@@ -205,6 +205,7 @@ void decode_kernel(DecodeArgs a) {
   constexpr int WPITCH = RW + 4;           // staged row pitch in elements (8 bytes of padding: the
                                            // column reads are 8-byte transposing LDS reads)
   static_assert(STEPS * RPS == RW && NTW * 16 == RW, "state rows must tile the wave");
+  static_assert(STEPS % 4 == 0, "a lane's state rows are read in fours");
 
   extern __shared__ __align__(16) float smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -291,6 +292,7 @@ void decode_kernel(DecodeArgs a) {
   const bool lin_call = a.linear != 0 && piece == 0;
   const int f0 = wave * RW;
   const int lr = lane / LPR, c4 = (lane % LPR) * 4;
+  const int r0 = f0 + lr * STEPS;  // the lane's STEPS consecutive state rows r0 .. r0 + STEPS - 1
   uint4 wst[WCH];  // bf16: this wave's Wf columns, 16-byte row pieces
   Frag<T> wb[KS][NTW];
   if constexpr (sizeof(T) == 2) {
@@ -309,7 +311,7 @@ void decode_kernel(DecodeArgs a) {
   }
   float4 sr[STEPS];
 #pragma unroll
-  for (int s = 0; s < STEPS; ++s) sr[s] = bload_f4_s<NT>(rS, lin_call ? uint32_t(((f0 + s * RPS + lr) * D + c4) * 4) : kOOB);
+  for (int s = 0; s < STEPS; ++s) sr[s] = bload_f4_s<NT>(rS, lin_call ? uint32_t(((r0 + s) * D + c4) * 4) : kOOB);
   float zf = bload_f(rz, lin_call && lane < RW ? uint32_t((f0 + lane) * 4) : kOOB);
   // the new token's element tid % D (its own score, and the ring write at the end)
   const T kraw = bload_elem(rk, uint32_t(tid % D) * ES, T());
@@ -540,29 +542,40 @@ void decode_kernel(DecodeArgs a) {
   //         of the launch.)
   const bool early = fold;  // fold before the read-out
   const float* pk = ph + G * DF;
-  // S' = S + sum_j phi(k_j)^T v_j on the wave's rows (and z'), written back
+  // S' = S + sum_j phi(k_j)^T v_j on the wave's rows (and z'), written back.
+  // The lane's rows are consecutive, so a token's weights for them come from
+  // LDS in 16-byte reads; tokens go two at a time, their reads issued
+  // together.  Every row is written on a fold: with up to kFoldPeriod tokens
+  // a row none of them touches is rare.
   auto fold_rows = [&](float4 (&rows)[STEPS], float& zrow) {
-    uint32_t touched = 0;
     float dz = 0.f;
-    for (int i = 0; i < npend; ++i) {
-      const float4 vv = *reinterpret_cast<const float4*>(pvl + i * D + c4);
+    for (int i = 0; i < npend; i += 2) {
+      const int i1 = i + 1 < npend ? i + 1 : i;
+      const float sc1 = i + 1 < npend ? 1.f : 0.f;  // an odd count: the last pair's second token weighs 0
+      const float4 v0 = *reinterpret_cast<const float4*>(pvl + i * D + c4);
+      float4 v1 = *reinterpret_cast<const float4*>(pvl + i1 * D + c4);
+      v1 = make_float4(v1.x * sc1, v1.y * sc1, v1.z * sc1, v1.w * sc1);
+      float w0[STEPS], w1[STEPS];
+#pragma unroll
+      for (int s = 0; s < STEPS; s += 4) {
+        const float4 a = *reinterpret_cast<const float4*>(pk + i * DF + r0 + s);
+        const float4 b = *reinterpret_cast<const float4*>(pk + i1 * DF + r0 + s);
+        w0[s] = a.x; w0[s + 1] = a.y; w0[s + 2] = a.z; w0[s + 3] = a.w;
+        w1[s] = b.x; w1[s + 1] = b.y; w1[s + 2] = b.z; w1[s + 3] = b.w;
+      }
 #pragma unroll
       for (int s = 0; s < STEPS; ++s) {
-        const float w = pk[i * DF + f0 + s * RPS + lr];
-        touched |= uint32_t(w != 0.f) << s;
-        rows[s].x = fmaf(w, vv.x, rows[s].x);
-        rows[s].y = fmaf(w, vv.y, rows[s].y);
-        rows[s].z = fmaf(w, vv.z, rows[s].z);
-        rows[s].w = fmaf(w, vv.w, rows[s].w);
+        rows[s].x = fmaf(w1[s], v1.x, fmaf(w0[s], v0.x, rows[s].x));
+        rows[s].y = fmaf(w1[s], v1.y, fmaf(w0[s], v0.y, rows[s].y));
+        rows[s].z = fmaf(w1[s], v1.z, fmaf(w0[s], v0.z, rows[s].z));
+        rows[s].w = fmaf(w1[s], v1.w, fmaf(w0[s], v0.w, rows[s].w));
       }
-      if (lane < RW) dz += pk[i * DF + f0 + lane];
+      if (lane < RW) dz += pk[i * DF + f0 + lane] + sc1 * pk[i1 * DF + f0 + lane];
     }
     zrow += dz;
-    // On the first fold every row is written, whatever the memory held.
 #pragma unroll
-    for (int s = 0; s < STEPS; ++s)
-      if (!s_nonzero || gated || ((touched >> s) & 1u)) store_nt(S + (f0 + s * RPS + lr) * D + c4, rows[s]);
-    if (lane < RW && (dz != 0.f || !s_nonzero || gated)) z[f0 + lane] = zrow;
+    for (int s = 0; s < STEPS; ++s) store_nt(S + (r0 + s) * D + c4, rows[s]);
+    if (lane < RW) z[f0 + lane] = zrow;
   };
   if (lin) {
     // S, z are zero until the first fold (their memory is not read as such)
@@ -581,12 +594,16 @@ void decode_kernel(DecodeArgs a) {
       const float* pq = ph + hh * DF;
       float4 n4 = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-      for (int s = 0; s < STEPS; ++s) {
-        const float w = pq[f0 + s * RPS + lr];
-        n4.x = fmaf(w, sr[s].x, n4.x);
-        n4.y = fmaf(w, sr[s].y, n4.y);
-        n4.z = fmaf(w, sr[s].z, n4.z);
-        n4.w = fmaf(w, sr[s].w, n4.w);
+      for (int s = 0; s < STEPS; s += 4) {
+        const float4 w4 = *reinterpret_cast<const float4*>(pq + r0 + s);
+        const float w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          n4.x = fmaf(w[u], sr[s + u].x, n4.x);
+          n4.y = fmaf(w[u], sr[s + u].y, n4.y);
+          n4.z = fmaf(w[u], sr[s + u].z, n4.z);
+          n4.w = fmaf(w[u], sr[s + u].w, n4.w);
+        }
       }
       // the RPS row groups of the wave are summed in the merge (no
       // cross-lane exchange here); the denominator partial over the wave's
