@@ -80,9 +80,8 @@ struct WindowTile {
 // whose L2s are not coherent with each other: the records were written
 // through to memory and are read from there, every load of the workgroup
 // issued before the first wait.
-template <typename T, int D, int DF>
+template <typename T, int D, int DF, int NP, int EPT>
 __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& L, int rem, int64_t p) {
-  constexpr int EPT = 4;                   // output elements per thread whose loads go first
   static_assert(kMaxPieces * kMaxG <= kThreads, "one (piece, head) scalar pair per thread");
   __shared__ float pw[kThreads];  // [piece][G]: m
   __shared__ float pe[kThreads];  // [piece][G]: the piece's weight e^(m - M)
@@ -116,7 +115,7 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
   const float l0 = bload_f_sys(r0, mok && mpc == 0 ? mo + 4 : kOOB);
   const float l1 = bload_f_sys(r1, mok && mpc > 0 ? (mpc - 1) * rs + mo + 4 : kOOB);
   const float dnv = bload_f_sys(r0, tid < G ? uint32_t(tid * RH + 2) * 4 : kOOB);  // linear denominator
-  float v[EPT][kMaxPieces], nmv[EPT];
+  float v[EPT][NP], nmv[EPT];
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     const int i = tid + e * kThreads;
@@ -125,7 +124,7 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
     const bool ok = i < n;
     v[e][0] = bload_f_sys(r0, ok ? o : kOOB);
 #pragma unroll
-    for (int pc = 1; pc < kMaxPieces; ++pc) v[e][pc] = bload_f_sys(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
+    for (int pc = 1; pc < NP; ++pc) v[e][pc] = bload_f_sys(r1, ok && pc < np ? (pc - 1) * rs + o : kOOB);
     nmv[e] = bload_f_sys(r0, ok ? o + D * 4 : kOOB);
   }
   // every thread writes its slot (kThreads slots; no branch, so the loads
@@ -138,7 +137,7 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
   if (mok) {
     float M = -INFINITY;
 #pragma unroll
-    for (int pc = 0; pc < kMaxPieces; ++pc)
+    for (int pc = 0; pc < NP; ++pc)
       if (pc < np) M = fmaxf(M, pw[pc * G + mh]);
     const float w = mm == -INFINITY ? 0.f : exp2f(mm - M);
     pe[tid] = w;
@@ -146,12 +145,12 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
     if (mpc == 0) pm[mh] = M;
   }
   __syncthreads();
-  auto out_elem = [&](int i, const float (&vp)[kMaxPieces], float nm) {
+  auto out_elem = [&](int i, const float (&vp)[NP], float nm) {
     const int hh = i / D;
     const float M = pm[hh];
     float Ls = 0.f, Ac = 0.f;
 #pragma unroll
-    for (int pc = 0; pc < kMaxPieces; ++pc) {
+    for (int pc = 0; pc < NP; ++pc) {
       if (pc < np) {
         Ls += pl[pc * G + hh];
         Ac = fmaf(vp[pc], pe[pc * G + hh], Ac);
@@ -178,10 +177,10 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
   for (int i = tid + EPT * kThreads; i < n; i += kThreads) {  // G * D > EPT * 256 (large G)
     const int hh = i / D, c = i - hh * D;
     const uint32_t o = uint32_t(hh * RH + 3 + c) * 4;
-    float vp[kMaxPieces];
+    float vp[NP];
     vp[0] = bload_f_sys(r0, o);
 #pragma unroll
-    for (int pc = 1; pc < kMaxPieces; ++pc) vp[pc] = bload_f_sys(r1, pc < np ? (pc - 1) * rs + o : kOOB);
+    for (int pc = 1; pc < NP; ++pc) vp[pc] = bload_f_sys(r1, pc < np ? (pc - 1) * rs + o : kOOB);
     out_elem(i, vp, bload_f_sys(r0, o + D * 4));
   }
   if (tid == 0) *pos_ptr = p + 1;
@@ -813,7 +812,19 @@ void decode_kernel(DecodeArgs a) {
       if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
-    if (last) merge_unit<T, D, DF>(a, L, rem, p);
+    if (last) {
+      const bool wide = G * D > 2 * kThreads;
+      if (L.npiece <= 4) {
+        if (wide) merge_unit<T, D, DF, 4, 4>(a, L, rem, p);
+        else merge_unit<T, D, DF, 4, 2>(a, L, rem, p);
+      } else if (L.npiece <= 8) {
+        if (wide) merge_unit<T, D, DF, 8, 4>(a, L, rem, p);
+        else merge_unit<T, D, DF, 8, 2>(a, L, rem, p);
+      } else {
+        if (wide) merge_unit<T, D, DF, kMaxPieces, 4>(a, L, rem, p);
+        else merge_unit<T, D, DF, kMaxPieces, 2>(a, L, rem, p);
+      }
+    }
   }
 
   // ---- 7. the new token into its ring slot (no token of this step reads
