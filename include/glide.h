@@ -172,8 +172,8 @@ glide_status glide_state_layout(const glide_config* cfg, int32_t layer, glide_la
  * 1 GiB (at least one).  Decode uses the workspace only when a launch has
  * fewer (sequence, KV head) units than the device holds resident decode
  * workgroups in one round (two per compute unit: 512 on MI355X): it then
- * splits long windows over several workgroups, whose partial results it
- * holds.  The size bounds that for every call on any device (at most 1024
+ * splits long windows (more than 256 tokens) over several workgroups, whose
+ * partial results it holds.  The size bounds that for every call on any device (at most 1024
  * records; a call over any subset of the layers).  0 if cfg is invalid. */
 size_t glide_workspace_bytes(const glide_config* cfg, int64_t max_total_tokens);
 

@@ -232,6 +232,14 @@ def test_workspace_sizes():
     big = mk(n_layers=4, batch=128, n_q_heads=16, n_kv_heads=8, windows=[0, 5, 64, 100])
     assert big.workspace_bytes(0) == 256
     assert g.workspace_bytes(100000) > g.workspace_bytes(10)
+    # a window of fewer than 10 tiles of 32 tokens (window + 1 tile) is never
+    # split, whatever the batch: no partial records
+    assert mk(n_layers=3, batch=1, windows=[0, 5, 255]).workspace_bytes(0) == 256
+    assert mk(n_layers=3, batch=1, windows=[0, 5, 288]).workspace_bytes(0) > 256
+    # a split gives every piece 4 tiles or more: a 10-tile window at most 2
+    # pieces per unit (12 units here: B=2 x 2 KV heads x 3 layers)
+    w10 = mk(n_layers=3, batch=2, n_q_heads=8, n_kv_heads=2, windows=[288, 288, 288])
+    assert w10.workspace_bytes(0) <= align(2 * 12 * 4 * (2 * 128 + 3) * 4)
 
 
 def _prefill(g, cu, total, chunk=0, ws_bytes=None, state=256, ptrs=(4096,) * 6, gates=None):
