@@ -173,10 +173,10 @@ def test_split_and_unsplit_paths():
 
 @pytest.mark.parametrize("per_layer_call", [False, True])
 @pytest.mark.parametrize("batch,Hkv", [(1, 8), (2, 4), (1, 3)])
-def test_split_pieces_on_one_xcd(batch, Hkv, per_layer_call):
-    """Split windows at 8B-like shapes: a unit's pieces share a workgroup
-    index modulo 8 (rows of B*Hkv workgroups padded to a multiple of 8), and
-    their records meet in one L2.  Long windows, several pieces per unit,
+def test_split_pieces(batch, Hkv, per_layer_call):
+    """Split windows at 8B-like shapes: long windows, several pieces per
+    unit (short pieces: the state pass weighed as a latency chain), merged
+    by whichever piece finishes last through records written to memory,
     whole-stack and per-layer calls, against the oracle."""
     case = Case([0, 16, 300, 1100, 2100], batch=batch, Hq=4 * Hkv, Hkv=Hkv, d=128, Df=128,
                 dtype=torch.bfloat16, seed=11 + batch + Hkv)
@@ -203,3 +203,28 @@ def test_split_pieces_on_one_xcd(batch, Hkv, per_layer_call):
     case.check_state(st, k, v, [p + n for p in pos], f"B={batch} Hkv={Hkv}")
     for l in range(case.L):
         assert int(case.g.layer_views(st, l)["cnt"].abs().max()) == 0, f"layer {l}: split counts not reset"
+
+
+def test_long_pieces():
+    """A call over one long-window layer with 256 units (batch 32, 8 KV
+    heads): two pieces per unit of more than 32 tiles each, the launch
+    bandwidth-bound, so piece 0's share is cut by the state pass's bytes
+    (4 tiles) instead of its latency; against the oracle."""
+    batch, Hkv = 32, 8
+    case = Case([2100], batch=batch, Hq=4 * Hkv, Hkv=Hkv, d=128, Df=128, dtype=torch.bfloat16, seed=29)
+    pos = [2150 + 13 * b for b in range(batch)]
+    n = 4
+    q, k, v = case.tokens(max(pos) + n)
+    st = case.new_state()
+    case.load_state_from_oracle(st, q, k, v, pos)
+    phi = case.phi_w.cuda()
+    outs = []
+    for step in range(n):
+        sel = lambda x: torch.stack([x[:, b, pos[b] + step] for b in range(batch)], 1).contiguous().cuda()
+        qs, ks, vs = sel(q), sel(k), sel(v)
+        o = torch.empty_like(qs)
+        case.g.decode_step(st, phi, qs, ks, vs, o, case.ws)
+        outs.append(o)
+    case.check_decode(torch.stack(outs, 2).cpu(), q, k, v, pos, n, "B=32 one long layer")
+    case.check_state(st, k, v, [p + n for p in pos], "B=32 one long layer")
+    assert int(case.g.layer_views(st, 0)["cnt"].abs().max()) == 0, "split counts not reset"
