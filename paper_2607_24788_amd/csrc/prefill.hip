@@ -905,16 +905,20 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) {
           if (!interior) {
-            // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row exists
+            // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row
+            // exists: one interval [olo, ohi] of offsets per row (empty for a
+            // row that does not exist), tested without branches
             const int base = int(kb - (t0 + ti[qt]));
             const int64_t offlo = klo - kb;  // first in-band offset of the tile (<= 31)
             const int lo = offlo < -1 ? -1 : int(offlo);
+            const int olo = max(lo, 1 - W - base);
+            const int ohi = rv[qt] ? -base : -1;
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
               for (int i = 0; i < 4; ++i) {
                 const int off = 8 * lg + 4 * t + i;
-                const bool ok = rv[qt] && off >= lo && base + off <= 0 && base + off > -W;
+                const bool ok = (off >= olo) & (off <= ohi);
                 sc[qt][t][i] = ok ? sc[qt][t][i] : -INFINITY;
               }
           }
