@@ -782,9 +782,11 @@ void prefill_main(PrefillArgs a) {
   // zeros with no memory access.  New tokens' rows are Hkv * D elements
   // apart; history rows (a continuing prefill) are consecutive.
   Frag<T> sk, sv;
-  const bool stager = tid < 32 * CPR;  // wave-uniform
+  // wave-uniform; every thread when the tile's chunks cover the workgroup
+  const bool stager = 32 * CPR >= kMT || tid < 32 * CPR;
   const int srr = tid / CPR, sch = tid - srr * CPR;
   const uint32_t rowb = uint32_t(a.Hkv) * D * sizeof(T);
+  const uint32_t nbytes = uint32_t(a.seq_len[bl]) * rowb;  // the sequence's new rows
   auto fetch = [&](int n) {
     if (stager) {
       const int64_t jt = kb0 + 32 * int64_t(n);   // the tile's first key (uniform)
@@ -793,11 +795,10 @@ void prefill_main(PrefillArgs a) {
       const int jr = int(jt - sr.p0) + srr;        // key relative to the first new token
       const T* kn = sr.kin + (int64_t(sr.start) * a.Hkv + g) * D;
       const T* vn = sr.vin + (int64_t(sr.start) * a.Hkv + g) * D;
-      const uint32_t nb = uint32_t(a.seq_len[bl]) * rowb;
       const uint32_t cb = uint32_t(8 * sizeof(T)) * sch;  // the thread's 8-element chunk of the row
       const uint32_t on = ok && jr >= 0 ? uint32_t(jr) * rowb + cb : kOOB;
-      bload_frag(sk, make_rsrc(kn, nb), on);
-      bload_frag(sv, make_rsrc(vn, nb), on);
+      bload_frag(sk, make_rsrc(kn, nbytes), on);
+      bload_frag(sv, make_rsrc(vn, nbytes), on);
       if (jt < sr.p0) {  // the tile reaches into the history rows
         const uint32_t hb = uint32_t(sr.p0 - sr.h0) * D * sizeof(T);
         const uint32_t oh = ok && jr < 0 ? uint32_t(jr + int(sr.p0 - sr.h0)) * uint32_t(D * sizeof(T)) + cb : kOOB;
@@ -893,10 +894,12 @@ void prefill_main(PrefillArgs a) {
             for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
           }
         }
-        const int64_t kb = kb0 + 32 * int64_t(n);
+        // the tile's first key, relative to the chunk's first token t0 (a
+        // band spans less than 2^31 keys: 32-bit arithmetic)
+        const int kb = int(kb0 - t0) + 32 * n;
         // keys [kb, kb+31] lie inside the band of every row of the pass
         // (tokens t0+ti_min .. t0+ti_max) for all but the edge tiles
-        const bool interior = kb >= t0 + ti_max - W + 1 && kb + 31 <= t0 + ti_min;
+        const bool interior = kb >= ti_max - W + 1 && kb + 31 <= ti_min;
         // raw scores, -inf outside the band (edge tiles; set in place), and
         // each row's tile max (the scale sc2 > 0 joins the exponent's FMA;
         // the max is taken raw)
@@ -908,9 +911,9 @@ void prefill_main(PrefillArgs a) {
             // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row
             // exists: one interval [olo, ohi] of offsets per row (empty for a
             // row that does not exist), tested without branches
-            const int base = int(kb - (t0 + ti[qt]));
-            const int64_t offlo = klo - kb;  // first in-band offset of the tile (<= 31)
-            const int lo = offlo < -1 ? -1 : int(offlo);
+            const int base = kb - ti[qt];
+            const int offlo = int(klo - t0) - kb;  // first in-band offset of the tile (<= 31)
+            const int lo = offlo < -1 ? -1 : offlo;
             const int olo = max(lo, 1 - W - base);
             const int ohi = rv[qt] ? -base : -1;
 #pragma unroll
