@@ -755,14 +755,37 @@ void prefill_main(PrefillArgs a) {
   // delayed keys i' of the chunk (key j = t0 - Wd + i'), a slab of SL at a time
   Frag<T> kst[VPT], vst[VPT];
   bool sok[VPT];
+  // Key and value rows are read through buffer descriptors with 32-bit
+  // byte offsets per lane (the host guarantees a sequence's rows span less
+  // than 2 GiB): a row that is not needed, or a history row of a slab that
+  // has none, reads zeros with no memory access.  New tokens' rows are
+  // Hkv * D elements apart; history rows (a continuing prefill) are
+  // consecutive.
+  const uint32_t rowb = uint32_t(a.Hkv) * D * sizeof(T);
+  const uint32_t nbytes = uint32_t(a.seq_len[bl]) * rowb;  // the sequence's new rows
+  const T* kn0 = sr.kin + (int64_t(sr.start) * a.Hkv + g) * D;  // this KV head's first new row
+  const T* vn0 = sr.vin + (int64_t(sr.start) * a.Hkv + g) * D;
+  const uint32_t hbytes = uint32_t(sr.p0 - sr.h0) * D * sizeof(T);  // the history rows
   auto load_slab = [&](int s0) {
+    const int64_t jb = t0 - Wd + s0;  // the slab's first key (uniform)
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
       const int id = tid + u * kMT, r = id / CPR, ch = id - r * CPR;
-      const int64_t j = t0 - Wd + s0 + r;
+      const int64_t j = jb + r;
       sok[u] = s0 + r < nk && j >= 0;
-      kst[u].load((sok[u] ? sr.k(j) : sr.k_safe()) + 8 * ch);
-      vst[u].load((sok[u] ? sr.v(j) : sr.v_safe()) + 8 * ch);
+      const int jr = int(j - sr.p0);  // key relative to the first new token
+      const uint32_t cb = uint32_t(8 * sizeof(T)) * ch;
+      const uint32_t on = sok[u] && jr >= 0 ? uint32_t(jr) * rowb + cb : kOOB;
+      bload_frag(kst[u], make_rsrc(kn0, nbytes), on);
+      bload_frag(vst[u], make_rsrc(vn0, nbytes), on);
+      if (jb < sr.p0) {  // the slab reaches into the history rows
+        const uint32_t oh = sok[u] && jr < 0 ? uint32_t(jr + int(sr.p0 - sr.h0)) * uint32_t(D * sizeof(T)) + cb : kOOB;
+        Frag<T> hk, hv;
+        bload_frag(hk, make_rsrc(sr.kh, hbytes), oh);
+        bload_frag(hv, make_rsrc(sr.vh, hbytes), oh);
+        kst[u] = frag_or(kst[u], hk);
+        vst[u] = frag_or(vst[u], hv);
+      }
     }
   };
   auto put_slab = [&]() {
@@ -785,8 +808,6 @@ void prefill_main(PrefillArgs a) {
   // wave-uniform; every thread when the tile's chunks cover the workgroup
   const bool stager = 32 * CPR >= kMT || tid < 32 * CPR;
   const int srr = tid / CPR, sch = tid - srr * CPR;
-  const uint32_t rowb = uint32_t(a.Hkv) * D * sizeof(T);
-  const uint32_t nbytes = uint32_t(a.seq_len[bl]) * rowb;  // the sequence's new rows
   auto fetch = [&](int n) {
     if (stager) {
       const int64_t jt = kb0 + 32 * int64_t(n);   // the tile's first key (uniform)
