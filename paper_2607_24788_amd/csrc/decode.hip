@@ -160,12 +160,12 @@ __device__ __forceinline__ void merge_unit(const DecodeArgs& a, const LayerArg& 
     float o;
     if (a.form != 0) {  // hybrid forms: each part over its own denominator
       o = Ac / Ls + (dn > 0.f ? nm / dn : 0.f);
-    } else if (dn > 0.f) {
-      const float c2 = fmaxf(M, log2f(dn));
-      const float ws = exp2f(M - c2), wlin = exp2f(-c2);
-      o = (Ac * ws + nm * wlin) / (Ls * ws + dn * wlin);
     } else {
-      o = Ac / Ls;
+      // (no branch: an empty linear part, dn = 0, weighs 0 and leaves Ac / Ls)
+      const bool lin = dn > 0.f;
+      const float c2 = fmaxf(M, lin ? log2f(dn) : -INFINITY);
+      const float ws = exp2f(M - c2), wlin = lin ? exp2f(-c2) : 0.f;
+      o = (Ac * ws + nm * wlin) / (Ls * ws + dn * wlin);
     }
     og[i] = from_f32<T>(o);
   };
@@ -755,20 +755,19 @@ void decode_kernel(DecodeArgs a) {
       M = sp;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wm[w * G + hh]);
+      // (no branches: a part with no scores has max -inf and weighs
+      // exp2(-inf) = 0; the frame is 0 when every part is empty, and the
+      // new token's value is selected only when it was scored)
+      const float Mf = M == -INFINITY ? 0.f : M;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        const float mw = wm[w * G + hh];
-        if (mw != -INFINITY) {
-          const float e = exp2f(mw - M);
-          Ls = fmaf(wl[w * G + hh], e, Ls);
-          Ac = fmaf(wacc[(w * G + hh) * D + c], e, Ac);
-        }
+        const float e = __builtin_amdgcn_exp2f(wm[w * G + hh] - Mf);
+        Ls = fmaf(wl[w * G + hh], e, Ls);
+        Ac = fmaf(wacc[(w * G + hh) * D + c], e, Ac);
       }
-      if (sp != -INFINITY) {
-        const float e = exp2f(sp - M);
-        Ls += e;
-        Ac = fmaf(vpl[c], e, Ac);
-      }
+      const float ep = __builtin_amdgcn_exp2f(sp - Mf);
+      Ls += ep;
+      Ac = sp != -INFINITY ? fmaf(vpl[c], ep, Ac) : Ac;
     }
     if (split) {
       const uint32_t ro = uint32_t(hh * (2 * D + 3)) * 4;
@@ -785,13 +784,11 @@ void decode_kernel(DecodeArgs a) {
     if (a.form != 0) {  // the Appendix's hybrid forms: two normalised outputs added
       o = (W > 0 ? Ac / Ls : 0.f) + (dn > 0.f ? nm / dn : 0.f);
     } else if (W > 0) {
-      if (dn > 0.f) {
-        const float c2 = fmaxf(M, log2f(dn));
-        const float ws = exp2f(M - c2), wlin = exp2f(-c2);
-        o = (Ac * ws + nm * wlin) / (Ls * ws + dn * wlin);
-      } else {
-        o = Ac / Ls;
-      }
+      // (no branch: an empty linear part, dn = 0, weighs 0 and leaves Ac / Ls)
+      const bool lin_part = dn > 0.f;
+      const float c2 = fmaxf(M, lin_part ? log2f(dn) : -INFINITY);
+      const float ws = exp2f(M - c2), wlin = lin_part ? exp2f(-c2) : 0.f;
+      o = (Ac * ws + nm * wlin) / (Ls * ws + dn * wlin);
     } else {
       o = dn > 0.f ? nm / dn : 0.f;
     }
