@@ -68,13 +68,6 @@ struct SeqRows {
     if (j >= h0) return vh + (j - h0) * D;
     return nullptr;
   }
-  // A key/value row that always exists (the sequence's first new token):
-  // masked-off lanes load from it, so that every load is unconditional and
-  // the zeros are selected where the value is used.  (A load skipped by a
-  // branch whose other side zeroes the register makes the wave wait for the
-  // loads in flight, serialising the prefetches.)
-  __device__ const T* k_safe() const { return kin + (int64_t(start) * Hkv + g) * D; }
-  __device__ const T* v_safe() const { return vin + (int64_t(start) * Hkv + g) * D; }
   // packed query row of new token i (0-based within the call) and head hh of the group
   __device__ int64_t qrow(int i, int hh) const { return (int64_t(start) + i) * Hq + int64_t(g) * G + hh; }
 };
@@ -255,19 +248,6 @@ struct SlabKeys {
   Frag<T> x[D / 32];
   bool ok;  // the lane's key row exists (else it counts as zeros)
 };
-// krow(r) is the address of key row r of the slab, or nullptr (zeros); such
-// rows are loaded from safe and masked in phi_slab.
-template <typename T, int D, int DF, int NK, typename RowFn>
-__device__ __forceinline__ void slab_keys(SlabKeys<T, D, DF>& sk, int nw, RowFn krow, const T* safe) {
-  constexpr int FT = DF / 16;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
-  const int kt = slab_key_tile<D, DF, NK>(nw);
-  const T* src = krow(16 * kt + hq);
-  sk.ok = src != nullptr;
-  if (!sk.ok) src = safe;
-#pragma unroll
-  for (int kk = 0; kk < D / 32; ++kk) sk.x[kk].load(src + 32 * kk + 8 * lg);
-}
 // kw: the weight of the lane's key row (16 kt + hq) multiplied into its
 // features (a gated segment's decay; 1 otherwise).
 template <typename T, int D, int DF, int NK, int PHI, bool kLds>
@@ -482,14 +462,53 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
   SlabKeys<T, D, DF> kx;
   Frag<T> vx[VPT];
   bool vok[VPT];
+  // Rows through buffer descriptors with 32-bit byte offsets per lane (the
+  // host guarantees a sequence's rows span less than 2 GiB): a row past the
+  // segment, or a history row of a slab that has none, reads zeros with no
+  // memory access.  New tokens' rows are Hkv * D elements apart; history
+  // rows (a continuing prefill) are consecutive.
+  const uint32_t rowb = uint32_t(a.Hkv) * D * sizeof(T);
+  const brsrc_t rkn = make_rsrc(sr.kin + (int64_t(sr.start) * a.Hkv + g) * D, uint32_t(a.seq_len[bl]) * rowb);
+  const brsrc_t rvn = make_rsrc(sr.vin + (int64_t(sr.start) * a.Hkv + g) * D, uint32_t(a.seq_len[bl]) * rowb);
+  const int nhist = int(sr.p0 - sr.h0);
+  const brsrc_t rkh = make_rsrc(sr.kh, uint32_t(nhist) * D * sizeof(T));
+  const brsrc_t rvh = make_rsrc(sr.vh, uint32_t(nhist) * D * sizeof(T));
+  // row j (absolute), byte cb of the row: its offset among the new rows
+  // and among the history rows (kOOB where it is not one, or not wanted)
+  auto offs = [&](int64_t j, uint32_t cb, bool ok, uint32_t& on, uint32_t& oh) {
+    const int jr = int(j - sr.p0);
+    on = ok && jr >= 0 ? uint32_t(jr) * rowb + cb : kOOB;
+    oh = ok && jr < 0 ? uint32_t(jr + nhist) * uint32_t(D * sizeof(T)) + cb : kOOB;
+  };
   auto load_slab = [&](int64_t j0) {
-    slab_keys<T, D, DF, kSegSlab>(kx, kSegWaves, [&](int r) { return j0 + r < jhi ? sr.k(j0 + r) : nullptr; },
-                                   sr.k_safe());
+    const bool hist = j0 < sr.p0;  // the slab reaches into the history rows (uniform)
+    {  // the lane's key row of the slab's key tile (phi_slab's A fragments)
+      const int64_t j = j0 + 16 * slab_key_tile<D, DF, kSegSlab>(kSegWaves) + hq;
+      kx.ok = j < jhi;
+#pragma unroll
+      for (int kk = 0; kk < D / 32; ++kk) {
+        uint32_t on, oh;
+        offs(j, uint32_t((32 * kk + 8 * lg) * sizeof(T)), kx.ok, on, oh);
+        bload_frag(kx.x[kk], rkn, on);
+        if (hist) {
+          Frag<T> h;
+          bload_frag(h, rkh, oh);
+          kx.x[kk] = frag_or(kx.x[kk], h);
+        }
+      }
+    }
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
       const int id = tid + u * kSegThreads, r = id / CPR, ch = id - r * CPR;
       vok[u] = j0 + r < jhi;
-      vx[u].load((vok[u] ? sr.v(j0 + r) : sr.v_safe()) + 8 * ch);
+      uint32_t on, oh;
+      offs(j0 + r, uint32_t(8 * sizeof(T)) * ch, vok[u], on, oh);
+      bload_frag(vx[u], rvn, on);
+      if (hist) {
+        Frag<T> h;
+        bload_frag(h, rvh, oh);
+        vx[u] = frag_or(vx[u], h);
+      }
     }
   };
   if (jlo < jhi) load_slab(jlo);
