@@ -44,9 +44,7 @@ namespace {
 
 constexpr int kThreads = 256;  // helper kernels
 constexpr int kWaves = 4;
-constexpr int kMT = 512;       // main kernel: 8 waves, 32 query rows each
-constexpr int kMW = 8;
-constexpr int kRB = 32 * kMW;  // query rows per pass of a chunk
+constexpr int kRB = 256;       // main kernel: query rows per pass of a chunk
 constexpr float kLog2e = 1.4426950408889634f;
 
 // Rows of one (sequence, KV head) of a layer: new tokens come from the
@@ -234,7 +232,7 @@ __device__ __forceinline__ void stage_wf(const T* Wf, T* Wn) {
 }
 
 // phi of NK keys (16 per key tile) into LDS pk[NK][row_t<DF>] (element type,
-// natural layout).  The NK/16 x DF/16 output tiles are spread over the nw
+// natural layout).  The NK/16 x DF/16 output tiles are spread over the NW
 // waves of the workgroup so that every tile of a wave has the same key tile
 // (slab_key_tile): phi_slab takes that tile's key rows as A fragments x
 // (rows that do not exist are zeros).
@@ -250,19 +248,21 @@ struct SlabKeys {
 };
 // kw: the weight of the lane's key row (16 kt + hq) multiplied into its
 // features (a gated segment's decay; 1 otherwise).
-template <typename T, int D, int DF, int NK, int PHI, bool kLds>
+template <typename T, int D, int DF, int NK, int PHI, int NW, bool kLds>
 __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const Frag<T> (&x)[D / 32], T* pk,
-                                         int nw, int rlo, int rhi, float kw = 1.f) {
+                                         int rlo, int rhi, float kw = 1.f) {
   constexpr int KS = D / 32, FT = DF / 16, PROW = row_t<DF>();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hq = lane & 15, lg = lane >> 4;
-  const int per = (NK / 16) * FT / nw;
+  constexpr int per = (NK / 16) * FT / NW;
+  static_assert(per >= 1 && per * NW == (NK / 16) * FT, "phi tiles must spread evenly over the waves");
   if constexpr (PHI == GLIDE_PHI_SOFTMAX) {
     // The softmax map needs each key row's max and sum over all DF features;
     // the row's feature tiles are spread over WPK = FT / per waves (per <= 4
     // tiles each, one key tile per wave).  Each wave reduces its part (its
     // lanes, then the row's 4 lane groups), the parts meet in the 16 spare
     // elements at the end of the row, two barriers apart.
-    constexpr int kPerMax = 4;
+    constexpr int kPerMax = per;
+    static_assert(FT % per == 0 && FT / per <= 4, "a row's parts fit the row's spare elements");
     const int kt = (wave * per) / FT, ft0 = (wave * per) % FT, wk = ft0 / per, WPK = FT / per;
     const int key = 16 * kt + hq;
     f32x4_t acc[kPerMax];
@@ -525,8 +525,8 @@ __global__ __launch_bounds__(kSegThreads) void prefill_segsum(PrefillArgs a) {
         const int64_t j = j0 + 16 * slab_key_tile<D, DF, kSegSlab>(kSegWaves) + hq;
         kw = j < jhi ? decay_exp(float(gend - gt.at(j))) : 0.f;
       }
-      phi_slab<T, D, DF, kSegSlab, PHI>(WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))}, x,
-                                        lds_fresh(pk), kSegWaves, 0, nrow < kSegSlab ? int(nrow) : kSegSlab, kw);
+      phi_slab<T, D, DF, kSegSlab, PHI, kSegWaves>(WfCols<T, D, DF, true>{lds_fresh(static_cast<const T*>(Wn))}, x,
+                                                   lds_fresh(pk), 0, nrow < kSegSlab ? int(nrow) : kSegSlab, kw);
     }
     {
       T* vw = lds_fresh(vs);
@@ -632,6 +632,15 @@ __global__ __launch_bounds__(kThreads) void prefill_scan(PrefillArgs a) {
 // are loaded before this pass's output stores.  Loads and stores retire in
 // order, so a load issued after the stores could only be waited for together
 // with them.
+//
+// A pass's 256 rows are spread over MW waves, 256 / MW rows (16-row q-tiles)
+// each: every K and V fragment read from a band tile feeds 256 / (16 MW)
+// q-tiles' MFMAs.  The workgroup's LDS (about 155 KB) admits one workgroup
+// per CU, so MW waves run MW / 4 per SIMD with 512 / (MW / 4) registers
+// each.
+template <typename T, int D>
+constexpr int main_waves() { return 8; }
+
 template <typename T, int D, int DF>
 struct MainLds {
   static constexpr int NBUF = 2;  // band stages
@@ -667,19 +676,22 @@ struct MainLds {
 // (every factor <= 1, whatever the gates), and on the chunk's last pass
 // S_{c+1} = e^{G_e - G_{t0-1}} S_c + sum_j e^{G_e - G_j} phi(k_j)^T v_j,
 // G_e the chunk's last token, after the masked block has read phi(k).
-template <typename T, int D, int DF, int PHI, int PASS, bool GATED = false>
-__global__ __launch_bounds__(kMT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+template <typename T, int D, int DF, int PHI, int PASS, bool GATED, int MW>
+__global__ __launch_bounds__(64 * MW) __attribute__((amdgpu_waves_per_eu(MW / 4, MW / 4)))
 void prefill_main(PrefillArgs a) {
   using LD = MainLds<T, D, DF>;
+  constexpr int NTH = 64 * MW, QT = kRB / (16 * MW);  // threads; 16-row q-tiles per wave
+  static_assert(QT * 16 * MW == kRB, "a pass's rows must spread evenly over the waves");
   constexpr int KS = D / 32, KSF = DF / 32, CT = D / 16, FT = DF / 16;
-  constexpr int NT = FT * CT / kMW;            // S tiles per wave (state update)
+  constexpr int NT = FT * CT / MW;            // S tiles per wave (state update)
   constexpr int SL = LD::SLAB;
   constexpr int SROW = LD::SROW, PROW = LD::PROW, VROW = LD::VROW, KROW = LD::KROW;
   constexpr int BAND = LD::BAND;
   constexpr int CPR = D / 8;                   // 8-element chunks per K/V row
-  constexpr int VPT = SL * CPR / kMT;          // slab chunks per thread (keys; values alike)
-  static_assert(NT * kMW == FT * CT, "S tiles must spread evenly over the waves");
-  static_assert(32 * CPR <= kMT && VPT >= 1 && VPT * kMT == SL * CPR, "staging must divide evenly");
+  constexpr int VPT = SL * CPR / NTH;          // slab chunks per thread (keys; values alike)
+  constexpr int SPT = (32 * CPR + NTH - 1) / NTH;  // band tile chunks per thread
+  static_assert(NT * MW == FT * CT, "S tiles must spread evenly over the waves");
+  static_assert(VPT >= 1 && VPT * NTH == SL * CPR && (SPT == 1 || SPT * NTH == 32 * CPR), "staging must divide evenly");
   // static LDS: the layout is fixed per instantiation
   __shared__ __align__(16) char smem[LD::bytes];
   T* Wn = reinterpret_cast<T*>(smem + LD::wn);          // [D][WROW]    Wf
@@ -736,8 +748,8 @@ void prefill_main(PrefillArgs a) {
   int c0 = s_lo, rb = 0, nk = 0, nrow = 0, ti_min = 0, ti_max = 0, ntile = 0;
   bool last_pass = true;
   int64_t t0 = 0, klo = 0, khi = 0, kb0 = 0;
-  int ti[2], hh[2];  // this lane's query row (row hq) in each of its two 16-row q-tiles
-  bool rv[2];
+  int ti[QT], hh[QT];  // this lane's query row (row hq) in each of its 16-row q-tiles
+  bool rv[QT];
   auto geom = [&]() {
     nk = min(s_hi, c0 + C) - c0;
     t0 = sr.p0 + c0;
@@ -747,8 +759,8 @@ void prefill_main(PrefillArgs a) {
     ti_min = rb / G;
     ti_max = (r_end - 1) / G;
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
-      const int r = rb + 32 * wave + 16 * qt + hq;
+    for (int qt = 0; qt < QT; ++qt) {
+      const int r = rb + 16 * QT * wave + 16 * qt + hq;
       rv[qt] = r < nrow;
       const int rr = rv[qt] ? r : rb;
       ti[qt] = rr / G;
@@ -764,16 +776,15 @@ void prefill_main(PrefillArgs a) {
 
   // ---- loads into registers (all unconditional; rows that do not exist are
   //      read from a row that does and replaced by zeros where stored)
-  Frag<T> qf[2][KS];
+  Frag<T> qf[QT][KS];
   auto load_q = [&]() {
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) qf[qt][kk].load(Q + sr.qrow(c0 + ti[qt], hh[qt]) * D + 32 * kk + 8 * lg);
   };
   // delayed keys i' of the chunk (key j = t0 - Wd + i'), a slab of SL at a time
   Frag<T> kst[VPT], vst[VPT];
-  bool sok[VPT];
   // Key and value rows are read through buffer descriptors with 32-bit
   // byte offsets per lane (the host guarantees a sequence's rows span less
   // than 2 GiB): a row that is not needed, or a history row of a slab that
@@ -789,16 +800,16 @@ void prefill_main(PrefillArgs a) {
     const int64_t jb = t0 - Wd + s0;  // the slab's first key (uniform)
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
-      const int id = tid + u * kMT, r = id / CPR, ch = id - r * CPR;
+      const int id = tid + u * NTH, r = id / CPR, ch = id - r * CPR;
       const int64_t j = jb + r;
-      sok[u] = s0 + r < nk && j >= 0;
+      const bool ok = s0 + r < nk && j >= 0;
       const int jr = int(j - sr.p0);  // key relative to the first new token
       const uint32_t cb = uint32_t(8 * sizeof(T)) * ch;
-      const uint32_t on = sok[u] && jr >= 0 ? uint32_t(jr) * rowb + cb : kOOB;
+      const uint32_t on = ok && jr >= 0 ? uint32_t(jr) * rowb + cb : kOOB;
       bload_frag(kst[u], make_rsrc(kn0, nbytes), on);
       bload_frag(vst[u], make_rsrc(vn0, nbytes), on);
       if (jb < sr.p0) {  // the slab reaches into the history rows
-        const uint32_t oh = sok[u] && jr < 0 ? uint32_t(jr + int(sr.p0 - sr.h0)) * uint32_t(D * sizeof(T)) + cb : kOOB;
+        const uint32_t oh = ok && jr < 0 ? uint32_t(jr + int(sr.p0 - sr.h0)) * uint32_t(D * sizeof(T)) + cb : kOOB;
         Frag<T> hk, hv;
         bload_frag(hk, make_rsrc(sr.kh, hbytes), oh);
         bload_frag(hv, make_rsrc(sr.vh, hbytes), oh);
@@ -807,14 +818,15 @@ void prefill_main(PrefillArgs a) {
       }
     }
   };
+  // (rows outside the slab were read as zeros: stored as they are)
   auto put_slab = [&]() {
     T* krw = lds_fresh(kr);
     T* vsw = lds_fresh(vs);
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
-      const int id = tid + u * kMT, r = id / CPR, ch = id - r * CPR;
-      store8(krw + r * KROW + 8 * ch, frag_keep(kst[u], sok[u]));
-      store8(vsw + r * VROW + 8 * ch, frag_keep(vst[u], sok[u]));
+      const int id = tid + u * NTH, r = id / CPR, ch = id - r * CPR;
+      store8(krw + r * KROW + 8 * ch, kst[u]);
+      store8(vsw + r * VROW + 8 * ch, vst[u]);
     }
   };
   // band tiles: this thread's chunk of tile n (K and V), for buffer n % 2
@@ -823,45 +835,53 @@ void prefill_main(PrefillArgs a) {
   // row outside the band, or a history row of a tile that has none, reads
   // zeros with no memory access.  New tokens' rows are Hkv * D elements
   // apart; history rows (a continuing prefill) are consecutive.
-  Frag<T> sk, sv;
+  Frag<T> sk[SPT], sv[SPT];
   // wave-uniform; every thread when the tile's chunks cover the workgroup
-  const bool stager = 32 * CPR >= kMT || tid < 32 * CPR;
-  const int srr = tid / CPR, sch = tid - srr * CPR;
+  const bool stager = 32 * CPR >= NTH || tid < 32 * CPR;
   auto fetch = [&](int n) {
     if (stager) {
       const int64_t jt = kb0 + 32 * int64_t(n);   // the tile's first key (uniform)
       const int lo = int(klo - jt), hi = int(khi - jt);
-      const bool ok = srr >= lo && srr <= hi;
-      const int jr = int(jt - sr.p0) + srr;        // key relative to the first new token
       const T* kn = sr.kin + (int64_t(sr.start) * a.Hkv + g) * D;
       const T* vn = sr.vin + (int64_t(sr.start) * a.Hkv + g) * D;
-      const uint32_t cb = uint32_t(8 * sizeof(T)) * sch;  // the thread's 8-element chunk of the row
-      const uint32_t on = ok && jr >= 0 ? uint32_t(jr) * rowb + cb : kOOB;
-      bload_frag(sk, make_rsrc(kn, nbytes), on);
-      bload_frag(sv, make_rsrc(vn, nbytes), on);
-      if (jt < sr.p0) {  // the tile reaches into the history rows
-        const uint32_t hb = uint32_t(sr.p0 - sr.h0) * D * sizeof(T);
-        const uint32_t oh = ok && jr < 0 ? uint32_t(jr + int(sr.p0 - sr.h0)) * uint32_t(D * sizeof(T)) + cb : kOOB;
-        Frag<T> hk, hv;
-        bload_frag(hk, make_rsrc(sr.kh, hb), oh);
-        bload_frag(hv, make_rsrc(sr.vh, hb), oh);
-        sk = frag_or(sk, hk);
-        sv = frag_or(sv, hv);
+#pragma unroll
+      for (int u = 0; u < SPT; ++u) {
+        const int id = tid + u * NTH, srr = id / CPR, sch = id - srr * CPR;
+        const bool ok = srr >= lo && srr <= hi;
+        const int jr = int(jt - sr.p0) + srr;      // key relative to the first new token
+        const uint32_t cb = uint32_t(8 * sizeof(T)) * sch;  // the thread's 8-element chunk of the row
+        const uint32_t on = ok && jr >= 0 ? uint32_t(jr) * rowb + cb : kOOB;
+        bload_frag(sk[u], make_rsrc(kn, nbytes), on);
+        bload_frag(sv[u], make_rsrc(vn, nbytes), on);
+        if (jt < sr.p0) {  // the tile reaches into the history rows
+          const uint32_t hb = uint32_t(sr.p0 - sr.h0) * D * sizeof(T);
+          const uint32_t oh = ok && jr < 0 ? uint32_t(jr + int(sr.p0 - sr.h0)) * uint32_t(D * sizeof(T)) + cb : kOOB;
+          Frag<T> hk, hv;
+          bload_frag(hk, make_rsrc(sr.kh, hb), oh);
+          bload_frag(hv, make_rsrc(sr.vh, hb), oh);
+          sk[u] = frag_or(sk[u], hk);
+          sv[u] = frag_or(sv[u], hv);
+        }
       }
     }
   };
   auto store = [&](int n) {
     if (stager) {
       T* kt = lds_fresh(bnd + (n & 1) * BAND);
-      store8(kt + srr * KROW + 8 * sch, sk);
-      store8(kt + 32 * KROW + srr * VROW + 8 * sch, sv);
+#pragma unroll
+      for (int u = 0; u < SPT; ++u) {
+        const int id = tid + u * NTH, srr = id / CPR, sch = id - srr * CPR;
+        store8(kt + srr * KROW + 8 * sch, sk[u]);
+        store8(kt + 32 * KROW + srr * VROW + 8 * sch, sv[u]);
+      }
     }
   };
-  // (with a band, the first slab of delayed keys is loaded only after it:
-  // its registers are not held through the band loop)
+  // (the first slab of delayed keys is loaded after the band, with or
+  // without one: its registers are not held through the band loop, and
+  // every path issues its loads in the same order, so the compiler's
+  // memory-counter waits for the queries do not also wait for the slab)
   auto prefetch = [&]() {
     load_q();  // the band's queries, then the feature map's input
-    if (linear && W == 0) load_slab(0);
     if (W > 0) fetch(0);
   };
 
@@ -871,20 +891,20 @@ void prefill_main(PrefillArgs a) {
   //         segment start (the scan's record), fp32, into LDS (S transposed);
   //         they stay there for the whole walk
   if (linear) {
-    if constexpr (LD::kWfLds) stage_wf<T, D, DF, kMT>(reinterpret_cast<const T*>(static_cast<const char*>(L.wf) + int64_t(g) * a.wf_hs), Wn);
+    if constexpr (LD::kWfLds) stage_wf<T, D, DF, NTH>(reinterpret_cast<const T*>(static_cast<const char*>(L.wf) + int64_t(g) * a.wf_hs), Wn);
     const float* S0 = L.seg + (int64_t(a.seg0 + sg) * a.Hkv + g) * (int64_t(DF) * D + DF);
-    constexpr int NS = DF * D / 4 / kMT;
-    static_assert(NS * kMT * 4 == DF * D, "even split");
+    constexpr int NS = DF * D / 4 / NTH;
+    static_assert(NS * NTH * 4 == DF * D, "even split");
     float4 x[NS];
 #pragma unroll
     for (int u = 0; u < NS; ++u) {
-      const int i = tid + u * kMT, f = i / (D / 4), c4 = 4 * (i - f * (D / 4));
+      const int i = tid + u * NTH, f = i / (D / 4), c4 = 4 * (i - f * (D / 4));
       x[u] = *reinterpret_cast<const float4*>(S0 + f * D + c4);
     }
     const float zv = tid < DF ? S0[DF * D + tid] : 0.f;
 #pragma unroll
     for (int u = 0; u < NS; ++u) {
-      const int i = tid + u * kMT, f = i / (D / 4), c4 = 4 * (i - f * (D / 4));
+      const int i = tid + u * NTH, f = i / (D / 4), c4 = 4 * (i - f * (D / 4));
       St[(c4 + 0) * SROW + f] = x[u].x;
       St[(c4 + 1) * SROW + f] = x[u].y;
       St[(c4 + 2) * SROW + f] = x[u].z;
@@ -895,23 +915,27 @@ void prefill_main(PrefillArgs a) {
   __syncthreads();  // Wf, S, z staged
 
   while (true) {
-    f32x4_t acc[2][CT];  // transposed: value columns 16ct+4lg+i of query row hq
+    f32x4_t acc[QT][CT];  // transposed: value columns 16ct+4lg+i of query row hq
+    float m_run[QT], l_run[QT];
+    float m_use[QT];  // m_run, or 0 while it is -inf
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int qt = 0; qt < QT; ++qt) {
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct) acc[qt][ct] = zero4();
-    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+      m_run[qt] = -INFINITY;
+      l_run[qt] = 0.f;
+      m_use[qt] = 0.f;
+    }
 
     // ---- 1. banded window attention, keys [klo, khi], 32-key tiles, two
     //         LDS stages (the previous pass ended at a barrier: the shared
     //         region is free)
-    float m_use[2] = {0.f, 0.f};  // m_run, or 0 while it is -inf
     if (W > 0) {
       refresh();
       store(0);  // tile 0 was fetched with the pass's other prefetches
       if (qneg) {
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
+        for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
           for (int kk = 0; kk < KS; ++kk) qf[qt][kk].negate();
       }
@@ -921,19 +945,25 @@ void prefill_main(PrefillArgs a) {
         const T* kt = lds_fresh(static_cast<const T*>(bnd) + (n & 1) * BAND);
         const T* vt = kt + 32 * KROW;
         // scores: key row m of sub-tile t is key kb + 8(m/4) + 4t + m%4
-        f32x4_t sc[2][2];
+        f32x4_t sc[QT][2];
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
+        for (int qt = 0; qt < QT; ++qt) sc[qt][0] = sc[qt][1] = zero4();
+        // the tile's K fragments, all issued before the first score MFMA
+        Frag<T> kfr[2][KS];
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) {
-            Frag<T> fa;
-            fa.load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * KROW + 32 * kk + 8 * lg);
+          for (int kk = 0; kk < KS; ++kk) kfr[t][kk].load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * KROW + 32 * kk + 8 * lg);
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, qf[qt][kk], sc[qt][t]);
-          }
-        }
+        for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) sc[qt][t] = mma(kfr[t][kk], qf[qt][kk], sc[qt][t]);
+        // the V column fragments, in flight during the softmax
+        Frag<T> fvr[CT];
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) load_colfrag(fvr[ct], vt, VROW, 8 * lg, 16 * ct);
         // the tile's first key, relative to the chunk's first token t0 (a
         // band spans less than 2^31 keys: 32-bit arithmetic)
         const int kb = int(kb0 - t0) + 32 * n;
@@ -943,10 +973,10 @@ void prefill_main(PrefillArgs a) {
         // raw scores, -inf outside the band (edge tiles; set in place), and
         // each row's tile max (the scale sc2 > 0 joins the exponent's FMA;
         // the max is taken raw)
-        float mx[2];
-        Frag<T> pf[2];
+        float mx[QT];
+        Frag<T> pf[QT];
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
+        for (int qt = 0; qt < QT; ++qt) {
           if (!interior) {
             // j - tq = base + off;  valid: j >= klo, tq - W < j <= tq, row
             // exists: one interval [olo, ohi] of offsets per row (empty for a
@@ -975,9 +1005,12 @@ void prefill_main(PrefillArgs a) {
         // lazy rescale (one test for both row tiles): the running max moves
         // only when a score exceeds it by more than 2^8, so p = 2^(s - m) <=
         // 256 and acc, l stay in range
-        if (__any(mx[0] > m_run[0] + 8.f || mx[1] > m_run[1] + 8.f)) {
+        bool up = false;
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt) {
+        for (int qt = 0; qt < QT; ++qt) up = up || mx[qt] > m_run[qt] + 8.f;
+        if (__any(up)) {
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) {
             const float m_new = fmaxf(m_run[qt], mx[qt]);
             const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
             l_run[qt] *= alpha;
@@ -990,7 +1023,7 @@ void prefill_main(PrefillArgs a) {
           }
         }
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
+        for (int qt = 0; qt < QT; ++qt) {
           float pv[8], ps = 0.f;
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
@@ -1001,12 +1034,9 @@ void prefill_main(PrefillArgs a) {
           l_run[qt] += ps;
         }
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          Frag<T> fv;
-          load_colfrag(fv, vt, VROW, 8 * lg, 16 * ct);
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
-        }
+          for (int qt = 0; qt < QT; ++qt) acc[qt][ct] = mma(fvr[ct], pf[qt], acc[qt][ct]);
         if (n + 1 < ntile) store(n + 1);
         __syncthreads();
       }
@@ -1018,10 +1048,10 @@ void prefill_main(PrefillArgs a) {
     //         -60 first (the band's terms rescaled to match) so that 2^-m
     //         stays finite; without a band (W = 0) m = 0.
     if (linear) {
-      if (W > 0) load_slab(0);  // behind the feature map and the read-out
-      float qscale[2];
+      load_slab(0);  // behind the feature map and the read-out
+      float qscale[QT];
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
+      for (int qt = 0; qt < QT; ++qt) {
         const bool none = m_run[qt] == -INFINITY;
         const float m0 = none ? 0.f : fmaxf(m_run[qt], -60.f);
         const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m0);
@@ -1037,40 +1067,57 @@ void prefill_main(PrefillArgs a) {
         qscale[qt] = (W > 0 && qneg) ? -__builtin_amdgcn_exp2f(-m0) : __builtin_amdgcn_exp2f(-m0);
       }
       // gated: G_t - G_{t0-1} of each row and its read-out factor
-      float gqr[2] = {0.f, 0.f}, fq[2] = {1.f, 1.f};
+      float gqr[QT], fq[QT];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        gqr[qt] = 0.f;
+        fq[qt] = 1.f;
+      }
       double gref = 0.0;
       if constexpr (GATED) {
         gref = gt.at(t0 - 1);
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
+        for (int qt = 0; qt < QT; ++qt) {
           gqr[qt] = float(gt.at(t0 + ti[qt]) - gref);
           fq[qt] = decay_exp(gqr[qt]);
         }
       }
       // phi(q) 2^-m, transposed: lane (row hq, group lg) gets features
       // 32kf+4lg+i and 32kf+16+4lg+i of its query row in fragment kf
-      Frag<T> pqf[2][KSF];
+      Frag<T> pqf[QT][KSF];
       const auto wf = wf_cols();
       // the softmax map: each query row's max and 1 / sum over its DF
       // features, from a first pass (running max and rescaled sum per lane,
       // then over the row's 4 lane groups)
-      float qmax[2] = {0.f, 0.f}, qinv[2] = {1.f, 1.f};
+      float qmax[QT], qinv[QT];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        qmax[qt] = 0.f;
+        qinv[qt] = 1.f;
+      }
       if constexpr (PHI == GLIDE_PHI_SOFTMAX) {
-        float m[2] = {-INFINITY, -INFINITY}, sm[2] = {0.f, 0.f};
+        float m[QT], sm[QT];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          m[qt] = -INFINITY;
+          sm[qt] = 0.f;
+        }
 #pragma unroll
         for (int kf = 0; kf < KSF; ++kf) {
 #pragma unroll
           for (int half = 0; half < 2; ++half) {
-            f32x4_t ph[2] = {zero4(), zero4()};
+            f32x4_t ph[QT];
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) ph[qt] = zero4();
 #pragma unroll
             for (int kk = 0; kk < KS; ++kk) {
               Frag<T> wa;
               wf.col(wa, kk, 32 * kf + 16 * half);
 #pragma unroll
-              for (int qt = 0; qt < 2; ++qt) ph[qt] = mma(wa, qf[qt][kk], ph[qt]);
+              for (int qt = 0; qt < QT; ++qt) ph[qt] = mma(wa, qf[qt][kk], ph[qt]);
             }
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) {
+            for (int qt = 0; qt < QT; ++qt) {
               float y[4], mg = -INFINITY;
 #pragma unroll
               for (int i = 0; i < 4; ++i) {
@@ -1087,7 +1134,7 @@ void prefill_main(PrefillArgs a) {
           }
         }
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
+        for (int qt = 0; qt < QT; ++qt) {
 #pragma unroll
           for (int off = 16; off < 64; off <<= 1) {
             const float mo = __shfl_xor(m[qt], off), so = __shfl_xor(sm[qt], off);
@@ -1102,19 +1149,21 @@ void prefill_main(PrefillArgs a) {
       }
 #pragma unroll
       for (int kf = 0; kf < KSF; ++kf) {
-        float pv[2][8];
+        float pv[QT][8];
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-          f32x4_t ph[2] = {zero4(), zero4()};
+          f32x4_t ph[QT];
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) ph[qt] = zero4();
 #pragma unroll
           for (int kk = 0; kk < KS; ++kk) {
             Frag<T> wa;
             wf.col(wa, kk, 32 * kf + 16 * half);
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) ph[qt] = mma(wa, qf[qt][kk], ph[qt]);
+            for (int qt = 0; qt < QT; ++qt) ph[qt] = mma(wa, qf[qt][kk], ph[qt]);
           }
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt)
+          for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               if constexpr (PHI == 0)
@@ -1128,15 +1177,15 @@ void prefill_main(PrefillArgs a) {
             }
         }
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) pqf[qt][kf].set8(pv[qt]);
+        for (int qt = 0; qt < QT; ++qt) pqf[qt][kf].set8(pv[qt]);
       }
       // read-out (phi(q).S_c)^T = S_c^T phi(q)^T, and phi(q).z_c
       const float* Sr = lds_fresh(static_cast<const float*>(St)) + hq * SROW;
 #pragma unroll
       for (int kf = 0; kf < KSF; ++kf) {
-        Frag<T> rq[2];  // the read-out's phi(q): decayed when gated
+        Frag<T> rq[QT];  // the read-out's phi(q): decayed when gated
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
+        for (int qt = 0; qt < QT; ++qt) {
           if constexpr (GATED) {
             float x[8];
             pqf[qt][kf].to_floats(x);
@@ -1152,13 +1201,13 @@ void prefill_main(PrefillArgs a) {
           Frag<T> fs;
           load_row2_f32(fs, Sr + 16 * ct * SROW, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fs, rq[qt], acc[qt][ct]);
+          for (int qt = 0; qt < QT; ++qt) acc[qt][ct] = mma(fs, rq[qt], acc[qt][ct]);
         }
       }
-      float den[2];
+      float den[QT];
       const float* zr = lds_fresh(static_cast<const float*>(zs));
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
+      for (int qt = 0; qt < QT; ++qt) {
         float dz = 0.f;
 #pragma unroll
         for (int kf = 0; kf < KSF; ++kf) {
@@ -1193,15 +1242,15 @@ void prefill_main(PrefillArgs a) {
         }
         __syncthreads();  // keys and values staged; the read-outs of S_c, z_c are done
         {
-          const int kt = slab_key_tile<D, DF, SL>(kMW);
+          const int kt = slab_key_tile<D, DF, SL>(MW);
           const T* krr = lds_fresh(static_cast<const T*>(kr));
           Frag<T> x[KS];
 #pragma unroll
           for (int kk = 0; kk < KS; ++kk) x[kk].load(krr + (16 * kt + hq) * KROW + 32 * kk + 8 * lg);
           // the slab's keys: i' = s0 + r < nk, and key t0 - Wd + i' >= 0
           const int64_t rlo = int64_t(Wd) - t0 - s0;
-          phi_slab<T, D, DF, SL, PHI>(wf_cols(), x, lds_fresh(pk), kMW, rlo > 0 ? int(rlo < SL ? rlo : SL) : 0,
-                                      nk - s0);
+          phi_slab<T, D, DF, SL, PHI, MW>(wf_cols(), x, lds_fresh(pk), rlo > 0 ? int(rlo < SL ? rlo : SL) : 0,
+                                          nk - s0);
         }
         __syncthreads();
         const T* pkr = lds_fresh(static_cast<const T*>(pk));
@@ -1247,9 +1296,9 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
         for (int kb = 0; kb < SL / 32; ++kb) {
           if (s0 + 32 * kb > ti_max) break;
-          f32x4_t sc[2][2];
+          f32x4_t sc[QT][2];
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt) sc[qt][0] = sc[qt][1] = zero4();
+          for (int qt = 0; qt < QT; ++qt) sc[qt][0] = sc[qt][1] = zero4();
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
             const T* prow = pkr + (32 * kb + 8 * (hq >> 2) + 4 * t + (hq & 3)) * PROW;
@@ -1258,12 +1307,12 @@ void prefill_main(PrefillArgs a) {
               Frag<T> fa;
               load_row2(fa, prow, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
 #pragma unroll
-              for (int qt = 0; qt < 2; ++qt) sc[qt][t] = mma(fa, pqf[qt][kf], sc[qt][t]);
+              for (int qt = 0; qt < QT; ++qt) sc[qt][t] = mma(fa, pqf[qt][kf], sc[qt][t]);
             }
           }
-          Frag<T> pf[2];
+          Frag<T> pf[QT];
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt) {
+          for (int qt = 0; qt < QT; ++qt) {
             float pv[8];
 #pragma unroll
             for (int t = 0; t < 2; ++t)
@@ -1281,7 +1330,7 @@ void prefill_main(PrefillArgs a) {
             Frag<T> fv;
             load_colfrag(fv, vsr, VROW, 32 * kb + 8 * lg, 16 * ct);
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
+            for (int qt = 0; qt < QT; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
           }
         }
         if constexpr (GATED) {
@@ -1291,7 +1340,7 @@ void prefill_main(PrefillArgs a) {
             __syncthreads();
             const float gend_rel = float(gt.at(t0 + nk - 1) - gref);
             T* pkw = lds_fresh(pk);
-            for (int e = tid; e < SL * DF; e += kMT) {
+            for (int e = tid; e < SL * DF; e += NTH) {
               const int r = e / DF, f = e - r * DF;
               pkw[r * PROW + f] = from_f32<T>(to_f32(pkw[r * PROW + f]) * decay_exp(gend_rel - gk_lds[r]));
             }
@@ -1302,15 +1351,18 @@ void prefill_main(PrefillArgs a) {
       }
       // the shared denominator: band sum + linear part (per-lane partials)
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) l_run[qt] += den[qt];
+      for (int qt = 0; qt < QT; ++qt) l_run[qt] += den[qt];
     }
 
     // ---- 3. the next pass's loads, then this pass's outputs: value columns
     //         16ct+4lg .. +3 of query row hq
-    int64_t orow[2];
+    int64_t orow[QT];
+    bool ov[QT];
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) orow[qt] = sr.qrow(c0 + ti[qt], hh[qt]) * D + 4 * lg;
-    const bool ov[2] = {rv[0], rv[1]};
+    for (int qt = 0; qt < QT; ++qt) {
+      orow[qt] = sr.qrow(c0 + ti[qt], hh[qt]) * D + 4 * lg;
+      ov[qt] = rv[qt];
+    }
     const bool more = !(last_pass && c0 + C >= s_hi);
     if (more) {
       if (last_pass) {
@@ -1328,7 +1380,7 @@ void prefill_main(PrefillArgs a) {
     refresh();
     prefetch();
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       const float ls = lg_sum(l_run[qt]);
       const float inv = ls > 0.f ? 1.f / ls : 0.f;
       if (ov[qt]) {
@@ -1437,30 +1489,31 @@ __global__ void prefill_advance(PrefillArgs a) {
 // (the grid's last dimension runs over them, longest windows first).
 template <typename T, int D, int DF>
 hipError_t layer_t(const PrefillArgs& a, hipStream_t s) {
+  constexpr int MW = main_waves<T, D>();
   hipError_t e;
   const unsigned nl = unsigned(a.nlayer);
   bool window = false;
   for (int i = 0; i < a.nlayer; ++i) window = window || a.layers[i].W > 0;
   auto main = [&](int pass) {
-    const dim3 grid(a.nseg, a.Hkv, nl), block(kMT);
+    const dim3 grid(a.nseg, a.Hkv, nl), block(64 * MW);
     if (a.gated) {  // the shared denominator only
-      if (a.phi == GLIDE_PHI_SOFTMAX) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 0, true>), grid, block, 0, s, a);
-      else if (a.phi) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 0, true>), grid, block, 0, s, a);
-      else hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 0, true>), grid, block, 0, s, a);
+      if (a.phi == GLIDE_PHI_SOFTMAX) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 0, true, MW>), grid, block, 0, s, a);
+      else if (a.phi) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 0, true, MW>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 0, true, MW>), grid, block, 0, s, a);
       return;
     }
     if (a.phi == GLIDE_PHI_SOFTMAX) {
-      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 0>), grid, block, 0, s, a);
-      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 1>), grid, block, 0, s, a);
-      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 2>), grid, block, 0, s, a);
+      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 0, false, MW>), grid, block, 0, s, a);
+      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 1, false, MW>), grid, block, 0, s, a);
+      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 2, 2, false, MW>), grid, block, 0, s, a);
     } else if (a.phi) {
-      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 0>), grid, block, 0, s, a);
-      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 1>), grid, block, 0, s, a);
-      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 2>), grid, block, 0, s, a);
+      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 0, false, MW>), grid, block, 0, s, a);
+      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 1, false, MW>), grid, block, 0, s, a);
+      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 1, 2, false, MW>), grid, block, 0, s, a);
     } else {
-      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 0>), grid, block, 0, s, a);
-      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 1>), grid, block, 0, s, a);
-      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 2>), grid, block, 0, s, a);
+      if (pass == 0) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 0, false, MW>), grid, block, 0, s, a);
+      if (pass == 1) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 1, false, MW>), grid, block, 0, s, a);
+      if (pass == 2) hipLaunchKernelGGL((prefill_main<T, D, DF, 0, 2, false, MW>), grid, block, 0, s, a);
     }
   };
   if (a.gated) {  // the new tokens' cumulative log-gates, before any kernel reads them
