@@ -316,24 +316,31 @@ __device__ __forceinline__ void phi_slab(const WfCols<T, D, DF, kLds>& wf, const
       if (u < per) store4(pk + key * PROW + 16 * (ft0 + u) + 4 * lg, is_key ? acc[u] : zero4(), kw / tot);
     return;
   }
+  // transposed (Wf^T K^T): lane (hq, lg) gets features 16ft+4lg .. +3 of
+  // key 16kt+hq, one 4-element store per tile.  The wave's tiles share the
+  // key tile; their Wf fragments are read one reduction step at a time for
+  // all tiles, so the tiles' MFMA chains interleave.
+  f32x4_t acc[per];
+#pragma unroll
+  for (int u = 0; u < per; ++u) acc[u] = zero4();
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    Frag<T> wb[per];
+#pragma unroll
+    for (int u = 0; u < per; ++u) wf.col(wb[u], kk, 16 * ((wave * per + u) % FT));
+#pragma unroll
+    for (int u = 0; u < per; ++u) acc[u] = mma(wb[u], x[kk], acc[u]);
+  }
+#pragma unroll
   for (int u = 0; u < per; ++u) {
     const int tile = wave * per + u, kt = tile / FT, ft = tile - kt * FT;
-    // transposed (Wf^T K^T): lane (hq, lg) gets features 16ft+4lg .. +3 of
-    // key 16kt+hq, one 4-element store
-    f32x4_t acc = zero4();
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      Frag<T> wb;
-      wf.col(wb, kk, 16 * ft);
-      acc = mma(wb, x[kk], acc);
-    }
     // rows outside [rlo, rhi) are no keys (zero rows): their features must
     // be 0, which ReLU gives by itself and ELU + 1 (phi(0) = 1) does not
     const int key = 16 * kt + hq;
     if constexpr (PHI == 0) {
-      store4(pk + key * PROW + 16 * ft + 4 * lg, act4(acc, 0), kw);
+      store4(pk + key * PROW + 16 * ft + 4 * lg, act4(acc[u], 0), kw);
     } else {
-      store4(pk + key * PROW + 16 * ft + 4 * lg, key >= rlo && key < rhi ? act4(acc, PHI) : zero4(), kw);
+      store4(pk + key * PROW + 16 * ft + 4 * lg, key >= rlo && key < rhi ? act4(acc[u], PHI) : zero4(), kw);
     }
   }
 }
@@ -745,7 +752,7 @@ void prefill_main(PrefillArgs a) {
 
   // ---- pass geometry: chunk c0 (nk tokens from absolute position t0), rows
   //      [rb, rb + kRB) of its nrow = nk * G query rows
-  int c0 = s_lo, rb = 0, nk = 0, nrow = 0, ti_min = 0, ti_max = 0, ntile = 0;
+  int c0 = s_lo, rb = 0, nk = 0, nrow = 0, ti_min = 0, ti_max = 0, wti_max = 0, ntile = 0;
   bool last_pass = true;
   int64_t t0 = 0, klo = 0, khi = 0, kb0 = 0;
   int ti[QT], hh[QT];  // this lane's query row (row hq) in each of its 16-row q-tiles
@@ -758,6 +765,7 @@ void prefill_main(PrefillArgs a) {
     const int r_end = min(nrow, rb + kRB);
     ti_min = rb / G;
     ti_max = (r_end - 1) / G;
+    wti_max = min(r_end - 1, rb + 16 * QT * (wave + 1) - 1) / G;
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       const int r = rb + 16 * QT * wave + 16 * qt + hq;
@@ -1150,30 +1158,38 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
       for (int kf = 0; kf < KSF; ++kf) {
         float pv[QT][8];
+        // the 32 columns' Wf fragments, read in one batch
+        Frag<T> wa[2][KS];
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) wf.col(wa[half][kk], kk, 32 * kf + 16 * half);
+        f32x4_t ph[2][QT];
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) ph[half][qt] = zero4();
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+          for (int half = 0; half < 2; ++half)
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) ph[half][qt] = mma(wa[half][kk], qf[qt][kk], ph[half][qt]);
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-          f32x4_t ph[QT];
-#pragma unroll
-          for (int qt = 0; qt < QT; ++qt) ph[qt] = zero4();
-#pragma unroll
-          for (int kk = 0; kk < KS; ++kk) {
-            Frag<T> wa;
-            wf.col(wa, kk, 32 * kf + 16 * half);
-#pragma unroll
-            for (int qt = 0; qt < QT; ++qt) ph[qt] = mma(wa, qf[qt][kk], ph[qt]);
-          }
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               if constexpr (PHI == 0)
-                pv[qt][4 * half + i] = fmaxf(ph[qt][i] * qscale[qt], 0.f);
+                pv[qt][4 * half + i] = fmaxf(ph[half][qt][i] * qscale[qt], 0.f);
               else if constexpr (PHI == GLIDE_PHI_SOFTMAX)
                 pv[qt][4 * half + i] =
-                    __builtin_amdgcn_exp2f(((qscale[qt] < 0.f ? -ph[qt][i] : ph[qt][i]) - qmax[qt]) * kLog2e) *
+                    __builtin_amdgcn_exp2f(((qscale[qt] < 0.f ? -ph[half][qt][i] : ph[half][qt][i]) - qmax[qt]) * kLog2e) *
                     qinv[qt] * fabsf(qscale[qt]);
               else  // (qscale's sign undoes the band's query negation)
-                pv[qt][4 * half + i] = feat_act(qscale[qt] < 0.f ? -ph[qt][i] : ph[qt][i], PHI) * fabsf(qscale[qt]);
+                pv[qt][4 * half + i] =
+                    feat_act(qscale[qt] < 0.f ? -ph[half][qt][i] : ph[half][qt][i], PHI) * fabsf(qscale[qt]);
             }
         }
 #pragma unroll
@@ -1196,12 +1212,18 @@ void prefill_main(PrefillArgs a) {
             rq[qt] = pqf[qt][kf];
           }
         }
+        // S^T rows read four column tiles at a time
+        constexpr int CB = CT < 4 ? CT : 4;
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          Frag<T> fs;
-          load_row2_f32(fs, Sr + 16 * ct * SROW, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
+        for (int c0 = 0; c0 < CT; c0 += CB) {
+          Frag<T> fs[CB];
 #pragma unroll
-          for (int qt = 0; qt < QT; ++qt) acc[qt][ct] = mma(fs, rq[qt], acc[qt][ct]);
+          for (int c = 0; c < CB; ++c)
+            load_row2_f32(fs[c], Sr + 16 * (c0 + c) * SROW, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
+#pragma unroll
+          for (int c = 0; c < CB; ++c)
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) acc[qt][c0 + c] = mma(fs[c], rq[qt], acc[qt][c0 + c]);
         }
       }
       float den[QT];
@@ -1293,23 +1315,32 @@ void prefill_main(PrefillArgs a) {
         if (!GATED && last_pass) state_update(1.f);
         // scores: key row m of sub-tile t of 32-key block kb is
         // i' = s0 + 32kb + 8(m/4) + 4t + m%4
+        // (a block of keys after every row of this wave is skipped: the
+        // wave's rows are consecutive, its last token is wti_max)
 #pragma unroll
         for (int kb = 0; kb < SL / 32; ++kb) {
-          if (s0 + 32 * kb > ti_max) break;
+          if (s0 + 32 * kb > wti_max) break;
           f32x4_t sc[QT][2];
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) sc[qt][0] = sc[qt][1] = zero4();
+          // the block's phi(k) fragments, then its V column fragments (in
+          // flight during the mask), each read in one batch
+          Frag<T> fa[2][KSF];
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
             const T* prow = pkr + (32 * kb + 8 * (hq >> 2) + 4 * t + (hq & 3)) * PROW;
 #pragma unroll
-            for (int kf = 0; kf < KSF; ++kf) {
-              Frag<T> fa;
-              load_row2(fa, prow, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
-#pragma unroll
-              for (int qt = 0; qt < QT; ++qt) sc[qt][t] = mma(fa, pqf[qt][kf], sc[qt][t]);
-            }
+            for (int kf = 0; kf < KSF; ++kf) load_row2(fa[t][kf], prow, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
           }
+#pragma unroll
+          for (int kf = 0; kf < KSF; ++kf)
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+              for (int qt = 0; qt < QT; ++qt) sc[qt][t] = mma(fa[t][kf], pqf[qt][kf], sc[qt][t]);
+          Frag<T> fv[CT];
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) load_colfrag(fv[ct], vsr, VROW, 32 * kb + 8 * lg, 16 * ct);
           Frag<T> pf[QT];
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) {
@@ -1326,12 +1357,9 @@ void prefill_main(PrefillArgs a) {
             den[qt] += pf[qt].sum();
           }
 #pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            Frag<T> fv;
-            load_colfrag(fv, vsr, VROW, 32 * kb + 8 * lg, 16 * ct);
+          for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-            for (int qt = 0; qt < QT; ++qt) acc[qt][ct] = mma(fv, pf[qt], acc[qt][ct]);
-          }
+            for (int qt = 0; qt < QT; ++qt) acc[qt][ct] = mma(fv[ct], pf[qt], acc[qt][ct]);
         }
         if constexpr (GATED) {
           if (last_pass) {
