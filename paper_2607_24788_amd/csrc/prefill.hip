@@ -732,6 +732,7 @@ void prefill_main(PrefillArgs a) {
   // around the running max (every weight still comes out as exactly 1).
   const bool qneg = a.tau < 0.f;
   const float sc2 = fmaxf(fabsf(a.tau) * kLog2e, 1e-30f);
+  const float inv_sc2 = 1.f / sc2;
   const T* Q = static_cast<const T*>(L.q);
   T* O = static_cast<T*>(L.out);
   // the global bases, made opaque once per pass: row addresses are then
@@ -926,6 +927,7 @@ void prefill_main(PrefillArgs a) {
     f32x4_t acc[QT][CT];  // transposed: value columns 16ct+4lg+i of query row hq
     float m_run[QT], l_run[QT];
     float m_use[QT];  // m_run, or 0 while it is -inf
+    float s_up[QT];   // raw score above which the band's running max moves
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
 #pragma unroll
@@ -933,6 +935,7 @@ void prefill_main(PrefillArgs a) {
       m_run[qt] = -INFINITY;
       l_run[qt] = 0.f;
       m_use[qt] = 0.f;
+      s_up[qt] = -INFINITY;
     }
 
     // ---- 1. banded window attention, keys [klo, khi], 32-key tiles, two
@@ -978,10 +981,7 @@ void prefill_main(PrefillArgs a) {
         // keys [kb, kb+31] lie inside the band of every row of the pass
         // (tokens t0+ti_min .. t0+ti_max) for all but the edge tiles
         const bool interior = kb >= ti_max - W + 1 && kb + 31 <= ti_min;
-        // raw scores, -inf outside the band (edge tiles; set in place), and
-        // each row's tile max (the scale sc2 > 0 joins the exponent's FMA;
-        // the max is taken raw)
-        float mx[QT];
+        // raw scores, -inf outside the band (edge tiles; set in place)
         Frag<T> pf[QT];
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
@@ -1003,27 +1003,32 @@ void prefill_main(PrefillArgs a) {
                 sc[qt][t][i] = ok ? sc[qt][t][i] : -INFINITY;
               }
           }
-          float x = fmaxf(sc[qt][0][0], sc[qt][1][0]);
+        }
+        // lazy rescale (one test for all the wave's rows): the running max
+        // moves only when a score exceeds it by more than 2^8 (a raw score
+        // above s_up = (m + 8) / sc2), so p = 2^(s - m) <= 256 and acc, l
+        // stay in range; only then are the rows' tile maxima taken
+        bool up = false;
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
           for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int i = 1; i < 4; ++i) x = fmaxf(x, sc[qt][t][i]);
-          mx[qt] = lg_max(x) * sc2;
-        }
-        // lazy rescale (one test for both row tiles): the running max moves
-        // only when a score exceeds it by more than 2^8, so p = 2^(s - m) <=
-        // 256 and acc, l stay in range
-        bool up = false;
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) up = up || mx[qt] > m_run[qt] + 8.f;
+            for (int i = 0; i < 4; ++i) up = up | (sc[qt][t][i] > s_up[qt]);
         if (__any(up)) {
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) {
-            const float m_new = fmaxf(m_run[qt], mx[qt]);
+            float x = fmaxf(sc[qt][0][0], sc[qt][1][0]);
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+              for (int i = 1; i < 4; ++i) x = fmaxf(x, sc[qt][t][i]);
+            const float m_new = fmaxf(m_run[qt], lg_max(x) * sc2);
             const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
             l_run[qt] *= alpha;
             m_run[qt] = m_new;
             m_use[qt] = m_new == -INFINITY ? 0.f : m_new;
+            s_up[qt] = (m_new + 8.f) * inv_sc2;
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
