@@ -733,6 +733,7 @@ void prefill_main(PrefillArgs a) {
   const bool qneg = a.tau < 0.f;
   const float sc2 = fmaxf(fabsf(a.tau) * kLog2e, 1e-30f);
   const float inv_sc2 = 1.f / sc2;
+  constexpr bool kOnesSum = sizeof(T) == 2;  // the band's row sums on the matrix cores
   const T* Q = static_cast<const T*>(L.q);
   T* O = static_cast<T*>(L.out);
   // the global bases, made opaque once per pass: row addresses are then
@@ -951,6 +952,16 @@ void prefill_main(PrefillArgs a) {
           for (int kk = 0; kk < KS; ++kk) qf[qt][kk].negate();
       }
       __syncthreads();
+      // bf16: each row's sum of the weights is a matrix product too, P^T
+      // times a ones fragment, on the weights as rounded for P V (every
+      // lane of the row's 16-lane column holds the full sum)
+      f32x4_t lsum[QT];
+      Frag<T> ones;
+      if constexpr (kOnesSum) {
+        ones.v = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) lsum[qt] = zero4();
+      }
       for (int n = 0; n < ntile; ++n) {
         if (n + 1 < ntile) fetch(n + 1);
         const T* kt = lds_fresh(static_cast<const T*>(bnd) + (n & 1) * BAND);
@@ -1026,6 +1037,10 @@ void prefill_main(PrefillArgs a) {
             const float m_new = fmaxf(m_run[qt], lg_max(x) * sc2);
             const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qt] - m_new);
             l_run[qt] *= alpha;
+            if constexpr (kOnesSum) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) lsum[qt][i] *= alpha;
+            }
             m_run[qt] = m_new;
             m_use[qt] = m_new == -INFINITY ? 0.f : m_new;
             s_up[qt] = (m_new + 8.f) * inv_sc2;
@@ -1037,21 +1052,31 @@ void prefill_main(PrefillArgs a) {
         }
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
-          float pv[8], ps = 0.f;
+          float pv[8];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            pv[i] = __builtin_amdgcn_exp2f(fmaf(sc[qt][i >> 2][i & 3], sc2, -m_use[qt]));
-            ps += pv[i];
-          }
+          for (int i = 0; i < 8; ++i) pv[i] = __builtin_amdgcn_exp2f(fmaf(sc[qt][i >> 2][i & 3], sc2, -m_use[qt]));
           pf[qt].set8(pv);
-          l_run[qt] += ps;
+          if constexpr (!kOnesSum) {
+            float ps = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ps += pv[i];
+            l_run[qt] += ps;
+          }
         }
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) acc[qt][ct] = mma(fvr[ct], pf[qt], acc[qt][ct]);
+        if constexpr (kOnesSum) {
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) lsum[qt] = mma(ones, pf[qt], lsum[qt]);
+        }
         if (n + 1 < ntile) store(n + 1);
         __syncthreads();
+      }
+      if constexpr (kOnesSum) {
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) l_run[qt] += lg == 0 ? lsum[qt][0] : 0.f;
       }
     }
 
