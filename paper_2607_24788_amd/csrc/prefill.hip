@@ -966,7 +966,11 @@ void prefill_main(PrefillArgs a) {
         if (n + 1 < ntile) fetch(n + 1);
         const T* kt = lds_fresh(static_cast<const T*>(bnd) + (n & 1) * BAND);
         const T* vt = kt + 32 * KROW;
-        // scores: key row m of sub-tile t is key kb + 8(m/4) + 4t + m%4
+        // scores: key row m of sub-tile t is key kb + 16t + m, so that a
+        // 16-lane group's K reads cover 16 consecutive rows (distinct LDS
+        // banks); lane (hq, lg) then holds the scores of keys 16t + 4lg + i,
+        // the order its P^T fragment gives P V's reduction (V read at rows
+        // 4lg .. 4lg+3 and 16+4lg .. 16+4lg+3 alike)
         f32x4_t sc[QT][2];
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) sc[qt][0] = sc[qt][1] = zero4();
@@ -975,7 +979,7 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) kfr[t][kk].load(kt + (8 * (hq >> 2) + 4 * t + (hq & 3)) * KROW + 32 * kk + 8 * lg);
+          for (int kk = 0; kk < KS; ++kk) kfr[t][kk].load(kt + (16 * t + hq) * KROW + 32 * kk + 8 * lg);
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
@@ -985,7 +989,7 @@ void prefill_main(PrefillArgs a) {
         // the V column fragments, in flight during the softmax
         Frag<T> fvr[CT];
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) load_colfrag(fvr[ct], vt, VROW, 8 * lg, 16 * ct);
+        for (int ct = 0; ct < CT; ++ct) load_colfrag2(fvr[ct], vt, VROW, 4 * lg, 16 + 4 * lg, 16 * ct);
         // the tile's first key, relative to the chunk's first token t0 (a
         // band spans less than 2^31 keys: 32-bit arithmetic)
         const int kb = int(kb0 - t0) + 32 * n;
@@ -1009,7 +1013,7 @@ void prefill_main(PrefillArgs a) {
             for (int t = 0; t < 2; ++t)
 #pragma unroll
               for (int i = 0; i < 4; ++i) {
-                const int off = 8 * lg + 4 * t + i;
+                const int off = 16 * t + 4 * lg + i;
                 const bool ok = (off >= olo) & (off <= ohi);
                 sc[qt][t][i] = ok ? sc[qt][t][i] : -INFINITY;
               }
