@@ -1326,10 +1326,12 @@ void prefill_main(PrefillArgs a) {
 #pragma unroll
             for (int kh = 0; kh < SL / 32; ++kh) {
               Frag<T> fa, fb;
-              load_colfrag(fa, pkr, PROW, 32 * kh + 8 * lg, 16 * ft);
-              load_colfrag(fb, vsr, VROW, 32 * kh + 8 * lg, 16 * ct);
+              // keys 32kh + 4lg .. +3 and 32kh + 16 + 4lg .. +3 (distinct
+              // LDS banks within each 32-lane half)
+              load_colfrag2(fa, pkr, PROW, 32 * kh + 4 * lg, 32 * kh + 16 + 4 * lg, 16 * ft);
+              load_colfrag2(fb, vsr, VROW, 32 * kh + 4 * lg, 32 * kh + 16 + 4 * lg, 16 * ct);
               d = mma(fa, fb, d);
-              if (ct == 0) zp += fa.sum();  // keys 32kh+8lg.. of feature 16ft+hq
+              if (ct == 0) zp += fa.sum();  // those keys' feature 16ft+hq
             }
             float4* sp = reinterpret_cast<float4*>(Sw + (16 * ct + hq) * SROW + 16 * ft + 4 * lg);
             float4 s4 = *sp;
@@ -1348,7 +1350,8 @@ void prefill_main(PrefillArgs a) {
         };
         if (!GATED && last_pass) state_update(1.f);
         // scores: key row m of sub-tile t of 32-key block kb is
-        // i' = s0 + 32kb + 8(m/4) + 4t + m%4
+        // i' = s0 + 32kb + 16t + m (consecutive rows per lane group), so lane
+        // (hq, lg) holds keys 32kb + 16t + 4lg + i
         // (a block of keys after every row of this wave is skipped: the
         // wave's rows are consecutive, its last token is wti_max)
 #pragma unroll
@@ -1362,7 +1365,7 @@ void prefill_main(PrefillArgs a) {
           Frag<T> fa[2][KSF];
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
-            const T* prow = pkr + (32 * kb + 8 * (hq >> 2) + 4 * t + (hq & 3)) * PROW;
+            const T* prow = pkr + (32 * kb + 16 * t + hq) * PROW;
 #pragma unroll
             for (int kf = 0; kf < KSF; ++kf) load_row2(fa[t][kf], prow, 32 * kf + 4 * lg, 32 * kf + 16 + 4 * lg);
           }
@@ -1374,7 +1377,7 @@ void prefill_main(PrefillArgs a) {
               for (int qt = 0; qt < QT; ++qt) sc[qt][t] = mma(fa[t][kf], pqf[qt][kf], sc[qt][t]);
           Frag<T> fv[CT];
 #pragma unroll
-          for (int ct = 0; ct < CT; ++ct) load_colfrag(fv[ct], vsr, VROW, 32 * kb + 8 * lg, 16 * ct);
+          for (int ct = 0; ct < CT; ++ct) load_colfrag2(fv[ct], vsr, VROW, 32 * kb + 4 * lg, 32 * kb + 16 + 4 * lg, 16 * ct);
           Frag<T> pf[QT];
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) {
@@ -1383,7 +1386,7 @@ void prefill_main(PrefillArgs a) {
             for (int t = 0; t < 2; ++t)
 #pragma unroll
               for (int i = 0; i < 4; ++i) {
-                const int kr_ = 32 * kb + 8 * lg + 4 * t + i;  // the key within the slab
+                const int kr_ = 32 * kb + 16 * t + 4 * lg + i;  // the key within the slab
                 const float w = GATED ? decay_exp(gqr[qt] - gk_lds[kr_]) : 1.f;
                 pv[4 * t + i] = (s0 + kr_ <= ti[qt]) ? sc[qt][t][i] * w : 0.f;
               }
