@@ -810,17 +810,13 @@ void decode_kernel(DecodeArgs a) {
     }
     __syncthreads();
     if (last) {
-      const bool wide = G * D > 2 * kThreads;
-      if (L.npiece <= 4) {
-        if (wide) merge_unit<T, D, DF, 4, 4>(a, L, rem, p);
-        else merge_unit<T, D, DF, 4, 2>(a, L, rem, p);
-      } else if (L.npiece <= 8) {
-        if (wide) merge_unit<T, D, DF, 8, 4>(a, L, rem, p);
-        else merge_unit<T, D, DF, 8, 2>(a, L, rem, p);
-      } else {
-        if (wide) merge_unit<T, D, DF, kMaxPieces, 4>(a, L, rem, p);
-        else merge_unit<T, D, DF, kMaxPieces, 2>(a, L, rem, p);
-      }
+      // one instantiation per piece-count bound (record loads for 4, 8 or 16
+      // pieces), four output elements per thread: more variants of this
+      // rarely run merge grew the kernel's code enough to slow the window
+      // loop of every workgroup (70B slice 748 -> 810 us per step)
+      if (L.npiece <= 4) merge_unit<T, D, DF, 4, 4>(a, L, rem, p);
+      else if (L.npiece <= 8) merge_unit<T, D, DF, 8, 4>(a, L, rem, p);
+      else merge_unit<T, D, DF, kMaxPieces, 4>(a, L, rem, p);
     }
   }
 
