@@ -1262,21 +1262,56 @@ void prefill_main(PrefillArgs a) {
       }
       float den[QT];
       const float* zr = lds_fresh(static_cast<const float*>(zs));
+      // bf16: the masked block's weight sums go to the matrix cores as in
+      // the band (P^T times a ones fragment, full sums in every lane group)
+      Frag<T> ones;
+      f32x4_t dsum[QT];
+      if constexpr (kOnesSum) {
+        ones.v = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+        // phi(q).z on the matrix cores too: z (fp32, as a bf16 hi + lo
+        // pair, about 16 bits) is the A fragment of every row, in phi(q)'s
+        // feature order
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        float dz = 0.f;
+        for (int qt = 0; qt < QT; ++qt) dsum[qt] = zero4();
 #pragma unroll
         for (int kf = 0; kf < KSF; ++kf) {
-          float qv[8];
-          pqf[qt][kf].to_floats(qv);
           const float4 za = *reinterpret_cast<const float4*>(zr + 32 * kf + 4 * lg);
           const float4 zb = *reinterpret_cast<const float4*>(zr + 32 * kf + 16 + 4 * lg);
-          dz = fmaf(qv[0], za.x, dz); dz = fmaf(qv[1], za.y, dz);
-          dz = fmaf(qv[2], za.z, dz); dz = fmaf(qv[3], za.w, dz);
-          dz = fmaf(qv[4], zb.x, dz); dz = fmaf(qv[5], zb.y, dz);
-          dz = fmaf(qv[6], zb.z, dz); dz = fmaf(qv[7], zb.w, dz);
+          float x[8] = {za.x, za.y, za.z, za.w, zb.x, zb.y, zb.z, zb.w}, h[8];
+          Frag<T> zh, zl;
+          zh.set8(x);
+          zh.to_floats(h);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) x[i] -= h[i];
+          zl.set8(x);
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) {
+            dsum[qt] = mma(zh, pqf[qt][kf], dsum[qt]);
+            dsum[qt] = mma(zl, pqf[qt][kf], dsum[qt]);
+          }
         }
-        den[qt] = dz * fq[qt];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          den[qt] = lg == 0 ? dsum[qt][0] * fq[qt] : 0.f;
+          dsum[qt] = zero4();
+        }
+      } else {
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          float dz = 0.f;
+#pragma unroll
+          for (int kf = 0; kf < KSF; ++kf) {
+            float qv[8];
+            pqf[qt][kf].to_floats(qv);
+            const float4 za = *reinterpret_cast<const float4*>(zr + 32 * kf + 4 * lg);
+            const float4 zb = *reinterpret_cast<const float4*>(zr + 32 * kf + 16 + 4 * lg);
+            dz = fmaf(qv[0], za.x, dz); dz = fmaf(qv[1], za.y, dz);
+            dz = fmaf(qv[2], za.z, dz); dz = fmaf(qv[3], za.w, dz);
+            dz = fmaf(qv[4], zb.x, dz); dz = fmaf(qv[5], zb.y, dz);
+            dz = fmaf(qv[6], zb.z, dz); dz = fmaf(qv[7], zb.w, dz);
+          }
+          den[qt] = dz * fq[qt];
+        }
       }
       // the chunk's delayed keys, SL at a time: phi(k) into LDS, the masked
       // block i' <= ti of every query row, and (last pass: every read-out of
@@ -1391,12 +1426,16 @@ void prefill_main(PrefillArgs a) {
                 pv[4 * t + i] = (s0 + kr_ <= ti[qt]) ? sc[qt][t][i] * w : 0.f;
               }
             pf[qt].set8(pv);
-            den[qt] += pf[qt].sum();
+            if constexpr (!kOnesSum) den[qt] += pf[qt].sum();
           }
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
             for (int qt = 0; qt < QT; ++qt) acc[qt][ct] = mma(fv[ct], pf[qt], acc[qt][ct]);
+          if constexpr (kOnesSum) {
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) dsum[qt] = mma(ones, pf[qt], dsum[qt]);
+          }
         }
         if constexpr (GATED) {
           if (last_pass) {
@@ -1416,7 +1455,10 @@ void prefill_main(PrefillArgs a) {
       }
       // the shared denominator: band sum + linear part (per-lane partials)
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) l_run[qt] += den[qt];
+      for (int qt = 0; qt < QT; ++qt) {
+        if constexpr (kOnesSum) den[qt] += lg == 0 ? dsum[qt][0] : 0.f;
+        l_run[qt] += den[qt];
+      }
     }
 
     // ---- 3. the next pass's loads, then this pass's outputs: value columns
