@@ -316,7 +316,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested); the hybrid-attention "
-              "step has no multi-GPU path in this build", file=sys.stderr)
+              "step is implemented for one GPU (sharding across GPUs is a design note only)", file=sys.stderr)
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)
